@@ -1,0 +1,223 @@
+/*
+ * dopr.h -- C ABI of the DoPR online-scoring hot path on MI355X (gfx950).
+ *
+ * DoPR (Reusable Compressed Document Prefixes for Efficient LLM Reranking)
+ * scores a (query, document) pair by running only the query tokens and one
+ * scoring token through the reranker, while every layer's attention also sees
+ * the document's compressed prefix key/value states, computed offline and
+ * injected as a pre-filled cache (Sec. 3.1, Eq. 3; Sec. 3.3; Sec. 3.4).  This
+ * library implements one decoder layer's share of that online step:
+ *
+ *   dopr_store_*       the HBM-resident prefix store of per-document K/V
+ *                      states (Sec. 3.3: query-independent, reused across
+ *                      queries; bf16 per Table 7).
+ *   dopr_prefix_attn   batched GQA attention in which each pair's online
+ *                      tokens attend to [that document's prefix ; their own
+ *                      causal keys] (Sec. 3.4; the query/score tokens see the
+ *                      document only through its prefix states, Sec. 3.2.2).
+ *   dopr_score_logits  the relevance score read off the score token's state
+ *                      (Sec. 3.2.3, Eq. for s(q,d)), as a yes/no logit pair.
+ *
+ * Conventions shared by every call
+ *   - All device buffers are allocated by the caller and passed as raw device
+ *     pointers; the library never calls hipMalloc/hipFree.  Buffers must stay
+ *     alive until the stream has passed the call.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *     Every call is asynchronous on that stream unless stated otherwise.
+ *   - bf16 means IEEE bfloat16 bit patterns (uint16); fp32 means IEEE float.
+ *   - head_dim D must be 128.  n_q_heads must be a multiple of n_kv_heads;
+ *     q head h reads kv head h / (n_q_heads / n_kv_heads).
+ *   - Every call returns a dopr_status_t.  Host-checkable argument errors are
+ *     returned before anything is launched.  Errors found on the device (a
+ *     doc id that is out of range or not resident, malformed cu_seqlens) are
+ *     deferred: the affected outputs are written as zeros, nothing is read
+ *     out of bounds, and dopr_check_status() reports the error.
+ *   - No C++ exception crosses this ABI and the library never aborts.
+ *   - Calls that share a store and overlap on different streams may race on
+ *     the store's deferred status word only (never on data).
+ */
+#ifndef DOPR_H
+#define DOPR_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  DOPR_OK = 0,
+  DOPR_ERR_INVALID_ARG = -1, /* null pointer, bad size, bad shape          */
+  DOPR_ERR_UNSUPPORTED = -2, /* valid but not implemented (e.g. D != 128)  */
+  DOPR_ERR_DOC_RANGE = -3,   /* doc id outside [0,n_docs) or not resident  */
+  DOPR_ERR_WORKSPACE = -4,   /* workspace or pool smaller than required    */
+  DOPR_ERR_HIP = -5,         /* a HIP runtime call failed                  */
+  DOPR_ERR_SEQLEN = -6       /* cu_seqlens not monotone, T_p < 1,
+                                T_p > max_tokens or cu[P] != total_tokens  */
+} dopr_status_t;
+
+/* Opaque store handle.  The library owns only this small host struct; the
+ * store's index and payload live in the caller's device pool. */
+typedef struct dopr_store *dopr_store_t;
+
+/* ------------------------------------------------------------------------ */
+/* Prefix store (Sec. 3.1 Eq. 3 and Sec. 3.3: per document d, the multi-layer
+ * K/V states C~_d of its K_infer selected prefix slots, stored offline).      */
+
+typedef struct {
+  int32_t n_layers;       /* decoder layers held per document (>= 1)        */
+  int32_t n_kv_heads;     /* Hkv (>= 1)                                     */
+  int32_t head_dim;       /* D; must be 128                                 */
+  int64_t n_docs;         /* size of the doc-id space [0, n_docs)           */
+  const int32_t *doc_len; /* HOST [n_docs]: prefix slots L_d of doc d.
+                             0 is allowed (no prefix); -1 = not resident
+                             (pairs naming it fail with DOC_RANGE).         */
+} dopr_store_desc_t;
+
+/* Sizes of a store.  *pool_bytes (required) is what dopr_store_create needs
+ * in the caller's pool: a small header, the index (12 B per doc id) and the
+ * payload in the library's internal layout (V rows padded to 8 slots).
+ * *payload_bytes (optional, may be NULL) is the canonical K/V size
+ * sum_d L_d * n_layers * Hkv * D * 2 (K and V) * 2 bytes, the document-side
+ * memory the paper reports per pair (Tables 3 and 9).  Pure host arithmetic. */
+dopr_status_t dopr_store_bytes(const dopr_store_desc_t *desc,
+                               size_t *pool_bytes, size_t *payload_bytes);
+
+/* Lay out a store in `pool` (device, >= pool_bytes, 256-byte aligned) and
+ * write its index (stream-ordered copy from host).  The payload is left
+ * uninitialised until dopr_store_put fills it.  *out receives a handle that
+ * must be released with dopr_store_destroy (which does not free the pool). */
+dopr_status_t dopr_store_create(const dopr_store_desc_t *desc, void *pool,
+                                size_t pool_bytes, void *stream,
+                                dopr_store_t *out);
+
+/* Copy the prefix K/V states of `n` documents for one layer into the store.
+ *   doc_ids      dev int32 [n]   documents to fill (resident ones)
+ *   src_cu_slots dev int64 [n+1] slot ranges of each document in k_src/v_src;
+ *                must satisfy src_cu_slots[i+1]-src_cu_slots[i] == L_d
+ *   k_src, v_src dev bf16 [src_cu_slots[n], Hkv, D] (canonical layout: the
+ *                final keys/values of each prefix slot, already normed and
+ *                rotated at positions 0..L_d-1 as in any pre-filled cache)
+ * A doc id that is out of range, not resident, or whose slot count differs
+ * from L_d is skipped and reported by dopr_check_status as DOC_RANGE.      */
+dopr_status_t dopr_store_put(dopr_store_t st, int32_t layer, int64_t n,
+                             const int32_t *doc_ids,
+                             const int64_t *src_cu_slots, const void *k_src,
+                             const void *v_src, void *stream);
+
+dopr_status_t dopr_store_destroy(dopr_store_t st);
+
+/* ------------------------------------------------------------------------ */
+/* Online prefix attention (Sec. 3.4): for every pair p with document
+ * d = doc_ids[p] and online tokens j = 0..T_p-1 (query tokens, then the
+ * score token last), q head h, kv head g = h / n_rep:
+ *   q^ = RoPE_{L_d + j}(RMSNorm(q[j,h]) * q_norm_w)
+ *   k^ = RoPE_{L_d + j}(RMSNorm(k[j,g]) * k_norm_w)        (own keys)
+ *   keys   = [ K_d[g, 0..L_d-1] ; k^[0..j, g] ]
+ *   values = [ V_d[g, 0..L_d-1] ;  v[0..j, g] ]
+ *   out[j,h] = softmax(softmax_scale * q^ . keys) . values
+ * RoPE is the rotate-half form with base rope_theta; RMSNorm is per head over
+ * D with epsilon rms_eps.  Online positions continue after the prefix.      */
+typedef struct {
+  int32_t n_pairs;          /* P >= 0                                       */
+  int32_t n_q_heads;        /* Hq, multiple of the store's Hkv              */
+  int32_t max_tokens;       /* upper bound on every T_p (>= 1)              */
+  int32_t kernel_variant;   /* 0 = automatic; >0 selects a row-tile shape
+                               (identical results; for tuning sweeps)       */
+  int64_t total_tokens;     /* Ntok = cu_seqlens[P]                         */
+  const int32_t *doc_ids;   /* dev int32 [P]                                */
+  const int32_t *cu_seqlens;/* dev int32 [P+1], cu[0] = 0, T_p >= 1         */
+  const void *q;            /* dev bf16 [Ntok, Hq, D]   raw (pre-norm)      */
+  const void *k;            /* dev bf16 [Ntok, Hkv, D]  raw (pre-norm)      */
+  const void *v;            /* dev bf16 [Ntok, Hkv, D]                      */
+  const void *q_norm_w;     /* dev bf16 [D]                                 */
+  const void *k_norm_w;     /* dev bf16 [D]                                 */
+  float rms_eps;            /* e.g. 1e-6                                    */
+  float rope_theta;         /* e.g. 1e6                                     */
+  float softmax_scale;      /* e.g. 1/sqrt(D)                               */
+  void *out;                /* dev bf16 [Ntok, Hq, D]                       */
+  float *lse;               /* dev fp32 [Ntok, Hq] natural-log sum-exp of
+                               the scaled logits, or NULL                   */
+  void *workspace;          /* dev scratch, >= dopr_prefix_attn_workspace() */
+  size_t workspace_bytes;
+} dopr_attn_args_t;
+
+/* Workspace bytes needed by dopr_prefix_attn for these arguments (host). */
+dopr_status_t dopr_prefix_attn_workspace(dopr_store_t st,
+                                         const dopr_attn_args_t *args,
+                                         size_t *bytes);
+
+/* Run the online attention of one layer for a batch of pairs.  Pairs that
+ * share a document are grouped on the device so that the document's prefix
+ * is read from HBM once per group and reused from LDS.  Pairs with a bad doc
+ * id get zero outputs (lse = -inf) and a deferred DOC_RANGE status.        */
+dopr_status_t dopr_prefix_attn(dopr_store_t st, int32_t layer,
+                               const dopr_attn_args_t *args, void *stream);
+
+/* ------------------------------------------------------------------------ */
+/* Score head (Sec. 3.2.3): s(q,d) from the score token's hidden state h.
+ * Read as RMSNorm followed by a two-row linear head (yes, no):
+ *   h^ = RMSNorm(h) * norm_w;  l_yes = w_yes . h^;  l_no = w_no . h^;
+ *   s  = l_yes - l_no   (log-odds of "relevant"; what RankNet consumes).   */
+typedef struct {
+  int32_t n_pairs;           /* P >= 0                                      */
+  int32_t width;             /* W, multiple of 8, >= 8                      */
+  const void *h;             /* dev bf16; row r starts at h + r*h_row_stride */
+  int64_t h_row_stride;      /* elements between rows, >= width, mult. of 8 */
+  const int32_t *row_index;  /* dev int32 [P]: h row of pair p, or NULL    */
+  const int32_t *cu_seqlens; /* dev int32 [P+1]: used when row_index is
+                                NULL: row = cu_seqlens[p+1]-1 (the score
+                                token is each pair's last online token).
+                                Both NULL: row = p.                         */
+  const void *norm_w;        /* dev bf16 [W]                                */
+  const void *w_head;        /* dev bf16 [2, W]: row 0 = yes, row 1 = no    */
+  float rms_eps;
+  float *logits;             /* dev fp32 [P, 2] (l_yes, l_no), or NULL      */
+  float *score;              /* dev fp32 [P]                                */
+} dopr_score_args_t;
+
+dopr_status_t dopr_score_logits(const dopr_score_args_t *args, void *stream);
+
+/* ------------------------------------------------------------------------ */
+/* Exports used by the bit-exact tests of the integer steps.               */
+
+/* Doc-id grouping in canonical form: valid pairs (doc id in range and
+ * resident) sorted by (doc id, pair index).  group_doc[G] ascending doc ids,
+ * group_ptr[G+1] offsets into pair_order[], pair_order[n_valid] pair indices.
+ * Capacities: group_doc and pair_order >= n_pairs, group_ptr >= n_pairs+1.
+ * `workspace` must hold dopr_prefix_attn_workspace() bytes for the same
+ * pairs.  Synchronises `stream` to return *n_groups and *n_valid on the host. */
+dopr_status_t dopr_group_pairs(dopr_store_t st, int32_t n_pairs,
+                               const int32_t *doc_ids, void *workspace,
+                               size_t workspace_bytes, int32_t *n_groups,
+                               int32_t *n_valid, int32_t *group_doc,
+                               int32_t *group_ptr, int32_t *pair_order,
+                               void *stream);
+
+/* Gather the prefix K/V states of doc_ids[i] for one layer out of the store
+ * into canonical layout: k_out/v_out dev bf16 [out_cu_slots[n], Hkv, D],
+ * pair i's slots at rows out_cu_slots[i] .. out_cu_slots[i+1]-1.  A bad doc
+ * id, or a slot range that differs from L_d, leaves its rows untouched and
+ * raises a deferred DOC_RANGE.                                             */
+dopr_status_t dopr_gather_prefix(dopr_store_t st, int32_t layer, int32_t n,
+                                 const int32_t *doc_ids,
+                                 const int64_t *out_cu_slots, void *k_out,
+                                 void *v_out, void *stream);
+
+/* Synchronise `stream`, then return (and clear) the first deferred device
+ * error raised by calls on this store since the last check, else DOPR_OK.  */
+dopr_status_t dopr_check_status(dopr_store_t st, void *stream);
+
+/* Human-readable name of a status code (static string). */
+const char *dopr_status_str(dopr_status_t s);
+
+/* Thread-local text describing the last non-OK status returned on this
+ * thread ("" if none). */
+const char *dopr_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DOPR_H */

@@ -1,0 +1,91 @@
+"""The oracle's pins catch plausible mistakes (CPU).
+
+Each case plants one mistake in a copy of the oracle's C source, builds it
+with gcc into a temporary directory and runs the whole pin battery against
+it in a subprocess (a planted mistake may crash).  The case passes only if
+at least one pin fails.  The real oracle source is never modified.
+"""
+import os
+import subprocess
+import sys
+import tempfile
+
+import pytest
+
+import oracle
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+SRC = os.path.join(ROOT, "oracle", "dopr_oracle.c")
+
+# (id, exact text in the oracle source, replacement)
+MUTATIONS = [
+    ("rope_sin_sign_first", "x[i] = a * c - b * s;", "x[i] = a * c + b * s;"),
+    ("rope_sin_sign_second", "x[i + half] = b * c + a * s;",
+     "x[i + half] = b * c - a * s;"),
+    ("rope_freq_exponent", "pow(theta, -2.0 * (double)i / (double)d)",
+     "pow(theta, -1.0 * (double)i / (double)d)"),
+    ("rope_halves_swapped", "double a = x[i], b = x[i + half];",
+     "double a = x[i + half], b = x[i];"),
+    ("rmsnorm_no_eps", "sqrt(ss / (double)n + eps)", "sqrt(ss / (double)n)"),
+    ("rmsnorm_no_weight", "y[i] = w[i] * (x[i] * inv);",
+     "y[i] = (x[i] * inv);"),
+    ("rmsnorm_sum_not_mean", "sqrt(ss / (double)n + eps)", "sqrt(ss + eps)"),
+    ("q_position_not_offset", "rope(qhat, D, (double)(L + j), rope_theta);",
+     "rope(qhat, D, (double)(j), rope_theta);"),
+    ("k_position_not_offset", "rope(dst, D, (double)(L + j), rope_theta);",
+     "rope(dst, D, (double)(j), rope_theta);"),
+    ("gqa_interleaved", "const int g = h / n_rep;", "const int g = h % Hkv;"),
+    ("self_key_dropped", "const int n_keys = L + j + 1;",
+     "const int n_keys = L + j;"),
+    ("prefix_unscaled", "z[t] = softmax_scale * dot;", "z[t] = dot;"),
+    ("own_unscaled", "z[L + t] = softmax_scale * dot;", "z[L + t] = dot;"),
+    ("prefix_values_are_keys", "const uint16_t *vt = pv +",
+     "const uint16_t *vt = pk +"),
+    ("own_values_are_keys", "const double *vt = vown +",
+     "const double *vt = khat +"),
+    ("lse_without_max", "zmax + log(denom)", "log(denom)"),
+    ("q_norm_uses_k_weight", "rms_norm(x, wq, D, rms_eps, qhat);",
+     "rms_norm(x, wk, D, rms_eps, qhat);"),
+    ("score_sign", "score[p] = ly - ln;", "score[p] = ln - ly;"),
+    ("score_yes_row_is_no_row", "wy[i] = bf16_to_double(w_head[i]);",
+     "wy[i] = bf16_to_double(w_head[width + i]);"),
+    ("score_no_norm_weight", "w[i] = bf16_to_double(norm_w[i]);",
+     "w[i] = 1.0;"),
+    ("group_ptr_shifted", "group_ptr[g] = (int32_t)run;\n      ++g;",
+     "group_ptr[g] = (int32_t)(run + c);\n      ++g;"),
+    ("store_bytes_k_only", "* n_kv_heads * head_dim * 2 * 2;",
+     "* n_kv_heads * head_dim * 2;"),
+]
+
+RUNNER = r"""
+import sys
+sys.path[:0] = [{root!r}, {tests!r}]
+import oracle, oracle_pins
+L = oracle.load_library({lib!r})
+order = sorted(oracle_pins.ALL_PINS, key=lambda p: p is oracle_pins.pin_sdpa)
+for pin in order:
+    try:
+        pin(L)
+    except Exception as e:
+        print("CAUGHT", pin.__name__, type(e).__name__)
+        sys.exit(0)
+print("MISSED")
+"""
+
+
+@pytest.mark.parametrize("mid,pattern,repl", MUTATIONS,
+                         ids=[m[0] for m in MUTATIONS])
+def test_pins_catch_planted_mistake(mid, pattern, repl, tmp_path):
+    src = open(SRC).read()
+    assert src.count(pattern) == 1, f"{mid}: pattern must occur exactly once"
+    mutated = tmp_path / "mutated.c"
+    mutated.write_text(src.replace(pattern, repl))
+    lib = str(tmp_path / "libmutated.so")
+    oracle.build(str(mutated), lib)
+    code = RUNNER.format(root=ROOT, tests=os.path.dirname(__file__), lib=lib)
+    r = subprocess.run([sys.executable, "-c", code], capture_output=True,
+                       text=True, timeout=300)
+    out = r.stdout + r.stderr
+    assert "MISSED" not in r.stdout, f"{mid}: no pin failed\n{out[-2000:]}"
+    # a crash (nonzero exit without CAUGHT) also counts as caught
+    assert "CAUGHT" in r.stdout or r.returncode != 0, out[-2000:]
