@@ -1,0 +1,299 @@
+#!/usr/bin/env python3
+"""Throughput of the DoPR online scoring step on one MI355X.
+
+One step = one batch of (query, document) pairs through one decoder layer's
+online path: device-side grouping by document, prefix attention over the HBM
+prefix store plus causal own keys (QK-RMSNorm + RoPE, GQA, online softmax),
+and the yes/no score head on each pair's score token.  Inputs are seeded
+synthetic tensors already resident in HBM when timing starts.
+
+Prints one JSON line: pairs/s per decoder layer (whole job), the attention
+kernel's achieved algorithmic HBM GB/s against the 8 TB/s peak, and the
+float64 CPU oracle timed on a bounded sample of the same workload.
+"""
+import argparse
+import ctypes
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = ("query-doc pairs/sec per decoder layer; achieved HBM GB/s vs "
+          "MI355X peak")
+PEAK_HBM_GBS = 8000.0
+PEAK_BF16_TFLOPS = 2500.0
+
+DESCRIPTIONS = {
+    "tiny": "tiny: 1 layer, 16q/8kv heads, D=128, 8 docs x 16 slots, "
+            "4 queries x (15+1) tokens x 8 docs = 32 pairs",
+    "qwen3_0p6b": "Qwen3-0.6B-shaped layer: 16q/8kv heads, D=128, 10k docs x "
+                  "32 slots, 64 queries x 100 docs, T=31+1",
+    "qwen3_4b": "Qwen3-4B-shaped layer: 32q/8kv heads, D=128, 100k docs x 64 "
+                "slots, 4096 pairs Zipf(1.1) reuse, T=8..64+1",
+    "qwen3_8b": "Qwen3-8B-shaped layer: 32q/8kv heads, D=128, 20k docs x 256 "
+                "slots (2048-token docs at 8x), 256 queries x 100 docs, "
+                "T=128+1",
+    "qwen3_8b_ragged": "Qwen3-8B-shaped layer, ragged: 32q/8kv heads, "
+                       "prefixes 8..256 slots over 1M doc ids, 16384 pairs "
+                       "(50% Zipf reuse), T=16..128+1",
+    "qwen3_8b_ragged_x8": "as qwen3_8b_ragged with 8x longer (uncompressed) "
+                          "prefixes, 64..2048 slots",
+}
+
+
+def log(msg):
+    print(f"[bench {time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr,
+          flush=True)
+
+
+class HipEvents:
+    """Raw hipEvent_t handles (the library records them on its stream)."""
+
+    def __init__(self, n):
+        self.hip = ctypes.CDLL("libamdhip64.so")
+        self.hip.hipEventCreate.argtypes = [ctypes.c_void_p]
+        self.hip.hipEventElapsedTime.argtypes = [
+            ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+        self.hip.hipEventSynchronize.argtypes = [ctypes.c_void_p]
+        self.hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+        self.ev = []
+        for _ in range(n):
+            e = ctypes.c_void_p(0)
+            rc = self.hip.hipEventCreate(ctypes.byref(e))
+            if rc != 0:
+                raise RuntimeError(f"hipEventCreate failed: {rc}")
+            self.ev.append(e.value)
+
+    def elapsed_ms(self, a, b):
+        self.hip.hipEventSynchronize(ctypes.c_void_p(self.ev[b]))
+        ms = ctypes.c_float(0)
+        rc = self.hip.hipEventElapsedTime(ctypes.byref(ms),
+                                          ctypes.c_void_p(self.ev[a]),
+                                          ctypes.c_void_p(self.ev[b]))
+        if rc != 0:
+            raise RuntimeError(f"hipEventElapsedTime failed: {rc}")
+        return ms.value
+
+    def close(self):
+        for e in self.ev:
+            self.hip.hipEventDestroy(ctypes.c_void_p(e))
+
+
+def algorithmic_work(st):
+    """Bytes the step must move (each unique prefix once, each online row
+    once) and the attention flops."""
+    uniq = np.unique(st.doc_ids)
+    L = st.doc_len[uniq].astype(np.int64)
+    hkv, hq, D = st.n_kv_heads, st.n_q_heads, st.head_dim
+    prefix = int(L.sum()) * hkv * D * 2 * 2
+    ntok = st.n_tokens
+    qkv = ntok * (hq + 2 * hkv) * D * 2
+    out = ntok * hq * D * 2
+    meta = st.n_pairs * 8 + len(uniq) * 12
+    T = st.seqlens.astype(np.int64)
+    Lp = st.doc_len[st.doc_ids].astype(np.int64)
+    keys = (T * Lp + T * (T + 1) // 2).sum()      # sum_p sum_j (L + j + 1)
+    flops = int(4 * hq * D * keys)
+    score_bytes = st.n_pairs * hq * D * 2
+    return dict(prefix=prefix, qkv=qkv, out=out, meta=meta,
+                total=prefix + qkv + out + meta, flops=flops,
+                exps=int(hq * keys), unique_docs=int(len(uniq)),
+                score_bytes=score_bytes)
+
+
+def bits(t):
+    import torch
+    return t.detach().cpu().contiguous().view(torch.int16).numpy().view(
+        np.uint16)
+
+
+def cpu_baseline(st, k_src, v_src, doc_off, online, prm, seconds):
+    """The float64 oracle on a bounded sample of the same workload's pairs
+    (deterministic order), on this host's cores."""
+    import torch
+
+    import oracle
+    L = oracle.lib()
+    threads = oracle.max_threads(L)
+    rng = np.random.default_rng(99)
+    order = rng.permutation(st.n_pairs)
+    cu = st.cu_seqlens.astype(np.int64)
+    dev = k_src.device
+
+    def run(pairs):
+        docs = np.unique(st.doc_ids[pairs])
+        sub_off = np.full(st.n_docs, -1, np.int64)
+        idx, pos = [], 0
+        for d in docs:
+            n = int(st.doc_len[d])
+            sub_off[d] = pos
+            idx.append(np.arange(doc_off[d], doc_off[d] + n))
+            pos += n
+        it = torch.from_numpy(np.concatenate(idx)).to(dev)
+        tok = np.concatenate([np.arange(cu[p], cu[p + 1]) for p in pairs])
+        tt = torch.from_numpy(tok).to(dev)
+        lens = cu[pairs + 1] - cu[pairs]
+        scu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+        args = (st.doc_ids[pairs], scu, st.doc_len, sub_off,
+                bits(k_src.index_select(0, it)),
+                bits(v_src.index_select(0, it)),
+                bits(online["q"].index_select(0, tt)),
+                bits(online["k"].index_select(0, tt)),
+                bits(online["v"].index_select(0, tt)),
+                bits(prm["q_norm_w"]), bits(prm["k_norm_w"]))
+        nw, wh = bits(prm["norm_w"]), bits(prm["w_head"])
+        t0 = time.perf_counter()
+        out, _, _ = oracle.prefix_attn(*args, n_q_heads=st.n_q_heads,
+                                       n_kv_heads=st.n_kv_heads, L=L)
+        h = out[scu[1:] - 1].reshape(len(pairs), -1)
+        oracle.score(h, nw, wh, L=L)
+        return time.perf_counter() - t0
+
+    # calibrate on one pair per thread, then size the sample to the budget
+    first = order[:min(threads, st.n_pairs)]
+    t_first = run(first)
+    per_pair = t_first / len(first) * min(threads, len(first)) / threads
+    n_more = int(max(0.0, seconds - t_first) / max(per_pair, 1e-9))
+    n_more = min(n_more, st.n_pairs - len(first))
+    n_more = n_more // threads * threads
+    total_t, total_n = t_first, len(first)
+    if n_more > 0:
+        more = order[len(first):len(first) + n_more]
+        total_t += run(more)
+        total_n += len(more)
+    return {"value": round(total_n / total_t, 3), "unit": "pairs/s",
+            "cores": int(threads), "kind": "oracle",
+            "sample": f"{total_n} of {st.n_pairs} pairs (seeded random "
+                      f"order), float64 C oracle incl. score head, "
+                      f"{total_t:.1f}s"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", default="qwen3_8b",
+                    choices=sorted(DESCRIPTIONS))
+    ap.add_argument("--variant", type=int, default=0)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py: this build runs on one GPU only; the online path "
+              "has no inter-GPU step (see DESIGN.md for how it would "
+              "shard). Run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import workloads
+    from paper_2609_03311_amd import dopr_check_status, pipeline
+
+    st = workloads.make(args.config)
+    dev = "cuda"
+    log(f"{args.config}: P={st.n_pairs} Ntok={st.n_tokens} "
+        f"unique docs={len(np.unique(st.doc_ids))}")
+    k_src, v_src, doc_off, _ = workloads.prefix_source(st, dev, 1)
+    online = workloads.online_inputs(st, dev, 3)
+    prm = workloads.params(st, dev, 6)
+    store = pipeline.make_store(st.doc_len, st.n_kv_heads, k_src, v_src,
+                                device=dev)
+    step = pipeline.OnlineStep(store, n_pairs=st.n_pairs,
+                               n_q_heads=st.n_q_heads,
+                               total_tokens=st.n_tokens,
+                               max_tokens=int(st.seqlens.max()),
+                               kernel_variant=args.variant, device=dev)
+    doc_ids = torch.from_numpy(st.doc_ids).to(dev)
+    cu = torch.from_numpy(st.cu_seqlens).to(dev)
+    torch.cuda.synchronize()
+    log("inputs resident; warming up")
+
+    ev = HipEvents(2 * args.steps)
+
+    def one_step(i=None):
+        timing = None if i is None else (ev.ev[2 * i], ev.ev[2 * i + 1])
+        step.attention(0, doc_ids, cu, online["q"], online["k"],
+                       online["v"], prm["q_norm_w"], prm["k_norm_w"],
+                       timing=timing)
+        step.score_head(cu, prm["norm_w"], prm["w_head"])
+
+    for _ in range(args.warmup):
+        one_step()
+    torch.cuda.synchronize()
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    t0.record()
+    for i in range(args.steps):
+        one_step(i)
+    t1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    ms_step = t0.elapsed_time(t1) / args.steps
+    attn_ms = [ev.elapsed_ms(2 * i, 2 * i + 1) for i in range(args.steps)]
+    ev.close()
+    status = dopr_check_status(store)
+    if status != 0:
+        raise SystemExit(f"device status {status} after the timed steps")
+    attn_avg = float(np.mean(attn_ms))
+    log(f"step {ms_step:.3f} ms (wall {wall / args.steps * 1e3:.3f} ms), "
+        f"attention kernel avg {attn_avg:.3f} ms "
+        f"(min {min(attn_ms):.3f}, max {max(attn_ms):.3f})")
+
+    w = algorithmic_work(st)
+    achieved = w["total"] / (attn_avg * 1e-3) / 1e9
+    result = {
+        "metric": METRIC,
+        "value": round(st.n_pairs / (ms_step * 1e-3), 1),
+        "unit": "pairs/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1) bf16 prefix states and online "
+                "q/k/v; no datasets or weights)",
+        "config": {
+            "workload": DESCRIPTIONS[args.config],
+            "name": args.config,
+            "pairs": st.n_pairs,
+            "online_tokens": st.n_tokens,
+            "unique_docs": w["unique_docs"],
+            "kernel_variant": args.variant,
+            "parallelism": "single GPU",
+        },
+        "attention_ms": round(attn_avg, 4),
+        "algorithmic_gb": round(w["total"] / 1e9, 4),
+        "prefix_gb": round(w["prefix"] / 1e9, 4),
+        "prefix_gbps": round(w["prefix"] / (attn_avg * 1e-3) / 1e9, 1),
+        "attention_tflops": round(w["flops"] / (attn_avg * 1e-3) / 1e12, 1),
+        "roofline": {
+            "bound": "hbm",
+            "achieved": round(achieved, 1),
+            "peak": PEAK_HBM_GBS,
+            "unit": "GB/s",
+            "frac": round(achieved / PEAK_HBM_GBS, 4),
+            "traffic": None,
+        },
+    }
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle on a bounded sample")
+        result["cpu_baseline"] = cpu_baseline(st, k_src, v_src, doc_off,
+                                              online, prm, args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -141,6 +141,10 @@ typedef struct {
                                the scaled logits, or NULL                   */
   void *workspace;          /* dev scratch, >= dopr_prefix_attn_workspace() */
   size_t workspace_bytes;
+  void *timing_begin;       /* optional hipEvent_t recorded on the stream
+                               right before the attention kernel, or NULL  */
+  void *timing_end;         /* optional hipEvent_t recorded right after it,
+                               or NULL (profiling of the dominant kernel)   */
 } dopr_attn_args_t;
 
 /* Workspace bytes needed by dopr_prefix_attn for these arguments (host). */

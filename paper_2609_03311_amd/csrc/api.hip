@@ -1,0 +1,412 @@
+// api.hip -- host side of the C ABI declared in include/dopr.h: argument
+// validation, store layout, workspace sizing and kernel launches.  Nothing
+// here allocates device memory; every device buffer comes from the caller.
+#include <cmath>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "internal.hpp"
+
+using namespace dopr;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+dopr_status_t fail(dopr_status_t s, const std::string &msg) {
+  g_last_error = std::string(dopr_status_str(s)) + ": " + msg;
+  return s;
+}
+
+dopr_status_t hip_fail(hipError_t e, const char *what) {
+  return fail(DOPR_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+dopr_status_t ok() {
+  g_last_error.clear();
+  return DOPR_OK;
+}
+
+bool aligned16(const void *p) {
+  return (reinterpret_cast<uintptr_t>(p) & 15) == 0;
+}
+
+hipStream_t as_stream(void *s) { return static_cast<hipStream_t>(s); }
+
+struct StoreLayout {
+  size_t len_off = 0, off_off = 0, payload_off = 0, total = 0;
+  size_t payload_canonical = 0;
+  int32_t max_len = 0;
+};
+
+// Offsets of the pool sections; optionally the per-document block offsets.
+dopr_status_t layout_store(const dopr_store_desc_t *d, StoreLayout *lay,
+                           std::vector<int64_t> *doc_off) {
+  if (!d) return fail(DOPR_ERR_INVALID_ARG, "desc is NULL");
+  if (d->n_docs < 0 || d->n_docs > INT32_MAX)
+    return fail(DOPR_ERR_INVALID_ARG, "n_docs must be in [0, 2^31)");
+  if (d->n_docs > 0 && !d->doc_len)
+    return fail(DOPR_ERR_INVALID_ARG, "doc_len is NULL");
+  if (d->n_layers < 1 || d->n_kv_heads < 1)
+    return fail(DOPR_ERR_INVALID_ARG, "n_layers and n_kv_heads must be >= 1");
+  if (d->head_dim != kHeadDim)
+    return fail(DOPR_ERR_UNSUPPORTED, "head_dim must be 128");
+  size_t off = align_up(sizeof(int32_t) * kStatusWords, kAlign);
+  lay->len_off = off;
+  off = align_up(off + sizeof(int32_t) * (size_t)d->n_docs, kAlign);
+  lay->off_off = off;
+  off = align_up(off + sizeof(int64_t) * (size_t)d->n_docs, kAlign);
+  lay->payload_off = off;
+  int64_t elems = 0;
+  size_t canon = 0;
+  int32_t max_len = 0;
+  if (doc_off) doc_off->assign((size_t)d->n_docs, -1);
+  for (int64_t i = 0; i < d->n_docs; ++i) {
+    const int32_t L = d->doc_len[i];
+    if (L < -1)
+      return fail(DOPR_ERR_INVALID_ARG,
+                  "doc_len entries must be >= 0, or -1 (not resident)");
+    if (L < 0) continue;
+    if (doc_off) (*doc_off)[i] = elems;
+    elems += (int64_t)d->n_layers * layer_block_elems(L, d->n_kv_heads);
+    canon += (size_t)L * d->n_layers * d->n_kv_heads * kHeadDim * 2 * 2;
+    if (L > max_len) max_len = L;
+  }
+  lay->total = off + sizeof(uint16_t) * (size_t)elems;
+  lay->payload_canonical = canon;
+  lay->max_len = max_len;
+  return DOPR_OK;
+}
+
+int32_t default_rows_per_item(int32_t variant) {
+  (void)variant;
+  return 1024;
+}
+
+// Validation shared by the workspace query and the attention call.
+dopr_status_t check_attn(const dopr_store *st, const dopr_attn_args_t *a,
+                         PlanShape *shape, int32_t *n_rep) {
+  if (!st) return fail(DOPR_ERR_INVALID_ARG, "store is NULL");
+  if (!a) return fail(DOPR_ERR_INVALID_ARG, "args is NULL");
+  if (a->n_pairs < 0) return fail(DOPR_ERR_INVALID_ARG, "n_pairs < 0");
+  if (a->n_q_heads < 1 || a->n_q_heads % st->n_kv_heads)
+    return fail(DOPR_ERR_INVALID_ARG,
+                "n_q_heads must be a positive multiple of n_kv_heads");
+  if (a->max_tokens < 1 || a->max_tokens > (1 << 20))
+    return fail(DOPR_ERR_INVALID_ARG, "max_tokens must be in [1, 2^20]");
+  if (a->total_tokens < a->n_pairs)
+    return fail(DOPR_ERR_INVALID_ARG,
+                "total_tokens must be >= n_pairs (every T_p >= 1)");
+  *n_rep = a->n_q_heads / st->n_kv_heads;
+  if (a->total_tokens * (int64_t)(*n_rep) > INT32_MAX)
+    return fail(DOPR_ERR_UNSUPPORTED, "total_tokens * n_rep must be < 2^31");
+  if (a->kernel_variant < 0 || a->kernel_variant > 2)
+    return fail(DOPR_ERR_INVALID_ARG, "kernel_variant must be 0, 1 or 2");
+  if (!(a->softmax_scale > 0.f) || !std::isfinite(a->softmax_scale))
+    return fail(DOPR_ERR_INVALID_ARG, "softmax_scale must be finite and > 0");
+  if (!(a->rope_theta > 1.f) || !std::isfinite(a->rope_theta))
+    return fail(DOPR_ERR_INVALID_ARG, "rope_theta must be finite and > 1");
+  if (!(a->rms_eps >= 0.f) || !std::isfinite(a->rms_eps))
+    return fail(DOPR_ERR_INVALID_ARG, "rms_eps must be finite and >= 0");
+  shape->n_pairs = a->n_pairs;
+  shape->n_rep = *n_rep;
+  shape->max_tokens = a->max_tokens;
+  shape->rows_per_item = default_rows_per_item(a->kernel_variant);
+  shape->n_docs = st->n_docs;
+  shape->total_tokens = a->total_tokens;
+  shape->max_len = st->max_len;
+  return DOPR_OK;
+}
+
+dopr_status_t check_device(const dopr_store *st) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev != st->device)
+    return fail(DOPR_ERR_INVALID_ARG,
+                "current device differs from the store's device");
+  return DOPR_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *dopr_status_str(dopr_status_t s) {
+  switch (s) {
+    case DOPR_OK: return "DOPR_OK";
+    case DOPR_ERR_INVALID_ARG: return "DOPR_ERR_INVALID_ARG";
+    case DOPR_ERR_UNSUPPORTED: return "DOPR_ERR_UNSUPPORTED";
+    case DOPR_ERR_DOC_RANGE: return "DOPR_ERR_DOC_RANGE";
+    case DOPR_ERR_WORKSPACE: return "DOPR_ERR_WORKSPACE";
+    case DOPR_ERR_HIP: return "DOPR_ERR_HIP";
+    case DOPR_ERR_SEQLEN: return "DOPR_ERR_SEQLEN";
+  }
+  return "DOPR_ERR_UNKNOWN";
+}
+
+const char *dopr_last_error(void) { return g_last_error.c_str(); }
+
+dopr_status_t dopr_store_bytes(const dopr_store_desc_t *desc,
+                               size_t *pool_bytes, size_t *payload_bytes) {
+  if (!pool_bytes) return fail(DOPR_ERR_INVALID_ARG, "pool_bytes is NULL");
+  StoreLayout lay;
+  dopr_status_t s = layout_store(desc, &lay, nullptr);
+  if (s != DOPR_OK) return s;
+  *pool_bytes = lay.total;
+  if (payload_bytes) *payload_bytes = lay.payload_canonical;
+  return ok();
+}
+
+dopr_status_t dopr_store_create(const dopr_store_desc_t *desc, void *pool,
+                                size_t pool_bytes, void *stream,
+                                dopr_store_t *out) {
+  if (!out) return fail(DOPR_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  StoreLayout lay;
+  std::vector<int64_t> doc_off;
+  dopr_status_t s = layout_store(desc, &lay, &doc_off);
+  if (s != DOPR_OK) return s;
+  if (!pool) return fail(DOPR_ERR_INVALID_ARG, "pool is NULL");
+  if (reinterpret_cast<uintptr_t>(pool) % kAlign)
+    return fail(DOPR_ERR_INVALID_ARG, "pool must be 256-byte aligned");
+  if (pool_bytes < lay.total)
+    return fail(DOPR_ERR_WORKSPACE,
+                "pool holds " + std::to_string(pool_bytes) + " bytes, store needs " +
+                    std::to_string(lay.total));
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  dopr_store *st = new (std::nothrow) dopr_store{};
+  if (!st) return fail(DOPR_ERR_INVALID_ARG, "host allocation failed");
+  char *base = static_cast<char *>(pool);
+  st->n_layers = desc->n_layers;
+  st->n_kv_heads = desc->n_kv_heads;
+  st->head_dim = desc->head_dim;
+  st->n_docs = desc->n_docs;
+  st->pool = base;
+  st->pool_bytes = pool_bytes;
+  st->d_status = reinterpret_cast<int32_t *>(base);
+  st->d_len = reinterpret_cast<int32_t *>(base + lay.len_off);
+  st->d_off = reinterpret_cast<int64_t *>(base + lay.off_off);
+  st->d_payload = reinterpret_cast<uint16_t *>(base + lay.payload_off);
+  st->max_len = lay.max_len;
+  st->device = dev;
+  hipStream_t hs = as_stream(stream);
+  e = hipMemsetAsync(st->d_status, 0, sizeof(int32_t) * kStatusWords, hs);
+  if (e == hipSuccess && desc->n_docs > 0)
+    e = hipMemcpyAsync(st->d_len, desc->doc_len,
+                       sizeof(int32_t) * (size_t)desc->n_docs,
+                       hipMemcpyHostToDevice, hs);
+  if (e == hipSuccess && desc->n_docs > 0)
+    e = hipMemcpyAsync(st->d_off, doc_off.data(),
+                       sizeof(int64_t) * (size_t)desc->n_docs,
+                       hipMemcpyHostToDevice, hs);
+  if (e == hipSuccess) e = hipStreamSynchronize(hs);
+  if (e != hipSuccess) {
+    delete st;
+    return hip_fail(e, "store index upload");
+  }
+  *out = st;
+  return ok();
+}
+
+dopr_status_t dopr_store_put(dopr_store_t st, int32_t layer, int64_t n,
+                             const int32_t *doc_ids,
+                             const int64_t *src_cu_slots, const void *k_src,
+                             const void *v_src, void *stream) {
+  if (!st) return fail(DOPR_ERR_INVALID_ARG, "store is NULL");
+  if (layer < 0 || layer >= st->n_layers)
+    return fail(DOPR_ERR_INVALID_ARG, "layer out of range");
+  if (n < 0 || n > INT32_MAX) return fail(DOPR_ERR_INVALID_ARG, "bad n");
+  if (n == 0) return ok();
+  if (!doc_ids || !src_cu_slots || !k_src || !v_src)
+    return fail(DOPR_ERR_INVALID_ARG, "NULL buffer");
+  if (!aligned16(k_src) || !aligned16(v_src))
+    return fail(DOPR_ERR_INVALID_ARG, "k_src/v_src must be 16-byte aligned");
+  dopr_status_t s = check_device(st);
+  if (s != DOPR_OK) return s;
+  hipError_t e = launch_store_put(*st, layer, n, doc_ids, src_cu_slots,
+                                  static_cast<const uint16_t *>(k_src),
+                                  static_cast<const uint16_t *>(v_src),
+                                  as_stream(stream));
+  if (e != hipSuccess) return hip_fail(e, "store_put launch");
+  return ok();
+}
+
+dopr_status_t dopr_store_destroy(dopr_store_t st) {
+  delete st;
+  return ok();
+}
+
+dopr_status_t dopr_prefix_attn_workspace(dopr_store_t st,
+                                         const dopr_attn_args_t *args,
+                                         size_t *bytes) {
+  if (!bytes) return fail(DOPR_ERR_INVALID_ARG, "bytes is NULL");
+  PlanShape shape;
+  int32_t n_rep = 0;
+  dopr_status_t s = check_attn(st, args, &shape, &n_rep);
+  if (s != DOPR_OK) return s;
+  *bytes = plan_bytes(shape);
+  return ok();
+}
+
+dopr_status_t dopr_prefix_attn(dopr_store_t st, int32_t layer,
+                               const dopr_attn_args_t *a, void *stream) {
+  PlanShape shape;
+  int32_t n_rep = 0;
+  dopr_status_t s = check_attn(st, a, &shape, &n_rep);
+  if (s != DOPR_OK) return s;
+  if (layer < 0 || layer >= st->n_layers)
+    return fail(DOPR_ERR_INVALID_ARG, "layer out of range");
+  if (a->n_pairs == 0) return ok();
+  if (!a->doc_ids || !a->cu_seqlens || !a->q || !a->k || !a->v ||
+      !a->q_norm_w || !a->k_norm_w || !a->out || !a->workspace)
+    return fail(DOPR_ERR_INVALID_ARG, "NULL buffer");
+  if (!aligned16(a->q) || !aligned16(a->k) || !aligned16(a->v) ||
+      !aligned16(a->out) || !aligned16(a->q_norm_w) || !aligned16(a->k_norm_w))
+    return fail(DOPR_ERR_INVALID_ARG,
+                "q, k, v, out and norm weights must be 16-byte aligned");
+  if (reinterpret_cast<uintptr_t>(a->workspace) % kAlign)
+    return fail(DOPR_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+  const size_t need = plan_bytes(shape);
+  if (a->workspace_bytes < need)
+    return fail(DOPR_ERR_WORKSPACE,
+                "workspace holds " + std::to_string(a->workspace_bytes) +
+                    " bytes, needs " + std::to_string(need));
+  s = check_device(st);
+  if (s != DOPR_OK) return s;
+  const Plan plan = plan_carve(a->workspace, shape);
+  AttnCall call{st, layer, a, n_rep};
+  hipStream_t hs = as_stream(stream);
+  hipError_t e = launch_plan(call, plan, shape, hs);
+  if (e != hipSuccess) return hip_fail(e, "scheduler launch");
+  e = launch_attention(call, plan, shape, hs);
+  if (e != hipSuccess) return hip_fail(e, "attention launch");
+  return ok();
+}
+
+dopr_status_t dopr_score_logits(const dopr_score_args_t *a, void *stream) {
+  if (!a) return fail(DOPR_ERR_INVALID_ARG, "args is NULL");
+  if (a->n_pairs < 0) return fail(DOPR_ERR_INVALID_ARG, "n_pairs < 0");
+  if (a->width < 8 || a->width % 8)
+    return fail(DOPR_ERR_INVALID_ARG, "width must be a multiple of 8, >= 8");
+  if (a->h_row_stride < a->width || a->h_row_stride % 8)
+    return fail(DOPR_ERR_INVALID_ARG,
+                "h_row_stride must be >= width and a multiple of 8");
+  if (!(a->rms_eps >= 0.f) || !std::isfinite(a->rms_eps))
+    return fail(DOPR_ERR_INVALID_ARG, "rms_eps must be finite and >= 0");
+  if (a->n_pairs == 0) return ok();
+  if (!a->h || !a->norm_w || !a->w_head || !a->score)
+    return fail(DOPR_ERR_INVALID_ARG, "NULL buffer");
+  if (!aligned16(a->h) || !aligned16(a->norm_w) || !aligned16(a->w_head))
+    return fail(DOPR_ERR_INVALID_ARG, "h, norm_w, w_head must be 16-byte aligned");
+  hipError_t e = launch_score(a, as_stream(stream));
+  if (e != hipSuccess) return hip_fail(e, "score launch");
+  return ok();
+}
+
+dopr_status_t dopr_group_pairs(dopr_store_t st, int32_t n_pairs,
+                               const int32_t *doc_ids, void *workspace,
+                               size_t workspace_bytes, int32_t *n_groups,
+                               int32_t *n_valid, int32_t *group_doc,
+                               int32_t *group_ptr, int32_t *pair_order,
+                               void *stream) {
+  if (!st) return fail(DOPR_ERR_INVALID_ARG, "store is NULL");
+  if (!n_groups || !n_valid)
+    return fail(DOPR_ERR_INVALID_ARG, "n_groups/n_valid is NULL");
+  if (n_pairs < 0) return fail(DOPR_ERR_INVALID_ARG, "n_pairs < 0");
+  *n_groups = 0;
+  *n_valid = 0;
+  if (n_pairs == 0) return ok();
+  if (!doc_ids || !workspace || !group_doc || !group_ptr || !pair_order)
+    return fail(DOPR_ERR_INVALID_ARG, "NULL buffer");
+  if (reinterpret_cast<uintptr_t>(workspace) % kAlign)
+    return fail(DOPR_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+  dopr_status_t s = check_device(st);
+  if (s != DOPR_OK) return s;
+  dopr_attn_args_t a{};
+  a.n_pairs = n_pairs;
+  a.n_q_heads = st->n_kv_heads;
+  a.max_tokens = 1;
+  a.total_tokens = n_pairs;
+  a.doc_ids = doc_ids;
+  a.cu_seqlens = nullptr;
+  a.rope_theta = 1e6f;
+  a.softmax_scale = 1.f;
+  PlanShape shape{n_pairs, 1, 1, default_rows_per_item(0), st->n_docs,
+                  (int64_t)n_pairs, st->max_len};
+  const size_t need = plan_bytes(shape);
+  if (workspace_bytes < need)
+    return fail(DOPR_ERR_WORKSPACE, "workspace too small for grouping");
+  const Plan plan = plan_carve(workspace, shape);
+  AttnCall call{st, 0, &a, 1};
+  hipStream_t hs = as_stream(stream);
+  hipError_t e = launch_plan(call, plan, shape, hs);
+  if (e != hipSuccess) return hip_fail(e, "scheduler launch");
+  int64_t totals[4] = {0, 0, 0, 0};
+  e = hipMemcpyAsync(totals, plan.counters + kCounters, sizeof(totals),
+                     hipMemcpyDeviceToHost, hs);
+  if (e == hipSuccess) e = hipStreamSynchronize(hs);
+  if (e != hipSuccess) return hip_fail(e, "grouping readback");
+  const int32_t nv = (int32_t)(totals[0] & 0xffffffff);
+  const int32_t ng = (int32_t)(totals[0] >> 32);
+  if (nv > 0)
+    e = hipMemcpyAsync(pair_order, plan.pair_order, sizeof(int32_t) * nv,
+                       hipMemcpyDeviceToDevice, hs);
+  if (e == hipSuccess && ng > 0)
+    e = hipMemcpyAsync(group_doc, plan.group_doc, sizeof(int32_t) * ng,
+                       hipMemcpyDeviceToDevice, hs);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(group_ptr, plan.group_ptr, sizeof(int32_t) * (ng + 1),
+                       hipMemcpyDeviceToDevice, hs);
+  if (e == hipSuccess) e = hipStreamSynchronize(hs);
+  if (e != hipSuccess) return hip_fail(e, "grouping copy-out");
+  *n_groups = ng;
+  *n_valid = nv;
+  return ok();
+}
+
+dopr_status_t dopr_gather_prefix(dopr_store_t st, int32_t layer, int32_t n,
+                                 const int32_t *doc_ids,
+                                 const int64_t *out_cu_slots, void *k_out,
+                                 void *v_out, void *stream) {
+  if (!st) return fail(DOPR_ERR_INVALID_ARG, "store is NULL");
+  if (layer < 0 || layer >= st->n_layers)
+    return fail(DOPR_ERR_INVALID_ARG, "layer out of range");
+  if (n < 0) return fail(DOPR_ERR_INVALID_ARG, "n < 0");
+  if (n == 0) return ok();
+  if (!doc_ids || !out_cu_slots || !k_out || !v_out)
+    return fail(DOPR_ERR_INVALID_ARG, "NULL buffer");
+  if (!aligned16(k_out) || !aligned16(v_out))
+    return fail(DOPR_ERR_INVALID_ARG, "k_out/v_out must be 16-byte aligned");
+  dopr_status_t s = check_device(st);
+  if (s != DOPR_OK) return s;
+  hipError_t e = launch_gather(*st, layer, n, doc_ids, out_cu_slots,
+                               static_cast<uint16_t *>(k_out),
+                               static_cast<uint16_t *>(v_out),
+                               as_stream(stream));
+  if (e != hipSuccess) return hip_fail(e, "gather launch");
+  return ok();
+}
+
+dopr_status_t dopr_check_status(dopr_store_t st, void *stream) {
+  if (!st) return fail(DOPR_ERR_INVALID_ARG, "store is NULL");
+  hipStream_t hs = as_stream(stream);
+  int32_t code = 0;
+  hipError_t e = hipStreamSynchronize(hs);
+  if (e == hipSuccess)
+    e = hipMemcpy(&code, st->d_status + kStatusFirstError, sizeof(code),
+                  hipMemcpyDeviceToHost);
+  const int32_t zero = 0;
+  if (e == hipSuccess)
+    e = hipMemcpy(st->d_status + kStatusFirstError, &zero, sizeof(zero),
+                  hipMemcpyHostToDevice);
+  if (e != hipSuccess) return hip_fail(e, "status readback");
+  if (code != 0)
+    return fail((dopr_status_t)code, "deferred device-side error");
+  return ok();
+}
+
+}  // extern "C"

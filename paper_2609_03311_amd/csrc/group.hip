@@ -1,0 +1,375 @@
+// group.hip -- per-batch scheduling of the online attention (integer work).
+//
+// Online, every candidate pair retrieves its document's prefix states
+// (Sec. 3.4).  Pairs that name the same document are grouped so that one
+// workgroup serves all of them and the document's prefix is read once per
+// group: this is the paper's cross-query reuse of a document's prefix
+// (Sec. 3.3, Sec. 4.5.2) applied inside one batch.  Everything here runs on
+// the device with no host synchronisation:
+//   1. validate each pair (doc id range/residency, token range) and count
+//      pairs per document;
+//   2. exclusive scan over the doc-id space -> first slot and group index
+//      of every document (a counting sort: groups come out in ascending doc
+//      id, the canonical order);
+//   3. place pairs into their document's slots, then order each group's
+//      members by pair index (stable, deterministic);
+//   4. stacked-row offsets (T_p * n_rep rows per pair, in grouped order);
+//   5. split each group's rows into work items of bounded size;
+//   6. the rotary cos/sin table for positions 0 .. max_L + max_tokens - 1.
+#include <cmath>
+
+#include "internal.hpp"
+
+namespace dopr {
+namespace {
+
+constexpr int kScanThreads = 1024;
+constexpr int kScanTile = 2 * kScanThreads;
+constexpr int kThreads = 256;
+
+enum Total { kTotDocs = 0, kTotRows = 1, kTotItems = 2, kTotals = 4 };
+enum NextSlots { kNextQueues = 8 };
+
+inline unsigned blocks_for(int64_t n, int t) {
+  int64_t b = (n + t - 1) / t;
+  return (unsigned)(b < 1 ? 1 : b);
+}
+
+// Exclusive block-wide scan of two values per thread (1024 threads).
+// Returns the prefix of the thread's first value; *block_total gets the sum.
+__device__ int64_t block_scan2(int64_t a0, int64_t a1, int64_t *block_total) {
+  __shared__ int64_t wsum[kScanThreads / 64 + 1];
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  const int64_t t = a0 + a1;
+  int64_t x = t;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    int64_t y = __shfl_up(x, off, 64);
+    if (lane >= off) x += y;
+  }
+  if (lane == 63) wsum[wid] = x;
+  __syncthreads();
+  if (wid == 0) {
+    constexpr int nw = kScanThreads / 64;
+    int64_t w = lane < nw ? wsum[lane] : 0;
+    int64_t s = w;
+#pragma unroll
+    for (int off = 1; off < nw; off <<= 1) {
+      int64_t y = __shfl_up(s, off, 64);
+      if (lane >= off) s += y;
+    }
+    if (lane < nw) wsum[lane] = s - w;
+    if (lane == nw - 1) wsum[nw] = s;
+  }
+  __syncthreads();
+  const int64_t prefix = wsum[wid] + x - t;
+  *block_total = wsum[kScanThreads / 64];
+  __syncthreads();
+  return prefix;
+}
+
+__global__ __launch_bounds__(kScanThreads) void k_scan_reduce(
+    const int64_t *data, int64_t n, int64_t *blk) {
+  const int64_t i0 = (int64_t)blockIdx.x * kScanTile + 2 * threadIdx.x;
+  const int64_t a0 = i0 < n ? data[i0] : 0;
+  const int64_t a1 = i0 + 1 < n ? data[i0 + 1] : 0;
+  int64_t tot;
+  block_scan2(a0, a1, &tot);
+  if (threadIdx.x == 0) blk[blockIdx.x] = tot;
+}
+
+__global__ __launch_bounds__(kScanThreads) void k_scan_top(int64_t *blk,
+                                                           int64_t nb,
+                                                           int64_t *total) {
+  int64_t carry = 0;
+  for (int64_t base = 0; base < nb; base += kScanTile) {
+    const int64_t i0 = base + 2 * threadIdx.x;
+    const int64_t a0 = i0 < nb ? blk[i0] : 0;
+    const int64_t a1 = i0 + 1 < nb ? blk[i0 + 1] : 0;
+    int64_t tot;
+    const int64_t pre = block_scan2(a0, a1, &tot);
+    if (i0 < nb) blk[i0] = carry + pre;
+    if (i0 + 1 < nb) blk[i0 + 1] = carry + pre + a0;
+    carry += tot;
+  }
+  if (threadIdx.x == 0) *total = carry;
+}
+
+__global__ __launch_bounds__(kScanThreads) void k_scan_apply(
+    int64_t *data, int64_t n, const int64_t *blk) {
+  const int64_t i0 = (int64_t)blockIdx.x * kScanTile + 2 * threadIdx.x;
+  const int64_t a0 = i0 < n ? data[i0] : 0;
+  const int64_t a1 = i0 + 1 < n ? data[i0 + 1] : 0;
+  int64_t tot;
+  const int64_t pre = block_scan2(a0, a1, &tot) + blk[blockIdx.x];
+  if (i0 < n) data[i0] = pre;
+  if (i0 + 1 < n) data[i0 + 1] = pre + a0;
+}
+
+// In-place exclusive scan of n int64 values; the grand total goes to *total.
+hipError_t exclusive_scan(int64_t *data, int64_t n, int64_t *blk,
+                          int64_t *total, hipStream_t s) {
+  const unsigned nb = blocks_for(n, kScanTile);
+  hipLaunchKernelGGL(k_scan_reduce, dim3(nb), dim3(kScanThreads), 0, s, data,
+                     n, blk);
+  hipLaunchKernelGGL(k_scan_top, dim3(1), dim3(kScanThreads), 0, s, blk,
+                     (int64_t)nb, total);
+  hipLaunchKernelGGL(k_scan_apply, dim3(nb), dim3(kScanThreads), 0, s, data,
+                     n, blk);
+  return hipGetLastError();
+}
+
+struct PlanArgs {
+  const int32_t *doc_ids, *cu, *doc_len;
+  int64_t n_docs, total_tokens;
+  int32_t n_pairs, n_rep, max_tokens, rows_per_item;
+  int32_t *status;
+};
+
+__global__ __launch_bounds__(kThreads) void k_plan_init(Plan pl, int64_t n_docs,
+                                                        int64_t *totals,
+                                                        int32_t *next) {
+  const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (i < n_docs) {
+    pl.cnt[i] = 0;
+    pl.fill[i] = 0;
+  }
+  if (i < kCounters) pl.counters[i] = 0;
+  if (i < kTotals) totals[i] = 0;
+  if (i < kNextQueues) next[i] = 0;
+}
+
+// Step 1: validate every pair and count pairs per document.
+__global__ __launch_bounds__(kThreads) void k_pair_meta(Plan pl, PlanArgs a) {
+  const int32_t p = blockIdx.x * kThreads + threadIdx.x;
+  if (p >= a.n_pairs) return;
+  if (a.cu) {  // grouping-only calls pass no token ranges
+    if (p == 0 && a.cu[0] != 0) raise_status(a.status, DOPR_ERR_SEQLEN);
+    if (p == a.n_pairs - 1 && (int64_t)a.cu[a.n_pairs] != a.total_tokens)
+      raise_status(a.status, DOPR_ERR_SEQLEN);
+    const int64_t t0 = a.cu[p], t1 = a.cu[p + 1];
+    const bool well = t0 >= 0 && t1 >= t0 + 1 && t1 <= a.total_tokens &&
+                      t1 - t0 <= a.max_tokens;
+    if (!well) {
+      raise_status(a.status, DOPR_ERR_SEQLEN);
+      pl.pair_flag[p] = 0;
+      return;
+    }
+  }
+  const int32_t d = a.doc_ids[p];
+  if (d < 0 || (int64_t)d >= a.n_docs || a.doc_len[d] < 0) {
+    raise_status(a.status, DOPR_ERR_DOC_RANGE);
+    pl.pair_flag[p] = 2;
+    pl.invalid[atomicAdd(&pl.counters[kCntInvalid], 1)] = p;
+    return;
+  }
+  pl.pair_flag[p] = 1;
+  atomicAdd(&pl.cnt[d], 1);
+}
+
+__global__ __launch_bounds__(kThreads) void k_doc_pack(Plan pl, int64_t n_docs) {
+  const int64_t d = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (d >= n_docs) return;
+  const int32_t c = pl.cnt[d];
+  pl.doc_scan[d] = c > 0 ? ((int64_t)1 << 32) | (int64_t)c : 0;
+}
+
+// Step 3a: each valid pair takes a slot in its document's range (arbitrary
+// order within the range; fixed by k_rank).
+__global__ __launch_bounds__(kThreads) void k_place(Plan pl, PlanArgs a) {
+  const int32_t p = blockIdx.x * kThreads + threadIdx.x;
+  if (p >= a.n_pairs || pl.pair_flag[p] != 1) return;
+  const int32_t d = a.doc_ids[p];
+  const int32_t slot = (int32_t)(pl.doc_scan[d] & 0xffffffff) +
+                       atomicAdd(&pl.fill[d], 1);
+  pl.tmp_order[slot] = p;
+}
+
+// Step 3b + 4: rank each pair within its group by pair index, write the
+// canonical order, the group table and the pair's stacked-row count.
+__global__ __launch_bounds__(kThreads) void k_rank(Plan pl, PlanArgs a,
+                                                   const int64_t *totals) {
+  const int32_t i = blockIdx.x * kThreads + threadIdx.x;
+  const int32_t n_valid = (int32_t)(totals[kTotDocs] & 0xffffffff);
+  const int32_t n_groups = (int32_t)(totals[kTotDocs] >> 32);
+  if (i > a.n_pairs) return;
+  if (i >= n_valid) {
+    pl.prow[i] = 0;
+    if (i == n_valid) pl.group_ptr[n_groups] = n_valid;
+    return;
+  }
+  const int32_t v = pl.tmp_order[i];
+  const int32_t d = a.doc_ids[v];
+  const int64_t packed = pl.doc_scan[d];
+  const int32_t s0 = (int32_t)(packed & 0xffffffff);
+  const int32_t c = pl.cnt[d];
+  int32_t rank = 0;
+  for (int32_t k = s0; k < s0 + c; ++k) rank += pl.tmp_order[k] < v;
+  pl.pair_order[s0 + rank] = v;
+  const int64_t T = a.cu ? (int64_t)(a.cu[v + 1] - a.cu[v]) : 1;
+  pl.prow[s0 + rank] = T * a.n_rep;
+  if (rank == 0) {
+    const int32_t gi = (int32_t)(packed >> 32);
+    pl.group_doc[gi] = d;
+    pl.group_ptr[gi] = s0;
+  }
+}
+
+// Step 5a: work items per group.
+__global__ __launch_bounds__(kThreads) void k_items_count(Plan pl, PlanArgs a,
+                                                          const int64_t *totals) {
+  const int32_t g = blockIdx.x * kThreads + threadIdx.x;
+  const int32_t n_groups = (int32_t)(totals[kTotDocs] >> 32);
+  if (g > a.n_pairs) return;
+  if (g >= n_groups) {
+    pl.item_scan[g] = 0;
+    return;
+  }
+  const int64_t rows = pl.prow[pl.group_ptr[g + 1]] - pl.prow[pl.group_ptr[g]];
+  pl.item_scan[g] = (rows + a.rows_per_item - 1) / a.rows_per_item;
+}
+
+// Step 5b: split a group's rows into near-equal items, boundaries on
+// multiples of 32 rows.
+__global__ __launch_bounds__(kThreads) void k_items_emit(Plan pl, PlanArgs a,
+                                                         const int64_t *totals) {
+  const int32_t g = blockIdx.x * kThreads + threadIdx.x;
+  const int32_t n_groups = (int32_t)(totals[kTotDocs] >> 32);
+  if (g >= n_groups) return;
+  if (g == 0 && totals[kTotItems] > pl.items_cap)
+    raise_status(a.status, DOPR_ERR_SEQLEN);
+  const int64_t first = pl.item_scan[g];
+  const int64_t n_it = pl.item_scan[g + 1] - first;
+  const int64_t base = pl.prow[pl.group_ptr[g]];
+  const int64_t R = pl.prow[pl.group_ptr[g + 1]] - base;
+  for (int64_t it = 0; it < n_it; ++it) {
+    const int64_t idx = first + it;
+    if (idx >= pl.items_cap) break;
+    const int64_t b0 = base + ((it * R / n_it) & ~(int64_t)31);
+    const int64_t b1 =
+        it + 1 < n_it ? base + (((it + 1) * R / n_it) & ~(int64_t)31)
+                      : base + R;
+    pl.items[idx] = make_int4(g, (int32_t)b0, (int32_t)b1, 0);
+  }
+}
+
+// Step 6: rotary table, (cos, sin)(pos * theta^(-2i/D)) in double, stored
+// as float.
+__global__ __launch_bounds__(kThreads) void k_rope_table(float2 *tab,
+                                                         int32_t n_pos,
+                                                         double log_theta) {
+  const int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (e >= (int64_t)n_pos * kRopeHalf) return;
+  const int32_t pos = (int32_t)(e / kRopeHalf), i = (int32_t)(e % kRopeHalf);
+  const double freq = exp(-2.0 * (double)i / (double)kHeadDim * log_theta);
+  double sn, cs;
+  sincos((double)pos * freq, &sn, &cs);
+  tab[e] = make_float2((float)cs, (float)sn);
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+
+namespace {
+struct Carver {
+  char *base;
+  size_t off = 0;
+  template <class T>
+  T *take(int64_t n) {
+    T *p = reinterpret_cast<T *>(base ? base + off : nullptr);
+    off = align_up(off + sizeof(T) * (size_t)(n > 0 ? n : 1), kAlign);
+    return p;
+  }
+};
+
+Plan carve(void *ws, const PlanShape &s, size_t *bytes) {
+  Carver c{static_cast<char *>(ws)};
+  Plan pl{};
+  const int64_t P = s.n_pairs;
+  pl.counters = c.take<int32_t>(kCounters + kTotals * 2 + kNextQueues);
+  pl.cnt = c.take<int32_t>(s.n_docs);
+  pl.fill = c.take<int32_t>(s.n_docs);
+  pl.doc_scan = c.take<int64_t>(s.n_docs);
+  const int64_t scan_n = s.n_docs > P + 1 ? s.n_docs : P + 1;
+  pl.scan_blocks_cap = (scan_n + kScanTile - 1) / kScanTile;
+  pl.blk = c.take<int64_t>(pl.scan_blocks_cap);
+  pl.pair_flag = c.take<int32_t>(P);
+  pl.invalid = c.take<int32_t>(P);
+  pl.tmp_order = c.take<int32_t>(P);
+  pl.pair_order = c.take<int32_t>(P);
+  pl.group_doc = c.take<int32_t>(P);
+  pl.group_ptr = c.take<int32_t>(P + 1);
+  pl.prow = c.take<int64_t>(P + 1);
+  pl.item_scan = c.take<int64_t>(P + 1);
+  const int64_t rows = s.total_tokens * s.n_rep;
+  const int64_t cap = P + (rows + s.rows_per_item - 1) / s.rows_per_item + 1;
+  pl.items_cap = (int32_t)cap;
+  pl.items = c.take<int4>(cap);
+  pl.rope_pos = s.max_len + s.max_tokens;
+  pl.rope = c.take<float2>((int64_t)pl.rope_pos * kRopeHalf);
+  *bytes = c.off;
+  return pl;
+}
+}  // namespace
+
+// Totals and queue cursors live right after the int32 counters.
+int64_t *plan_totals(const Plan &pl) {
+  return reinterpret_cast<int64_t *>(pl.counters + kCounters);
+}
+int32_t *plan_next(const Plan &pl) {
+  return pl.counters + kCounters + kTotals * 2;
+}
+
+size_t plan_bytes(const PlanShape &s) {
+  size_t b = 0;
+  carve(nullptr, s, &b);
+  return b;
+}
+
+Plan plan_carve(void *ws, const PlanShape &s) {
+  size_t b = 0;
+  return carve(ws, s, &b);
+}
+
+hipError_t launch_plan(const AttnCall &c, const Plan &pl,
+                       const PlanShape &shape, hipStream_t s) {
+  const dopr_attn_args_t *a = c.a;
+  PlanArgs pa{a->doc_ids,        a->cu_seqlens,      c.st->d_len,
+              c.st->n_docs,      a->total_tokens,    a->n_pairs,
+              c.n_rep,           a->max_tokens,      shape.rows_per_item,
+              c.st->d_status};
+  int64_t *totals = plan_totals(pl);
+  const int64_t P = a->n_pairs;
+  const int64_t init_n = c.st->n_docs > kCounters ? c.st->n_docs : kCounters;
+  hipLaunchKernelGGL(k_plan_init, dim3(blocks_for(init_n, kThreads)),
+                     dim3(kThreads), 0, s, pl, c.st->n_docs, totals,
+                     plan_next(pl));
+  hipLaunchKernelGGL(k_pair_meta, dim3(blocks_for(P, kThreads)),
+                     dim3(kThreads), 0, s, pl, pa);
+  hipLaunchKernelGGL(k_doc_pack, dim3(blocks_for(c.st->n_docs, kThreads)),
+                     dim3(kThreads), 0, s, pl, c.st->n_docs);
+  hipError_t e = exclusive_scan(pl.doc_scan, c.st->n_docs, pl.blk,
+                                totals + kTotDocs, s);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_place, dim3(blocks_for(P, kThreads)), dim3(kThreads),
+                     0, s, pl, pa);
+  hipLaunchKernelGGL(k_rank, dim3(blocks_for(P + 1, kThreads)),
+                     dim3(kThreads), 0, s, pl, pa, totals);
+  e = exclusive_scan(pl.prow, P + 1, pl.blk, totals + kTotRows, s);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_items_count, dim3(blocks_for(P + 1, kThreads)),
+                     dim3(kThreads), 0, s, pl, pa, totals);
+  e = exclusive_scan(pl.item_scan, P + 1, pl.blk, totals + kTotItems, s);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_items_emit, dim3(blocks_for(P, kThreads)),
+                     dim3(kThreads), 0, s, pl, pa, totals);
+  const double log_theta = std::log((double)a->rope_theta);
+  hipLaunchKernelGGL(k_rope_table,
+                     dim3(blocks_for((int64_t)pl.rope_pos * kRopeHalf,
+                                     kThreads)),
+                     dim3(kThreads), 0, s, pl.rope, pl.rope_pos, log_theta);
+  return hipGetLastError();
+}
+
+}  // namespace dopr

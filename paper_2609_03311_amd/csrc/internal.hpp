@@ -1,0 +1,141 @@
+// internal.hpp -- shared declarations of the DoPR HIP library (not part of
+// the public ABI; the public contract is include/dopr.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+#include "dopr.h"
+
+namespace dopr {
+
+constexpr int kHeadDim = 128;
+constexpr int kAlign = 256;
+constexpr int kRopeHalf = kHeadDim / 2;
+
+inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+__host__ __device__ inline int32_t pad8(int32_t n) { return (n + 7) & ~7; }
+
+// Device status words at the head of every store pool.
+enum StatusSlot { kStatusFirstError = 0, kStatusWords = 64 };
+
+// Store layout inside the caller's pool:
+//   [status words | doc_len int32[n_docs] | doc_off int64[n_docs] | payload]
+// Each resident document owns one contiguous block of the payload; for layer
+// l and kv head g the block holds
+//   K  [L][D]   at  blk + l*Hkv*D*(L+Lp) + g*L*D
+//   Vt [D][Lp]  at  blk + l*Hkv*D*(L+Lp) + Hkv*L*D + g*D*Lp
+// with Lp = L rounded up to 8 (V is stored transposed so the PV contraction
+// over keys reads 16-byte runs; the pad columns are zero).
+struct StoreView {
+  const int32_t *doc_len;  // [n_docs], -1 = not resident
+  const int64_t *doc_off;  // [n_docs], element offset of the doc block
+  uint16_t *payload;
+  int64_t n_docs;
+  int32_t n_layers, n_kv_heads;
+};
+
+__host__ __device__ inline int64_t layer_block_elems(int32_t L, int32_t hkv) {
+  return (int64_t)hkv * kHeadDim * ((int64_t)L + pad8(L));
+}
+__host__ __device__ inline int64_t k_offset(int64_t blk, int32_t L, int32_t hkv,
+                                            int32_t layer, int32_t g) {
+  return blk + layer * layer_block_elems(L, hkv) + (int64_t)g * L * kHeadDim;
+}
+__host__ __device__ inline int64_t vt_offset(int64_t blk, int32_t L,
+                                             int32_t hkv, int32_t layer,
+                                             int32_t g) {
+  return blk + layer * layer_block_elems(L, hkv) +
+         (int64_t)hkv * L * kHeadDim + (int64_t)g * kHeadDim * pad8(L);
+}
+
+}  // namespace dopr
+
+struct dopr_store {
+  int32_t n_layers, n_kv_heads, head_dim;
+  int64_t n_docs;
+  char *pool;
+  size_t pool_bytes;
+  int32_t *d_status;
+  int32_t *d_len;
+  int64_t *d_off;
+  uint16_t *d_payload;
+  int32_t max_len;  // largest L over resident documents
+  int device;
+  dopr::StoreView view() const {
+    return {d_len, d_off, d_payload, n_docs, n_layers, n_kv_heads};
+  }
+};
+
+namespace dopr {
+
+// ---------------------------------------------------------------------------
+// Per-call plan built on the device by the grouping kernels (workspace).
+enum Counter {
+  kCntValid = 0,     // pairs with a valid, resident document
+  kCntGroups = 1,    // distinct documents among them
+  kCntItems = 2,     // attention work items
+  kCntInvalid = 3,   // pairs whose outputs must be zeroed
+  kCntRows = 4,      // stacked rows (tokens * n_rep) of valid pairs (low)
+  kCounters = 16
+};
+
+struct Plan {
+  int32_t *counters;    // [kCounters]
+  int32_t *cnt;         // [n_docs]   pairs per document
+  int32_t *fill;        // [n_docs]   placement cursor per document
+  int64_t *doc_scan;    // [n_docs]   (has_pairs << 32 | count), scanned
+  int64_t *blk;         // scan block sums
+  int32_t *pair_flag;   // [P] 1 = valid, 0 = skip, 2 = zero outputs
+  int32_t *invalid;     // [P] pairs whose outputs are zeroed
+  int32_t *tmp_order;   // [P]
+  int32_t *pair_order;  // [P]
+  int32_t *group_doc;   // [P]
+  int32_t *group_ptr;   // [P+1]
+  int64_t *prow;        // [P+1] stacked-row offsets, sorted pair order
+  int64_t *item_scan;   // [P+1] work items per group, scanned
+  int4 *items;          // [items_cap] (group, row0, row1, 0)
+  float2 *rope;         // [rope_pos][64] (cos, sin)
+  int32_t items_cap;
+  int32_t rope_pos;
+  int64_t scan_blocks_cap;
+};
+
+struct PlanShape {
+  int32_t n_pairs, n_rep, max_tokens, rows_per_item;
+  int64_t n_docs, total_tokens;
+  int32_t max_len;
+};
+
+size_t plan_bytes(const PlanShape &s);
+Plan plan_carve(void *ws, const PlanShape &s);
+
+// Launchers (return hipError_t of the last launch).
+hipError_t launch_store_put(const dopr_store &st, int32_t layer, int64_t n,
+                            const int32_t *doc_ids, const int64_t *src_cu,
+                            const uint16_t *k, const uint16_t *v,
+                            hipStream_t s);
+hipError_t launch_gather(const dopr_store &st, int32_t layer, int32_t n,
+                         const int32_t *doc_ids, const int64_t *out_cu,
+                         uint16_t *k, uint16_t *v, hipStream_t s);
+
+struct AttnCall {
+  const dopr_store *st;
+  int32_t layer;
+  const dopr_attn_args_t *a;
+  int32_t n_rep;
+};
+hipError_t launch_plan(const AttnCall &c, const Plan &plan,
+                       const PlanShape &shape, hipStream_t s);
+hipError_t launch_attention(const AttnCall &c, const Plan &plan,
+                            const PlanShape &shape, hipStream_t s);
+hipError_t launch_score(const dopr_score_args_t *a, hipStream_t s);
+
+// Record a deferred error code in a status word (first error wins).
+__device__ inline void raise_status(int32_t *status, int32_t code) {
+  atomicCAS(status, 0, code);
+}
+
+}  // namespace dopr

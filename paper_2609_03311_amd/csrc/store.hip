@@ -1,0 +1,117 @@
+// store.hip -- filling and reading back the HBM prefix store.
+//
+// The store holds, per resident document d and layer l, the prefix K/V
+// states of its L_d slots (Sec. 3.3: computed offline, query-independent).
+// Keys are kept row-major [L][D]; values are kept transposed [D][Lp] so the
+// attention kernel's PV contraction (over keys) reads contiguous 16-byte
+// runs.  These kernels run offline (ingest) or in tests only.
+#include "internal.hpp"
+
+namespace dopr {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kTile = 64;  // slots per transpose tile
+
+__device__ bool doc_ok(const StoreView &sv, int32_t d) {
+  return d >= 0 && (int64_t)d < sv.n_docs && sv.doc_len[d] >= 0;
+}
+
+// One workgroup per (document i, kv head g).
+__global__ __launch_bounds__(kThreads) void k_store_put(
+    StoreView sv, int32_t *status, int32_t layer, const int32_t *doc_ids,
+    const int64_t *src_cu, const uint16_t *ksrc, const uint16_t *vsrc) {
+  const int64_t i = blockIdx.x;
+  const int g = blockIdx.y, hkv = sv.n_kv_heads;
+  const int32_t d = doc_ids[i];
+  const int64_t s0 = src_cu[i], s1 = src_cu[i + 1];
+  if (!doc_ok(sv, d) || s1 - s0 != sv.doc_len[d]) {
+    if (threadIdx.x == 0 && g == 0) raise_status(status, DOPR_ERR_DOC_RANGE);
+    return;
+  }
+  const int32_t L = sv.doc_len[d], Lp = pad8(L);
+  const int64_t blk = sv.doc_off[d];
+  uint16_t *K = sv.payload + k_offset(blk, L, hkv, layer, g);
+  uint16_t *VT = sv.payload + vt_offset(blk, L, hkv, layer, g);
+
+  for (int64_t gi = threadIdx.x; gi < (int64_t)L * 16; gi += kThreads) {
+    const int64_t row = gi >> 4;
+    const int c = gi & 15;
+    const uint4 *src = reinterpret_cast<const uint4 *>(
+        ksrc + ((s0 + row) * hkv + g) * kHeadDim);
+    reinterpret_cast<uint4 *>(K + row * kHeadDim)[c] = src[c];
+  }
+
+  __shared__ uint16_t tile[kTile][kHeadDim + 2];
+  for (int t0 = 0; t0 < Lp; t0 += kTile) {
+    for (int gi = threadIdx.x; gi < kTile * 16; gi += kThreads) {
+      const int r = gi >> 4, c = gi & 15, slot = t0 + r;
+      uint4 val = make_uint4(0, 0, 0, 0);
+      if (slot < L)
+        val = reinterpret_cast<const uint4 *>(
+            vsrc + ((s0 + slot) * hkv + g) * kHeadDim)[c];
+      uint32_t *dst = reinterpret_cast<uint32_t *>(&tile[r][c * 8]);
+      dst[0] = val.x; dst[1] = val.y; dst[2] = val.z; dst[3] = val.w;
+    }
+    __syncthreads();
+    for (int e = threadIdx.x; e < kHeadDim * kTile; e += kThreads) {
+      const int dd = e / kTile, r = e % kTile, slot = t0 + r;
+      if (slot < Lp) VT[(int64_t)dd * Lp + slot] = tile[r][dd];
+    }
+    __syncthreads();
+  }
+}
+
+// Inverse of k_store_put into canonical [slots][Hkv][D] rows.
+__global__ __launch_bounds__(kThreads) void k_gather(
+    StoreView sv, int32_t *status, int32_t layer, const int32_t *doc_ids,
+    const int64_t *out_cu, uint16_t *kout, uint16_t *vout) {
+  const int64_t i = blockIdx.x;
+  const int g = blockIdx.y, hkv = sv.n_kv_heads;
+  const int32_t d = doc_ids[i];
+  const int64_t o0 = out_cu[i], o1 = out_cu[i + 1];
+  if (!doc_ok(sv, d) || o1 - o0 != sv.doc_len[d]) {
+    if (threadIdx.x == 0 && g == 0) raise_status(status, DOPR_ERR_DOC_RANGE);
+    return;
+  }
+  const int32_t L = sv.doc_len[d], Lp = pad8(L);
+  const int64_t blk = sv.doc_off[d];
+  const uint16_t *K = sv.payload + k_offset(blk, L, hkv, layer, g);
+  const uint16_t *VT = sv.payload + vt_offset(blk, L, hkv, layer, g);
+  for (int64_t gi = threadIdx.x; gi < (int64_t)L * 16; gi += kThreads) {
+    const int64_t row = gi >> 4;
+    const int c = gi & 15;
+    reinterpret_cast<uint4 *>(kout + ((o0 + row) * hkv + g) * kHeadDim)[c] =
+        reinterpret_cast<const uint4 *>(K + row * kHeadDim)[c];
+  }
+  for (int64_t e = threadIdx.x; e < (int64_t)L * kHeadDim; e += kThreads) {
+    const int64_t slot = e / kHeadDim;
+    const int dd = e % kHeadDim;
+    vout[((o0 + slot) * hkv + g) * kHeadDim + dd] = VT[(int64_t)dd * Lp + slot];
+  }
+}
+
+}  // namespace
+
+hipError_t launch_store_put(const dopr_store &st, int32_t layer, int64_t n,
+                            const int32_t *doc_ids, const int64_t *src_cu,
+                            const uint16_t *k, const uint16_t *v,
+                            hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  dim3 grid((unsigned)n, (unsigned)st.n_kv_heads);
+  hipLaunchKernelGGL(k_store_put, grid, dim3(kThreads), 0, s, st.view(),
+                     st.d_status, layer, doc_ids, src_cu, k, v);
+  return hipGetLastError();
+}
+
+hipError_t launch_gather(const dopr_store &st, int32_t layer, int32_t n,
+                         const int32_t *doc_ids, const int64_t *out_cu,
+                         uint16_t *k, uint16_t *v, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  dim3 grid((unsigned)n, (unsigned)st.n_kv_heads);
+  hipLaunchKernelGGL(k_gather, grid, dim3(kThreads), 0, s, st.view(),
+                     st.d_status, layer, doc_ids, out_cu, k, v);
+  return hipGetLastError();
+}
+
+}  // namespace dopr

@@ -1,0 +1,83 @@
+"""One decoder layer's online DoPR step on an HBM prefix store.
+
+A thin convenience layer over the C ABI: it allocates device buffers with
+torch and issues the library calls; all computation runs in the HIP kernels.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+from . import (dopr_prefix_attn, dopr_prefix_attn_workspace,
+               dopr_score_logits, dopr_store_create, dopr_store_put)
+
+HEAD_DIM = 128
+
+
+def make_store(doc_len, n_kv_heads, k_src, v_src, *, n_layers=1, layer=0,
+               device="cuda", stream=None):
+    """Create a store for `doc_len` and fill `layer` from canonical prefix
+    states k_src/v_src [slots, Hkv, D] (bf16, device) holding the resident
+    documents' slots in ascending doc-id order."""
+    import torch
+    doc_len = np.ascontiguousarray(doc_len, np.int32)
+    store = dopr_store_create(n_layers, n_kv_heads, HEAD_DIM, doc_len,
+                              device=device, stream=stream)
+    res = np.nonzero(doc_len >= 0)[0].astype(np.int32)
+    if res.size:
+        cu = np.zeros(res.size + 1, np.int64)
+        np.cumsum(doc_len[res], out=cu[1:])
+        ids = torch.from_numpy(res).to(device)
+        cu_t = torch.from_numpy(cu).to(device)
+        dopr_store_put(store, layer, ids, cu_t, k_src, v_src, stream=stream)
+    return store
+
+
+class OnlineStep:
+    """Reusable buffers for the per-batch step: prefix attention over the
+    store, then the score head on each pair's score-token output row."""
+
+    def __init__(self, store, *, n_pairs, n_q_heads, total_tokens,
+                 max_tokens, kernel_variant=0, device="cuda", with_lse=False):
+        import torch
+        self.store = store
+        self.n_pairs = n_pairs
+        self.n_q_heads = n_q_heads
+        self.total_tokens = total_tokens
+        self.max_tokens = max_tokens
+        self.kernel_variant = kernel_variant
+        nbytes = dopr_prefix_attn_workspace(
+            store, n_pairs=n_pairs, n_q_heads=n_q_heads,
+            max_tokens=max_tokens, total_tokens=total_tokens,
+            kernel_variant=kernel_variant)
+        self.workspace = torch.empty(max(nbytes, 256), dtype=torch.uint8,
+                                     device=device)
+        self.out = torch.empty((total_tokens, n_q_heads, HEAD_DIM),
+                               dtype=torch.bfloat16, device=device)
+        self.lse = (torch.empty((total_tokens, n_q_heads), dtype=torch.float32,
+                                device=device) if with_lse else None)
+        self.score = torch.empty(n_pairs, dtype=torch.float32, device=device)
+        self.logits = torch.empty((n_pairs, 2), dtype=torch.float32,
+                                  device=device)
+
+    def attention(self, layer, doc_ids, cu_seqlens, q, k, v, q_norm_w,
+                  k_norm_w, stream=None, **kw):
+        dopr_prefix_attn(self.store, layer, doc_ids, cu_seqlens, q, k, v,
+                         q_norm_w, k_norm_w, self.out, self.workspace,
+                         max_tokens=self.max_tokens, lse=self.lse,
+                         total_tokens=self.total_tokens,
+                         kernel_variant=self.kernel_variant, stream=stream,
+                         **kw)
+
+    def score_head(self, cu_seqlens, norm_w, w_head, stream=None,
+                   rms_eps=1e-6):
+        width = self.n_q_heads * HEAD_DIM
+        dopr_score_logits(self.out, norm_w, w_head, self.score, width=width,
+                          h_row_stride=width, cu_seqlens=cu_seqlens,
+                          logits=self.logits, rms_eps=rms_eps,
+                          n_pairs=self.n_pairs, stream=stream)
+
+    def run(self, layer, doc_ids, cu_seqlens, q, k, v, q_norm_w, k_norm_w,
+            norm_w, w_head, stream=None):
+        self.attention(layer, doc_ids, cu_seqlens, q, k, v, q_norm_w,
+                       k_norm_w, stream=stream)
+        self.score_head(cu_seqlens, norm_w, w_head, stream=stream)

@@ -1,0 +1,170 @@
+"""GPU-side set-up for the parity tests: seeded inputs on the device, the
+HIP path through the C ABI, and the float64 oracle on the same bytes (copied
+device -> host; nothing the oracle reads comes from the HIP path)."""
+from __future__ import annotations
+
+import dataclasses
+import sys
+import time
+
+import numpy as np
+
+import oracle
+import refs
+import workloads
+
+
+def log(msg):
+    print(f"[{time.strftime('%H:%M:%S')}] {msg}", flush=True)
+    sys.stdout.flush()
+
+
+@dataclasses.dataclass
+class Case:
+    st: workloads.Structure
+    k_src: object
+    v_src: object
+    doc_off: np.ndarray      # row of each resident doc's first slot
+    online: dict
+    prm: dict
+    store: object
+    step: object
+    doc_ids: object
+    cu: object
+
+
+def setup(st, seed=0, key_scale=1.0, kernel_variant=0, device="cuda"):
+    import torch
+    from paper_2609_03311_amd import pipeline
+    log(f"setup {st.name}: P={st.n_pairs} Ntok={st.n_tokens} "
+        f"Hq={st.n_q_heads} Hkv={st.n_kv_heads} seed={seed} "
+        f"variant={kernel_variant}")
+    k_src, v_src, doc_off, _ = workloads.prefix_source(
+        st, device, seed * 100 + 1, key_scale)
+    online = workloads.online_inputs(st, device, seed * 100 + 3)
+    prm = workloads.params(st, device, seed * 100 + 6)
+    store = pipeline.make_store(st.doc_len, st.n_kv_heads, k_src, v_src,
+                                device=device)
+    max_t = int(st.seqlens.max()) if st.n_pairs else 1
+    step = pipeline.OnlineStep(store, n_pairs=st.n_pairs,
+                               n_q_heads=st.n_q_heads,
+                               total_tokens=st.n_tokens, max_tokens=max_t,
+                               kernel_variant=kernel_variant, device=device,
+                               with_lse=True)
+    doc_ids = torch.from_numpy(st.doc_ids).to(device)
+    cu = torch.from_numpy(st.cu_seqlens).to(device)
+    torch.cuda.synchronize()
+    return Case(st, k_src, v_src, doc_off, online, prm, store, step, doc_ids,
+                cu)
+
+
+def run(case: Case):
+    import torch
+    from paper_2609_03311_amd import dopr_check_status
+    o = case.online
+    p = case.prm
+    case.step.run(0, case.doc_ids, case.cu, o["q"], o["k"], o["v"],
+                  p["q_norm_w"], p["k_norm_w"], p["norm_w"], p["w_head"])
+    torch.cuda.synchronize()
+    return dopr_check_status(case.store)
+
+
+def oracle_subset(case: Case, pairs):
+    """Oracle outputs for a subset of pairs (in the given order)."""
+    import torch
+    st = case.st
+    pairs = np.asarray(pairs, np.int64)
+    cu = st.cu_seqlens.astype(np.int64)
+    docs = np.unique(st.doc_ids[pairs])
+    docs = docs[(docs >= 0) & (docs < st.n_docs)]
+    docs = docs[st.doc_len[docs] >= 0]
+    # prefix slots of the needed documents, copied from the generator output
+    sub_off = np.full(st.n_docs, -1, np.int64)
+    rows, pos = [], 0
+    for d in docs:
+        L = int(st.doc_len[d])
+        sub_off[d] = pos
+        rows.append((int(case.doc_off[d]), L))
+        pos += L
+    idx = np.concatenate([np.arange(o, o + L) for o, L in rows]) if rows \
+        else np.zeros(0, np.int64)
+    it = torch.from_numpy(idx).to(case.k_src.device)
+    pk = refs.torch_bf16_to_bits(case.k_src.index_select(0, it))
+    pv = refs.torch_bf16_to_bits(case.v_src.index_select(0, it))
+    tok = np.concatenate([np.arange(cu[p], cu[p + 1]) for p in pairs])
+    tt = torch.from_numpy(tok).to(case.k_src.device)
+    q = refs.torch_bf16_to_bits(case.online["q"].index_select(0, tt))
+    k = refs.torch_bf16_to_bits(case.online["k"].index_select(0, tt))
+    v = refs.torch_bf16_to_bits(case.online["v"].index_select(0, tt))
+    lens = (cu[pairs + 1] - cu[pairs]).astype(np.int64)
+    sub_cu = np.zeros(len(pairs) + 1, np.int64)
+    np.cumsum(lens, out=sub_cu[1:])
+    t0 = time.time()
+    out, lse, status = oracle.prefix_attn(
+        st.doc_ids[pairs], sub_cu.astype(np.int32), st.doc_len, sub_off, pk,
+        pv, q, k, v, refs.torch_bf16_to_bits(case.prm["q_norm_w"]),
+        refs.torch_bf16_to_bits(case.prm["k_norm_w"]),
+        n_q_heads=st.n_q_heads, n_kv_heads=st.n_kv_heads)
+    h = out[sub_cu[1:] - 1].reshape(len(pairs), -1)
+    logits, s = oracle.score(h, refs.torch_bf16_to_bits(case.prm["norm_w"]),
+                             refs.torch_bf16_to_bits(case.prm["w_head"]))
+    log(f"oracle on {len(pairs)} pairs ({len(tok)} tokens): "
+        f"{time.time() - t0:.1f}s")
+    return dict(tok=tok, out=out, lse=lse, status=status, logits=logits,
+                score=s)
+
+
+def gpu_subset(case: Case, pairs, tok):
+    import torch
+    dev = case.step.out.device
+    tt = torch.from_numpy(np.asarray(tok, np.int64)).to(dev)
+    pt = torch.from_numpy(np.asarray(pairs, np.int64)).to(dev)
+    out = case.step.out.index_select(0, tt).float().cpu().numpy()
+    lse = case.step.lse.index_select(0, tt).cpu().numpy()
+    score = case.step.score.index_select(0, pt).cpu().numpy()
+    logits = case.step.logits.index_select(0, pt).cpu().numpy()
+    return dict(out=out, lse=lse, score=score, logits=logits)
+
+
+TOL = 2e-2  # max-abs on O and s (bf16 inputs, fp32 accumulation)
+
+
+def compare(case: Case, pairs, tol=TOL):
+    ref = oracle_subset(case, pairs)
+    got = gpu_subset(case, pairs, ref["tok"])
+    valid = ref["status"] == 0
+    e_out = float(np.abs(got["out"] - ref["out"]).max()) if got["out"].size \
+        else 0.0
+    fin = np.isfinite(ref["lse"])
+    e_lse = float(np.abs(got["lse"][fin] - ref["lse"][fin]).max()) \
+        if fin.any() else 0.0
+    e_s = float(np.abs(got["score"][valid] - ref["score"][valid]).max()) \
+        if valid.any() else 0.0
+    e_l = float(np.abs(got["logits"][valid] - ref["logits"][valid]).max()) \
+        if valid.any() else 0.0
+    mean_out = float(np.abs(got["out"] - ref["out"]).mean()) \
+        if got["out"].size else 0.0
+    log(f"{case.st.name}: {len(pairs)} pairs max|dO|={e_out:.3e} "
+        f"mean|dO|={mean_out:.3e} max|dlse|={e_lse:.3e} "
+        f"max|ds|={e_s:.3e} max|dlogit|={e_l:.3e}")
+    assert e_out <= tol, f"O max-abs {e_out} > {tol}"
+    assert e_s <= tol, f"score max-abs {e_s} > {tol}"
+    assert e_l <= tol, f"logit max-abs {e_l} > {tol}"
+    assert e_lse <= tol, f"lse max-abs {e_lse} > {tol}"
+    return dict(out=e_out, score=e_s, lse=e_lse)
+
+
+def sample_pairs(st, n_random, seed=0, include_largest_group=True,
+                 max_group=None):
+    rng = np.random.default_rng(1234 + seed)
+    P = st.n_pairs
+    picks = set(rng.choice(P, min(n_random, P), replace=False).tolist())
+    if include_largest_group and P:
+        u, c = np.unique(st.doc_ids, return_counts=True)
+        big = u[np.argmax(c)]
+        members = np.nonzero(st.doc_ids == big)[0]
+        if max_group is not None and len(members) > max_group:
+            members = np.sort(rng.choice(members, max_group, replace=False))
+        picks.update(members.tolist())
+    picks.update([0, P - 1])
+    return np.array(sorted(picks), np.int64)

@@ -1,0 +1,122 @@
+"""The C ABI on the CPU: the library loads, exports every function the header
+declares, the Python binding's struct layouts equal the C ones, and
+host-side validation returns the documented status codes without touching a
+GPU."""
+import ctypes
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+import oracle
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "dopr.h")
+
+
+def _D():
+    import paper_2609_03311_amd as D
+    D.lib()
+    return D
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(dopr_[a-z_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_function():
+    D = _D()
+    names = header_functions()
+    assert len(names) >= 12
+    L = ctypes.CDLL(D.LIB_PATH)
+    for n in names:
+        assert hasattr(L, n), f"{n} not exported"
+    assert set(names) == set(D.EXPORTS), "binding and header disagree"
+
+
+def test_struct_layouts_match_header(tmp_path):
+    D = _D()
+    probe = tmp_path / "probe.c"
+    structs = {"dopr_store_desc_t": D._StoreDesc,
+               "dopr_attn_args_t": D._AttnArgs,
+               "dopr_score_args_t": D._ScoreArgs}
+    lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "dopr.h"',
+             "int main(void) {"]
+    for cname, py in structs.items():
+        lines.append(f'printf("{cname} size %zu\\n", sizeof({cname}));')
+        for f, _ in py._fields_:
+            lines.append(f'printf("{cname} {f} %zu\\n", '
+                         f'offsetof({cname}, {f}));')
+    lines += ["return 0; }"]
+    probe.write_text("\n".join(lines))
+    exe = tmp_path / "probe"
+    subprocess.run(["gcc", "-std=c11", "-I", os.path.join(ROOT, "include"),
+                    str(probe), "-o", str(exe)], check=True)
+    out = subprocess.run([str(exe)], capture_output=True, text=True,
+                         check=True).stdout.split("\n")
+    got = {}
+    for line in out:
+        if line:
+            s, f, v = line.split()
+            got[(s, f)] = int(v)
+    for cname, py in structs.items():
+        assert got[(cname, "size")] == ctypes.sizeof(py), cname
+        for f, _ in py._fields_:
+            assert got[(cname, f)] == getattr(py, f).offset, (cname, f)
+
+
+def test_store_bytes_closed_form():
+    D = _D()
+    rng = np.random.default_rng(0)
+    for layers, hkv in [(1, 8), (36, 8), (28, 8), (3, 2)]:
+        doc_len = rng.integers(-1, 300, 500).astype(np.int32)
+        pool, payload = D.dopr_store_bytes(layers, hkv, 128, doc_len)
+        assert payload == oracle.store_payload_bytes(layers, hkv, 128,
+                                                     doc_len)
+        # index (12 B/doc) + payload with V rows padded to 8 slots
+        res = doc_len[doc_len >= 0].astype(np.int64)
+        padded = ((res + 7) // 8 * 8 + res).sum() * layers * hkv * 128 * 2
+        assert pool >= padded + 12 * len(doc_len)
+        assert pool <= padded + 12 * len(doc_len) + 3 * 256 + 256
+
+
+def test_host_validation_codes():
+    D = _D()
+    with pytest.raises(D.DoprError) as e:
+        D.dopr_store_bytes(1, 8, 64, [4])
+    assert e.value.status == D.DOPR_ERR_UNSUPPORTED
+    with pytest.raises(D.DoprError) as e:
+        D.dopr_store_bytes(1, 8, 128, [4, -2])
+    assert e.value.status == D.DOPR_ERR_INVALID_ARG
+    with pytest.raises(D.DoprError) as e:
+        D.dopr_store_bytes(0, 8, 128, [4])
+    assert e.value.status == D.DOPR_ERR_INVALID_ARG
+    L = D.lib()
+    a = D._AttnArgs()
+    n = ctypes.c_size_t(0)
+    assert L.dopr_prefix_attn_workspace(None, ctypes.byref(a),
+                                        ctypes.byref(n)) == \
+        D.DOPR_ERR_INVALID_ARG
+    assert "store is NULL" in D.dopr_last_error()
+    assert L.dopr_prefix_attn(None, 0, ctypes.byref(a), None) == \
+        D.DOPR_ERR_INVALID_ARG
+    s = D._ScoreArgs()
+    s.n_pairs, s.width, s.h_row_stride, s.rms_eps = 4, 12, 12, 1e-6
+    assert L.dopr_score_logits(ctypes.byref(s), None) == \
+        D.DOPR_ERR_INVALID_ARG
+    s.width, s.h_row_stride = 16, 8
+    assert L.dopr_score_logits(ctypes.byref(s), None) == \
+        D.DOPR_ERR_INVALID_ARG
+    s.h_row_stride = 16
+    assert L.dopr_score_logits(ctypes.byref(s), None) == \
+        D.DOPR_ERR_INVALID_ARG  # NULL buffers
+    s.n_pairs = 0
+    assert L.dopr_score_logits(ctypes.byref(s), None) == D.DOPR_OK
+    assert L.dopr_check_status(None, None) == D.DOPR_ERR_INVALID_ARG
+    assert D.dopr_status_str(D.DOPR_ERR_DOC_RANGE) == "DOPR_ERR_DOC_RANGE"
+    assert D.dopr_status_str(D.DOPR_ERR_SEQLEN) == "DOPR_ERR_SEQLEN"
+    assert L.dopr_store_destroy(None) == D.DOPR_OK

@@ -1,0 +1,134 @@
+"""Bit-exact checks of the integer steps and of the score head (GPU):
+doc-id grouping against the oracle's canonical CSR, prefix gather against the
+generator's bytes, store-put error handling, and the score kernel against the
+oracle on exactly-widened bf16 hidden states."""
+import numpy as np
+import pytest
+
+import oracle
+import refs
+import workloads
+from gpu_harness import log
+
+pytestmark = pytest.mark.gpu
+
+
+def _store(st, seed=1):
+    from paper_2609_03311_amd import pipeline
+    k, v, doc_off, cu = workloads.prefix_source(st, "cuda", seed)
+    return pipeline.make_store(st.doc_len, st.n_kv_heads, k, v), k, v, doc_off
+
+
+def _ws(store, P):
+    import torch
+    from paper_2609_03311_amd import dopr_prefix_attn_workspace
+    n = dopr_prefix_attn_workspace(store, n_pairs=P, n_q_heads=8,
+                                   max_tokens=1, total_tokens=P)
+    return torch.empty(n, dtype=torch.uint8, device="cuda")
+
+
+@pytest.mark.parametrize("name", ["tiny", "qwen3_0p6b", "qwen3_4b",
+                                  "qwen3_8b", "qwen3_8b_ragged", "random"])
+def test_grouping_bit_exact(name):
+    import torch
+    from paper_2609_03311_amd import (DOPR_ERR_DOC_RANGE, dopr_check_status,
+                                      dopr_group_pairs, dopr_store_create)
+    if name == "random":
+        rng = np.random.default_rng(0)
+        doc_len = rng.integers(-1, 9, 300).astype(np.int32)
+        doc_ids = rng.integers(-5, 310, 5000).astype(np.int32)
+    else:
+        st = workloads.make(name)
+        doc_len, doc_ids = st.doc_len, st.doc_ids
+    store = dopr_store_create(1, 8, 128, doc_len)   # payload left unfilled
+    ids = torch.from_numpy(doc_ids).cuda()
+    gd, gp, po = dopr_group_pairs(store, ids, _ws(store, len(doc_ids)))
+    rd, rp, ro = oracle.group(doc_ids, doc_len)
+    assert np.array_equal(gd.cpu().numpy(), rd)
+    assert np.array_equal(gp.cpu().numpy(), rp)
+    assert np.array_equal(po.cpu().numpy(), ro)
+    bad = ((doc_ids < 0) | (doc_ids >= len(doc_len))).any() or \
+        (doc_len[np.clip(doc_ids, 0, len(doc_len) - 1)] < 0).any()
+    want = DOPR_ERR_DOC_RANGE if bad else 0
+    assert dopr_check_status(store) == want
+    log(f"grouping {name}: {len(rd)} groups, {len(ro)} valid pairs")
+
+
+def test_gather_bit_exact():
+    import torch
+    from paper_2609_03311_amd import dopr_check_status, dopr_gather_prefix
+    st = workloads.qwen3_8b_ragged()
+    st = workloads.custom(st.doc_len, st.doc_ids[:64], st.seqlens[:64], 32,
+                          8)
+    store, k, v, doc_off = _store(st)
+    rng = np.random.default_rng(4)
+    res = st.resident_docs()
+    want = rng.choice(res, 50, replace=True).astype(np.int32)
+    lens = st.doc_len[want].astype(np.int64)
+    cu = np.zeros(len(want) + 1, np.int64)
+    np.cumsum(lens, out=cu[1:])
+    ko = torch.empty((int(cu[-1]), 8, 128), dtype=torch.bfloat16,
+                     device="cuda")
+    vo = torch.empty_like(ko)
+    dopr_gather_prefix(store, 0, torch.from_numpy(want).cuda(),
+                       torch.from_numpy(cu).cuda(), ko, vo)
+    assert dopr_check_status(store) == 0
+    idx = np.concatenate([np.arange(doc_off[d], doc_off[d] + st.doc_len[d])
+                          for d in want])
+    it = torch.from_numpy(idx).cuda()
+    assert torch.equal(ko.view(torch.int16),
+                       k.index_select(0, it).view(torch.int16))
+    assert torch.equal(vo.view(torch.int16),
+                       v.index_select(0, it).view(torch.int16))
+
+
+def test_store_put_rejects_bad_ids():
+    import torch
+    from paper_2609_03311_amd import (DOPR_ERR_DOC_RANGE, dopr_check_status,
+                                      dopr_store_put)
+    st = workloads.custom([4, -1, 6], [0], [1], 16, 8)
+    store, k, v, _ = _store(st)
+    ids = torch.tensor([1, 5, 0], dtype=torch.int32, device="cuda")
+    cu = torch.tensor([0, 4, 8, 12], dtype=torch.int64, device="cuda")
+    src = torch.zeros((12, 8, 128), dtype=torch.bfloat16, device="cuda")
+    dopr_store_put(store, 0, ids, cu, src, src)
+    assert dopr_check_status(store) == DOPR_ERR_DOC_RANGE
+
+
+@pytest.mark.parametrize("W,P,mode", [(2048, 300, "cu"), (4096, 64, "rows"),
+                                      (8, 5, "plain")])
+def test_score_head_parity(W, P, mode):
+    import torch
+    from paper_2609_03311_amd import dopr_score_logits
+    g = torch.Generator(device="cuda").manual_seed(W + P)
+    rows = 3 * P
+    h = (torch.randn((rows, W), generator=g, device="cuda") *
+         torch.rand((rows, 1), generator=g, device="cuda") * 3).to(
+        torch.bfloat16)
+    st = workloads.custom([1], [0], [1], 2, 2)
+    prm = workloads.params(st, "cuda", 77, width=W)
+    score = torch.empty(P, device="cuda")
+    logits = torch.empty((P, 2), device="cuda")
+    if mode == "cu":
+        cu = torch.arange(0, rows + 1, 3, dtype=torch.int32, device="cuda")
+        dopr_score_logits(h, prm["norm_w"], prm["w_head"], score,
+                          cu_seqlens=cu, logits=logits)
+        sel = np.arange(P) * 3 + 2
+    elif mode == "rows":
+        ri = torch.randperm(rows, generator=g, device="cuda")[:P].to(
+            torch.int32)
+        dopr_score_logits(h, prm["norm_w"], prm["w_head"], score,
+                          row_index=ri, logits=logits)
+        sel = ri.cpu().numpy()
+    else:
+        dopr_score_logits(h, prm["norm_w"], prm["w_head"], score,
+                          logits=logits, n_pairs=P)
+        sel = np.arange(P)
+    torch.cuda.synchronize()
+    hh = refs.bf16_bits_to_f64(refs.torch_bf16_to_bits(h))[sel]
+    rl, rs = oracle.score(hh, refs.torch_bf16_to_bits(prm["norm_w"]),
+                          refs.torch_bf16_to_bits(prm["w_head"]))
+    e = np.abs(score.cpu().numpy() - rs).max()
+    el = np.abs(logits.cpu().numpy() - rl).max()
+    log(f"score W={W} P={P} {mode}: max|ds|={e:.2e} max|dlogit|={el:.2e}")
+    assert e < 2e-2 and el < 2e-2
