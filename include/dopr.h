@@ -123,8 +123,12 @@ typedef struct {
   int32_t n_pairs;          /* P >= 0                                       */
   int32_t n_q_heads;        /* Hq, multiple of the store's Hkv              */
   int32_t max_tokens;       /* upper bound on every T_p (>= 1)              */
-  int32_t kernel_variant;   /* 0 = automatic; >0 selects a row-tile shape
-                               (identical results; for tuning sweeps)       */
+  int32_t kernel_variant;   /* 0 = automatic; 1..3 select a row-tile shape
+                               (identical results; for tuning sweeps);
+                               4 = exact running-max softmax for every row
+                               (slower; the reference for the fast path);
+                               5 = self-check: the fast pass queues every
+                               work unit for the exact pass (tests only)   */
   int64_t total_tokens;     /* Ntok = cu_seqlens[P]                         */
   const int32_t *doc_ids;   /* dev int32 [P]                                */
   const int32_t *cu_seqlens;/* dev int32 [P+1], cu[0] = 0, T_p >= 1         */

@@ -35,7 +35,7 @@ bool aligned16(const void *p) {
 hipStream_t as_stream(void *s) { return static_cast<hipStream_t>(s); }
 
 struct StoreLayout {
-  size_t len_off = 0, off_off = 0, payload_off = 0, total = 0;
+  size_t len_off = 0, off_off = 0, kmax_off = 0, payload_off = 0, total = 0;
   size_t payload_canonical = 0;
   int32_t max_len = 0;
 };
@@ -57,6 +57,10 @@ dopr_status_t layout_store(const dopr_store_desc_t *d, StoreLayout *lay,
   off = align_up(off + sizeof(int32_t) * (size_t)d->n_docs, kAlign);
   lay->off_off = off;
   off = align_up(off + sizeof(int64_t) * (size_t)d->n_docs, kAlign);
+  lay->kmax_off = off;
+  off = align_up(off + sizeof(float) * (size_t)d->n_docs * d->n_layers *
+                           d->n_kv_heads,
+                 kAlign);
   lay->payload_off = off;
   int64_t elems = 0;
   size_t canon = 0;
@@ -81,7 +85,7 @@ dopr_status_t layout_store(const dopr_store_desc_t *d, StoreLayout *lay,
 
 int32_t default_rows_per_item(int32_t variant) {
   (void)variant;
-  return 1024;
+  return 2048;
 }
 
 // Validation shared by the workspace query and the attention call.
@@ -101,8 +105,8 @@ dopr_status_t check_attn(const dopr_store *st, const dopr_attn_args_t *a,
   *n_rep = a->n_q_heads / st->n_kv_heads;
   if (a->total_tokens * (int64_t)(*n_rep) > INT32_MAX)
     return fail(DOPR_ERR_UNSUPPORTED, "total_tokens * n_rep must be < 2^31");
-  if (a->kernel_variant < 0 || a->kernel_variant > 2)
-    return fail(DOPR_ERR_INVALID_ARG, "kernel_variant must be 0, 1 or 2");
+  if (a->kernel_variant < 0 || a->kernel_variant > 5)
+    return fail(DOPR_ERR_INVALID_ARG, "kernel_variant must be in 0..5");
   if (!(a->softmax_scale > 0.f) || !std::isfinite(a->softmax_scale))
     return fail(DOPR_ERR_INVALID_ARG, "softmax_scale must be finite and > 0");
   if (!(a->rope_theta > 1.f) || !std::isfinite(a->rope_theta))
@@ -116,6 +120,7 @@ dopr_status_t check_attn(const dopr_store *st, const dopr_attn_args_t *a,
   shape->n_docs = st->n_docs;
   shape->total_tokens = a->total_tokens;
   shape->max_len = st->max_len;
+  shape->n_kv_heads = st->n_kv_heads;
   return DOPR_OK;
 }
 
@@ -190,6 +195,7 @@ dopr_status_t dopr_store_create(const dopr_store_desc_t *desc, void *pool,
   st->d_status = reinterpret_cast<int32_t *>(base);
   st->d_len = reinterpret_cast<int32_t *>(base + lay.len_off);
   st->d_off = reinterpret_cast<int64_t *>(base + lay.off_off);
+  st->d_kmax = reinterpret_cast<float *>(base + lay.kmax_off);
   st->d_payload = reinterpret_cast<uint16_t *>(base + lay.payload_off);
   st->max_len = lay.max_len;
   st->device = dev;
@@ -203,6 +209,11 @@ dopr_status_t dopr_store_create(const dopr_store_desc_t *desc, void *pool,
     e = hipMemcpyAsync(st->d_off, doc_off.data(),
                        sizeof(int64_t) * (size_t)desc->n_docs,
                        hipMemcpyHostToDevice, hs);
+  if (e == hipSuccess && desc->n_docs > 0)
+    e = hipMemsetAsync(st->d_kmax, 0,
+                       sizeof(float) * (size_t)desc->n_docs * desc->n_layers *
+                           desc->n_kv_heads,
+                       hs);
   if (e == hipSuccess) e = hipStreamSynchronize(hs);
   if (e != hipSuccess) {
     delete st;
@@ -335,8 +346,9 @@ dopr_status_t dopr_group_pairs(dopr_store_t st, int32_t n_pairs,
   a.cu_seqlens = nullptr;
   a.rope_theta = 1e6f;
   a.softmax_scale = 1.f;
-  PlanShape shape{n_pairs, 1, 1, default_rows_per_item(0), st->n_docs,
-                  (int64_t)n_pairs, st->max_len};
+  PlanShape shape{n_pairs,     1,          1, default_rows_per_item(0),
+                  st->n_docs,  (int64_t)n_pairs, st->max_len,
+                  st->n_kv_heads};
   const size_t need = plan_bytes(shape);
   if (workspace_bytes < need)
     return fail(DOPR_ERR_WORKSPACE, "workspace too small for grouping");

@@ -14,7 +14,8 @@
 //   3. place pairs into their document's slots, then order each group's
 //      members by pair index (stable, deterministic);
 //   4. stacked-row offsets (T_p * n_rep rows per pair, in grouped order);
-//   5. split each group's rows into work items of bounded size;
+//   5. split each group's rows into work items of bounded size, and a
+//      table from every 32-row block to the pair owning its first row;
 //   6. the rotary cos/sin table for positions 0 .. max_L + max_tokens - 1.
 #include <cmath>
 
@@ -28,7 +29,7 @@ constexpr int kScanTile = 2 * kScanThreads;
 constexpr int kThreads = 256;
 
 enum Total { kTotDocs = 0, kTotRows = 1, kTotItems = 2, kTotals = 4 };
-enum NextSlots { kNextQueues = 8 };
+enum NextSlots { kNextQueues = 16 };  // 8 XCD queues + the SAFE pass
 
 inline unsigned blocks_for(int64_t n, int t) {
   int64_t b = (n + t - 1) / t;
@@ -253,6 +254,34 @@ __global__ __launch_bounds__(kThreads) void k_items_emit(Plan pl, PlanArgs a,
   }
 }
 
+// Step 5c: owner of the first row of every 32-row block, so a row finds
+// its pair with one lookup and a short forward scan.
+__global__ __launch_bounds__(kThreads) void k_blk_pair(Plan pl,
+                                                       const int64_t *totals) {
+  const int32_t s = blockIdx.x * kThreads + threadIdx.x;
+  const int32_t n_valid = (int32_t)(totals[kTotDocs] & 0xffffffff);
+  if (s >= n_valid) return;
+  int64_t b0 = (pl.prow[s] + 31) >> 5, b1 = (pl.prow[s + 1] + 31) >> 5;
+  if (b1 > pl.blk_cap) b1 = pl.blk_cap;
+  for (int64_t b = b0; b < b1; ++b) pl.blk_pair[b] = s;
+}
+
+// Bound on the norm of every own key k^ = RoPE(RMSNorm(k) * w): an
+// RMS-normed vector has norm <= sqrt(D), the gain scales it by at most
+// max|w|, rotation keeps it, and bf16 rounding adds at most 2^-8.
+__global__ __launch_bounds__(128) void k_norm_bound(const uint16_t *kw,
+                                                    float *kown) {
+  __shared__ float red[2];
+  float a = 0.f;
+  if (kw) a = fabsf(__uint_as_float((uint32_t)kw[threadIdx.x] << 16));
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) a = fmaxf(a, __shfl_xor(a, off, 64));
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = a;
+  __syncthreads();
+  if (threadIdx.x == 0)
+    *kown = fmaxf(red[0], red[1]) * sqrtf((float)kHeadDim) * 1.01f;
+}
+
 // Step 6: rotary table, (cos, sin)(pos * theta^(-2i/D)) in double, stored
 // as float.
 __global__ __launch_bounds__(kThreads) void k_rope_table(float2 *tab,
@@ -306,6 +335,10 @@ Plan carve(void *ws, const PlanShape &s, size_t *bytes) {
   const int64_t cap = P + (rows + s.rows_per_item - 1) / s.rows_per_item + 1;
   pl.items_cap = (int32_t)cap;
   pl.items = c.take<int4>(cap);
+  pl.blk_cap = (int32_t)((rows + 31) / 32 + 1);
+  pl.blk_pair = c.take<int32_t>(pl.blk_cap);
+  pl.fix = c.take<int32_t>(cap * (s.n_kv_heads > 0 ? s.n_kv_heads : 1));
+  pl.kown = c.take<float>(1);
   pl.rope_pos = s.max_len + s.max_tokens;
   pl.rope = c.take<float2>((int64_t)pl.rope_pos * kRopeHalf);
   *bytes = c.off;
@@ -364,6 +397,10 @@ hipError_t launch_plan(const AttnCall &c, const Plan &pl,
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_items_emit, dim3(blocks_for(P, kThreads)),
                      dim3(kThreads), 0, s, pl, pa, totals);
+  hipLaunchKernelGGL(k_blk_pair, dim3(blocks_for(P, kThreads)),
+                     dim3(kThreads), 0, s, pl, totals);
+  hipLaunchKernelGGL(k_norm_bound, dim3(1), dim3(kHeadDim), 0, s,
+                     static_cast<const uint16_t *>(a->k_norm_w), pl.kown);
   const double log_theta = std::log((double)a->rope_theta);
   hipLaunchKernelGGL(k_rope_table,
                      dim3(blocks_for((int64_t)pl.rope_pos * kRopeHalf,

@@ -22,7 +22,11 @@ __host__ __device__ inline int32_t pad8(int32_t n) { return (n + 7) & ~7; }
 enum StatusSlot { kStatusFirstError = 0, kStatusWords = 64 };
 
 // Store layout inside the caller's pool:
-//   [status words | doc_len int32[n_docs] | doc_off int64[n_docs] | payload]
+//   [status words | doc_len int32[n_docs] | doc_off int64[n_docs] |
+//    kmax fp32[n_docs][n_layers][Hkv] | payload]
+// kmax holds an upper bound on the L2 norm of every stored key of a
+// document's (layer, kv head) slice (0 when L = 0); the attention kernel uses
+// it to bound logits.
 // Each resident document owns one contiguous block of the payload; for layer
 // l and kv head g the block holds
 //   K  [L][D]   at  blk + l*Hkv*D*(L+Lp) + g*L*D
@@ -32,6 +36,7 @@ enum StatusSlot { kStatusFirstError = 0, kStatusWords = 64 };
 struct StoreView {
   const int32_t *doc_len;  // [n_docs], -1 = not resident
   const int64_t *doc_off;  // [n_docs], element offset of the doc block
+  float *kmax;             // [n_docs][n_layers][Hkv] key-norm bound
   uint16_t *payload;
   int64_t n_docs;
   int32_t n_layers, n_kv_heads;
@@ -61,11 +66,12 @@ struct dopr_store {
   int32_t *d_status;
   int32_t *d_len;
   int64_t *d_off;
+  float *d_kmax;
   uint16_t *d_payload;
   int32_t max_len;  // largest L over resident documents
   int device;
   dopr::StoreView view() const {
-    return {d_len, d_off, d_payload, n_docs, n_layers, n_kv_heads};
+    return {d_len, d_off, d_kmax, d_payload, n_docs, n_layers, n_kv_heads};
   }
 };
 
@@ -79,6 +85,7 @@ enum Counter {
   kCntItems = 2,     // attention work items
   kCntInvalid = 3,   // pairs whose outputs must be zeroed
   kCntRows = 4,      // stacked rows (tokens * n_rep) of valid pairs (low)
+  kCntFix = 5,       // work units queued for the exact (SAFE) pass
   kCounters = 16
 };
 
@@ -96,9 +103,13 @@ struct Plan {
   int32_t *group_ptr;   // [P+1]
   int64_t *prow;        // [P+1] stacked-row offsets, sorted pair order
   int64_t *item_scan;   // [P+1] work items per group, scanned
+  int32_t *blk_pair;    // [blk_cap] sorted pair owning row 32*b
   int4 *items;          // [items_cap] (group, row0, row1, 0)
+  int32_t *fix;         // [items_cap * Hkv] work units for the SAFE pass
+  float *kown;          // bound on |k^| of own keys: sqrt(D) * max|w_k|
   float2 *rope;         // [rope_pos][64] (cos, sin)
   int32_t items_cap;
+  int32_t blk_cap;
   int32_t rope_pos;
   int64_t scan_blocks_cap;
 };
@@ -106,7 +117,7 @@ struct Plan {
 struct PlanShape {
   int32_t n_pairs, n_rep, max_tokens, rows_per_item;
   int64_t n_docs, total_tokens;
-  int32_t max_len;
+  int32_t max_len, n_kv_heads;
 };
 
 size_t plan_bytes(const PlanShape &s);

@@ -34,12 +34,41 @@ __global__ __launch_bounds__(kThreads) void k_store_put(
   uint16_t *K = sv.payload + k_offset(blk, L, hkv, layer, g);
   uint16_t *VT = sv.payload + vt_offset(blk, L, hkv, layer, g);
 
+  // Copy K and track the largest key norm of the slice (16 lanes per row;
+  // rows are 16-lane aligned so a row's lanes run the loop together).
+  float norm2_max = 0.f;
   for (int64_t gi = threadIdx.x; gi < (int64_t)L * 16; gi += kThreads) {
     const int64_t row = gi >> 4;
     const int c = gi & 15;
     const uint4 *src = reinterpret_cast<const uint4 *>(
         ksrc + ((s0 + row) * hkv + g) * kHeadDim);
-    reinterpret_cast<uint4 *>(K + row * kHeadDim)[c] = src[c];
+    const uint4 u = src[c];
+    reinterpret_cast<uint4 *>(K + row * kHeadDim)[c] = u;
+    const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+    float ss = 0.f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float lo = __uint_as_float(w[i] << 16);
+      const float hi = __uint_as_float(w[i] & 0xffff0000u);
+      ss = fmaf(lo, lo, ss);
+      ss = fmaf(hi, hi, ss);
+    }
+#pragma unroll
+    for (int off = 1; off < 16; off <<= 1) ss += __shfl_xor(ss, off, 64);
+    norm2_max = fmaxf(norm2_max, ss);
+  }
+  __shared__ float red[kThreads / 64];
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1)
+    norm2_max = fmaxf(norm2_max, __shfl_xor(norm2_max, off, 64));
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = norm2_max;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float m = 0.f;
+    for (int w2 = 0; w2 < kThreads / 64; ++w2) m = fmaxf(m, red[w2]);
+    // relative slack covers the fp32 rounding of the sum and the sqrt
+    sv.kmax[((int64_t)d * sv.n_layers + layer) * hkv + g] =
+        sqrtf(m) * 1.0001f;
   }
 
   __shared__ uint16_t tile[kTile][kHeadDim + 2];

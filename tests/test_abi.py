@@ -77,11 +77,13 @@ def test_store_bytes_closed_form():
         pool, payload = D.dopr_store_bytes(layers, hkv, 128, doc_len)
         assert payload == oracle.store_payload_bytes(layers, hkv, 128,
                                                      doc_len)
-        # index (12 B/doc) + payload with V rows padded to 8 slots
+        # index (12 B/doc), key-norm bounds (4 B per doc, layer and kv
+        # head) and the payload with V rows padded to 8 slots
         res = doc_len[doc_len >= 0].astype(np.int64)
         padded = ((res + 7) // 8 * 8 + res).sum() * layers * hkv * 128 * 2
-        assert pool >= padded + 12 * len(doc_len)
-        assert pool <= padded + 12 * len(doc_len) + 3 * 256 + 256
+        index = (12 + 4 * layers * hkv) * len(doc_len)
+        assert pool >= padded + index
+        assert pool <= padded + index + 4 * 256 + 256
 
 
 def test_host_validation_codes():

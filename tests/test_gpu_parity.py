@@ -65,7 +65,7 @@ SWEEP = [
 ]
 
 
-@pytest.mark.parametrize("variant", [1, 2])
+@pytest.mark.parametrize("variant", [1, 2, 3, 4])
 @pytest.mark.parametrize("i", range(len(SWEEP)))
 def test_shape_sweep(i, variant):
     Hq, Hkv, lens, P, Ts = SWEEP[i]
@@ -179,4 +179,61 @@ def test_deterministic_and_tiling_invariant():
         c.online[key].copy_(a.online[key].index_select(0, segt))
     run(c)
     assert torch.equal(c.step.out, o1.index_select(0, segt))
+    _free()
+
+
+def test_fallback_pipeline_matches_exact_mode():
+    """Self-check mode makes the fast pass queue every work unit, so the
+    exact pass recomputes all of them through the same flag -> queue ->
+    recompute path that extreme inputs take; the result must match the
+    oracle and be bitwise equal to exact mode."""
+    import torch
+    st = _structure(31, 32, 8, [256, 70, 0, 9], 14, [129, 20, 1], "self")
+    case = setup(st, seed=17, kernel_variant=5)
+    assert run(case) == 0
+    compare(case, np.arange(st.n_pairs))
+    flagged = case.step.out.clone()
+    case.step.kernel_variant = 4
+    assert run(case) == 0
+    assert torch.equal(flagged, case.step.out)
+    _free()
+
+
+def test_extreme_key_norms_take_exact_pass():
+    """Keys whose logits jump by ~10^3 after the first chunk defeat the fixed
+    softmax reference (the first chunk's max plus headroom lies far below the
+    later logits): the fast pass overflows on those rows and must hand their
+    work units to the exact pass.  Doc 0's first 32 slots are zero keys and
+    slots 32..95 are +/-1000 * k*.  With |k| ~ 1e4 the logits' absolute
+    error from bf16 operands (scale * |q^| * |k| * 2^-9 ~ 20) exceeds any
+    useful tolerance against the float64 oracle for rows with a small
+    winning margin, so doc 0 is checked against exact mode (same operands)
+    and for finiteness, and the untouched doc 1 against the oracle."""
+    import torch
+    from paper_2609_03311_amd import pipeline
+    st = workloads.custom([96, 40], [0, 1, 0], [20, 9, 5], 32, 8,
+                          name="extreme")
+    case = setup(st, seed=13)
+    k = case.k_src.float()
+    kstar = k[40].clone()                    # [Hkv, D] random directions
+    sign = torch.tensor([(-1.0) ** t for t in range(64)],
+                        device=k.device)[:, None, None]
+    k[0:32] = 0.0
+    k[32:96] = 1000.0 * sign * kstar[None]
+    case.k_src.copy_(k.to(torch.bfloat16))
+    case.store = pipeline.make_store(st.doc_len, st.n_kv_heads, case.k_src,
+                                     case.v_src)
+    case.step.store = case.store
+    assert run(case) == 0
+    fast = case.step.out.clone()
+    assert torch.isfinite(fast.float()).all()
+    case.step.kernel_variant = 4
+    assert run(case) == 0
+    exact = case.step.out.clone()
+    d = (fast.float() - exact.float()).abs().max().item()
+    log(f"extreme: fast vs exact-mode max diff {d:.3e}")
+    assert d < 2e-2
+    case.step.kernel_variant = 0
+    assert run(case) == 0
+    compare(case, np.array([1]))
     _free()
