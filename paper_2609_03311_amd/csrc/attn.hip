@@ -92,13 +92,15 @@ struct AttnParams {
   float eps, c;      // c = softmax_scale * log2(e)
 };
 
+// 160 KB: the whole LDS of a CU.  The own-key chunk is double-buffered; at
+// item boundaries (no own chunk in flight) its first words carry the work
+// index broadcast and the per-wave overflow flags.
 struct Smem {
-  uint16_t pk[PSEG * D];   // prefix K   [key][D]    (granules swizzled)
-  uint16_t pvt[D * PSEG];  // prefix V^T [d][key]    (row stride PSEG)
-  uint16_t ok[KC * D];     // own k^     [key][D]
-  uint16_t ovt[D * KC];    // own v^T    [d][key]
-  int w;
-  int bad;
+  uint16_t pk[PSEG * D];      // prefix K   [key][D]    (granules swizzled)
+  uint16_t pvt[D * PSEG];     // prefix V^T [d][key]    (row stride PSEG)
+  uint16_t ok[2][KC * D];     // own k^     [key][D]
+  uint16_t ovt[2][D * KC];    // own v^T    [d][key]
+  __device__ int *words() { return reinterpret_cast<int *>(ok[0]); }
 };
 
 __device__ __forceinline__ int perm32(int m) {
@@ -265,13 +267,13 @@ __device__ __forceinline__ void wait_vmem() {
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 }
 
-// Own-key chunk: raw k/v rows of 32 online tokens of one pair, held in
-// registers between the prefetch and the LDS stage.  Thread (kk = t / 8,
-// sub = t % 8) of the first 256 threads handles head dims 8*sub..8*sub+7 and
-// their rotate-half partners 64+8*sub..64+8*sub+7.
+// Own-key chunk: raw k/v rows and rotary factors of 32 online tokens of one
+// pair, held in registers between the prefetch and the LDS stage.  Thread
+// (kk = t / 8, sub = t % 8) of the first 256 threads handles head dims
+// 8*sub..8*sub+7 and their rotate-half partners 64+8*sub..64+8*sub+7.
 struct OwnRegs {
   uint4 k0, k1, v0, v1;
-  int pos;
+  float4 r0, r1, r2, r3;
   bool valid;
 };
 
@@ -288,20 +290,26 @@ __device__ __forceinline__ void own_load(const AttnParams &P, const OwnStep &o,
   const int kk = (threadIdx.x >> 3) & 31, sub = threadIdx.x & 7;
   const int jk = o.c0 + kk;
   r.valid = threadIdx.x < 256 && jk < o.T;
-  r.pos = L + jk;
   if (r.valid) {
     const int64_t off = ((o.tok0 + jk) * P.Hkv + g) * (int64_t)D;
     r.k0 = *reinterpret_cast<const uint4 *>(P.k + off + 8 * sub);
     r.k1 = *reinterpret_cast<const uint4 *>(P.k + off + 64 + 8 * sub);
     r.v0 = *reinterpret_cast<const uint4 *>(P.v + off + 8 * sub);
     r.v1 = *reinterpret_cast<const uint4 *>(P.v + off + 64 + 8 * sub);
+    const float4 *cq = reinterpret_cast<const float4 *>(
+        P.rope + (int64_t)(L + jk) * kRopeHalf + 8 * sub);
+    r.r0 = cq[0];
+    r.r1 = cq[1];
+    r.r2 = cq[2];
+    r.r3 = cq[3];
   }
 }
 
 // k^ = RoPE(RMSNorm(k) * w) into sm.ok; v transposed into sm.ovt.  Rows of
 // keys past the pair's end are zero.
 __device__ __forceinline__ void own_stage(const AttnParams &P,
-                                          const OwnRegs &r, Smem &sm) {
+                                          const OwnRegs &r, Smem &sm,
+                                          int buf) {
   if (threadIdx.x >= 256) return;
   const int kk = threadIdx.x >> 3, sub = threadIdx.x & 7;
   float x[16], vv[16];
@@ -325,11 +333,9 @@ __device__ __forceinline__ void own_stage(const AttnParams &P,
     float w0[8], w1[8];
     unpack8(*reinterpret_cast<const uint4 *>(P.kw + 8 * sub), w0);
     unpack8(*reinterpret_cast<const uint4 *>(P.kw + 64 + 8 * sub), w1);
-    const float4 *cq = reinterpret_cast<const float4 *>(
-        P.rope + (int64_t)r.pos * kRopeHalf + 8 * sub);
-    const float4 q0 = cq[0], q1 = cq[1], q2 = cq[2], q3 = cq[3];
-    const float cs[16] = {q0.x, q0.y, q0.z, q0.w, q1.x, q1.y, q1.z, q1.w,
-                          q2.x, q2.y, q2.z, q2.w, q3.x, q3.y, q3.z, q3.w};
+    const float cs[16] = {r.r0.x, r.r0.y, r.r0.z, r.r0.w, r.r1.x, r.r1.y,
+                          r.r1.z, r.r1.w, r.r2.x, r.r2.y, r.r2.z, r.r2.w,
+                          r.r3.x, r.r3.y, r.r3.z, r.r3.w};
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       const float a = x[e] * inv * w0[e], b = x[8 + e] * inv * w1[e];
@@ -338,16 +344,17 @@ __device__ __forceinline__ void own_stage(const AttnParams &P,
       x[8 + e] = fmaf(b, co, a * si);
     }
   }
-  *reinterpret_cast<uint4 *>(sm.ok + ok_off(kk, sub)) = as_uint4(to_bf16x8(x));
-  *reinterpret_cast<uint4 *>(sm.ok + ok_off(kk, sub + 8)) =
+  *reinterpret_cast<uint4 *>(sm.ok[buf] + ok_off(kk, sub)) =
+      as_uint4(to_bf16x8(x));
+  *reinterpret_cast<uint4 *>(sm.ok[buf] + ok_off(kk, sub + 8)) =
       as_uint4(to_bf16x8(x + 8));
   const bf16x8 v0 = to_bf16x8(vv), v1 = to_bf16x8(vv + 8);
   const int gr = kk >> 3, in = kk & 7;
+  __bf16 *ovt = reinterpret_cast<__bf16 *>(sm.ovt[buf]);
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
-    reinterpret_cast<__bf16 *>(sm.ovt)[ovt_off(8 * sub + e, gr) + in] = v0[e];
-    reinterpret_cast<__bf16 *>(sm.ovt)[ovt_off(64 + 8 * sub + e, gr) + in] =
-        v1[e];
+    ovt[ovt_off(8 * sub + e, gr) + in] = v0[e];
+    ovt[ovt_off(64 + 8 * sub + e, gr) + in] = v1[e];
   }
 }
 
@@ -369,40 +376,43 @@ __device__ __forceinline__ void attend(const uint16_t *kbase, int krow0,
                                        int key0, int lim, const RowInfo *ri,
                                        int s_cur) {
   const int krow = perm32(lq);
-  // All K fragments are read before the QK products and all V^T fragments
-  // before the softmax, so LDS latency overlaps MFMA and VALU work instead
-  // of stalling each product (the sched barriers pin this order).
-  bf16x8 kf[8];
-#pragma unroll
-  for (int s = 0; s < 8; ++s) {
-    const int gr = 2 * s + hf;
-    const int off = own_lds ? ok_off(krow, gr) : pk_off(krow0 + krow, gr);
-    kf[s] = *reinterpret_cast<const bf16x8 *>(kbase + off);
-  }
-  __builtin_amdgcn_sched_barrier(0);
+  // K fragments are read RA at a time ahead of the QK products, and the
+  // first RA V^T fragments before the softmax, so LDS latency overlaps MFMA
+  // and VALU work instead of stalling each product (the sched barriers pin
+  // the order; RA trades registers for latency hiding).
+  constexpr int RA = NQB == 2 ? 8 : 4;
   floatx16 S[NQB];
 #pragma unroll
   for (int qb = 0; qb < NQB; ++qb)
 #pragma unroll
     for (int i = 0; i < 16; ++i) S[qb][i] = 0.f;
 #pragma unroll
-  for (int s = 0; s < 8; ++s)
+  for (int s0 = 0; s0 < 8; s0 += RA) {
+    bf16x8 kf[RA];
 #pragma unroll
-    for (int qb = 0; qb < NQB; ++qb)
-      S[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[s], qf[qb][s], S[qb],
-                                                      0, 0, 0);
-  const int vrow = perm32(lq);
-  bf16x8 vf[4][2];
-#pragma unroll
-  for (int db = 0; db < 4; ++db) {
-    const int d = 32 * db + vrow;
-#pragma unroll
-    for (int t = 0; t < 2; ++t) {
-      const int gr = vt_gr0 + 2 * hf + t;
-      const int off = own_lds ? ovt_off(d, gr) : pvt_off(d, gr);
-      vf[db][t] = *reinterpret_cast<const bf16x8 *>(vt_rows + off);
+    for (int s = 0; s < RA; ++s) {
+      const int gr = 2 * (s0 + s) + hf;
+      const int off = own_lds ? ok_off(krow, gr) : pk_off(krow0 + krow, gr);
+      kf[s] = *reinterpret_cast<const bf16x8 *>(kbase + off);
     }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int s = 0; s < RA; ++s)
+#pragma unroll
+      for (int qb = 0; qb < NQB; ++qb)
+        S[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[s], qf[qb][s0 + s],
+                                                        S[qb], 0, 0, 0);
   }
+  const int vrow = perm32(lq);
+  bf16x8 vf[8];
+  auto vread = [&](int f) {  // fragment f = (db, t) = (f / 2, f % 2)
+    const int d = 32 * (f >> 1) + vrow;
+    const int gr = vt_gr0 + 2 * hf + (f & 1);
+    const int off = own_lds ? ovt_off(d, gr) : pvt_off(d, gr);
+    vf[f] = *reinterpret_cast<const bf16x8 *>(vt_rows + off);
+  };
+#pragma unroll
+  for (int f = 0; f < RA; ++f) vread(f);
   __builtin_amdgcn_sched_barrier(0);
   bf16x8 pb[NQB][2];
 #pragma unroll
@@ -467,13 +477,16 @@ __device__ __forceinline__ void attend(const uint16_t *kbase, int krow0,
     }
   }
 #pragma unroll
-  for (int db = 0; db < 4; ++db)
+  for (int f = 0; f < 8; ++f) {
+    if (f + RA < 8 && f % RA == 0) {
 #pragma unroll
-    for (int t = 0; t < 2; ++t)
+      for (int g2 = 0; g2 < RA; ++g2) vread(f + RA + g2);
+    }
 #pragma unroll
-      for (int qb = 0; qb < NQB; ++qb)
-        acc[qb].o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-            vf[db][t], pb[qb][t], acc[qb].o[db], 0, 0, 0);
+    for (int qb = 0; qb < NQB; ++qb)
+      acc[qb].o[f >> 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+          vf[f], pb[qb][f & 1], acc[qb].o[f >> 1], 0, 0, 0);
+  }
 }
 
 template <int WAVES, int NQB, bool SAFE>
@@ -495,14 +508,12 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((
   const float kown = *P.kown;
 
   for (;;) {
-    if (threadIdx.x == 0) {
-      sm.w = atomicAdd(&P.next[queue], 1);
-      sm.bad = 0;
-    }
+    if (threadIdx.x == 0) sm.words()[0] = atomicAdd(&P.next[queue], 1);
     __syncthreads();
-    int64_t w = SAFE ? (int64_t)sm.w : queue + 8 * (int64_t)sm.w;
-    __syncthreads();
+    const int slot = sm.words()[0];
+    int64_t w = SAFE ? (int64_t)slot : queue + 8 * (int64_t)slot;
     if (w >= n_work) break;
+    bool wave_bad = false;
     if (SAFE) w = P.fix[w];
     const int item = (int)(w / P.Hkv), g = (int)(w % P.Hkv);
     const int4 it = P.items[item];
@@ -581,11 +592,14 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((
                                qf, acc, lq, hf, P.c, n_full * KC, n, ri, 0);
       }
 
-      // Own causal keys, pair by pair, chunk by chunk.
+      // Own causal keys, pair by pair, chunk by chunk, double-buffered: the
+      // next chunk's raw k/v are loaded while the current one is consumed,
+      // then normed/rotated into the other buffer; one barrier per chunk.
+      __syncthreads();  // the previous pass's last own chunk is consumed
+      own_stage(P, orr, sm, 0);
+      __syncthreads();
+      int buf = 0;
       while (os.s <= s_hi) {
-        __syncthreads();
-        own_stage(P, orr, sm);
-        __syncthreads();
         // next step: next chunk of this pair, else first chunk of the next
         const int64_t srow0 = P.prow[os.s], srow1 = P.prow[os.s + 1];
         const int64_t hi_row = (srow1 < pass_end ? srow1 : pass_end) - 1;
@@ -602,14 +616,18 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((
             nx.T = P.cu[nx.pr + 1] - P.cu[nx.pr];
           }
         }
-        if (nx.s <= s_hi) own_load(P, nx, g, L, orr);
+        const bool more = nx.s <= s_hi;
+        if (more) own_load(P, nx, g, L, orr);
         bool need = false;
 #pragma unroll
         for (int qb = 0; qb < NQB; ++qb)
           need = need || (ri[qb].s == os.s && ri[qb].j >= os.c0);
         if (__any(need))  // wave-uniform: skip chunks no row of the wave sees
-          attend<2, NQB, SAFE>(sm.ok, 0, sm.ovt, true, 0, qf, acc, lq, hf,
-                               P.c, os.c0, 0, ri, os.s);
+          attend<2, NQB, SAFE>(sm.ok[buf], 0, sm.ovt[buf], true, 0, qf, acc,
+                               lq, hf, P.c, os.c0, 0, ri, os.s);
+        if (more) own_stage(P, orr, sm, buf ^ 1);
+        __syncthreads();
+        buf ^= 1;
         os = nx;
       }
 
@@ -635,12 +653,19 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((
           P.lse[ri[qb].tok * P.Hq + ri[qb].head] =
               (acc[qb].m + __log2f(lt)) * kLn2;
       }
-      if (!SAFE && (__any(bad) || P.flag_all) && lane == 0)
-        atomicOr(&sm.bad, 1);
+      wave_bad = wave_bad || __any(bad) || P.flag_all;
     }
-    __syncthreads();  // LDS is rewritten by the next item; sm.bad is final
-    if (!SAFE && threadIdx.x == 0 && sm.bad)
-      P.fix[atomicAdd(&P.counters[kCntFix], 1)] = (int32_t)w;
+    __syncthreads();  // every wave is done with this item's LDS
+    if (!SAFE) {
+      if (lane == 0) sm.words()[1 + wave] = wave_bad;
+      __syncthreads();
+      if (threadIdx.x == 0) {
+        bool any_bad = false;
+        for (int i = 0; i < WAVES; ++i) any_bad = any_bad || sm.words()[1 + i];
+        if (any_bad) P.fix[atomicAdd(&P.counters[kCntFix], 1)] = (int32_t)w;
+      }
+      __syncthreads();
+    }
   }
 }
 
