@@ -107,6 +107,23 @@ def algorithmic_work(st):
                 score_bytes=score_bytes)
 
 
+def measured_traffic(config, variant):
+    """HBM bytes per attention launch from the committed rocprofv3 counter
+    summary of this workload, or None when there is none or the kernel's
+    sources changed since the counters were taken."""
+    from paper_2609_03311_amd import profiling
+    path = os.path.join(ROOT, "profiles",
+                        f"k_prefix_attn_{config}_traffic.txt")
+    vals = profiling.read_summary(path)
+    if variant != 0 or "traffic_bytes_per_launch" not in vals:
+        return None
+    if vals.get("kernel_source_sha") != profiling.kernel_source_sha():
+        log(f"{os.path.basename(path)} describes other kernel sources; "
+            "traffic = null")
+        return None
+    return int(float(vals["traffic_bytes_per_launch"]))
+
+
 def bits(t):
     import torch
     return t.detach().cpu().contiguous().view(torch.int16).numpy().view(
@@ -185,14 +202,16 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
-                    help="first run a plain 1 GiB device copy, the "
-                         "reference for scaling HBM traffic counters")
+                    help="first run a plain streaming kernel that reads "
+                         "and writes 1 GiB, the reference for scaling HBM "
+                         "traffic counters")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py: this build runs on one GPU only; the online path "
-              "has no inter-GPU step (see DESIGN.md for how it would "
-              "shard). Run with --gpus 1.", file=sys.stderr)
+        print("bench.py measures one GPU only: the online scoring step has "
+              "no inter-GPU part (pairs would be sharded by document, each "
+              "GPU serving its own shard of the prefix store). Run with "
+              "--gpus 1.", file=sys.stderr)
         sys.exit(2)
 
     import torch
@@ -220,13 +239,14 @@ def main():
     log("inputs resident; warming up")
 
     if args.copy_calibration:
-        src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        # a plain streaming kernel (int32 bitwise NOT) that reads and writes
+        # exactly 1 GiB: the scale for the HBM traffic counters
+        src = torch.ones(1 << 28, dtype=torch.int32, device=dev)
         dst = torch.empty_like(src)
-        src.fill_(1)
         torch.cuda.synchronize()
-        dst.copy_(src)
+        torch.bitwise_not(src, out=dst)
         torch.cuda.synchronize()
-        log("calibration copy: 1 GiB read + 1 GiB written")
+        log("calibration kernel: 1 GiB read + 1 GiB written")
         del src, dst
 
     ev = HipEvents(2 * args.steps)
@@ -264,6 +284,7 @@ def main():
 
     w = algorithmic_work(st)
     achieved = w["total"] / (attn_avg * 1e-3) / 1e9
+    traffic = measured_traffic(args.config, args.variant)
     result = {
         "metric": METRIC,
         "value": round(st.n_pairs / (ms_step * 1e-3), 1),
@@ -298,7 +319,7 @@ def main():
             "peak": PEAK_HBM_GBS,
             "unit": "GB/s",
             "frac": round(achieved / PEAK_HBM_GBS, 4),
-            "traffic": None,
+            "traffic": traffic,
         },
     }
     if not args.no_cpu_baseline:

@@ -772,14 +772,15 @@ hipError_t launch_attention(const AttnCall &c, const Plan &pl,
   const bool exact = a->kernel_variant >= 4;
   p.flag_all = a->kernel_variant == 5;
   switch (a->kernel_variant) {
+    case 1:
+    case 5: e = launch_variant<4, 2, false>(p, s, 0); break;
     case 2: e = launch_variant<8, 1, false>(p, s, 0); break;
-    case 3: e = launch_variant<4, 1, false>(p, s, 0); break;
     case 4:
       hipLaunchKernelGGL(k_queue_all, dim3(256), dim3(256), 0, s, p.totals,
                          p.items_cap, p.Hkv, p.counters, p.fix);
       e = hipGetLastError();
       break;
-    default: e = launch_variant<4, 2, false>(p, s, 0); break;  // 0, 1, 5
+    default: e = launch_variant<4, 1, false>(p, s, 0); break;  // 0, 3
   }
   if (e != hipSuccess) return e;
   // Work units flagged by the fast pass (normally none) are recomputed with

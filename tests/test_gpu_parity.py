@@ -2,9 +2,11 @@
 
 Tolerance: max-abs 2e-2 on every compared element of O (bf16 output),
 the LSE, the yes/no logits and the score s (bf16 inputs, fp32 accumulation).
-Configs 1-2 are compared on every pair; configs 3-5 run at full size in the
-benchmark's launch configuration and are compared on sampled pairs (always
-including the most-reused document's group, which spans many work items).
+The tiny and Qwen3-0.6B-shaped workloads are compared on every pair; the
+Qwen3-4B- and 8B-shaped ones (uniform, ragged, and ragged with 8x prefixes)
+run at full size in the benchmark's launch configuration and are compared on
+sampled pairs (always including the most-reused document's group, which
+spans many work items).
 """
 import gc
 
