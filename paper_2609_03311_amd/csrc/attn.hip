@@ -20,7 +20,9 @@
 // buffer in 256-slot segments.  A pass gives each wave NQB x 32 rows; the
 // rows' own keys are normed/rotated cooperatively into a small LDS chunk
 // (the next chunk's raw k/v is prefetched into registers while the current
-// one is consumed) and masked per row: same pair and key <= row.
+// one is consumed) and masked per row: same pair and key <= row.  With 8
+// waves (two per SIMD) one wave's MFMA work overlaps the other's softmax
+// and memory latency; the kernel is written to fit 256 registers per lane.
 //
 // MFMA orientation (v_mfma_f32_32x32x16_bf16, A 32x16, B 16x32, C 32x32):
 //   S^T[key][q] = K[key][:] . Q^T[:][q]    A = K (LDS), B = Q^T (registers)
@@ -62,6 +64,7 @@ typedef float floatx16 __attribute__((ext_vector_type(16)));
 constexpr int D = kHeadDim;
 constexpr int KC = 32;      // keys per MFMA chunk
 constexpr int PSEG = 256;   // prefix slots resident in LDS at once
+constexpr int NCH = PSEG / KC;
 constexpr int kTotItems = 2;
 constexpr int kFixQueue = 8;  // cursor slot of the fixup pass
 constexpr float kLn2 = 0.69314718055994530942f;
@@ -71,14 +74,14 @@ constexpr float kLoOk = 0x1p-90f, kHiOk = 0x1p100f;
 
 struct AttnParams {
   const uint16_t *q, *k, *v, *qw, *kw;
-  const int32_t *cu;
   const int32_t *doc_len;
   const int64_t *doc_off;
   const float *kmax;
   const uint16_t *payload;
-  const int32_t *pair_order, *group_doc, *group_ptr, *blk_pair;
-  const int64_t *prow;
+  const int32_t *group_doc, *blk_pair;
   const int4 *items;
+  const int4 *spair;  // sorted pair: (tok0, T, first stacked row)
+  const int2 *utok;   // stacked token: (batch token, position in pair)
   const int64_t *totals;
   int32_t *next;
   int32_t *counters;
@@ -92,21 +95,24 @@ struct AttnParams {
   float eps, c;      // c = softmax_scale * log2(e)
 };
 
-// 160 KB: the whole LDS of a CU.  The own-key chunk is double-buffered; at
-// item boundaries (no own chunk in flight) its first words carry the work
-// index broadcast and the per-wave overflow flags.
+// 160 KB: the whole LDS of a CU.  Keys and values live in 32-key chunk
+// blocks of 8 KB -- K [32 keys][D] and V^T [D][32 keys], 16-byte granules
+// XOR-swizzled -- so prefix chunks and own-key chunks share one layout and
+// one set of per-lane read offsets.  The own-key chunk is double-buffered;
+// at item boundaries (no own chunk in flight) its first words carry the
+// work index broadcast and the per-wave overflow flags.
 struct Smem {
-  uint16_t pk[PSEG * D];      // prefix K   [key][D]    (granules swizzled)
-  uint16_t pvt[D * PSEG];     // prefix V^T [d][key]    (row stride PSEG)
-  uint16_t ok[2][KC * D];     // own k^     [key][D]
-  uint16_t ovt[2][D * KC];    // own v^T    [d][key]
+  uint16_t pk[NCH][KC * D];   // prefix K chunks
+  uint16_t pv[NCH][D * KC];   // prefix V^T chunks
+  uint16_t ok[2][KC * D];     // own k^
+  uint16_t ov[2][D * KC];     // own v^T
   __device__ int *words() { return reinterpret_cast<int *>(ok[0]); }
 };
 
 __device__ __forceinline__ int perm32(int m) {
   return ((m >> 2) & 1) * 16 + (m >> 3) * 4 + (m & 3);
 }
-// XOR swizzle of 16-byte granules: the 16 rows read together by a half
+// XOR swizzles of 16-byte granules: the 16 rows read together by a quarter
 // wave (perm32 of lanes 0..15 or 16..31) land on 16 distinct bank groups.
 __device__ __forceinline__ int swz(int row) {
   return (row & 3) | ((row >> 2) & 4) | ((row << 1) & 8);
@@ -114,17 +120,13 @@ __device__ __forceinline__ int swz(int row) {
 __device__ __forceinline__ int swz_v(int row) {
   return ((row >> 2) & 1) | ((row >> 3) & 2);
 }
-__device__ __forceinline__ int pk_off(int key, int gr) {
-  return key * D + ((gr ^ swz(key & 31)) << 3);
-}
-__device__ __forceinline__ int pvt_off(int d, int gr) {
-  return d * PSEG + ((gr ^ swz(d & 31)) << 3);
-}
-__device__ __forceinline__ int ok_off(int key, int gr) {
+// Element offsets inside a chunk block: K row `key` (0..31), granule gr
+// (0..15); V^T row d (0..127), granule g (0..3, keys 8g..8g+7).
+__device__ __forceinline__ int kc_off(int key, int gr) {
   return key * D + ((gr ^ swz(key)) << 3);
 }
-__device__ __forceinline__ int ovt_off(int d, int gr) {
-  return d * KC + ((gr ^ swz_v(d)) << 3);
+__device__ __forceinline__ int vc_off(int d, int g) {
+  return d * KC + ((g ^ swz_v(d)) << 3);
 }
 
 __device__ __forceinline__ void unpack8(const uint4 &u, float *f) {
@@ -149,68 +151,97 @@ __device__ __forceinline__ uint4 as_uint4(const bf16x8 &b) {
   return __builtin_bit_cast(uint4, b);
 }
 
-// Sorted pair owning stacked row r: the owner of r's 32-row block, then a
-// short forward scan.
-__device__ __forceinline__ int find_pair(const AttnParams &P, int r) {
-  int s = P.blk_pair[r >> 5];
-  while (P.prow[s + 1] <= r) ++s;
-  return s;
+// A zero the compiler cannot see through: offsetting a loop-invariant load
+// by it keeps the load (and its unpacked values) inside the loop instead of
+// hoisting them and holding the registers for the whole kernel.
+__device__ __forceinline__ int opaque_zero() {
+  int z;
+  asm volatile("s_mov_b32 %0, 0" : "=s"(z));
+  return z;
 }
 
-struct RowInfo {
-  int64_t tok;
-  int32_t s, j, head;
-  bool valid;
-};
+// Materialise a finished value here: an empty asm that "modifies" it stops
+// the compiler from sinking its computation (and the inputs it keeps alive)
+// down to the first use.
+__device__ __forceinline__ void pin(bf16x8 &x) {
+  uint4 u = __builtin_bit_cast(uint4, x);
+  asm volatile("" : "+v"(u.x), "+v"(u.y), "+v"(u.z), "+v"(u.w));
+  x = __builtin_bit_cast(bf16x8, u);
+}
+
+// acc + sum of squares of 8 packed bf16 values (products exact in fp32).
+__device__ __forceinline__ float sumsq8(const uint4 &u, float acc) {
+  const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const bf16x2 p = __builtin_bit_cast(bf16x2, w[i]);
+    acc = __builtin_amdgcn_fdot2_f32_bf16(p, p, acc, false);
+  }
+  return acc;
+}
+
+// Sorted pair owning stacked row r: the owner of r's 32-row block, then a
+// short forward scan (wave-uniform when r is).
+__device__ __forceinline__ int find_pair(const AttnParams &P, int r) {
+  int s = P.blk_pair[r >> 5];
+  while (P.spair[s + 1].z <= r) ++s;
+  return s;
+}
 
 // q^ = RoPE_pos(RMSNorm(q) * w) in the B-operand layout: lane half hf holds
 // head dims 16*s + 8*hf + e of its query column (k-step s = 0..7); the
 // rotate-half partner of dim i < 64 is dim i + 64 = k-step s + 4, same lane.
-// Returns an upper bound on |q^| after rounding to bf16.
+// Returns an upper bound on |q^| after rounding to bf16.  The raw row stays
+// packed until the norm is known; the rotation then runs one k-step pair at
+// a time (scheduling fences keep each step's gain and table loads local, so
+// the prologue needs few registers).
 __device__ __forceinline__ float q_fragments(const uint16_t *qrow,
                                              const uint16_t *w,
                                              const float2 *rope_row, int hf,
                                              float eps, bf16x8 *qf) {
-  float x[8][8];
+  uint4 raw[8];
 #pragma unroll
   for (int s = 0; s < 8; ++s)
-    unpack8(*reinterpret_cast<const uint4 *>(qrow + 16 * s + 8 * hf), x[s]);
+    raw[s] = *reinterpret_cast<const uint4 *>(qrow + 16 * s + 8 * hf);
+  // sum of squares straight from the packed pairs (v_dot2), so the
+  // unpacked row is not kept alive until the rotation
   float ss = 0.f;
 #pragma unroll
-  for (int s = 0; s < 8; ++s)
-#pragma unroll
-    for (int e = 0; e < 8; ++e) ss = fmaf(x[s][e], x[s][e], ss);
+  for (int s = 0; s < 8; ++s) ss = sumsq8(raw[s], ss);
   ss += __shfl_xor(ss, 32, 64);
   const float inv = rsqrtf(ss * (1.0f / D) + eps);
-#pragma unroll
-  for (int s = 0; s < 8; ++s) {
-    float wv[8];
-    unpack8(*reinterpret_cast<const uint4 *>(w + 16 * s + 8 * hf), wv);
-#pragma unroll
-    for (int e = 0; e < 8; ++e) x[s][e] *= inv * wv[e];
-  }
+  w += opaque_zero();
   float n2 = 0.f;
 #pragma unroll
   for (int s = 0; s < 4; ++s) {
+    __builtin_amdgcn_sched_barrier(0);
+    float x0[8], x1[8], w0[8], w1[8];
+    unpack8(raw[s], x0);
+    unpack8(raw[s + 4], x1);
+    unpack8(*reinterpret_cast<const uint4 *>(w + 16 * s + 8 * hf), w0);
+    unpack8(*reinterpret_cast<const uint4 *>(w + 16 * (s + 4) + 8 * hf), w1);
     const float4 *cs4 =
         reinterpret_cast<const float4 *>(rope_row + 16 * s + 8 * hf);
 #pragma unroll
     for (int e2 = 0; e2 < 4; ++e2) {
       const float4 t = cs4[e2];  // (cos, sin) of dims 2*e2 and 2*e2 + 1
       const int e = 2 * e2;
-      float a = x[s][e], b = x[s + 4][e];
-      x[s][e] = fmaf(a, t.x, -b * t.y);
-      x[s + 4][e] = fmaf(b, t.x, a * t.y);
+      float a = x0[e] * (inv * w0[e]), b = x1[e] * (inv * w1[e]);
+      x0[e] = fmaf(a, t.x, -b * t.y);
+      x1[e] = fmaf(b, t.x, a * t.y);
       n2 = fmaf(a, a, fmaf(b, b, n2));  // rotation preserves the norm
-      a = x[s][e + 1];
-      b = x[s + 4][e + 1];
-      x[s][e + 1] = fmaf(a, t.z, -b * t.w);
-      x[s + 4][e + 1] = fmaf(b, t.z, a * t.w);
+      a = x0[e + 1] * (inv * w0[e + 1]);
+      b = x1[e + 1] * (inv * w1[e + 1]);
+      x0[e + 1] = fmaf(a, t.z, -b * t.w);
+      x1[e + 1] = fmaf(b, t.z, a * t.w);
       n2 = fmaf(a, a, fmaf(b, b, n2));
     }
+    qf[s] = to_bf16x8(x0);
+    qf[s + 4] = to_bf16x8(x1);
+    pin(qf[s]);
+    pin(qf[s + 4]);
   }
-#pragma unroll
-  for (int s = 0; s < 8; ++s) qf[s] = to_bf16x8(x[s]);
+  __builtin_amdgcn_sched_barrier(0);
   n2 += __shfl_xor(n2, 32, 64);
   return sqrtf(n2) * 1.01f;  // bf16 rounding (2^-8) and fp32 slack
 }
@@ -219,9 +250,9 @@ __device__ __forceinline__ float q_fragments(const uint16_t *qrow,
 // global->LDS loads (no registers): lane i of a wave writes bytes
 // [16i, 16i+16) of the wave's 1 KB LDS block, so each lane fetches the
 // global granule that the swizzled layout puts in its slot.  K rows past n
-// are left stale (their logits are masked by a select).  V^T columns from
-// Lp up to the next multiple of 32 are zeroed (masked keys must multiply a
-// finite value); the store's own pad columns [L, Lp) are zero already.
+// are left stale (their logits are masked by a select).  V^T columns past
+// the stored ones (up to the chunk end) are zeroed instead: masked keys
+// must multiply a finite value.  The store's pad columns [L, Lp) are zero.
 template <int WAVES>
 __device__ __forceinline__ void stage_prefix(const uint16_t *Kp,
                                              const uint16_t *VTp, int Lp,
@@ -229,6 +260,7 @@ __device__ __forceinline__ void stage_prefix(const uint16_t *Kp,
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   // K: 1 KB block b = rows 4b..4b+3, lane -> (row, physical granule)
   const int kblocks = (n + 3) >> 2;
+  uint16_t *pk = sm.pk[0];
   for (int b = wave; b < kblocks; b += WAVES) {
     const int r = 4 * b + (lane >> 4), p = lane & 15;
     if (r < n) {
@@ -236,28 +268,24 @@ __device__ __forceinline__ void stage_prefix(const uint16_t *Kp,
       __builtin_amdgcn_global_load_lds(
           (const __attribute__((address_space(1))) void *)(
               Kp + (int64_t)(seg0 + r) * D + gr * 8),
-          (__attribute__((address_space(3))) void *)(sm.pk + b * 512), 16, 0,
-          0);
+          (__attribute__((address_space(3))) void *)(pk + b * 512), 16, 0, 0);
     }
   }
-  // V^T: 1 KB block b = rows d = 2b, 2b+1 (32 granules of 8 keys each)
+  // V^T: 1 KB block b = chunk b / 8, rows d = 16 (b % 8) .. + 15, four
+  // granules of 8 keys each
   const int lp = Lp - seg0 < PSEG ? Lp - seg0 : PSEG;  // stored columns
-  const int gl = lp >> 3;
-  for (int b = wave; b < D / 2; b += WAVES) {
-    const int d = 2 * b + (lane >> 5), p = lane & 31;
-    const int gr = p ^ swz(d & 31);
-    if (gr < gl)
+  const int vblocks = ((n + KC - 1) / KC) * 8;
+  uint16_t *pv = sm.pv[0];
+  for (int b = wave; b < vblocks; b += WAVES) {
+    const int d = 16 * (b & 7) + (lane >> 2), p = lane & 3;
+    const int key = KC * (b >> 3) + 8 * (p ^ swz_v(d));
+    if (key < lp)
       __builtin_amdgcn_global_load_lds(
           (const __attribute__((address_space(1))) void *)(
-              VTp + (int64_t)d * Lp + seg0 + 8 * gr),
-          (__attribute__((address_space(3))) void *)(sm.pvt + b * 512), 16,
-          0, 0);
-  }
-  const int gc = ((n + 31) & ~31) >> 3;  // granules through the chunk end
-  for (int e = threadIdx.x; e < D * 4; e += WAVES * 64) {
-    const int d = e >> 2, gr = gl + (e & 3);
-    if (gr < gc)
-      *reinterpret_cast<uint4 *>(sm.pvt + pvt_off(d, gr)) =
+              VTp + (int64_t)d * Lp + seg0 + key),
+          (__attribute__((address_space(3))) void *)(pv + b * 512), 16, 0, 0);
+    else
+      *reinterpret_cast<uint4 *>(pv + b * 512 + lane * 8) =
           make_uint4(0, 0, 0, 0);
   }
 }
@@ -267,94 +295,136 @@ __device__ __forceinline__ void wait_vmem() {
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 }
 
-// Own-key chunk: raw k/v rows and rotary factors of 32 online tokens of one
-// pair, held in registers between the prefetch and the LDS stage.  Thread
-// (kk = t / 8, sub = t % 8) of the first 256 threads handles head dims
-// 8*sub..8*sub+7 and their rotate-half partners 64+8*sub..64+8*sub+7.
+// One own-key chunk: 32 keys of one pair starting at key c0 (wave-uniform).
+struct OwnStep {
+  int s;     // sorted pair index
+  int c0;    // first own key of the chunk
+  int tok0;  // the pair's first batch token
+  int T;     // the pair's token count
+};
+
+// Raw k/v rows and rotary factors of one own-key chunk, held in registers
+// between the prefetch and the LDS stage.  Thread t handles key
+// kk = (t / 8) % 32, head dims 8*sub..8*sub+7 (sub = t % 8) and their
+// rotate-half partners 64+8*sub..64+8*sub+7.  With 8 waves the first 256
+// threads stage k^ and the other 256 stage v (one register set, two
+// roles); with 4 waves every thread stages both.
+template <int WAVES>
 struct OwnRegs {
-  uint4 k0, k1, v0, v1;
-  float4 r0, r1, r2, r3;
+  uint4 a0, a1;            // k (or v in the value role)
+  uint4 b0, b1;            // v when one thread has both roles (4 waves)
+  float4 r0, r1, r2, r3;   // (cos, sin) of the key's position
   bool valid;
 };
 
-struct OwnStep {
-  int s;      // sorted pair index
-  int c0;     // first own key of the chunk
-  int pr;     // pair index
-  int64_t tok0;
-  int T;
-};
+template <int WAVES>
+__device__ __forceinline__ bool key_role() {
+  return WAVES == 4 || threadIdx.x < 256;
+}
+template <int WAVES>
+__device__ __forceinline__ bool value_role() {
+  return WAVES == 4 || threadIdx.x >= 256;
+}
 
+template <int WAVES>
 __device__ __forceinline__ void own_load(const AttnParams &P, const OwnStep &o,
-                                         int g, int L, OwnRegs &r) {
-  const int kk = (threadIdx.x >> 3) & 31, sub = threadIdx.x & 7;
+                                         int g, int L, OwnRegs<WAVES> &r) {
+  // thread indices are recomputed here (opaque offset) rather than hoisted
+  // out of the kernel's loops with their derived addresses
+  const int t = threadIdx.x + opaque_zero();
+  const int kk = (t >> 3) & 31, sub = t & 7;
   const int jk = o.c0 + kk;
-  r.valid = threadIdx.x < 256 && jk < o.T;
+  r.valid = t < 256 * (WAVES / 4) && jk < o.T;
   if (r.valid) {
-    const int64_t off = ((o.tok0 + jk) * P.Hkv + g) * (int64_t)D;
-    r.k0 = *reinterpret_cast<const uint4 *>(P.k + off + 8 * sub);
-    r.k1 = *reinterpret_cast<const uint4 *>(P.k + off + 64 + 8 * sub);
-    r.v0 = *reinterpret_cast<const uint4 *>(P.v + off + 8 * sub);
-    r.v1 = *reinterpret_cast<const uint4 *>(P.v + off + 64 + 8 * sub);
-    const float4 *cq = reinterpret_cast<const float4 *>(
-        P.rope + (int64_t)(L + jk) * kRopeHalf + 8 * sub);
-    r.r0 = cq[0];
-    r.r1 = cq[1];
-    r.r2 = cq[2];
-    r.r3 = cq[3];
+    const int64_t off = ((int64_t)(o.tok0 + jk) * P.Hkv + g) * D;
+    if (key_role<WAVES>()) {
+      r.a0 = *reinterpret_cast<const uint4 *>(P.k + off + 8 * sub);
+      r.a1 = *reinterpret_cast<const uint4 *>(P.k + off + 64 + 8 * sub);
+      const float4 *cq = reinterpret_cast<const float4 *>(
+          P.rope + (int64_t)(L + jk) * kRopeHalf + 8 * sub);
+      r.r0 = cq[0];
+      r.r1 = cq[1];
+      r.r2 = cq[2];
+      r.r3 = cq[3];
+    }
+    if (WAVES == 4) {
+      r.b0 = *reinterpret_cast<const uint4 *>(P.v + off + 8 * sub);
+      r.b1 = *reinterpret_cast<const uint4 *>(P.v + off + 64 + 8 * sub);
+    } else if (value_role<WAVES>()) {
+      r.a0 = *reinterpret_cast<const uint4 *>(P.v + off + 8 * sub);
+      r.a1 = *reinterpret_cast<const uint4 *>(P.v + off + 64 + 8 * sub);
+    }
   }
 }
 
-// k^ = RoPE(RMSNorm(k) * w) into sm.ok; v transposed into sm.ovt.  Rows of
+// k^ = RoPE(RMSNorm(k) * w) into sm.ok; v transposed into sm.ov.  Rows of
 // keys past the pair's end are zero.
+template <int WAVES>
 __device__ __forceinline__ void own_stage(const AttnParams &P,
-                                          const OwnRegs &r, Smem &sm,
+                                          const OwnRegs<WAVES> &r, Smem &sm,
                                           int buf) {
-  if (threadIdx.x >= 256) return;
-  const int kk = threadIdx.x >> 3, sub = threadIdx.x & 7;
-  float x[16], vv[16];
-  if (r.valid) {
-    unpack8(r.k0, x);
-    unpack8(r.k1, x + 8);
-    unpack8(r.v0, vv);
-    unpack8(r.v1, vv + 8);
-  } else {
+  if (threadIdx.x >= 256 * (WAVES / 4)) return;
+  const int t = threadIdx.x + opaque_zero();
+  const int kk = (t >> 3) & 31, sub = t & 7;
+  if (key_role<WAVES>()) {
+    float x[16];
+    float ss = r.valid ? sumsq8(r.a1, sumsq8(r.a0, 0.f)) : 0.f;
+    if (r.valid) {
+      unpack8(r.a0, x);
+      unpack8(r.a1, x + 8);
+    } else {
 #pragma unroll
-    for (int e = 0; e < 16; ++e) x[e] = vv[e] = 0.f;
+      for (int e = 0; e < 16; ++e) x[e] = 0.f;
+    }
+    ss += __shfl_xor(ss, 1, 64);
+    ss += __shfl_xor(ss, 2, 64);
+    ss += __shfl_xor(ss, 4, 64);
+    if (r.valid) {
+      const float inv = rsqrtf(ss * (1.0f / D) + P.eps);
+      const uint16_t *kw = P.kw;
+      float w0[8], w1[8];
+      unpack8(*reinterpret_cast<const uint4 *>(kw + 8 * sub), w0);
+      unpack8(*reinterpret_cast<const uint4 *>(kw + 64 + 8 * sub), w1);
+      const float cs[16] = {r.r0.x, r.r0.y, r.r0.z, r.r0.w, r.r1.x, r.r1.y,
+                            r.r1.z, r.r1.w, r.r2.x, r.r2.y, r.r2.z, r.r2.w,
+                            r.r3.x, r.r3.y, r.r3.z, r.r3.w};
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float a = x[e] * inv * w0[e], b = x[8 + e] * inv * w1[e];
+        const float co = cs[2 * e], si = cs[2 * e + 1];
+        x[e] = fmaf(a, co, -b * si);
+        x[8 + e] = fmaf(b, co, a * si);
+      }
+    }
+    *reinterpret_cast<uint4 *>(sm.ok[buf] + kc_off(kk, sub)) =
+        as_uint4(to_bf16x8(x));
+    *reinterpret_cast<uint4 *>(sm.ok[buf] + kc_off(kk, sub + 8)) =
+        as_uint4(to_bf16x8(x + 8));
   }
-  float ss = 0.f;
+  if (value_role<WAVES>()) {
+    float vv[16];
+    const uint4 &v0 = WAVES == 4 ? r.b0 : r.a0;
+    const uint4 &v1 = WAVES == 4 ? r.b1 : r.a1;
+    if (r.valid) {
+      unpack8(v0, vv);
+      unpack8(v1, vv + 8);
+    } else {
 #pragma unroll
-  for (int e = 0; e < 16; ++e) ss = fmaf(x[e], x[e], ss);
-  ss += __shfl_xor(ss, 1, 64);
-  ss += __shfl_xor(ss, 2, 64);
-  ss += __shfl_xor(ss, 4, 64);
-  if (r.valid) {
-    const float inv = rsqrtf(ss * (1.0f / D) + P.eps);
-    float w0[8], w1[8];
-    unpack8(*reinterpret_cast<const uint4 *>(P.kw + 8 * sub), w0);
-    unpack8(*reinterpret_cast<const uint4 *>(P.kw + 64 + 8 * sub), w1);
-    const float cs[16] = {r.r0.x, r.r0.y, r.r0.z, r.r0.w, r.r1.x, r.r1.y,
-                          r.r1.z, r.r1.w, r.r2.x, r.r2.y, r.r2.z, r.r2.w,
-                          r.r3.x, r.r3.y, r.r3.z, r.r3.w};
+      for (int e = 0; e < 16; ++e) vv[e] = 0.f;
+    }
+    const bf16x8 h0 = to_bf16x8(vv), h1 = to_bf16x8(vv + 8);
+    // rows d = 8*sub + e and 64 + 8*sub + e, column kk: the swizzle of row
+    // d depends only on e >= 4 and sub, so two base addresses serve all 16
+    // stores (the rest are constant offsets)
+    const int gr = kk >> 3, in = kk & 7;
+    __bf16 *ov = reinterpret_cast<__bf16 *>(sm.ov[buf]);
+    const int b0 = vc_off(8 * sub, gr) + in, b1 = vc_off(8 * sub + 4, gr) + in;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      const float a = x[e] * inv * w0[e], b = x[8 + e] * inv * w1[e];
-      const float co = cs[2 * e], si = cs[2 * e + 1];
-      x[e] = fmaf(a, co, -b * si);
-      x[8 + e] = fmaf(b, co, a * si);
+      const int base = (e < 4 ? b0 + e * KC : b1 + (e - 4) * KC);
+      ov[base] = h0[e];
+      ov[base + 64 * KC] = h1[e];
     }
-  }
-  *reinterpret_cast<uint4 *>(sm.ok[buf] + ok_off(kk, sub)) =
-      as_uint4(to_bf16x8(x));
-  *reinterpret_cast<uint4 *>(sm.ok[buf] + ok_off(kk, sub + 8)) =
-      as_uint4(to_bf16x8(x + 8));
-  const bf16x8 v0 = to_bf16x8(vv), v1 = to_bf16x8(vv + 8);
-  const int gr = kk >> 3, in = kk & 7;
-  __bf16 *ovt = reinterpret_cast<__bf16 *>(sm.ovt[buf]);
-#pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    ovt[ovt_off(8 * sub + e, gr) + in] = v0[e];
-    ovt[ovt_off(64 + 8 * sub + e, gr) + in] = v1[e];
   }
 }
 
@@ -366,21 +436,36 @@ struct Acc {
   float m, l, mb;
 };
 
-// MODE 0: interior prefix chunk (no mask); 1: last prefix chunk (keys >=
-// lim masked); 2: own-key chunk (same pair and key <= row).
+// Per-lane element offsets of the MFMA A-operand fragments inside a chunk
+// block, the same for every chunk: K fragment s (k-step s: head dims
+// 16s + 8hf .. + 7 of key row perm32(lq)) and V^T fragment f = (db, t)
+// (head-dim row 32db + perm32(lq), keys 16hf + 8t .. + 7).  The V^T
+// offsets differ by whole rows across db, so two registers hold them.
+struct Frag {
+  int k[8], v[2];
+};
+__device__ __forceinline__ Frag frag_offsets(int lq, int hf) {
+  Frag f;
+  const int row = perm32(lq);
+#pragma unroll
+  for (int s = 0; s < 8; ++s) f.k[s] = kc_off(row, 2 * s + hf);
+  f.v[0] = vc_off(row, 2 * hf);
+  f.v[1] = vc_off(row, 2 * hf + 1);
+  return f;
+}
+
+// One 32-key chunk for NQB query blocks: S^T = K Q^T, weights, O^T += V^T P^T.
+// MODE 0: no mask; MODE 1: key index (0..31 within the chunk) must be
+// <= lim[qb] (a per-row limit, < 0 hides every key of the chunk).
 template <int MODE, int NQB, bool SAFE>
-__device__ __forceinline__ void attend(const uint16_t *kbase, int krow0,
-                                       const uint16_t *vt_rows, bool own_lds,
-                                       int vt_gr0, const bf16x8 (*qf)[8],
-                                       Acc *acc, int lq, int hf, float c,
-                                       int key0, int lim, const RowInfo *ri,
-                                       int s_cur) {
-  const int krow = perm32(lq);
-  // K fragments are read RA at a time ahead of the QK products, and the
-  // first RA V^T fragments before the softmax, so LDS latency overlaps MFMA
-  // and VALU work instead of stalling each product (the sched barriers pin
-  // the order; RA trades registers for latency hiding).
-  constexpr int RA = NQB == 2 ? 8 : 4;
+__device__ __forceinline__ void attend(const uint16_t *kblk,
+                                       const uint16_t *vblk, const Frag &fo,
+                                       const bf16x8 (*qf)[8], Acc *acc,
+                                       int hf, float c, const int *lim) {
+  // K fragments are read RA at a time ahead of the QK products, and V^T
+  // fragments RA at a time ahead of the PV products, so LDS latency
+  // overlaps MFMA and VALU work (RA trades registers for latency hiding).
+  constexpr int RA = 4;
   floatx16 S[NQB];
 #pragma unroll
   for (int qb = 0; qb < NQB; ++qb)
@@ -390,12 +475,8 @@ __device__ __forceinline__ void attend(const uint16_t *kbase, int krow0,
   for (int s0 = 0; s0 < 8; s0 += RA) {
     bf16x8 kf[RA];
 #pragma unroll
-    for (int s = 0; s < RA; ++s) {
-      const int gr = 2 * (s0 + s) + hf;
-      const int off = own_lds ? ok_off(krow, gr) : pk_off(krow0 + krow, gr);
-      kf[s] = *reinterpret_cast<const bf16x8 *>(kbase + off);
-    }
-    __builtin_amdgcn_sched_barrier(0);
+    for (int s = 0; s < RA; ++s)
+      kf[s] = *reinterpret_cast<const bf16x8 *>(kblk + fo.k[s0 + s]);
 #pragma unroll
     for (int s = 0; s < RA; ++s)
 #pragma unroll
@@ -403,28 +484,21 @@ __device__ __forceinline__ void attend(const uint16_t *kbase, int krow0,
         S[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[s], qf[qb][s0 + s],
                                                         S[qb], 0, 0, 0);
   }
-  const int vrow = perm32(lq);
-  bf16x8 vf[8];
-  auto vread = [&](int f) {  // fragment f = (db, t) = (f / 2, f % 2)
-    const int d = 32 * (f >> 1) + vrow;
-    const int gr = vt_gr0 + 2 * hf + (f & 1);
-    const int off = own_lds ? ovt_off(d, gr) : pvt_off(d, gr);
-    vf[f] = *reinterpret_cast<const bf16x8 *>(vt_rows + off);
-  };
+  bf16x8 vf[RA];
+  auto vread = [&](int f0) {  // fragments f0..f0+RA-1, f = (db, t)
 #pragma unroll
-  for (int f = 0; f < RA; ++f) vread(f);
-  __builtin_amdgcn_sched_barrier(0);
+    for (int f = f0; f < f0 + RA; ++f)
+      vf[f - f0] = *reinterpret_cast<const bf16x8 *>(
+          vblk + (f >> 1) * (32 * KC) + fo.v[f & 1]);
+  };
+  vread(0);
   bf16x8 pb[NQB][2];
 #pragma unroll
   for (int qb = 0; qb < NQB; ++qb) {
-    if (MODE != 0) {
+    if (MODE == 1) {
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int key = key0 + 16 * hf + i;
-        const bool ok = MODE == 1 ? key < lim
-                                  : (ri[qb].s == s_cur && key <= ri[qb].j);
-        S[qb][i] = ok ? S[qb][i] : -INFINITY;
-      }
+      for (int i = 0; i < 16; ++i)
+        S[qb][i] = 16 * hf + i <= lim[qb] ? S[qb][i] : -INFINITY;
     }
     Acc &A = acc[qb];
     if (SAFE) {
@@ -477,15 +551,14 @@ __device__ __forceinline__ void attend(const uint16_t *kbase, int krow0,
     }
   }
 #pragma unroll
-  for (int f = 0; f < 8; ++f) {
-    if (f + RA < 8 && f % RA == 0) {
+  for (int f0 = 0; f0 < 8; f0 += RA) {
+    if (f0 > 0) vread(f0);
 #pragma unroll
-      for (int g2 = 0; g2 < RA; ++g2) vread(f + RA + g2);
-    }
+    for (int f = f0; f < f0 + RA; ++f)
 #pragma unroll
-    for (int qb = 0; qb < NQB; ++qb)
-      acc[qb].o[f >> 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-          vf[f], pb[qb][f & 1], acc[qb].o[f >> 1], 0, 0, 0);
+      for (int qb = 0; qb < NQB; ++qb)
+        acc[qb].o[f >> 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+            vf[f - f0], pb[qb][f & 1], acc[qb].o[f >> 1], 0, 0, 0);
   }
 }
 
@@ -505,7 +578,7 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((
     if (n_items > P.items_cap) n_items = P.items_cap;
     n_work = n_items * P.Hkv;
   }
-  const float kown = *P.kown;
+  const Frag fo = frag_offsets(lq, hf);
 
   for (;;) {
     if (threadIdx.x == 0) sm.words()[0] = atomicAdd(&P.next[queue], 1);
@@ -517,40 +590,37 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((
     if (SAFE) w = P.fix[w];
     const int item = (int)(w / P.Hkv), g = (int)(w % P.Hkv);
     const int4 it = P.items[item];
-    const int group = it.x, row0 = it.y, row1 = it.z;
-    const int doc = P.group_doc[group];
+    const int row0 = it.y, row1 = it.z;
+    const int doc = P.group_doc[it.x];
     const int L = P.doc_len[doc], Lp = pad8(L);
     const int64_t blk = P.doc_off[doc];
     const uint16_t *Kp = P.payload + k_offset(blk, L, P.Hkv, P.layer, g);
     const uint16_t *VTp = P.payload + vt_offset(blk, L, P.Hkv, P.layer, g);
     const float kbound = fmaxf(
-        kown, P.kmax[((int64_t)doc * P.n_layers + P.layer) * P.Hkv + g]);
+        *P.kown, P.kmax[((int64_t)doc * P.n_layers + P.layer) * P.Hkv + g]);
     const int n_seg = (L + PSEG - 1) / PSEG;
     const bool resident = n_seg <= 1;
     if (resident && L > 0) stage_prefix<WAVES>(Kp, VTp, Lp, 0, L, sm);
 
     for (int pass0 = row0; pass0 < row1; pass0 += PASS) {
       const int pass_end = pass0 + PASS < row1 ? pass0 + PASS : row1;
-      RowInfo ri[NQB];
+      // Rows of this lane: batch token, position in the pair, q head.
+      int tokq[NQB], head[NQB];
+      bool valid[NQB];
       bf16x8 qf[NQB][8];
       Acc acc[NQB];
 #pragma unroll
       for (int qb = 0; qb < NQB; ++qb) {
         const int r = pass0 + (wave * NQB + qb) * 32 + lq;
-        ri[qb].valid = r < row1;
-        const int rc = ri[qb].valid ? r : row1 - 1;
-        const int s = find_pair(P, rc);
-        const int pr = P.pair_order[s];
-        const int rr = rc - (int)P.prow[s];
-        const int j = rr / P.n_rep, rep = rr - j * P.n_rep;
-        ri[qb].s = s;
-        ri[qb].j = j;
-        ri[qb].tok = (int64_t)P.cu[pr] + j;
-        ri[qb].head = g * P.n_rep + rep;
+        valid[qb] = r < row1;
+        const int rc = valid[qb] ? r : row1 - 1;
+        const int u = rc / P.n_rep;
+        const int2 tj = P.utok[u];
+        tokq[qb] = tj.x;
+        head[qb] = g * P.n_rep + (rc - u * P.n_rep);
         const float qn = q_fragments(
-            P.q + (ri[qb].tok * P.Hq + ri[qb].head) * D, P.qw,
-            P.rope + (int64_t)(L + j) * kRopeHalf, hf, P.eps, qf[qb]);
-        __builtin_amdgcn_sched_barrier(0);
+            P.q + ((int64_t)tokq[qb] * P.Hq + head[qb]) * D, P.qw,
+            P.rope + (int64_t)(L + tj.y) * kRopeHalf, hf, P.eps, qf[qb]);
         acc[qb].m = SAFE ? -INFINITY : INFINITY;
         acc[qb].mb = qn * kbound * P.c * 1.001f;
         acc[qb].l = 0.f;
@@ -560,16 +630,17 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((
           for (int i = 0; i < 16; ++i) acc[qb].o[db][i] = 0.f;
       }
 
-      const int s_lo = find_pair(P, pass0);
       const int s_hi = find_pair(P, pass_end - 1);
       OwnStep os;
-      os.s = s_lo;
+      os.s = find_pair(P, pass0);
       os.c0 = 0;
-      os.pr = P.pair_order[s_lo];
-      os.tok0 = P.cu[os.pr];
-      os.T = P.cu[os.pr + 1] - P.cu[os.pr];
-      OwnRegs orr;
-      if (n_seg == 0) own_load(P, os, g, L, orr);
+      {
+        const int4 sp = P.spair[os.s];
+        os.tok0 = sp.x;
+        os.T = sp.y;
+      }
+      OwnRegs<WAVES> orr;
+      if (n_seg == 0) own_load<WAVES>(P, os, g, L, orr);
 
       // Document prefix: every row sees all L slots.
       for (int sg = 0; sg < n_seg; ++sg) {
@@ -582,28 +653,32 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((
         wait_vmem();
         __syncthreads();
         // the first own chunk lands while the prefix is consumed
-        if (sg == 0) own_load(P, os, g, L, orr);
+        if (sg == 0) own_load<WAVES>(P, os, g, L, orr);
         const int n_full = n >> 5;
         for (int ck = 0; ck < n_full; ++ck)
-          attend<0, NQB, SAFE>(sm.pk, ck * KC, sm.pvt, false, ck * 4, qf, acc,
-                               lq, hf, P.c, 0, 0, ri, 0);
-        if (n & 31)
-          attend<1, NQB, SAFE>(sm.pk, n_full * KC, sm.pvt, false, n_full * 4,
-                               qf, acc, lq, hf, P.c, n_full * KC, n, ri, 0);
+          attend<0, NQB, SAFE>(sm.pk[ck], sm.pv[ck], fo, qf, acc, hf, P.c,
+                               nullptr);
+        if (n & 31) {
+          int lim[NQB];
+#pragma unroll
+          for (int qb = 0; qb < NQB; ++qb) lim[qb] = (n & 31) - 1;
+          attend<1, NQB, SAFE>(sm.pk[n_full], sm.pv[n_full], fo, qf, acc, hf,
+                               P.c, lim);
+        }
       }
 
       // Own causal keys, pair by pair, chunk by chunk, double-buffered: the
       // next chunk's raw k/v are loaded while the current one is consumed,
       // then normed/rotated into the other buffer; one barrier per chunk.
       __syncthreads();  // the previous pass's last own chunk is consumed
-      own_stage(P, orr, sm, 0);
+      own_stage<WAVES>(P, orr, sm, 0);
       __syncthreads();
       int buf = 0;
       while (os.s <= s_hi) {
         // next step: next chunk of this pair, else first chunk of the next
-        const int64_t srow0 = P.prow[os.s], srow1 = P.prow[os.s + 1];
-        const int64_t hi_row = (srow1 < pass_end ? srow1 : pass_end) - 1;
-        const int jmax = (int)((hi_row - srow0) / P.n_rep);
+        const int srow0 = P.spair[os.s].z, srow1 = P.spair[os.s + 1].z;
+        const int hi_row = (srow1 < pass_end ? srow1 : pass_end) - 1;
+        const int jmax = (hi_row - srow0) / P.n_rep;
         OwnStep nx = os;
         if (os.c0 + KC <= jmax) {
           nx.c0 = os.c0 + KC;
@@ -611,21 +686,26 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((
           nx.s = os.s + 1;
           nx.c0 = 0;
           if (nx.s <= s_hi) {
-            nx.pr = P.pair_order[nx.s];
-            nx.tok0 = P.cu[nx.pr];
-            nx.T = P.cu[nx.pr + 1] - P.cu[nx.pr];
+            const int4 sp = P.spair[nx.s];
+            nx.tok0 = sp.x;
+            nx.T = sp.y;
           }
         }
         const bool more = nx.s <= s_hi;
-        if (more) own_load(P, nx, g, L, orr);
+        if (more) own_load<WAVES>(P, nx, g, L, orr);
+        // per row: last visible key of this chunk (same pair, key <= row)
+        int lim[NQB];
         bool need = false;
 #pragma unroll
-        for (int qb = 0; qb < NQB; ++qb)
-          need = need || (ri[qb].s == os.s && ri[qb].j >= os.c0);
+        for (int qb = 0; qb < NQB; ++qb) {
+          const int jr = tokq[qb] - os.tok0;
+          lim[qb] = (unsigned)jr < (unsigned)os.T ? jr - os.c0 : -1;
+          need = need || lim[qb] >= 0;
+        }
         if (__any(need))  // wave-uniform: skip chunks no row of the wave sees
-          attend<2, NQB, SAFE>(sm.ok[buf], 0, sm.ovt[buf], true, 0, qf, acc,
-                               lq, hf, P.c, os.c0, 0, ri, os.s);
-        if (more) own_stage(P, orr, sm, buf ^ 1);
+          attend<1, NQB, SAFE>(sm.ok[buf], sm.ov[buf], fo, qf, acc, hf, P.c,
+                               lim);
+        if (more) own_stage<WAVES>(P, orr, sm, buf ^ 1);
         __syncthreads();
         buf ^= 1;
         os = nx;
@@ -636,22 +716,22 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((
 #pragma unroll
       for (int qb = 0; qb < NQB; ++qb) {
         const float lt = acc[qb].l + __shfl_xor(acc[qb].l, 32, 64);
-        if (!ri[qb].valid) continue;
+        if (!valid[qb]) continue;
         bad = bad || !(lt >= kLoOk && lt <= kHiOk);
         const float inv = 1.0f / lt;
-        uint16_t *orow = P.out + (ri[qb].tok * P.Hq + ri[qb].head) * D;
+        const int64_t orow = (int64_t)tokq[qb] * P.Hq + head[qb];
+        uint16_t *op = P.out + orow * D;
 #pragma unroll
         for (int db = 0; db < 4; ++db) {
           float o[16];
 #pragma unroll
           for (int i = 0; i < 16; ++i) o[i] = acc[qb].o[db][i] * inv;
-          uint4 *dst = reinterpret_cast<uint4 *>(orow + 32 * db + 16 * hf);
+          uint4 *dst = reinterpret_cast<uint4 *>(op + 32 * db + 16 * hf);
           dst[0] = as_uint4(to_bf16x8(o));
           dst[1] = as_uint4(to_bf16x8(o + 8));
         }
         if (P.lse && hf == 0)
-          P.lse[ri[qb].tok * P.Hq + ri[qb].head] =
-              (acc[qb].m + __log2f(lt)) * kLn2;
+          P.lse[orow] = (acc[qb].m + __log2f(lt)) * kLn2;
       }
       wave_bad = wave_bad || __any(bad) || P.flag_all;
     }
@@ -736,17 +816,15 @@ hipError_t launch_attention(const AttnCall &c, const Plan &pl,
   p.v = static_cast<const uint16_t *>(a->v);
   p.qw = static_cast<const uint16_t *>(a->q_norm_w);
   p.kw = static_cast<const uint16_t *>(a->k_norm_w);
-  p.cu = a->cu_seqlens;
   p.doc_len = st.d_len;
   p.doc_off = st.d_off;
   p.kmax = st.d_kmax;
   p.payload = st.d_payload;
-  p.pair_order = pl.pair_order;
   p.group_doc = pl.group_doc;
-  p.group_ptr = pl.group_ptr;
   p.blk_pair = pl.blk_pair;
-  p.prow = pl.prow;
   p.items = pl.items;
+  p.spair = pl.spair;
+  p.utok = pl.utok;
   p.totals = plan_totals(pl);
   p.next = plan_next(pl);
   p.counters = pl.counters;
@@ -774,13 +852,13 @@ hipError_t launch_attention(const AttnCall &c, const Plan &pl,
   switch (a->kernel_variant) {
     case 1:
     case 5: e = launch_variant<4, 2, false>(p, s, 0); break;
-    case 2: e = launch_variant<8, 1, false>(p, s, 0); break;
+    case 3: e = launch_variant<4, 1, false>(p, s, 0); break;
     case 4:
       hipLaunchKernelGGL(k_queue_all, dim3(256), dim3(256), 0, s, p.totals,
                          p.items_cap, p.Hkv, p.counters, p.fix);
       e = hipGetLastError();
       break;
-    default: e = launch_variant<4, 1, false>(p, s, 0); break;  // 0, 3
+    default: e = launch_variant<8, 1, false>(p, s, 0); break;  // 0, 2
   }
   if (e != hipSuccess) return e;
   // Work units flagged by the fast pass (normally none) are recomputed with

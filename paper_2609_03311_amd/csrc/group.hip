@@ -266,6 +266,29 @@ __global__ __launch_bounds__(kThreads) void k_blk_pair(Plan pl,
   for (int64_t b = b0; b < b1; ++b) pl.blk_pair[b] = s;
 }
 
+// Step 5d: per sorted pair (first token, token count, first stacked row),
+// with a sentinel row count after the last pair, and per stacked token u
+// (token-major: u = stacked row / n_rep) its (batch token, position in
+// pair).  One workgroup per sorted pair.
+__global__ __launch_bounds__(kThreads) void k_token_table(Plan pl, PlanArgs a,
+                                                          const int64_t *totals) {
+  const int32_t s = blockIdx.x;
+  const int32_t n_valid = (int32_t)(totals[kTotDocs] & 0xffffffff);
+  if (s > n_valid) return;
+  if (s == n_valid) {
+    if (threadIdx.x == 0)
+      pl.spair[s] = make_int4(0, 0, (int32_t)totals[kTotRows], 0);
+    return;
+  }
+  const int32_t pr = pl.pair_order[s];
+  const int32_t tok0 = a.cu[pr], T = a.cu[pr + 1] - tok0;
+  const int64_t r0 = pl.prow[s];
+  if (threadIdx.x == 0) pl.spair[s] = make_int4(tok0, T, (int32_t)r0, 0);
+  const int64_t u0 = r0 / a.n_rep;
+  for (int32_t j = threadIdx.x; j < T; j += kThreads)
+    pl.utok[u0 + j] = make_int2(tok0 + j, j);
+}
+
 // Bound on the norm of every own key k^ = RoPE(RMSNorm(k) * w): an
 // RMS-normed vector has norm <= sqrt(D), the gain scales it by at most
 // max|w|, rotation keeps it, and bf16 rounding adds at most 2^-8.
@@ -338,6 +361,8 @@ Plan carve(void *ws, const PlanShape &s, size_t *bytes) {
   pl.blk_cap = (int32_t)((rows + 31) / 32 + 1);
   pl.blk_pair = c.take<int32_t>(pl.blk_cap);
   pl.fix = c.take<int32_t>(cap * (s.n_kv_heads > 0 ? s.n_kv_heads : 1));
+  pl.spair = c.take<int4>(P + 1);
+  pl.utok = c.take<int2>(s.total_tokens);
   pl.kown = c.take<float>(1);
   pl.rope_pos = s.max_len + s.max_tokens;
   pl.rope = c.take<float2>((int64_t)pl.rope_pos * kRopeHalf);
@@ -399,6 +424,9 @@ hipError_t launch_plan(const AttnCall &c, const Plan &pl,
                      dim3(kThreads), 0, s, pl, pa, totals);
   hipLaunchKernelGGL(k_blk_pair, dim3(blocks_for(P, kThreads)),
                      dim3(kThreads), 0, s, pl, totals);
+  if (a->cu_seqlens)
+    hipLaunchKernelGGL(k_token_table, dim3((unsigned)(P + 1)),
+                       dim3(kThreads), 0, s, pl, pa, totals);
   hipLaunchKernelGGL(k_norm_bound, dim3(1), dim3(kHeadDim), 0, s,
                      static_cast<const uint16_t *>(a->k_norm_w), pl.kown);
   const double log_theta = std::log((double)a->rope_theta);

@@ -106,6 +106,8 @@ struct Plan {
   int32_t *blk_pair;    // [blk_cap] sorted pair owning row 32*b
   int4 *items;          // [items_cap] (group, row0, row1, 0)
   int32_t *fix;         // [items_cap * Hkv] work units for the SAFE pass
+  int4 *spair;          // [P+1] sorted pair: (tok0, T, first stacked row)
+  int2 *utok;           // [Ntok] stacked token: (batch token, position)
   float *kown;          // bound on |k^| of own keys: sqrt(D) * max|w_k|
   float2 *rope;         // [rope_pos][64] (cos, sin)
   int32_t items_cap;

@@ -22,7 +22,7 @@ import sys
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 KERNEL_SOURCES = ("csrc/attn.hip", "csrc/internal.hpp")
-ATTN_KERNEL = r"k_prefix_attn<4, 1, false>|k_prefix_attn<4,1,false>"
+ATTN_KERNEL = r"k_prefix_attn<8, 1, false>|k_prefix_attn<8,1,false>"
 CALIB_KERNEL = r"bitwise_not"
 CALIB_BYTES = 1 << 30
 
