@@ -34,18 +34,21 @@
 // key = 16*hf + i, d = 32*db + 16*hf + i.  With NQB = 2 every K/V fragment
 // read from LDS feeds two MFMAs.
 //
-// Softmax without a running maximum.  Every key a row can see has a known
-// norm bound (stored prefix keys: a per-slice maximum written when the store
-// is filled; own keys: an RMS-normed vector has norm <= sqrt(D), times the
-// largest gain), so by Cauchy-Schwarz the row's scaled logits are <= a bound
-// B.  The row uses the fixed reference m = min(B, first chunk's max + 80) (in
-// log2 units): exp2(s*c - m) is then never large, and the row's largest term
-// is >= 2^-80, so the normaliser l = sum exp2(...) stays in a safe range
-// without the per-chunk max reduction and accumulator rescale of the usual
-// online softmax.  A work unit in which some row ends with l outside
-// [2^-90, 2^100] (only possible for extreme key norms) is queued and
-// recomputed by a second launch of the same kernel in SAFE mode, which
-// tracks the running max exactly.
+// Softmax without a running maximum.  q^ is scaled by softmax_scale *
+// log2(e) before it is rounded to bf16, so the products are logits in log2
+// units.  Every key a row can see has a known norm bound (stored prefix
+// keys: a per-slice maximum written when the store is filled; own keys and
+// queries: an RMS-normed vector has norm <= sqrt(D), times the largest
+// gain), so by Cauchy-Schwarz every logit of a work unit lies in [-B, B].
+// When B <= 64 the weights are exp2(logit) directly: no term exceeds 2^64
+// and the largest is >= 2^-64, so the normaliser is safe with no reference
+// at all.  Otherwise a row uses the fixed reference m = min(B, its first
+// chunk's max + 80): terms stay <= 2^0 or bounded and the largest is
+// >= 2^-80, with no per-chunk max reduction or accumulator rescale.  A work
+// unit in which some row still ends with l outside [2^-90, 2^100] (only
+// possible for extreme key norms) is queued and recomputed by a second
+// launch of the same kernel in SAFE mode, which tracks the running max
+// exactly.
 #include <cmath>
 
 #include "internal.hpp"
@@ -71,6 +74,11 @@ constexpr float kLn2 = 0.69314718055994530942f;
 constexpr float kTau = 8.0f;       // SAFE mode: lazy-rescale threshold
 constexpr float kHeadroom = 80.f;  // reference <= first max + 80 (log2)
 constexpr float kLoOk = 0x1p-90f, kHiOk = 0x1p100f;
+constexpr float kNoRefBound = 64.f;  // |logit| <= 64: weights exp2(logit)
+// Fix-up list entries: work unit index, plus this bit when the unit was not
+// computed by the fast pass (its logit bound exceeds kNoRefBound); those
+// run the bounded-reference mode first, the others the exact mode.
+constexpr int32_t kFixUnscored = 1 << 30;
 
 struct AttnParams {
   const uint16_t *q, *k, *v, *qw, *kw;
@@ -188,62 +196,65 @@ __device__ __forceinline__ int find_pair(const AttnParams &P, int r) {
   return s;
 }
 
-// q^ = RoPE_pos(RMSNorm(q) * w) in the B-operand layout: lane half hf holds
-// head dims 16*s + 8*hf + e of its query column (k-step s = 0..7); the
-// rotate-half partner of dim i < 64 is dim i + 64 = k-step s + 4, same lane.
-// Returns an upper bound on |q^| after rounding to bf16.  The raw row stays
+// c * q^ with q^ = RoPE_pos(RMSNorm(q) * w), in the B-operand layout: lane
+// half hf holds head dims 16*s + 8*hf + e of its query column (k-step
+// s = 0..7); the rotate-half partner of dim i < 64 is dim i + 64 = k-step
+// s + 4, same lane.  c = softmax_scale * log2(e).  The raw row stays
 // packed until the norm is known; the rotation then runs one k-step pair at
-// a time (scheduling fences keep each step's gain and table loads local, so
-// the prologue needs few registers).
-__device__ __forceinline__ float q_fragments(const uint16_t *qrow,
-                                             const uint16_t *w,
-                                             const float2 *rope_row, int hf,
-                                             float eps, bf16x8 *qf) {
-  uint4 raw[8];
+// a time, each finished fragment pinned in place so the compiler does not
+// keep the step's inputs alive until the first product.
+__device__ __forceinline__ void q_fragments(const uint16_t *qrow,
+                                            const uint16_t *w,
+                                            const float2 *rope_row, int hf,
+                                            float eps, float c, bf16x8 *qf) {
+  // every load is issued up front (one round trip to memory): the raw row,
+  // the gains (packed) and this lane's 32 (cos, sin) pairs
+  uint4 raw[8], wr[8];
+  float4 cs[16];
 #pragma unroll
   for (int s = 0; s < 8; ++s)
     raw[s] = *reinterpret_cast<const uint4 *>(qrow + 16 * s + 8 * hf);
+  w += opaque_zero();
+#pragma unroll
+  for (int s = 0; s < 8; ++s)
+    wr[s] = *reinterpret_cast<const uint4 *>(w + 16 * s + 8 * hf);
+#pragma unroll
+  for (int s = 0; s < 4; ++s)
+#pragma unroll
+    for (int e2 = 0; e2 < 4; ++e2)
+      cs[4 * s + e2] =
+          reinterpret_cast<const float4 *>(rope_row + 16 * s + 8 * hf)[e2];
   // sum of squares straight from the packed pairs (v_dot2), so the
   // unpacked row is not kept alive until the rotation
   float ss = 0.f;
 #pragma unroll
   for (int s = 0; s < 8; ++s) ss = sumsq8(raw[s], ss);
   ss += __shfl_xor(ss, 32, 64);
-  const float inv = rsqrtf(ss * (1.0f / D) + eps);
-  w += opaque_zero();
-  float n2 = 0.f;
+  const float inv = c * rsqrtf(ss * (1.0f / D) + eps);
 #pragma unroll
   for (int s = 0; s < 4; ++s) {
-    __builtin_amdgcn_sched_barrier(0);
     float x0[8], x1[8], w0[8], w1[8];
     unpack8(raw[s], x0);
     unpack8(raw[s + 4], x1);
-    unpack8(*reinterpret_cast<const uint4 *>(w + 16 * s + 8 * hf), w0);
-    unpack8(*reinterpret_cast<const uint4 *>(w + 16 * (s + 4) + 8 * hf), w1);
-    const float4 *cs4 =
-        reinterpret_cast<const float4 *>(rope_row + 16 * s + 8 * hf);
+    unpack8(wr[s], w0);
+    unpack8(wr[s + 4], w1);
 #pragma unroll
     for (int e2 = 0; e2 < 4; ++e2) {
-      const float4 t = cs4[e2];  // (cos, sin) of dims 2*e2 and 2*e2 + 1
+      const float4 t = cs[4 * s + e2];  // (cos, sin) of dims 2e2, 2e2 + 1
       const int e = 2 * e2;
       float a = x0[e] * (inv * w0[e]), b = x1[e] * (inv * w1[e]);
       x0[e] = fmaf(a, t.x, -b * t.y);
       x1[e] = fmaf(b, t.x, a * t.y);
-      n2 = fmaf(a, a, fmaf(b, b, n2));  // rotation preserves the norm
       a = x0[e + 1] * (inv * w0[e + 1]);
       b = x1[e + 1] * (inv * w1[e + 1]);
       x0[e + 1] = fmaf(a, t.z, -b * t.w);
       x1[e + 1] = fmaf(b, t.z, a * t.w);
-      n2 = fmaf(a, a, fmaf(b, b, n2));
     }
     qf[s] = to_bf16x8(x0);
     qf[s + 4] = to_bf16x8(x1);
     pin(qf[s]);
     pin(qf[s + 4]);
   }
-  __builtin_amdgcn_sched_barrier(0);
-  n2 += __shfl_xor(n2, 32, 64);
-  return sqrtf(n2) * 1.01f;  // bf16 rounding (2^-8) and fp32 slack
 }
 
 // Stage prefix slots [seg0, seg0 + n) of kv head g into LDS with direct
@@ -428,12 +439,13 @@ __device__ __forceinline__ void own_stage(const AttnParams &P,
   }
 }
 
-// Softmax state of one query block (per lane: one query column).
-//   fast mode: m = fixed reference (+inf until the row sees a key), mb = the
-//   row's logit bound (log2 units);  SAFE mode: m = running reference.
+// Softmax state of one query block (per lane: one query column), log2
+// units.  m is the reference subtracted from the logits: 0 in mode 0; in
+// mode 1 fixed at the first visible chunk (+inf before); in mode 2 (SAFE)
+// the running maximum (-inf before).
 struct Acc {
   floatx16 o[4];
-  float m, l, mb;
+  float m, l;
 };
 
 // Per-lane element offsets of the MFMA A-operand fragments inside a chunk
@@ -457,11 +469,13 @@ __device__ __forceinline__ Frag frag_offsets(int lq, int hf) {
 // One 32-key chunk for NQB query blocks: S^T = K Q^T, weights, O^T += V^T P^T.
 // MODE 0: no mask; MODE 1: key index (0..31 within the chunk) must be
 // <= lim[qb] (a per-row limit, < 0 hides every key of the chunk).
-template <int MODE, int NQB, bool SAFE>
+// SMX 0: weights exp2(S); 1: exp2(S - m), m fixed at the first visible
+// chunk to min(B, max + 80); 2: exact running maximum.
+template <int MODE, int NQB, int SMX>
 __device__ __forceinline__ void attend(const uint16_t *kblk,
                                        const uint16_t *vblk, const Frag &fo,
                                        const bf16x8 (*qf)[8], Acc *acc,
-                                       int hf, float c, const int *lim) {
+                                       int hf, float B, const int *lim) {
   // K fragments are read RA at a time ahead of the QK products, and V^T
   // fragments RA at a time ahead of the PV products, so LDS latency
   // overlaps MFMA and VALU work (RA trades registers for latency hiding).
@@ -501,14 +515,13 @@ __device__ __forceinline__ void attend(const uint16_t *kblk,
         S[qb][i] = 16 * hf + i <= lim[qb] ? S[qb][i] : -INFINITY;
     }
     Acc &A = acc[qb];
-    if (SAFE) {
+    if (SMX == 2) {
       float mx = -INFINITY;
 #pragma unroll
       for (int i = 0; i < 16; ++i) mx = fmaxf(mx, S[qb][i]);
       mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      const float mxs = mx * c;
-      const bool need = mxs > A.m + kTau;
-      const float mnew = need ? mxs : A.m;
+      const bool need = mx > A.m + kTau;
+      const float mnew = need ? mx : A.m;
       const float alpha = need ? __builtin_amdgcn_exp2f(A.m - mnew) : 1.0f;
       A.l *= alpha;
       A.m = mnew;
@@ -518,20 +531,24 @@ __device__ __forceinline__ void attend(const uint16_t *kblk,
 #pragma unroll
           for (int i = 0; i < 16; ++i) A.o[db][i] *= alpha;
       }
-    } else if (__any(A.m == INFINITY)) {
+    } else if (SMX == 1 && __any(A.m == INFINITY)) {
       // first chunk with visible keys: fix the row's reference
       float mx = -INFINITY;
 #pragma unroll
       for (int i = 0; i < 16; ++i) mx = fmaxf(mx, S[qb][i]);
       mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      if (A.m == INFINITY && mx > -INFINITY)
-        A.m = fminf(A.mb, fmaf(mx, c, kHeadroom));
+      if (A.m == INFINITY && mx > -INFINITY) A.m = fminf(B, mx + kHeadroom);
     }
-    const float muse = A.m == -INFINITY ? 0.f : A.m;
     float p[16];
+    if (SMX == 0) {
 #pragma unroll
-    for (int i = 0; i < 16; ++i)
-      p[i] = __builtin_amdgcn_exp2f(fmaf(S[qb][i], c, -muse));
+      for (int i = 0; i < 16; ++i) p[i] = __builtin_amdgcn_exp2f(S[qb][i]);
+    } else {
+      const float muse = A.m == -INFINITY || A.m == INFINITY ? 0.f : A.m;
+#pragma unroll
+      for (int i = 0; i < 16; ++i)
+        p[i] = __builtin_amdgcn_exp2f(S[qb][i] - muse);
+    }
     pb[qb][0] = to_bf16x8(p);
     pb[qb][1] = to_bf16x8(p + 8);
     // The normaliser sums the same bf16 weights the PV product uses, two at
@@ -562,10 +579,179 @@ __device__ __forceinline__ void attend(const uint16_t *kblk,
   }
 }
 
+// The passes of one work unit (an item for one kv head) with softmax mode
+// SMX fixed, so every loop below is straight-line code over one set of
+// accumulators.  Returns whether some row of this wave left the range the
+// fast modes guarantee (the unit is then recomputed in SAFE mode).
+template <int WAVES, int NQB, int SMX>
+__device__ __forceinline__ bool run_unit(const AttnParams &P, Smem &sm,
+                                         const Frag &fo, int g, int row0,
+                                         int row1, int L, int Lp,
+                                         const uint16_t *Kp,
+                                         const uint16_t *VTp, float B) {
+  constexpr int PASS = WAVES * NQB * 32;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lq = lane & 31, hf = lane >> 5;
+  const int n_seg = (L + PSEG - 1) / PSEG;
+  const bool resident = n_seg <= 1;
+  bool wave_bad = false;
+
+  // (batch token, position) of this lane's rows, loaded one pass ahead so
+  // a pass starts with one round trip to memory (q rows, rotary factors)
+  int2 tj_next[NQB];
+#pragma unroll
+  for (int qb = 0; qb < NQB; ++qb) {
+    const int r = row0 + (wave * NQB + qb) * 32 + lq;
+    tj_next[qb] = P.utok[(r < row1 ? r : row1 - 1) / P.n_rep];
+  }
+  for (int pass0 = row0; pass0 < row1; pass0 += PASS) {
+    const int pass_end = pass0 + PASS < row1 ? pass0 + PASS : row1;
+    // Rows of this lane: batch token, position in the pair, q head.
+    int tokq[NQB], head[NQB];
+    bool valid[NQB];
+    bf16x8 qf[NQB][8];
+    Acc acc[NQB];
+    // a wave whose rows all lie past the item's end (the tail pass of an
+    // item) computes nothing; it still stages and meets the barriers
+    const bool live = pass0 + wave * NQB * 32 < row1;
+#pragma unroll
+    for (int qb = 0; qb < NQB; ++qb) {
+      const int r = pass0 + (wave * NQB + qb) * 32 + lq;
+      valid[qb] = r < row1;
+      const int rc = valid[qb] ? r : row1 - 1;
+      const int u = rc / P.n_rep;
+      const int2 tj = tj_next[qb];
+      tokq[qb] = tj.x;
+      head[qb] = g * P.n_rep + (rc - u * P.n_rep);
+      if (live)
+        q_fragments(P.q + ((int64_t)tokq[qb] * P.Hq + head[qb]) * D, P.qw,
+                    P.rope + (int64_t)(L + tj.y) * kRopeHalf, hf, P.eps,
+                    P.c, qf[qb]);
+      acc[qb].m = SMX == 2 ? -INFINITY : (SMX == 1 ? INFINITY : 0.f);
+      acc[qb].l = 0.f;
+#pragma unroll
+      for (int db = 0; db < 4; ++db)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) acc[qb].o[db][i] = 0.f;
+    }
+
+    // next pass's rows
+#pragma unroll
+    for (int qb = 0; qb < NQB; ++qb) {
+      const int r = pass0 + PASS + (wave * NQB + qb) * 32 + lq;
+      tj_next[qb] = P.utok[(r < row1 ? r : row1 - 1) / P.n_rep];
+    }
+    const int s_hi = find_pair(P, pass_end - 1);
+    OwnStep os;
+    os.s = find_pair(P, pass0);
+    os.c0 = 0;
+    {
+      const int4 sp = P.spair[os.s];
+      os.tok0 = sp.x;
+      os.T = sp.y;
+    }
+    OwnRegs<WAVES> orr;
+    if (n_seg == 0) own_load<WAVES>(P, os, g, L, orr);
+
+    // Document prefix: every row sees all L slots.
+    for (int sg = 0; sg < n_seg; ++sg) {
+      const int seg0 = sg * PSEG;
+      const int n = L - seg0 < PSEG ? L - seg0 : PSEG;
+      if (!resident) {
+        __syncthreads();
+        stage_prefix<WAVES>(Kp, VTp, Lp, seg0, n, sm);
+      }
+      wait_vmem();
+      __syncthreads();
+      // the first own chunk lands while the prefix is consumed
+      if (sg == 0) own_load<WAVES>(P, os, g, L, orr);
+      const int n_full = live ? n >> 5 : 0;
+      for (int ck = 0; ck < n_full; ++ck)
+        attend<0, NQB, SMX>(sm.pk[ck], sm.pv[ck], fo, qf, acc, hf, B,
+                            nullptr);
+      if (live && (n & 31)) {
+        int lim[NQB];
+#pragma unroll
+        for (int qb = 0; qb < NQB; ++qb) lim[qb] = (n & 31) - 1;
+        attend<1, NQB, SMX>(sm.pk[n_full], sm.pv[n_full], fo, qf, acc, hf,
+                            B, lim);
+      }
+    }
+
+    // Own causal keys, pair by pair, chunk by chunk, double-buffered: the
+    // next chunk's raw k/v are loaded while the current one is consumed,
+    // then normed/rotated into the other buffer; one barrier per chunk.
+    __syncthreads();  // the previous pass's last own chunk is consumed
+    own_stage<WAVES>(P, orr, sm, 0);
+    __syncthreads();
+    int buf = 0;
+    while (os.s <= s_hi) {
+      // next step: next chunk of this pair, else first chunk of the next
+      const int srow0 = P.spair[os.s].z, srow1 = P.spair[os.s + 1].z;
+      const int hi_row = (srow1 < pass_end ? srow1 : pass_end) - 1;
+      const int jmax = (hi_row - srow0) / P.n_rep;
+      OwnStep nx = os;
+      if (os.c0 + KC <= jmax) {
+        nx.c0 = os.c0 + KC;
+      } else {
+        nx.s = os.s + 1;
+        nx.c0 = 0;
+        if (nx.s <= s_hi) {
+          const int4 sp = P.spair[nx.s];
+          nx.tok0 = sp.x;
+          nx.T = sp.y;
+        }
+      }
+      const bool more = nx.s <= s_hi;
+      if (more) own_load<WAVES>(P, nx, g, L, orr);
+      // per row: last visible key of this chunk (same pair, key <= row)
+      int lim[NQB];
+      bool need = false;
+#pragma unroll
+      for (int qb = 0; qb < NQB; ++qb) {
+        const int jr = tokq[qb] - os.tok0;
+        lim[qb] = (unsigned)jr < (unsigned)os.T ? jr - os.c0 : -1;
+        need = need || (valid[qb] && lim[qb] >= 0);
+      }
+      if (__any(need))  // wave-uniform: skip chunks no row of the wave sees
+        attend<1, NQB, SMX>(sm.ok[buf], sm.ov[buf], fo, qf, acc, hf, B,
+                            lim);
+      if (more) own_stage<WAVES>(P, orr, sm, buf ^ 1);
+      __syncthreads();
+      buf ^= 1;
+      os = nx;
+    }
+
+    // Normalise; write O (bf16) and the natural-log LSE.
+    bool bad = false;
+#pragma unroll
+    for (int qb = 0; qb < NQB; ++qb) {
+      const float lt = acc[qb].l + __shfl_xor(acc[qb].l, 32, 64);
+      if (!valid[qb]) continue;
+      bad = bad || !(lt >= kLoOk && lt <= kHiOk);
+      const float inv = 1.0f / lt;
+      const int64_t orow = (int64_t)tokq[qb] * P.Hq + head[qb];
+      uint16_t *op = P.out + orow * D;
+#pragma unroll
+      for (int db = 0; db < 4; ++db) {
+        float o[16];
+#pragma unroll
+        for (int i = 0; i < 16; ++i) o[i] = acc[qb].o[db][i] * inv;
+        uint4 *dst = reinterpret_cast<uint4 *>(op + 32 * db + 16 * hf);
+        dst[0] = as_uint4(to_bf16x8(o));
+        dst[1] = as_uint4(to_bf16x8(o + 8));
+      }
+      if (P.lse && hf == 0)
+        P.lse[orow] = (acc[qb].m + __log2f(lt)) * kLn2;
+    }
+    wave_bad = wave_bad || __any(bad);
+  }
+  return wave_bad;
+}
+
 template <int WAVES, int NQB, bool SAFE>
 __global__ __launch_bounds__(WAVES * 64) __attribute__((
     amdgpu_waves_per_eu(WAVES / 4, WAVES / 4))) void k_prefix_attn(AttnParams P) {
-  constexpr int PASS = WAVES * NQB * 32;
   __shared__ __attribute__((aligned(16))) Smem sm;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int lq = lane & 31, hf = lane >> 5;
@@ -587,7 +773,12 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((
     int64_t w = SAFE ? (int64_t)slot : queue + 8 * (int64_t)slot;
     if (w >= n_work) break;
     bool wave_bad = false;
-    if (SAFE) w = P.fix[w];
+    bool unscored = false;
+    if (SAFE) {
+      w = P.fix[w];
+      unscored = (w & kFixUnscored) != 0;
+      w &= ~(int64_t)kFixUnscored;
+    }
     const int item = (int)(w / P.Hkv), g = (int)(w % P.Hkv);
     const int4 it = P.items[item];
     const int row0 = it.y, row1 = it.z;
@@ -596,155 +787,47 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((
     const int64_t blk = P.doc_off[doc];
     const uint16_t *Kp = P.payload + k_offset(blk, L, P.Hkv, P.layer, g);
     const uint16_t *VTp = P.payload + vt_offset(blk, L, P.Hkv, P.layer, g);
+    // every logit of this unit lies in [-B, B] (log2 units)
     const float kbound = fmaxf(
-        *P.kown, P.kmax[((int64_t)doc * P.n_layers + P.layer) * P.Hkv + g]);
+        P.kown[0], P.kmax[((int64_t)doc * P.n_layers + P.layer) * P.Hkv + g]);
+    const float B = P.c * P.kown[1] * kbound * 1.001f;
     const int n_seg = (L + PSEG - 1) / PSEG;
     const bool resident = n_seg <= 1;
-    if (resident && L > 0) stage_prefix<WAVES>(Kp, VTp, Lp, 0, L, sm);
-
-    for (int pass0 = row0; pass0 < row1; pass0 += PASS) {
-      const int pass_end = pass0 + PASS < row1 ? pass0 + PASS : row1;
-      // Rows of this lane: batch token, position in the pair, q head.
-      int tokq[NQB], head[NQB];
-      bool valid[NQB];
-      bf16x8 qf[NQB][8];
-      Acc acc[NQB];
-#pragma unroll
-      for (int qb = 0; qb < NQB; ++qb) {
-        const int r = pass0 + (wave * NQB + qb) * 32 + lq;
-        valid[qb] = r < row1;
-        const int rc = valid[qb] ? r : row1 - 1;
-        const int u = rc / P.n_rep;
-        const int2 tj = P.utok[u];
-        tokq[qb] = tj.x;
-        head[qb] = g * P.n_rep + (rc - u * P.n_rep);
-        const float qn = q_fragments(
-            P.q + ((int64_t)tokq[qb] * P.Hq + head[qb]) * D, P.qw,
-            P.rope + (int64_t)(L + tj.y) * kRopeHalf, hf, P.eps, qf[qb]);
-        acc[qb].m = SAFE ? -INFINITY : INFINITY;
-        acc[qb].mb = qn * kbound * P.c * 1.001f;
-        acc[qb].l = 0.f;
-#pragma unroll
-        for (int db = 0; db < 4; ++db)
-#pragma unroll
-          for (int i = 0; i < 16; ++i) acc[qb].o[db][i] = 0.f;
-      }
-
-      const int s_hi = find_pair(P, pass_end - 1);
-      OwnStep os;
-      os.s = find_pair(P, pass0);
-      os.c0 = 0;
-      {
-        const int4 sp = P.spair[os.s];
-        os.tok0 = sp.x;
-        os.T = sp.y;
-      }
-      OwnRegs<WAVES> orr;
-      if (n_seg == 0) own_load<WAVES>(P, os, g, L, orr);
-
-      // Document prefix: every row sees all L slots.
-      for (int sg = 0; sg < n_seg; ++sg) {
-        const int seg0 = sg * PSEG;
-        const int n = L - seg0 < PSEG ? L - seg0 : PSEG;
-        if (!resident) {
-          __syncthreads();
-          stage_prefix<WAVES>(Kp, VTp, Lp, seg0, n, sm);
-        }
-        wait_vmem();
-        __syncthreads();
-        // the first own chunk lands while the prefix is consumed
-        if (sg == 0) own_load<WAVES>(P, os, g, L, orr);
-        const int n_full = n >> 5;
-        for (int ck = 0; ck < n_full; ++ck)
-          attend<0, NQB, SAFE>(sm.pk[ck], sm.pv[ck], fo, qf, acc, hf, P.c,
-                               nullptr);
-        if (n & 31) {
-          int lim[NQB];
-#pragma unroll
-          for (int qb = 0; qb < NQB; ++qb) lim[qb] = (n & 31) - 1;
-          attend<1, NQB, SAFE>(sm.pk[n_full], sm.pv[n_full], fo, qf, acc, hf,
-                               P.c, lim);
-        }
-      }
-
-      // Own causal keys, pair by pair, chunk by chunk, double-buffered: the
-      // next chunk's raw k/v are loaded while the current one is consumed,
-      // then normed/rotated into the other buffer; one barrier per chunk.
-      __syncthreads();  // the previous pass's last own chunk is consumed
-      own_stage<WAVES>(P, orr, sm, 0);
-      __syncthreads();
-      int buf = 0;
-      while (os.s <= s_hi) {
-        // next step: next chunk of this pair, else first chunk of the next
-        const int srow0 = P.spair[os.s].z, srow1 = P.spair[os.s + 1].z;
-        const int hi_row = (srow1 < pass_end ? srow1 : pass_end) - 1;
-        const int jmax = (hi_row - srow0) / P.n_rep;
-        OwnStep nx = os;
-        if (os.c0 + KC <= jmax) {
-          nx.c0 = os.c0 + KC;
-        } else {
-          nx.s = os.s + 1;
-          nx.c0 = 0;
-          if (nx.s <= s_hi) {
-            const int4 sp = P.spair[nx.s];
-            nx.tok0 = sp.x;
-            nx.T = sp.y;
-          }
-        }
-        const bool more = nx.s <= s_hi;
-        if (more) own_load<WAVES>(P, nx, g, L, orr);
-        // per row: last visible key of this chunk (same pair, key <= row)
-        int lim[NQB];
-        bool need = false;
-#pragma unroll
-        for (int qb = 0; qb < NQB; ++qb) {
-          const int jr = tokq[qb] - os.tok0;
-          lim[qb] = (unsigned)jr < (unsigned)os.T ? jr - os.c0 : -1;
-          need = need || lim[qb] >= 0;
-        }
-        if (__any(need))  // wave-uniform: skip chunks no row of the wave sees
-          attend<1, NQB, SAFE>(sm.ok[buf], sm.ov[buf], fo, qf, acc, hf, P.c,
-                               lim);
-        if (more) own_stage<WAVES>(P, orr, sm, buf ^ 1);
-        __syncthreads();
-        buf ^= 1;
-        os = nx;
-      }
-
-      // Normalise; write O (bf16) and the natural-log LSE.
-      bool bad = false;
-#pragma unroll
-      for (int qb = 0; qb < NQB; ++qb) {
-        const float lt = acc[qb].l + __shfl_xor(acc[qb].l, 32, 64);
-        if (!valid[qb]) continue;
-        bad = bad || !(lt >= kLoOk && lt <= kHiOk);
-        const float inv = 1.0f / lt;
-        const int64_t orow = (int64_t)tokq[qb] * P.Hq + head[qb];
-        uint16_t *op = P.out + orow * D;
-#pragma unroll
-        for (int db = 0; db < 4; ++db) {
-          float o[16];
-#pragma unroll
-          for (int i = 0; i < 16; ++i) o[i] = acc[qb].o[db][i] * inv;
-          uint4 *dst = reinterpret_cast<uint4 *>(op + 32 * db + 16 * hf);
-          dst[0] = as_uint4(to_bf16x8(o));
-          dst[1] = as_uint4(to_bf16x8(o + 8));
-        }
-        if (P.lse && hf == 0)
-          P.lse[orow] = (acc[qb].m + __log2f(lt)) * kLn2;
-      }
-      wave_bad = wave_bad || __any(bad) || P.flag_all;
-    }
-    __syncthreads();  // every wave is done with this item's LDS
     if (!SAFE) {
+      if (B <= kNoRefBound) {
+        if (resident && L > 0) stage_prefix<WAVES>(Kp, VTp, Lp, 0, L, sm);
+        wave_bad = run_unit<WAVES, NQB, 0>(P, sm, fo, g, row0, row1, L, Lp,
+                                           Kp, VTp, B) ||
+                   P.flag_all;
+      }
+      __syncthreads();  // every wave is done with this item's LDS
       if (lane == 0) sm.words()[1 + wave] = wave_bad;
       __syncthreads();
       if (threadIdx.x == 0) {
         bool any_bad = false;
         for (int i = 0; i < WAVES; ++i) any_bad = any_bad || sm.words()[1 + i];
-        if (any_bad) P.fix[atomicAdd(&P.counters[kCntFix], 1)] = (int32_t)w;
+        if (B > kNoRefBound)
+          P.fix[atomicAdd(&P.counters[kCntFix], 1)] = (int32_t)w | kFixUnscored;
+        else if (any_bad)
+          P.fix[atomicAdd(&P.counters[kCntFix], 1)] = (int32_t)w;
       }
       __syncthreads();
+    } else {
+      if (resident && L > 0) stage_prefix<WAVES>(Kp, VTp, Lp, 0, L, sm);
+      // (self-check mode sends every unit to the exact mode)
+      bool exact = !unscored || P.flag_all;
+      if (!exact) {
+        wave_bad = run_unit<WAVES, NQB, 1>(P, sm, fo, g, row0, row1, L, Lp,
+                                           Kp, VTp, B);
+        __syncthreads();
+        if (lane == 0) sm.words()[1 + wave] = wave_bad;
+        __syncthreads();
+        for (int i = 0; i < WAVES; ++i) exact = exact || sm.words()[1 + i];
+        __syncthreads();
+      }
+      if (exact)
+        run_unit<WAVES, NQB, 2>(P, sm, fo, g, row0, row1, L, Lp, Kp, VTp, B);
+      __syncthreads();  // every wave is done with this item's LDS
     }
   }
 }
@@ -847,7 +930,6 @@ hipError_t launch_attention(const AttnCall &c, const Plan &pl,
     e = hipEventRecord(static_cast<hipEvent_t>(a->timing_begin), s);
     if (e != hipSuccess) return e;
   }
-  const bool exact = a->kernel_variant >= 4;
   p.flag_all = a->kernel_variant == 5;
   switch (a->kernel_variant) {
     case 1:
@@ -861,9 +943,9 @@ hipError_t launch_attention(const AttnCall &c, const Plan &pl,
     default: e = launch_variant<8, 1, false>(p, s, 0); break;  // 0, 2
   }
   if (e != hipSuccess) return e;
-  // Work units flagged by the fast pass (normally none) are recomputed with
-  // the exact running maximum; in exact mode that is every unit.
-  e = launch_variant<4, 1, true>(p, s, exact ? 0 : 64);
+  // Work units the fast pass flagged or left unscored (normally none) are
+  // computed here; in exact mode that is every unit.
+  e = launch_variant<4, 1, true>(p, s, 0);
   if (e != hipSuccess) return e;
   if (a->timing_end) {
     e = hipEventRecord(static_cast<hipEvent_t>(a->timing_end), s);

@@ -289,20 +289,30 @@ __global__ __launch_bounds__(kThreads) void k_token_table(Plan pl, PlanArgs a,
     pl.utok[u0 + j] = make_int2(tok0 + j, j);
 }
 
-// Bound on the norm of every own key k^ = RoPE(RMSNorm(k) * w): an
-// RMS-normed vector has norm <= sqrt(D), the gain scales it by at most
-// max|w|, rotation keeps it, and bf16 rounding adds at most 2^-8.
+// Bounds on the norms of every own key k^ and every query q^, each of the
+// form RoPE(RMSNorm(x) * w): an RMS-normed vector has norm <= sqrt(D), the
+// gain scales it by at most max|w|, rotation keeps it, and bf16 rounding
+// adds at most 2^-8.  bound[0] is for keys (w_k), bound[1] for queries.
 __global__ __launch_bounds__(128) void k_norm_bound(const uint16_t *kw,
-                                                    float *kown) {
-  __shared__ float red[2];
-  float a = 0.f;
+                                                    const uint16_t *qw,
+                                                    float *bound) {
+  __shared__ float red[2][2];
+  float a = 0.f, b = 0.f;
   if (kw) a = fabsf(__uint_as_float((uint32_t)kw[threadIdx.x] << 16));
+  if (qw) b = fabsf(__uint_as_float((uint32_t)qw[threadIdx.x] << 16));
 #pragma unroll
-  for (int off = 32; off > 0; off >>= 1) a = fmaxf(a, __shfl_xor(a, off, 64));
-  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = a;
+  for (int off = 32; off > 0; off >>= 1) {
+    a = fmaxf(a, __shfl_xor(a, off, 64));
+    b = fmaxf(b, __shfl_xor(b, off, 64));
+  }
+  if ((threadIdx.x & 63) == 0) {
+    red[0][threadIdx.x >> 6] = a;
+    red[1][threadIdx.x >> 6] = b;
+  }
   __syncthreads();
-  if (threadIdx.x == 0)
-    *kown = fmaxf(red[0], red[1]) * sqrtf((float)kHeadDim) * 1.01f;
+  if (threadIdx.x < 2)
+    bound[threadIdx.x] = fmaxf(red[threadIdx.x][0], red[threadIdx.x][1]) *
+                         sqrtf((float)kHeadDim) * 1.01f;
 }
 
 // Step 6: rotary table, (cos, sin)(pos * theta^(-2i/D)) in double, stored
@@ -363,7 +373,7 @@ Plan carve(void *ws, const PlanShape &s, size_t *bytes) {
   pl.fix = c.take<int32_t>(cap * (s.n_kv_heads > 0 ? s.n_kv_heads : 1));
   pl.spair = c.take<int4>(P + 1);
   pl.utok = c.take<int2>(s.total_tokens);
-  pl.kown = c.take<float>(1);
+  pl.kown = c.take<float>(2);
   pl.rope_pos = s.max_len + s.max_tokens;
   pl.rope = c.take<float2>((int64_t)pl.rope_pos * kRopeHalf);
   *bytes = c.off;
@@ -428,7 +438,8 @@ hipError_t launch_plan(const AttnCall &c, const Plan &pl,
     hipLaunchKernelGGL(k_token_table, dim3((unsigned)(P + 1)),
                        dim3(kThreads), 0, s, pl, pa, totals);
   hipLaunchKernelGGL(k_norm_bound, dim3(1), dim3(kHeadDim), 0, s,
-                     static_cast<const uint16_t *>(a->k_norm_w), pl.kown);
+                     static_cast<const uint16_t *>(a->k_norm_w),
+                     static_cast<const uint16_t *>(a->q_norm_w), pl.kown);
   const double log_theta = std::log((double)a->rope_theta);
   hipLaunchKernelGGL(k_rope_table,
                      dim3(blocks_for((int64_t)pl.rope_pos * kRopeHalf,

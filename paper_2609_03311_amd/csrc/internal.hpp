@@ -108,7 +108,7 @@ struct Plan {
   int32_t *fix;         // [items_cap * Hkv] work units for the SAFE pass
   int4 *spair;          // [P+1] sorted pair: (tok0, T, first stacked row)
   int2 *utok;           // [Ntok] stacked token: (batch token, position)
-  float *kown;          // bound on |k^| of own keys: sqrt(D) * max|w_k|
+  float *kown;          // [2] bounds on |k^| (own keys) and |q^|: sqrt(D) max|w|
   float2 *rope;         // [rope_pos][64] (cos, sin)
   int32_t items_cap;
   int32_t blk_cap;
