@@ -413,28 +413,26 @@ __device__ __forceinline__ void own_stage(const AttnParams &P,
         as_uint4(to_bf16x8(x + 8));
   }
   if (value_role<WAVES>()) {
-    float vv[16];
+    // a pure transpose: the bf16 halves are stored as they are (keys past
+    // the pair's end are written as zeros)
     const uint4 &v0 = WAVES == 4 ? r.b0 : r.a0;
     const uint4 &v1 = WAVES == 4 ? r.b1 : r.a1;
-    if (r.valid) {
-      unpack8(v0, vv);
-      unpack8(v1, vv + 8);
-    } else {
-#pragma unroll
-      for (int e = 0; e < 16; ++e) vv[e] = 0.f;
-    }
-    const bf16x8 h0 = to_bf16x8(vv), h1 = to_bf16x8(vv + 8);
+    const uint32_t h[8] = {r.valid ? v0.x : 0u, r.valid ? v0.y : 0u,
+                           r.valid ? v0.z : 0u, r.valid ? v0.w : 0u,
+                           r.valid ? v1.x : 0u, r.valid ? v1.y : 0u,
+                           r.valid ? v1.z : 0u, r.valid ? v1.w : 0u};
     // rows d = 8*sub + e and 64 + 8*sub + e, column kk: the swizzle of row
     // d depends only on e >= 4 and sub, so two base addresses serve all 16
     // stores (the rest are constant offsets)
     const int gr = kk >> 3, in = kk & 7;
-    __bf16 *ov = reinterpret_cast<__bf16 *>(sm.ov[buf]);
+    uint16_t *ov = sm.ov[buf];
     const int b0 = vc_off(8 * sub, gr) + in, b1 = vc_off(8 * sub + 4, gr) + in;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       const int base = (e < 4 ? b0 + e * KC : b1 + (e - 4) * KC);
-      ov[base] = h0[e];
-      ov[base + 64 * KC] = h1[e];
+      const uint32_t lo = h[e >> 1], hi = h[4 + (e >> 1)];
+      ov[base] = (uint16_t)((e & 1) ? lo >> 16 : lo);
+      ov[base + 64 * KC] = (uint16_t)((e & 1) ? hi >> 16 : hi);
     }
   }
 }
