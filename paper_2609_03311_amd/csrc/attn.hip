@@ -684,10 +684,12 @@ __device__ __forceinline__ bool run_unit(const AttnParams &P, Smem &sm,
     __syncthreads();
     int buf = 0;
     while (os.s <= s_hi) {
-      // next step: next chunk of this pair, else first chunk of the next
-      const int srow0 = P.spair[os.s].z, srow1 = P.spair[os.s + 1].z;
-      const int hi_row = (srow1 < pass_end ? srow1 : pass_end) - 1;
-      const int jmax = (hi_row - srow0) / P.n_rep;
+      // next step: next chunk of this pair, else first chunk of the next.
+      // Positions are stacked in descending order, so the pass's latest
+      // position of this pair is at its first row in the pass.
+      const int srow0 = P.spair[os.s].z;
+      const int lo_row = srow0 > pass0 ? srow0 : pass0;
+      const int jmax = os.T - 1 - (lo_row - srow0) / P.n_rep;
       OwnStep nx = os;
       if (os.c0 + KC <= jmax) {
         nx.c0 = os.c0 + KC;

@@ -269,7 +269,8 @@ __global__ __launch_bounds__(kThreads) void k_blk_pair(Plan pl,
 // Step 5d: per sorted pair (first token, token count, first stacked row),
 // with a sentinel row count after the last pair, and per stacked token u
 // (token-major: u = stacked row / n_rep) its (batch token, position in
-// pair).  One workgroup per sorted pair.
+// pair), positions descending within a pair.  One workgroup per sorted
+// pair.
 __global__ __launch_bounds__(kThreads) void k_token_table(Plan pl, PlanArgs a,
                                                           const int64_t *totals) {
   const int32_t s = blockIdx.x;
@@ -284,9 +285,12 @@ __global__ __launch_bounds__(kThreads) void k_token_table(Plan pl, PlanArgs a,
   const int32_t tok0 = a.cu[pr], T = a.cu[pr + 1] - tok0;
   const int64_t r0 = pl.prow[s];
   if (threadIdx.x == 0) pl.spair[s] = make_int4(tok0, T, (int32_t)r0, 0);
+  // A pair's tokens are stacked last position first: the first pass over
+  // the pair then holds its latest tokens (which see every own key) and the
+  // short final pass of an item its earliest ones (which see few).
   const int64_t u0 = r0 / a.n_rep;
   for (int32_t j = threadIdx.x; j < T; j += kThreads)
-    pl.utok[u0 + j] = make_int2(tok0 + j, j);
+    pl.utok[u0 + j] = make_int2(tok0 + (T - 1 - j), T - 1 - j);
 }
 
 // Bounds on the norms of every own key k^ and every query q^, each of the
