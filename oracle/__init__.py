@@ -50,6 +50,8 @@ def _bind(lib):
     lib.dopr_oracle_prefix_attn.argtypes = [
         i32, i32, i32, i32, P, P, i64, P, P, P, P, P, P, P, P, P,
         f64, f64, f64, P, P, P, i32]
+    lib.dopr_oracle_score_attn.restype = ctypes.c_int
+    lib.dopr_oracle_score_attn.argtypes = lib.dopr_oracle_prefix_attn.argtypes
     lib.dopr_oracle_score.restype = ctypes.c_int
     lib.dopr_oracle_score.argtypes = [i32, i32, P, P, P, f64, P, P]
     lib.dopr_oracle_group.restype = ctypes.c_int
@@ -92,13 +94,14 @@ def max_threads(L=None) -> int:
 def prefix_attn(doc_ids, cu_seqlens, doc_len, doc_off, prefix_k, prefix_v,
                 q, k, v, q_norm_w, k_norm_w, *, n_q_heads, n_kv_heads,
                 rms_eps=1e-6, rope_theta=1e6, softmax_scale=None,
-                threads=0, L=None):
+                threads=0, last_only=False, L=None):
     """Online prefix attention, float64.
 
     prefix_k/prefix_v: uint16 [slots, Hkv, D]; document d's slots start at
     row doc_off[d].  q: uint16 [Ntok, Hq, D]; k, v: uint16 [Ntok, Hkv, D].
     Returns (out float64 [Ntok, Hq, D], lse float64 [Ntok, Hq],
-    status int32 [P]).
+    status int32 [P]).  With last_only, only each pair's last (score) token
+    is computed and out/lse are [P, Hq, D] / [P, Hq], indexed by pair.
     """
     L = L or lib()
     doc_ids = _c(doc_ids, np.int32)
@@ -119,13 +122,15 @@ def prefix_attn(doc_ids, cu_seqlens, doc_len, doc_off, prefix_k, prefix_v,
     if softmax_scale is None:
         softmax_scale = 1.0 / np.sqrt(D)
     P = doc_ids.shape[0]
-    out = np.zeros((ntok, n_q_heads, D), np.float64)
-    lse = np.zeros((ntok, n_q_heads), np.float64)
+    n_rows = P if last_only else ntok
+    out = np.zeros((n_rows, n_q_heads, D), np.float64)
+    lse = np.zeros((n_rows, n_q_heads), np.float64)
     status = np.zeros(P, np.int32)
     if pk.size == 0:  # keep valid pointers for documents with no slots
         pk = np.zeros((1, n_kv_heads, D), np.uint16)
         pv = np.zeros((1, n_kv_heads, D), np.uint16)
-    rc = L.dopr_oracle_prefix_attn(
+    fn = L.dopr_oracle_score_attn if last_only else L.dopr_oracle_prefix_attn
+    rc = fn(
         P, n_q_heads, n_kv_heads, D, _p(doc_ids), _p(cu), doc_len.shape[0],
         _p(doc_len), _p(doc_off), _p(pk), _p(pv), _p(q), _p(k), _p(v),
         _p(wq), _p(wk), rms_eps, rope_theta, softmax_scale, _p(out), _p(lse),

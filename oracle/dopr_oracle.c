@@ -85,14 +85,17 @@ static int doc_is_valid(int32_t doc, int64_t n_docs, const int32_t *doc_len) {
  *   its lse is -inf).
  * Returns 0, or a negative code for malformed arguments.
  */
-int dopr_oracle_prefix_attn(
+/* last_only = 0: every online row, out/lse indexed by token.  last_only = 1:
+ * only each pair's last row j = T_p - 1 (its score token), out/lse indexed
+ * by pair; the own keys and values of all T_p tokens are still formed. */
+static int attention(
     int32_t n_pairs, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
     const int32_t *doc_ids, const int32_t *cu_seqlens, int64_t n_docs,
     const int32_t *doc_len, const int64_t *doc_off, const uint16_t *prefix_k,
     const uint16_t *prefix_v, const uint16_t *q, const uint16_t *k,
     const uint16_t *v, const uint16_t *q_norm_w, const uint16_t *k_norm_w,
     double rms_eps, double rope_theta, double softmax_scale, double *out,
-    double *lse, int32_t *pair_status, int32_t n_threads) {
+    double *lse, int32_t *pair_status, int32_t n_threads, int last_only) {
   if (n_pairs < 0 || n_q_heads <= 0 || n_kv_heads <= 0 || head_dim <= 0 ||
       head_dim % 2 || n_q_heads % n_kv_heads)
     return ORACLE_ERR_ARG;
@@ -119,15 +122,19 @@ int dopr_oracle_prefix_attn(
     const int64_t tok0 = cu_seqlens[p];
     const int T = cu_seqlens[p + 1] - cu_seqlens[p];
 
+    const int j0 = last_only ? T - 1 : 0;
+
     /* Step 1: retrieve C~_d for the candidate document (Sec. 3.4). */
     if (!doc_is_valid(doc, n_docs, doc_len)) {
       if (pair_status) pair_status[p] = ORACLE_ERR_DOC_RANGE;
-      for (int j = 0; j < T; ++j)
+      for (int j = j0; j < T; ++j) {
+        const int64_t row = last_only ? p : tok0 + j;
         for (int h = 0; h < Hq; ++h) {
-          double *o = out + ((tok0 + j) * Hq + h) * D;
+          double *o = out + (row * Hq + h) * D;
           for (int i = 0; i < D; ++i) o[i] = 0.0;
-          if (lse) lse[(tok0 + j) * Hq + h] = -INFINITY;
+          if (lse) lse[row * Hq + h] = -INFINITY;
         }
+      }
       continue;
     }
     if (pair_status) pair_status[p] = 0;
@@ -161,8 +168,10 @@ int dopr_oracle_prefix_attn(
 
     /* Step 3: every online token j of every q head h attends to all L
      * prefix slots of kv head g = h / n_rep and to its own keys 0..j. */
-    for (int j = 0; j < T; ++j)
+    for (int jq = j0; jq < T; ++jq)
       for (int h = 0; h < Hq; ++h) {
+        const int j = jq;
+        const int64_t orow = last_only ? p : tok0 + j;
         const int g = h / n_rep;
         const uint16_t *src = q + ((tok0 + j) * Hq + h) * D;
         for (int i = 0; i < D; ++i) x[i] = bf16_to_double(src[i]);
@@ -189,7 +198,7 @@ int dopr_oracle_prefix_attn(
           z[t] = exp(z[t] - zmax);
           denom += z[t];
         }
-        double *o = out + ((tok0 + j) * Hq + h) * D;
+        double *o = out + (orow * Hq + h) * D;
         for (int i = 0; i < D; ++i) o[i] = 0.0;
         for (int t = 0; t < L; ++t) {
           const uint16_t *vt = pv + ((int64_t)t * Hkv + g) * D;
@@ -201,13 +210,48 @@ int dopr_oracle_prefix_attn(
           const double pt = z[L + t] / denom;
           for (int i = 0; i < D; ++i) o[i] += pt * vt[i];
         }
-        if (lse) lse[(tok0 + j) * Hq + h] = zmax + log(denom);
+        if (lse) lse[orow * Hq + h] = zmax + log(denom);
       }
     free(khat); free(vown); free(x); free(qhat); free(z);
   }
   free(wq);
   free(wk);
   return failed ? ORACLE_ERR_NOMEM : ORACLE_OK;
+}
+
+int dopr_oracle_prefix_attn(
+    int32_t n_pairs, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
+    const int32_t *doc_ids, const int32_t *cu_seqlens, int64_t n_docs,
+    const int32_t *doc_len, const int64_t *doc_off, const uint16_t *prefix_k,
+    const uint16_t *prefix_v, const uint16_t *q, const uint16_t *k,
+    const uint16_t *v, const uint16_t *q_norm_w, const uint16_t *k_norm_w,
+    double rms_eps, double rope_theta, double softmax_scale, double *out,
+    double *lse, int32_t *pair_status, int32_t n_threads) {
+  return attention(n_pairs, n_q_heads, n_kv_heads, head_dim, doc_ids,
+                   cu_seqlens, n_docs, doc_len, doc_off, prefix_k, prefix_v,
+                   q, k, v, q_norm_w, k_norm_w, rms_eps, rope_theta,
+                   softmax_scale, out, lse, pair_status, n_threads, 0);
+}
+
+/*
+ * Last layer of the online pass: the score head reads only the score
+ * token's hidden state (Sec. 3.2.3), so only row j = T_p - 1 of every pair
+ * is needed.  Same arguments and the same attention as
+ * dopr_oracle_prefix_attn, restricted to that row: out [P, Hq, D] and lse
+ * [P, Hq] are indexed by pair.
+ */
+int dopr_oracle_score_attn(
+    int32_t n_pairs, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
+    const int32_t *doc_ids, const int32_t *cu_seqlens, int64_t n_docs,
+    const int32_t *doc_len, const int64_t *doc_off, const uint16_t *prefix_k,
+    const uint16_t *prefix_v, const uint16_t *q, const uint16_t *k,
+    const uint16_t *v, const uint16_t *q_norm_w, const uint16_t *k_norm_w,
+    double rms_eps, double rope_theta, double softmax_scale, double *out,
+    double *lse, int32_t *pair_status, int32_t n_threads) {
+  return attention(n_pairs, n_q_heads, n_kv_heads, head_dim, doc_ids,
+                   cu_seqlens, n_docs, doc_len, doc_off, prefix_k, prefix_v,
+                   q, k, v, q_norm_w, k_norm_w, rms_eps, rope_theta,
+                   softmax_scale, out, lse, pair_status, n_threads, 1);
 }
 
 /*

@@ -217,6 +217,45 @@ def pin_doc_range(L):
     assert np.abs(got - ref).max() < 1e-10
 
 
+def pin_score_rows(L):
+    """Last-layer scoring: each pair's score-token row, against the
+    brute force's last rows, then through the score head against torch;
+    bad documents give zero rows and lse -inf in the pair-indexed layout."""
+    import torch
+    import torch.nn.functional as F
+    for i, c in enumerate(CASES):
+        prob = make_problem(**c, seed=30 + i)
+        out, lse, st = run_oracle(prob, L, last_only=True)
+        assert (st == 0).all()
+        ref, ref_lse = refs.attention_concat_fp64(prob)
+        last = prob["cu_seqlens"][1:] - 1
+        P = len(prob["doc_ids"])
+        assert out.shape == (P, prob["n_q_heads"], 128)
+        assert np.abs(out - ref[last]).max() < 1e-10, i
+        assert np.abs(lse - ref_lse[last]).max() < 1e-10, i
+        W = prob["n_q_heads"] * 128
+        prm = workloads.params(workloads.custom([1], [0], [1],
+                                                prob["n_q_heads"],
+                                                prob["n_kv_heads"]),
+                               "cpu", 40 + i, width=W)
+        nw = refs.torch_bf16_to_bits(prm["norm_w"])
+        wh = refs.torch_bf16_to_bits(prm["w_head"])
+        logits, s = oracle.score(out.reshape(P, W), nw, wh, 1e-6, L=L)
+        hn = F.rms_norm(torch.from_numpy(ref[last].reshape(P, W)), (W,),
+                        torch.from_numpy(refs.bf16_bits_to_f64(nw)), 1e-6)
+        tl = F.linear(hn, torch.from_numpy(refs.bf16_bits_to_f64(wh))).numpy()
+        assert np.abs(logits - tl).max() < 1e-10, i
+    prob = make_problem([4, -1, 6], [0, 1, 5, -2, 2], [2, 3, 1, 2, 3], 4, 2,
+                        seed=82)
+    out, lse, st = run_oracle(prob, L, last_only=True)
+    assert list(st) == [0, oracle.ORACLE_DOC_RANGE, oracle.ORACLE_DOC_RANGE,
+                        oracle.ORACLE_DOC_RANGE, 0]
+    assert (out[1:4] == 0).all() and np.isneginf(lse[1:4]).all()
+    full, full_lse, _ = run_oracle(prob, L)
+    last = prob["cu_seqlens"][1:] - 1
+    assert np.abs(out[[0, 4]] - full[last[[0, 4]]]).max() < 1e-12
+
+
 def pin_score(L):
     """Score head vs torch (F.rms_norm then a [2, W] linear map), the
     yes/no swap and the sigmoid/softmax identity."""
@@ -298,4 +337,4 @@ def pin_store_bytes(L):
 ALL_PINS = [pin_sdpa, pin_concat_fp64, pin_no_prefix_is_causal_self_attention,
             pin_uniform_logits, pin_ones_values, pin_single_key,
             pin_relative_positions, pin_invariances, pin_doc_range,
-            pin_score, pin_group, pin_store_bytes]
+            pin_score_rows, pin_score, pin_group, pin_store_bytes]

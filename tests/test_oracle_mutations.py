@@ -47,6 +47,11 @@ MUTATIONS = [
     ("q_norm_uses_k_weight", "rms_norm(x, wq, D, rms_eps, qhat);",
      "rms_norm(x, wk, D, rms_eps, qhat);"),
     ("score_sign", "score[p] = ly - ln;", "score[p] = ln - ly;"),
+    ("score_rows_indexed_by_token",
+     "const int64_t orow = last_only ? p : tok0 + j;",
+     "const int64_t orow = tok0 + j;"),
+    ("score_rows_first_token", "for (int jq = j0; jq < T; ++jq)",
+     "for (int jq = 0; jq < (last_only ? 1 : T); ++jq)"),
     ("score_yes_row_is_no_row", "wy[i] = bf16_to_double(w_head[i]);",
      "wy[i] = bf16_to_double(w_head[width + i]);"),
     ("score_no_norm_weight", "w[i] = bf16_to_double(norm_w[i]);",
