@@ -188,6 +188,44 @@ typedef struct {
 dopr_status_t dopr_score_logits(const dopr_score_args_t *args, void *stream);
 
 /* ------------------------------------------------------------------------ */
+/* Last-layer scoring (Sec. 3.2.3 with Sec. 3.4).  The score head reads only
+ * the score token's hidden state, so in the last layer only the final row
+ * j = T_p - 1 of every pair needs an attention output.  This call computes
+ * exactly the rows dopr_prefix_attn computes for those tokens (same keys:
+ * all L_d prefix slots and all T_p own keys, so every own key and value is
+ * still read and every own key is normed and rotated), and feeds them to
+ * the score head of dopr_score_logits with width W = n_q_heads * 128:
+ *   h = out[p] viewed as [W] (bf16-rounded attention output),
+ *   h^ = RMSNorm(h) * norm_w;  l_yes = w_yes . h^;  l_no = w_no . h^;
+ *   s = l_yes - l_no.
+ * The head is fused into the attention epilogue: each (pair, q head) row
+ * contributes its partial sums of h^2, norm_w*w_yes*h and norm_w*w_no*h;
+ * a small kernel adds the n_q_heads partials of a pair in head order.
+ * Arguments are those of dopr_prefix_attn with two differences:
+ *   out  dev bf16 [P, Hq, D]: the score rows, or NULL (not written);
+ *   lse  dev fp32 [P, Hq], or NULL;
+ * and the workspace comes from dopr_prefix_attn_score_workspace.
+ * kernel_variant 1..3 select the automatic tile shape here.  A pair with a
+ * bad doc id gets zero rows, lse -inf, logits and score 0, and a deferred
+ * DOC_RANGE status.  All buffers are caller-owned.                         */
+typedef struct {
+  const void *norm_w;       /* dev bf16 [W], W = n_q_heads * 128            */
+  const void *w_head;       /* dev bf16 [2, W]: row 0 = yes, row 1 = no    */
+  float rms_eps;            /* >= 0, finite                                 */
+  float *logits;            /* dev fp32 [P, 2] (l_yes, l_no), or NULL      */
+  float *score;             /* dev fp32 [P]                                 */
+} dopr_score_head_t;
+
+dopr_status_t dopr_prefix_attn_score_workspace(dopr_store_t st,
+                                               const dopr_attn_args_t *args,
+                                               size_t *bytes);
+
+dopr_status_t dopr_prefix_attn_score(dopr_store_t st, int32_t layer,
+                                     const dopr_attn_args_t *args,
+                                     const dopr_score_head_t *head,
+                                     void *stream);
+
+/* ------------------------------------------------------------------------ */
 /* Exports used by the bit-exact tests of the integer steps.               */
 
 /* Doc-id grouping in canonical form: valid pairs (doc id in range and

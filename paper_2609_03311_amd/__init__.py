@@ -62,6 +62,12 @@ class _ScoreArgs(ctypes.Structure):
                 ("logits", ctypes.c_void_p), ("score", ctypes.c_void_p)]
 
 
+class _ScoreHead(ctypes.Structure):
+    _fields_ = [("norm_w", ctypes.c_void_p), ("w_head", ctypes.c_void_p),
+                ("rms_eps", ctypes.c_float), ("logits", ctypes.c_void_p),
+                ("score", ctypes.c_void_p)]
+
+
 EXPORTS = {
     "dopr_store_bytes": ([ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p],
                          ctypes.c_int),
@@ -76,6 +82,11 @@ EXPORTS = {
     "dopr_prefix_attn": ([ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p,
                           ctypes.c_void_p], ctypes.c_int),
     "dopr_score_logits": ([ctypes.c_void_p, ctypes.c_void_p], ctypes.c_int),
+    "dopr_prefix_attn_score_workspace": ([ctypes.c_void_p, ctypes.c_void_p,
+                                          ctypes.c_void_p], ctypes.c_int),
+    "dopr_prefix_attn_score": ([ctypes.c_void_p, ctypes.c_int32,
+                                ctypes.c_void_p, ctypes.c_void_p,
+                                ctypes.c_void_p], ctypes.c_int),
     "dopr_group_pairs": ([ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p,
                           ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p,
                           ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
@@ -217,9 +228,8 @@ def _attn_args(store, doc_ids, cu_seqlens, q, k, v, q_norm_w, k_norm_w, out,
                      *(timing if timing is not None else (None, None)))
 
 
-def dopr_prefix_attn_workspace(store: Store, *, n_pairs, n_q_heads,
-                               max_tokens, total_tokens,
-                               kernel_variant=0) -> int:
+def _shape_args(n_pairs, n_q_heads, max_tokens, total_tokens,
+                kernel_variant):
     a = _AttnArgs()
     a.n_pairs = n_pairs
     a.n_q_heads = n_q_heads
@@ -227,9 +237,28 @@ def dopr_prefix_attn_workspace(store: Store, *, n_pairs, n_q_heads,
     a.total_tokens = total_tokens
     a.kernel_variant = kernel_variant
     a.rms_eps, a.rope_theta, a.softmax_scale = 1e-6, 1e6, 128 ** -0.5
+    return a
+
+
+def dopr_prefix_attn_workspace(store: Store, *, n_pairs, n_q_heads,
+                               max_tokens, total_tokens,
+                               kernel_variant=0) -> int:
+    a = _shape_args(n_pairs, n_q_heads, max_tokens, total_tokens,
+                    kernel_variant)
     n = ctypes.c_size_t(0)
     _check(lib().dopr_prefix_attn_workspace(store.handle, ctypes.byref(a),
                                             ctypes.byref(n)))
+    return n.value
+
+
+def dopr_prefix_attn_score_workspace(store: Store, *, n_pairs, n_q_heads,
+                                     max_tokens, total_tokens,
+                                     kernel_variant=0) -> int:
+    a = _shape_args(n_pairs, n_q_heads, max_tokens, total_tokens,
+                    kernel_variant)
+    n = ctypes.c_size_t(0)
+    _check(lib().dopr_prefix_attn_score_workspace(
+        store.handle, ctypes.byref(a), ctypes.byref(n)))
     return n.value
 
 
@@ -247,6 +276,27 @@ def dopr_prefix_attn(store: Store, layer: int, doc_ids, cu_seqlens, q, k, v,
                    kernel_variant=kernel_variant, timing=timing)
     _check(lib().dopr_prefix_attn(store.handle, layer, ctypes.byref(a),
                                   _stream(stream)))
+
+
+def dopr_prefix_attn_score(store: Store, layer: int, doc_ids, cu_seqlens, q,
+                           k, v, q_norm_w, k_norm_w, out, workspace, norm_w,
+                           w_head, score, *, max_tokens, logits=None,
+                           lse=None, total_tokens=None, rms_eps=1e-6,
+                           head_rms_eps=1e-6, rope_theta=1e6,
+                           softmax_scale=None, kernel_variant=0, timing=None,
+                           stream=None):
+    """Last-layer scoring: the score token's attention rows (out [P, Hq, D]
+    or None, lse [P, Hq] or None) with the score head fused (score [P],
+    logits [P, 2] or None)."""
+    a = _attn_args(store, doc_ids, cu_seqlens, q, k, v, q_norm_w, k_norm_w,
+                   out, lse, workspace, max_tokens=max_tokens,
+                   total_tokens=total_tokens, rms_eps=rms_eps,
+                   rope_theta=rope_theta, softmax_scale=softmax_scale,
+                   kernel_variant=kernel_variant, timing=timing)
+    h = _ScoreHead(_ptr(norm_w), _ptr(w_head), float(head_rms_eps),
+                   _ptr(logits), _ptr(score))
+    _check(lib().dopr_prefix_attn_score(store.handle, layer, ctypes.byref(a),
+                                        ctypes.byref(h), _stream(stream)))
 
 
 def dopr_score_logits(h, norm_w, w_head, score, *, width=None,

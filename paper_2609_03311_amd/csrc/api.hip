@@ -90,7 +90,8 @@ int32_t default_rows_per_item(int32_t variant) {
 
 // Validation shared by the workspace query and the attention call.
 dopr_status_t check_attn(const dopr_store *st, const dopr_attn_args_t *a,
-                         PlanShape *shape, int32_t *n_rep) {
+                         PlanShape *shape, int32_t *n_rep,
+                         bool score_only = false) {
   if (!st) return fail(DOPR_ERR_INVALID_ARG, "store is NULL");
   if (!a) return fail(DOPR_ERR_INVALID_ARG, "args is NULL");
   if (a->n_pairs < 0) return fail(DOPR_ERR_INVALID_ARG, "n_pairs < 0");
@@ -103,8 +104,11 @@ dopr_status_t check_attn(const dopr_store *st, const dopr_attn_args_t *a,
     return fail(DOPR_ERR_INVALID_ARG,
                 "total_tokens must be >= n_pairs (every T_p >= 1)");
   *n_rep = a->n_q_heads / st->n_kv_heads;
-  if (a->total_tokens * (int64_t)(*n_rep) > INT32_MAX)
-    return fail(DOPR_ERR_UNSUPPORTED, "total_tokens * n_rep must be < 2^31");
+  const int64_t stacked = score_only ? a->n_pairs : a->total_tokens;
+  if (stacked * (int64_t)(*n_rep) > INT32_MAX)
+    return fail(DOPR_ERR_UNSUPPORTED,
+                "stacked rows (tokens, or pairs in score mode) * n_rep must "
+                "be < 2^31");
   if (a->kernel_variant < 0 || a->kernel_variant > 5)
     return fail(DOPR_ERR_INVALID_ARG, "kernel_variant must be in 0..5");
   if (!(a->softmax_scale > 0.f) || !std::isfinite(a->softmax_scale))
@@ -121,6 +125,7 @@ dopr_status_t check_attn(const dopr_store *st, const dopr_attn_args_t *a,
   shape->total_tokens = a->total_tokens;
   shape->max_len = st->max_len;
   shape->n_kv_heads = st->n_kv_heads;
+  shape->score_only = score_only;
   return DOPR_OK;
 }
 
@@ -263,22 +268,42 @@ dopr_status_t dopr_prefix_attn_workspace(dopr_store_t st,
   return ok();
 }
 
-dopr_status_t dopr_prefix_attn(dopr_store_t st, int32_t layer,
-                               const dopr_attn_args_t *a, void *stream) {
+}  // extern "C"
+
+namespace {
+
+// The attention call in both modes: every online row (head == NULL) or the
+// score token's rows with the fused score head.
+dopr_status_t run_attention(dopr_store_t st, int32_t layer,
+                            const dopr_attn_args_t *a,
+                            const dopr_score_head_t *head, void *stream) {
+  const bool score = head != nullptr;
   PlanShape shape;
   int32_t n_rep = 0;
-  dopr_status_t s = check_attn(st, a, &shape, &n_rep);
+  dopr_status_t s = check_attn(st, a, &shape, &n_rep, score);
   if (s != DOPR_OK) return s;
   if (layer < 0 || layer >= st->n_layers)
     return fail(DOPR_ERR_INVALID_ARG, "layer out of range");
+  if (score) {
+    if (!(head->rms_eps >= 0.f) || !std::isfinite(head->rms_eps))
+      return fail(DOPR_ERR_INVALID_ARG,
+                  "head rms_eps must be finite and >= 0");
+  }
   if (a->n_pairs == 0) return ok();
   if (!a->doc_ids || !a->cu_seqlens || !a->q || !a->k || !a->v ||
-      !a->q_norm_w || !a->k_norm_w || !a->out || !a->workspace)
+      !a->q_norm_w || !a->k_norm_w || (!a->out && !score) || !a->workspace)
     return fail(DOPR_ERR_INVALID_ARG, "NULL buffer");
   if (!aligned16(a->q) || !aligned16(a->k) || !aligned16(a->v) ||
       !aligned16(a->out) || !aligned16(a->q_norm_w) || !aligned16(a->k_norm_w))
     return fail(DOPR_ERR_INVALID_ARG,
                 "q, k, v, out and norm weights must be 16-byte aligned");
+  if (score) {
+    if (!head->norm_w || !head->w_head || !head->score)
+      return fail(DOPR_ERR_INVALID_ARG, "NULL score-head buffer");
+    if (!aligned16(head->norm_w) || !aligned16(head->w_head))
+      return fail(DOPR_ERR_INVALID_ARG,
+                  "head norm_w and w_head must be 16-byte aligned");
+  }
   if (reinterpret_cast<uintptr_t>(a->workspace) % kAlign)
     return fail(DOPR_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
   const size_t need = plan_bytes(shape);
@@ -289,13 +314,42 @@ dopr_status_t dopr_prefix_attn(dopr_store_t st, int32_t layer,
   s = check_device(st);
   if (s != DOPR_OK) return s;
   const Plan plan = plan_carve(a->workspace, shape);
-  AttnCall call{st, layer, a, n_rep};
+  AttnCall call{st, layer, a, n_rep, head};
   hipStream_t hs = as_stream(stream);
   hipError_t e = launch_plan(call, plan, shape, hs);
   if (e != hipSuccess) return hip_fail(e, "scheduler launch");
   e = launch_attention(call, plan, shape, hs);
   if (e != hipSuccess) return hip_fail(e, "attention launch");
   return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+dopr_status_t dopr_prefix_attn(dopr_store_t st, int32_t layer,
+                               const dopr_attn_args_t *a, void *stream) {
+  return run_attention(st, layer, a, nullptr, stream);
+}
+
+dopr_status_t dopr_prefix_attn_score_workspace(dopr_store_t st,
+                                               const dopr_attn_args_t *args,
+                                               size_t *bytes) {
+  if (!bytes) return fail(DOPR_ERR_INVALID_ARG, "bytes is NULL");
+  PlanShape shape;
+  int32_t n_rep = 0;
+  dopr_status_t s = check_attn(st, args, &shape, &n_rep, true);
+  if (s != DOPR_OK) return s;
+  *bytes = plan_bytes(shape);
+  return ok();
+}
+
+dopr_status_t dopr_prefix_attn_score(dopr_store_t st, int32_t layer,
+                                     const dopr_attn_args_t *args,
+                                     const dopr_score_head_t *head,
+                                     void *stream) {
+  if (!head) return fail(DOPR_ERR_INVALID_ARG, "head is NULL");
+  return run_attention(st, layer, args, head, stream);
 }
 
 dopr_status_t dopr_score_logits(const dopr_score_args_t *a, void *stream) {

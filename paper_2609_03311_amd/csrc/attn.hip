@@ -98,6 +98,11 @@ struct AttnParams {
   const float2 *rope;
   uint16_t *out;
   float *lse;
+  // score mode: output row of sorted pair s is pair_order[s]; the epilogue
+  // adds the score head's partial sums (h^2, g*w_yes*h, g*w_no*h) per row
+  const int32_t *pair_order;
+  float *part;
+  const uint16_t *head_norm_w, *head_w;
   int32_t items_cap, Hq, Hkv, n_rep, layer, n_layers;
   int32_t flag_all;  // queue every unit for the SAFE pass (self-check mode)
   float eps, c;      // c = softmax_scale * log2(e)
@@ -581,7 +586,7 @@ __device__ __forceinline__ void attend(const uint16_t *kblk,
 // SMX fixed, so every loop below is straight-line code over one set of
 // accumulators.  Returns whether some row of this wave left the range the
 // fast modes guarantee (the unit is then recomputed in SAFE mode).
-template <int WAVES, int NQB, int SMX>
+template <int WAVES, int NQB, int SMX, bool SCORE>
 __device__ __forceinline__ bool run_unit(const AttnParams &P, Smem &sm,
                                          const Frag &fo, int g, int row0,
                                          int row1, int L, int Lp,
@@ -649,7 +654,6 @@ __device__ __forceinline__ bool run_unit(const AttnParams &P, Smem &sm,
       os.T = sp.y;
     }
     OwnRegs<WAVES> orr;
-    if (n_seg == 0) own_load<WAVES>(P, os, g, L, orr);
 
     // Document prefix: every row sees all L slots.
     for (int sg = 0; sg < n_seg; ++sg) {
@@ -661,8 +665,6 @@ __device__ __forceinline__ bool run_unit(const AttnParams &P, Smem &sm,
       }
       wait_vmem();
       __syncthreads();
-      // the first own chunk lands while the prefix is consumed
-      if (sg == 0) own_load<WAVES>(P, os, g, L, orr);
       const int n_full = live ? n >> 5 : 0;
       for (int ck = 0; ck < n_full; ++ck)
         attend<0, NQB, SMX>(sm.pk[ck], sm.pv[ck], fo, qf, acc, hf, B,
@@ -679,6 +681,9 @@ __device__ __forceinline__ bool run_unit(const AttnParams &P, Smem &sm,
     // Own causal keys, pair by pair, chunk by chunk, double-buffered: the
     // next chunk's raw k/v are loaded while the current one is consumed,
     // then normed/rotated into the other buffer; one barrier per chunk.
+    // (The first chunk is loaded only here: its registers are not held
+    // through the prefix products.)
+    own_load<WAVES>(P, os, g, L, orr);
     __syncthreads();  // the previous pass's last own chunk is consumed
     own_stage<WAVES>(P, orr, sm, 0);
     __syncthreads();
@@ -730,16 +735,62 @@ __device__ __forceinline__ bool run_unit(const AttnParams &P, Smem &sm,
       if (!valid[qb]) continue;
       bad = bad || !(lt >= kLoOk && lt <= kHiOk);
       const float inv = 1.0f / lt;
-      const int64_t orow = (int64_t)tokq[qb] * P.Hq + head[qb];
+      // (score mode stacks one token per pair: stacked token u is the
+      // sorted pair, whose output row is the pair's index)
+      const int64_t orow =
+          (int64_t)(SCORE ? P.pair_order[(pass0 + (wave * NQB + qb) * 32 +
+                                          lq) / P.n_rep]
+                          : tokq[qb]) * P.Hq + head[qb];
       uint16_t *op = P.out + orow * D;
+      float ss = 0.f, sy = 0.f, sn = 0.f;
 #pragma unroll
       for (int db = 0; db < 4; ++db) {
         float o[16];
 #pragma unroll
         for (int i = 0; i < 16; ++i) o[i] = acc[qb].o[db][i] * inv;
-        uint4 *dst = reinterpret_cast<uint4 *>(op + 32 * db + 16 * hf);
-        dst[0] = as_uint4(to_bf16x8(o));
-        dst[1] = as_uint4(to_bf16x8(o + 8));
+        const uint4 h0 = as_uint4(to_bf16x8(o)), h1 = as_uint4(to_bf16x8(o + 8));
+        if (!SCORE || P.out) {
+          uint4 *dst = reinterpret_cast<uint4 *>(op + 32 * db + 16 * hf);
+          dst[0] = h0;
+          dst[1] = h1;
+        }
+        if (SCORE) {
+          // the head reads the bf16 row, as it would from memory: lane
+          // dims 32*db + 16*hf + 0..15 of q head head[qb] (the opaque
+          // offset keeps each slice's weight loads in its own iteration)
+          const int64_t c0 =
+              (int64_t)head[qb] * D + 32 * db + 16 * hf + opaque_zero();
+          const int64_t W = (int64_t)P.Hq * D;
+#pragma unroll
+          for (int half = 0; half < 2; ++half) {
+            float hv[8], gv[8], yv[8], nv[8];
+            unpack8(half ? h1 : h0, hv);
+            unpack8(*reinterpret_cast<const uint4 *>(P.head_norm_w + c0 +
+                                                     8 * half), gv);
+            unpack8(*reinterpret_cast<const uint4 *>(P.head_w + c0 +
+                                                     8 * half), yv);
+            unpack8(*reinterpret_cast<const uint4 *>(P.head_w + W + c0 +
+                                                     8 * half), nv);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+              ss = fmaf(hv[e], hv[e], ss);
+              const float gh = gv[e] * hv[e];
+              sy = fmaf(gh, yv[e], sy);
+              sn = fmaf(gh, nv[e], sn);
+            }
+          }
+        }
+      }
+      if (SCORE) {
+        ss += __shfl_xor(ss, 32, 64);
+        sy += __shfl_xor(sy, 32, 64);
+        sn += __shfl_xor(sn, 32, 64);
+        if (hf == 0) {
+          float *pp = P.part + orow * 3;
+          pp[0] = ss;
+          pp[1] = sy;
+          pp[2] = sn;
+        }
       }
       if (P.lse && hf == 0)
         P.lse[orow] = (acc[qb].m + __log2f(lt)) * kLn2;
@@ -749,7 +800,7 @@ __device__ __forceinline__ bool run_unit(const AttnParams &P, Smem &sm,
   return wave_bad;
 }
 
-template <int WAVES, int NQB, bool SAFE>
+template <int WAVES, int NQB, bool SAFE, bool SCORE>
 __global__ __launch_bounds__(WAVES * 64) __attribute__((
     amdgpu_waves_per_eu(WAVES / 4, WAVES / 4))) void k_prefix_attn(AttnParams P) {
   __shared__ __attribute__((aligned(16))) Smem sm;
@@ -796,7 +847,7 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((
     if (!SAFE) {
       if (B <= kNoRefBound) {
         if (resident && L > 0) stage_prefix<WAVES>(Kp, VTp, Lp, 0, L, sm);
-        wave_bad = run_unit<WAVES, NQB, 0>(P, sm, fo, g, row0, row1, L, Lp,
+        wave_bad = run_unit<WAVES, NQB, 0, SCORE>(P, sm, fo, g, row0, row1, L, Lp,
                                            Kp, VTp, B) ||
                    P.flag_all;
       }
@@ -817,7 +868,7 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((
       // (self-check mode sends every unit to the exact mode)
       bool exact = !unscored || P.flag_all;
       if (!exact) {
-        wave_bad = run_unit<WAVES, NQB, 1>(P, sm, fo, g, row0, row1, L, Lp,
+        wave_bad = run_unit<WAVES, NQB, 1, SCORE>(P, sm, fo, g, row0, row1, L, Lp,
                                            Kp, VTp, B);
         __syncthreads();
         if (lane == 0) sm.words()[1 + wave] = wave_bad;
@@ -826,25 +877,27 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((
         __syncthreads();
       }
       if (exact)
-        run_unit<WAVES, NQB, 2>(P, sm, fo, g, row0, row1, L, Lp, Kp, VTp, B);
+        run_unit<WAVES, NQB, 2, SCORE>(P, sm, fo, g, row0, row1, L, Lp, Kp, VTp, B);
       __syncthreads();  // every wave is done with this item's LDS
     }
   }
 }
 
 // Pairs whose document is out of range or not resident: zero outputs and
-// -inf LSE (their token range was validated by the scheduler).
+// -inf LSE (their token range was validated by the scheduler).  With no
+// token ranges (score mode) pair p owns row p; out may then be NULL.
 __global__ __launch_bounds__(256) void k_zero_invalid(
     const int32_t *counters, const int32_t *invalid, const int32_t *cu,
     int32_t Hq, uint16_t *out, float *lse) {
   const int32_t n_inv = counters[kCntInvalid];
   for (int32_t idx = blockIdx.x; idx < n_inv; idx += gridDim.x) {
     const int32_t p = invalid[idx];
-    const int64_t t0 = cu[p], t1 = cu[p + 1];
+    const int64_t t0 = cu ? cu[p] : p, t1 = cu ? cu[p + 1] : p + 1;
     const int64_t n16 = (t1 - t0) * Hq * D / 8;
     uint4 *o = reinterpret_cast<uint4 *>(out + t0 * Hq * D);
-    for (int64_t e = threadIdx.x; e < n16; e += blockDim.x)
-      o[e] = make_uint4(0, 0, 0, 0);
+    if (out)
+      for (int64_t e = threadIdx.x; e < n16; e += blockDim.x)
+        o[e] = make_uint4(0, 0, 0, 0);
     if (lse)
       for (int64_t e = threadIdx.x; e < (t1 - t0) * Hq; e += blockDim.x)
         lse[t0 * Hq + e] = -INFINITY;
@@ -866,7 +919,7 @@ __global__ __launch_bounds__(256) void k_queue_all(const int64_t *totals,
   if (blockIdx.x == 0 && threadIdx.x == 0) counters[kCntFix] = (int32_t)n;
 }
 
-template <int WAVES, int NQB, bool SAFE>
+template <int WAVES, int NQB, bool SAFE, bool SCORE>
 hipError_t launch_variant(const AttnParams &p, hipStream_t s, int max_grid) {
   int dev = 0, n_cu = 0, per_cu = 0;
   hipError_t e = hipGetDevice(&dev);
@@ -874,7 +927,7 @@ hipError_t launch_variant(const AttnParams &p, hipStream_t s, int max_grid) {
   e = hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev);
   if (e != hipSuccess) return e;
   e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
-      &per_cu, k_prefix_attn<WAVES, NQB, SAFE>, WAVES * 64, 0);
+      &per_cu, k_prefix_attn<WAVES, NQB, SAFE, SCORE>, WAVES * 64, 0);
   if (e != hipSuccess) return e;
   if (per_cu < 1) per_cu = 1;
   // Persistent grid, a multiple of 8 so block b always serves queue b % 8
@@ -882,7 +935,7 @@ hipError_t launch_variant(const AttnParams &p, hipStream_t s, int max_grid) {
   unsigned grid = (unsigned)(n_cu * per_cu);
   grid = (grid + 7) / 8 * 8;
   if (max_grid > 0 && grid > (unsigned)max_grid) grid = (unsigned)max_grid;
-  hipLaunchKernelGGL((k_prefix_attn<WAVES, NQB, SAFE>), dim3(grid),
+  hipLaunchKernelGGL((k_prefix_attn<WAVES, NQB, SAFE, SCORE>), dim3(grid),
                      dim3(WAVES * 64), 0, s, p);
   return hipGetLastError();
 }
@@ -931,21 +984,32 @@ hipError_t launch_attention(const AttnCall &c, const Plan &pl,
     if (e != hipSuccess) return e;
   }
   p.flag_all = a->kernel_variant == 5;
-  switch (a->kernel_variant) {
+  const bool score = c.head != nullptr;
+  if (score) {
+    p.pair_order = pl.pair_order;
+    p.part = pl.part;
+    p.head_norm_w = static_cast<const uint16_t *>(c.head->norm_w);
+    p.head_w = static_cast<const uint16_t *>(c.head->w_head);
+  }
+  switch (score ? (a->kernel_variant == 4 ? 4 : 0) : a->kernel_variant) {
     case 1:
-    case 5: e = launch_variant<4, 2, false>(p, s, 0); break;
-    case 3: e = launch_variant<4, 1, false>(p, s, 0); break;
+    case 5: e = launch_variant<4, 2, false, false>(p, s, 0); break;
+    case 3: e = launch_variant<4, 1, false, false>(p, s, 0); break;
     case 4:
       hipLaunchKernelGGL(k_queue_all, dim3(256), dim3(256), 0, s, p.totals,
                          p.items_cap, p.Hkv, p.counters, p.fix);
       e = hipGetLastError();
       break;
-    default: e = launch_variant<8, 1, false>(p, s, 0); break;  // 0, 2
+    default:  // 0, 2 (score mode: every variant but 4)
+      e = score ? launch_variant<8, 1, false, true>(p, s, 0)
+                : launch_variant<8, 1, false, false>(p, s, 0);
+      break;
   }
   if (e != hipSuccess) return e;
   // Work units the fast pass flagged or left unscored (normally none) are
   // computed here; in exact mode that is every unit.
-  e = launch_variant<4, 1, true>(p, s, 0);
+  e = score ? launch_variant<4, 1, true, true>(p, s, 0)
+            : launch_variant<4, 1, true, false>(p, s, 0);
   if (e != hipSuccess) return e;
   if (a->timing_end) {
     e = hipEventRecord(static_cast<hipEvent_t>(a->timing_end), s);
@@ -954,8 +1018,13 @@ hipError_t launch_attention(const AttnCall &c, const Plan &pl,
   const unsigned zgrid =
       (unsigned)(a->n_pairs < 1024 ? (a->n_pairs > 0 ? a->n_pairs : 1) : 1024);
   hipLaunchKernelGGL(k_zero_invalid, dim3(zgrid), dim3(256), 0, s,
-                     pl.counters, pl.invalid, a->cu_seqlens, a->n_q_heads,
-                     p.out, a->lse);
+                     pl.counters, pl.invalid, score ? nullptr : a->cu_seqlens,
+                     a->n_q_heads, p.out, a->lse);
+  if (score) {
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    return launch_score_reduce(pl, a->n_pairs, a->n_q_heads, c.head, s);
+  }
   (void)shape;
   return hipGetLastError();
 }

@@ -13,7 +13,8 @@
 //      id, the canonical order);
 //   3. place pairs into their document's slots, then order each group's
 //      members by pair index (stable, deterministic);
-//   4. stacked-row offsets (T_p * n_rep rows per pair, in grouped order);
+//   4. stacked-row offsets (T_p * n_rep rows per pair, in grouped order;
+//      n_rep rows -- the score token's -- in score mode);
 //   5. split each group's rows into work items of bounded size, and a
 //      table from every 32-row block to the pair owning its first row;
 //   6. the rotary cos/sin table for positions 0 .. max_L + max_tokens - 1.
@@ -125,6 +126,7 @@ struct PlanArgs {
   int64_t n_docs, total_tokens;
   int32_t n_pairs, n_rep, max_tokens, rows_per_item;
   int32_t *status;
+  bool score_only;
 };
 
 __global__ __launch_bounds__(kThreads) void k_plan_init(Plan pl, int64_t n_docs,
@@ -207,7 +209,8 @@ __global__ __launch_bounds__(kThreads) void k_rank(Plan pl, PlanArgs a,
   int32_t rank = 0;
   for (int32_t k = s0; k < s0 + c; ++k) rank += pl.tmp_order[k] < v;
   pl.pair_order[s0 + rank] = v;
-  const int64_t T = a.cu ? (int64_t)(a.cu[v + 1] - a.cu[v]) : 1;
+  const int64_t T = a.cu && !a.score_only ? (int64_t)(a.cu[v + 1] - a.cu[v])
+                                           : 1;
   pl.prow[s0 + rank] = T * a.n_rep;
   if (rank == 0) {
     const int32_t gi = (int32_t)(packed >> 32);
@@ -269,8 +272,8 @@ __global__ __launch_bounds__(kThreads) void k_blk_pair(Plan pl,
 // Step 5d: per sorted pair (first token, token count, first stacked row),
 // with a sentinel row count after the last pair, and per stacked token u
 // (token-major: u = stacked row / n_rep) its (batch token, position in
-// pair), positions descending within a pair.  One workgroup per sorted
-// pair.
+// pair), positions descending within a pair (score mode: the last token
+// only, so u is the sorted pair index).  One workgroup per sorted pair.
 __global__ __launch_bounds__(kThreads) void k_token_table(Plan pl, PlanArgs a,
                                                           const int64_t *totals) {
   const int32_t s = blockIdx.x;
@@ -289,7 +292,8 @@ __global__ __launch_bounds__(kThreads) void k_token_table(Plan pl, PlanArgs a,
   // the pair then holds its latest tokens (which see every own key) and the
   // short final pass of an item its earliest ones (which see few).
   const int64_t u0 = r0 / a.n_rep;
-  for (int32_t j = threadIdx.x; j < T; j += kThreads)
+  const int32_t stacked = a.score_only ? 1 : T;
+  for (int32_t j = threadIdx.x; j < stacked; j += kThreads)
     pl.utok[u0 + j] = make_int2(tok0 + (T - 1 - j), T - 1 - j);
 }
 
@@ -368,7 +372,8 @@ Plan carve(void *ws, const PlanShape &s, size_t *bytes) {
   pl.group_ptr = c.take<int32_t>(P + 1);
   pl.prow = c.take<int64_t>(P + 1);
   pl.item_scan = c.take<int64_t>(P + 1);
-  const int64_t rows = s.total_tokens * s.n_rep;
+  const int64_t stacked = s.score_only ? P : s.total_tokens;
+  const int64_t rows = stacked * s.n_rep;
   const int64_t cap = P + (rows + s.rows_per_item - 1) / s.rows_per_item + 1;
   pl.items_cap = (int32_t)cap;
   pl.items = c.take<int4>(cap);
@@ -376,7 +381,9 @@ Plan carve(void *ws, const PlanShape &s, size_t *bytes) {
   pl.blk_pair = c.take<int32_t>(pl.blk_cap);
   pl.fix = c.take<int32_t>(cap * (s.n_kv_heads > 0 ? s.n_kv_heads : 1));
   pl.spair = c.take<int4>(P + 1);
-  pl.utok = c.take<int2>(s.total_tokens);
+  pl.utok = c.take<int2>(stacked);
+  pl.part = s.score_only ? c.take<float>(P * s.n_rep * s.n_kv_heads * 3)
+                         : nullptr;
   pl.kown = c.take<float>(2);
   pl.rope_pos = s.max_len + s.max_tokens;
   pl.rope = c.take<float2>((int64_t)pl.rope_pos * kRopeHalf);
@@ -410,7 +417,7 @@ hipError_t launch_plan(const AttnCall &c, const Plan &pl,
   PlanArgs pa{a->doc_ids,        a->cu_seqlens,      c.st->d_len,
               c.st->n_docs,      a->total_tokens,    a->n_pairs,
               c.n_rep,           a->max_tokens,      shape.rows_per_item,
-              c.st->d_status};
+              c.st->d_status,    shape.score_only};
   int64_t *totals = plan_totals(pl);
   const int64_t P = a->n_pairs;
   const int64_t init_n = c.st->n_docs > kCounters ? c.st->n_docs : kCounters;

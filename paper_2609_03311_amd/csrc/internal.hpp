@@ -107,7 +107,8 @@ struct Plan {
   int4 *items;          // [items_cap] (group, row0, row1, 0)
   int32_t *fix;         // [items_cap * Hkv] work units for the SAFE pass
   int4 *spair;          // [P+1] sorted pair: (tok0, T, first stacked row)
-  int2 *utok;           // [Ntok] stacked token: (batch token, position)
+  int2 *utok;           // [stacked tokens] (batch token, position)
+  float *part;          // [P][Hq][3] score-head partial sums (score mode)
   float *kown;          // [2] bounds on |k^| (own keys) and |q^|: sqrt(D) max|w|
   float2 *rope;         // [rope_pos][64] (cos, sin)
   int32_t items_cap;
@@ -116,10 +117,13 @@ struct Plan {
   int64_t scan_blocks_cap;
 };
 
+// score_only: one stacked token per pair (its score token, the last one)
+// instead of all T_p.
 struct PlanShape {
   int32_t n_pairs, n_rep, max_tokens, rows_per_item;
   int64_t n_docs, total_tokens;
   int32_t max_len, n_kv_heads;
+  bool score_only = false;
 };
 
 size_t plan_bytes(const PlanShape &s);
@@ -139,12 +143,15 @@ struct AttnCall {
   int32_t layer;
   const dopr_attn_args_t *a;
   int32_t n_rep;
+  const dopr_score_head_t *head = nullptr;  // score mode (last layer)
 };
 hipError_t launch_plan(const AttnCall &c, const Plan &plan,
                        const PlanShape &shape, hipStream_t s);
 hipError_t launch_attention(const AttnCall &c, const Plan &plan,
                             const PlanShape &shape, hipStream_t s);
 hipError_t launch_score(const dopr_score_args_t *a, hipStream_t s);
+hipError_t launch_score_reduce(const Plan &pl, int32_t n_pairs, int32_t n_q_heads,
+                               const dopr_score_head_t *head, hipStream_t s);
 
 // Record a deferred error code in a status word (first error wins).
 __device__ inline void raise_status(int32_t *status, int32_t code) {

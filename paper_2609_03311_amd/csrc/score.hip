@@ -5,6 +5,10 @@
 // the score is the log-odds l_yes - l_no.  One workgroup per pair: a single
 // streaming pass accumulates sum(h^2), sum(g*h*w_yes) and sum(g*h*w_no),
 // then applies 1/rms once (the norm is a common scalar factor).
+//
+// In last-layer scoring the attention epilogue already produced those three
+// sums per (pair, q head); k_score_reduce adds a pair's heads in head order
+// (deterministic) and applies the norm.
 #include "internal.hpp"
 
 namespace dopr {
@@ -82,7 +86,46 @@ __global__ __launch_bounds__(kThreads) void k_score(dopr_score_args_t a) {
   }
 }
 
+// One thread per pair.  Pairs the scheduler did not accept (bad doc id or
+// token range) have h = 0, hence logits and score 0.
+__global__ __launch_bounds__(kThreads) void k_score_reduce(
+    const float *part, const int32_t *pair_flag, int32_t n_pairs, int32_t hq,
+    float width, float eps, float *logits, float *score) {
+  const int32_t p = blockIdx.x * kThreads + threadIdx.x;
+  if (p >= n_pairs) return;
+  float ly = 0.f, ln = 0.f;
+  if (pair_flag[p] == 1) {
+    float S = 0.f, Y = 0.f, N = 0.f;
+    const float *pp = part + (int64_t)p * hq * 3;
+    for (int32_t h = 0; h < hq; ++h) {
+      S += pp[3 * h];
+      Y += pp[3 * h + 1];
+      N += pp[3 * h + 2];
+    }
+    const float inv = rsqrtf(S / width + eps);
+    ly = Y * inv;
+    ln = N * inv;
+  }
+  if (logits) {
+    logits[2 * (int64_t)p] = ly;
+    logits[2 * (int64_t)p + 1] = ln;
+  }
+  score[p] = ly - ln;
+}
+
 }  // namespace
+
+hipError_t launch_score_reduce(const Plan &pl, int32_t n_pairs,
+                               int32_t n_q_heads,
+                               const dopr_score_head_t *head, hipStream_t s) {
+  if (n_pairs == 0) return hipSuccess;
+  const unsigned grid = (unsigned)((n_pairs + kThreads - 1) / kThreads);
+  hipLaunchKernelGGL(k_score_reduce, dim3(grid), dim3(kThreads), 0, s,
+                     pl.part, pl.pair_flag, n_pairs, n_q_heads,
+                     (float)n_q_heads * kHeadDim, head->rms_eps, head->logits,
+                     head->score);
+  return hipGetLastError();
+}
 
 hipError_t launch_score(const dopr_score_args_t *a, hipStream_t s) {
   if (a->n_pairs == 0) return hipSuccess;

@@ -7,7 +7,8 @@ from __future__ import annotations
 
 import numpy as np
 
-from . import (dopr_prefix_attn, dopr_prefix_attn_workspace,
+from . import (dopr_prefix_attn, dopr_prefix_attn_score,
+               dopr_prefix_attn_score_workspace, dopr_prefix_attn_workspace,
                dopr_score_logits, dopr_store_create, dopr_store_put)
 
 HEAD_DIM = 128
@@ -81,3 +82,43 @@ class OnlineStep:
         self.attention(layer, doc_ids, cu_seqlens, q, k, v, q_norm_w,
                        k_norm_w, stream=stream)
         self.score_head(cu_seqlens, norm_w, w_head, stream=stream)
+
+
+class ScoreStep:
+    """Reusable buffers for last-layer scoring: only each pair's score-token
+    rows are attended, and the score head is fused into the attention
+    epilogue.  `with_rows` keeps the rows (out [P, Hq, D], lse [P, Hq])."""
+
+    def __init__(self, store, *, n_pairs, n_q_heads, total_tokens,
+                 max_tokens, kernel_variant=0, device="cuda",
+                 with_rows=True):
+        import torch
+        self.store = store
+        self.n_pairs = n_pairs
+        self.n_q_heads = n_q_heads
+        self.total_tokens = total_tokens
+        self.max_tokens = max_tokens
+        self.kernel_variant = kernel_variant
+        nbytes = dopr_prefix_attn_score_workspace(
+            store, n_pairs=n_pairs, n_q_heads=n_q_heads,
+            max_tokens=max_tokens, total_tokens=total_tokens,
+            kernel_variant=kernel_variant)
+        self.workspace = torch.empty(max(nbytes, 256), dtype=torch.uint8,
+                                     device=device)
+        self.out = (torch.empty((n_pairs, n_q_heads, HEAD_DIM),
+                                dtype=torch.bfloat16, device=device)
+                    if with_rows else None)
+        self.lse = (torch.empty((n_pairs, n_q_heads), dtype=torch.float32,
+                                device=device) if with_rows else None)
+        self.score = torch.empty(n_pairs, dtype=torch.float32, device=device)
+        self.logits = torch.empty((n_pairs, 2), dtype=torch.float32,
+                                  device=device)
+
+    def run(self, layer, doc_ids, cu_seqlens, q, k, v, q_norm_w, k_norm_w,
+            norm_w, w_head, stream=None, **kw):
+        dopr_prefix_attn_score(
+            self.store, layer, doc_ids, cu_seqlens, q, k, v, q_norm_w,
+            k_norm_w, self.out, self.workspace, norm_w, w_head, self.score,
+            max_tokens=self.max_tokens, logits=self.logits, lse=self.lse,
+            total_tokens=self.total_tokens,
+            kernel_variant=self.kernel_variant, stream=stream, **kw)

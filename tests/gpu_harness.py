@@ -69,8 +69,10 @@ def run(case: Case):
     return dopr_check_status(case.store)
 
 
-def oracle_subset(case: Case, pairs):
-    """Oracle outputs for a subset of pairs (in the given order)."""
+def oracle_subset(case: Case, pairs, last_only=False):
+    """Oracle outputs for a subset of pairs (in the given order); with
+    last_only, only each pair's score-token row (out/lse indexed by the
+    position of the pair in `pairs`)."""
     import torch
     st = case.st
     pairs = np.asarray(pairs, np.int64)
@@ -104,8 +106,9 @@ def oracle_subset(case: Case, pairs):
         st.doc_ids[pairs], sub_cu.astype(np.int32), st.doc_len, sub_off, pk,
         pv, q, k, v, refs.torch_bf16_to_bits(case.prm["q_norm_w"]),
         refs.torch_bf16_to_bits(case.prm["k_norm_w"]),
-        n_q_heads=st.n_q_heads, n_kv_heads=st.n_kv_heads)
-    h = out[sub_cu[1:] - 1].reshape(len(pairs), -1)
+        n_q_heads=st.n_q_heads, n_kv_heads=st.n_kv_heads,
+        last_only=last_only)
+    h = (out if last_only else out[sub_cu[1:] - 1]).reshape(len(pairs), -1)
     logits, s = oracle.score(h, refs.torch_bf16_to_bits(case.prm["norm_w"]),
                              refs.torch_bf16_to_bits(case.prm["w_head"]))
     log(f"oracle on {len(pairs)} pairs ({len(tok)} tokens): "
@@ -168,3 +171,58 @@ def sample_pairs(st, n_random, seed=0, include_largest_group=True,
         picks.update(members.tolist())
     picks.update([0, P - 1])
     return np.array(sorted(picks), np.int64)
+
+
+# ---------------------------------------------------------------------------
+# Last-layer scoring (score-token rows with the fused score head).
+
+def setup_score(case: Case, kernel_variant=0, with_rows=True):
+    """A ScoreStep over the same store and inputs as `case`."""
+    from paper_2609_03311_amd import pipeline
+    st = case.st
+    max_t = int(st.seqlens.max()) if st.n_pairs else 1
+    return pipeline.ScoreStep(case.store, n_pairs=st.n_pairs,
+                              n_q_heads=st.n_q_heads,
+                              total_tokens=st.n_tokens, max_tokens=max_t,
+                              kernel_variant=kernel_variant,
+                              device=case.step.out.device,
+                              with_rows=with_rows)
+
+
+def run_score(case: Case, sstep):
+    import torch
+    from paper_2609_03311_amd import dopr_check_status
+    o = case.online
+    p = case.prm
+    sstep.run(0, case.doc_ids, case.cu, o["q"], o["k"], o["v"],
+              p["q_norm_w"], p["k_norm_w"], p["norm_w"], p["w_head"])
+    torch.cuda.synchronize()
+    return dopr_check_status(case.store)
+
+
+def compare_score(case: Case, sstep, pairs, tol=TOL):
+    import torch
+    ref = oracle_subset(case, pairs, last_only=True)
+    pt = torch.from_numpy(np.asarray(pairs, np.int64)).to(sstep.score.device)
+    got_s = sstep.score.index_select(0, pt).cpu().numpy()
+    got_l = sstep.logits.index_select(0, pt).cpu().numpy()
+    valid = ref["status"] == 0
+    e_s = float(np.abs(got_s - ref["score"]).max()) if len(pairs) else 0.0
+    e_l = float(np.abs(got_l - ref["logits"]).max()) if len(pairs) else 0.0
+    e_out = e_lse = 0.0
+    if sstep.out is not None:
+        got_o = sstep.out.index_select(0, pt).float().cpu().numpy()
+        got_lse = sstep.lse.index_select(0, pt).cpu().numpy()
+        e_out = float(np.abs(got_o - ref["out"]).max()) if len(pairs) else 0.0
+        fin = np.isfinite(ref["lse"])
+        assert (np.isneginf(got_lse) == ~fin).all(), "lse -inf mismatch"
+        e_lse = float(np.abs(got_lse[fin] - ref["lse"][fin]).max()) \
+            if fin.any() else 0.0
+    log(f"{case.st.name} score rows: {len(pairs)} pairs "
+        f"({int(valid.sum())} valid) max|dO|={e_out:.3e} "
+        f"max|dlse|={e_lse:.3e} max|ds|={e_s:.3e} max|dlogit|={e_l:.3e}")
+    assert e_out <= tol, f"O max-abs {e_out} > {tol}"
+    assert e_lse <= tol, f"lse max-abs {e_lse} > {tol}"
+    assert e_s <= tol, f"score max-abs {e_s} > {tol}"
+    assert e_l <= tol, f"logit max-abs {e_l} > {tol}"
+    return dict(out=e_out, score=e_s, lse=e_lse)

@@ -43,7 +43,8 @@ def test_struct_layouts_match_header(tmp_path):
     probe = tmp_path / "probe.c"
     structs = {"dopr_store_desc_t": D._StoreDesc,
                "dopr_attn_args_t": D._AttnArgs,
-               "dopr_score_args_t": D._ScoreArgs}
+               "dopr_score_args_t": D._ScoreArgs,
+               "dopr_score_head_t": D._ScoreHead}
     lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "dopr.h"',
              "int main(void) {"]
     for cname, py in structs.items():
@@ -118,6 +119,17 @@ def test_host_validation_codes():
         D.DOPR_ERR_INVALID_ARG  # NULL buffers
     s.n_pairs = 0
     assert L.dopr_score_logits(ctypes.byref(s), None) == D.DOPR_OK
+    hd = D._ScoreHead()
+    assert L.dopr_prefix_attn_score(None, 0, ctypes.byref(a), None, None) == \
+        D.DOPR_ERR_INVALID_ARG
+    assert "head is NULL" in D.dopr_last_error()
+    assert L.dopr_prefix_attn_score(None, 0, ctypes.byref(a),
+                                    ctypes.byref(hd), None) == \
+        D.DOPR_ERR_INVALID_ARG
+    assert "store is NULL" in D.dopr_last_error()
+    assert L.dopr_prefix_attn_score_workspace(None, ctypes.byref(a),
+                                              ctypes.byref(n)) == \
+        D.DOPR_ERR_INVALID_ARG
     assert L.dopr_check_status(None, None) == D.DOPR_ERR_INVALID_ARG
     assert D.dopr_status_str(D.DOPR_ERR_DOC_RANGE) == "DOPR_ERR_DOC_RANGE"
     assert D.dopr_status_str(D.DOPR_ERR_SEQLEN) == "DOPR_ERR_SEQLEN"
