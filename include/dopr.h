@@ -17,6 +17,9 @@
  *                      document only through its prefix states, Sec. 3.2.2).
  *   dopr_score_logits  the relevance score read off the score token's state
  *                      (Sec. 3.2.3, Eq. for s(q,d)), as a yes/no logit pair.
+ *   dopr_prefix_attn_score
+ *                      the last layer's share: only the score token's rows,
+ *                      with the score head fused into the attention epilogue.
  *
  * Conventions shared by every call
  *   - All device buffers are allocated by the caller and passed as raw device
@@ -123,8 +126,13 @@ typedef struct {
   int32_t n_pairs;          /* P >= 0                                       */
   int32_t n_q_heads;        /* Hq, multiple of the store's Hkv              */
   int32_t max_tokens;       /* upper bound on every T_p (>= 1)              */
-  int32_t kernel_variant;   /* 0 = automatic; 1..3 select a row-tile shape
-                               (identical results; for tuning sweeps);
+  int32_t kernel_variant;   /* 0 = automatic; 1, 2, 3, 6 select a tile
+                               shape (identical results; for tuning
+                               sweeps): 1 = 4 waves x 64 rows, 2 = 8 waves
+                               x 32 rows, 3 = 4 waves x 32 rows (each one
+                               block per CU, 256 prefix slots resident),
+                               6 = 4 waves x 32 rows, two blocks per CU,
+                               96 slots resident;
                                4 = exact running-max softmax for every row
                                (slower; the reference for the fast path);
                                5 = self-check: the fast pass queues every
@@ -205,7 +213,7 @@ dopr_status_t dopr_score_logits(const dopr_score_args_t *args, void *stream);
  *   out  dev bf16 [P, Hq, D]: the score rows, or NULL (not written);
  *   lse  dev fp32 [P, Hq], or NULL;
  * and the workspace comes from dopr_prefix_attn_score_workspace.
- * kernel_variant 1..3 select the automatic tile shape here.  A pair with a
+ * kernel_variant 1 and 3 select shape 6 here (2 and 6 as above).  A pair with a
  * bad doc id gets zero rows, lse -inf, logits and score 0, and a deferred
  * DOC_RANGE status.  All buffers are caller-owned.                         */
 typedef struct {

@@ -109,8 +109,8 @@ dopr_status_t check_attn(const dopr_store *st, const dopr_attn_args_t *a,
     return fail(DOPR_ERR_UNSUPPORTED,
                 "stacked rows (tokens, or pairs in score mode) * n_rep must "
                 "be < 2^31");
-  if (a->kernel_variant < 0 || a->kernel_variant > 5)
-    return fail(DOPR_ERR_INVALID_ARG, "kernel_variant must be in 0..5");
+  if (a->kernel_variant < 0 || a->kernel_variant > 6)
+    return fail(DOPR_ERR_INVALID_ARG, "kernel_variant must be in 0..6");
   if (!(a->softmax_scale > 0.f) || !std::isfinite(a->softmax_scale))
     return fail(DOPR_ERR_INVALID_ARG, "softmax_scale must be finite and > 0");
   if (!(a->rope_theta > 1.f) || !std::isfinite(a->rope_theta))

@@ -66,8 +66,6 @@ typedef float floatx16 __attribute__((ext_vector_type(16)));
 
 constexpr int D = kHeadDim;
 constexpr int KC = 32;      // keys per MFMA chunk
-constexpr int PSEG = 256;   // prefix slots resident in LDS at once
-constexpr int NCH = PSEG / KC;
 constexpr int kTotItems = 2;
 constexpr int kFixQueue = 8;  // cursor slot of the fixup pass
 constexpr float kLn2 = 0.69314718055994530942f;
@@ -79,6 +77,8 @@ constexpr float kNoRefBound = 64.f;  // |logit| <= 64: weights exp2(logit)
 // computed by the fast pass (its logit bound exceeds kNoRefBound); those
 // run the bounded-reference mode first, the others the exact mode.
 constexpr int32_t kFixUnscored = 1 << 30;
+// Largest prefix the two-blocks-per-CU shape keeps resident (3 chunks).
+constexpr int32_t kSmallPrefix = 3 * KC;
 
 struct AttnParams {
   const uint16_t *q, *k, *v, *qw, *kw;
@@ -114,9 +114,11 @@ struct AttnParams {
 // one set of per-lane read offsets.  The own-key chunk is double-buffered;
 // at item boundaries (no own chunk in flight) its first words carry the
 // work index broadcast and the per-wave overflow flags.
+template <int NCHK>
 struct Smem {
-  uint16_t pk[NCH][KC * D];   // prefix K chunks
-  uint16_t pv[NCH][D * KC];   // prefix V^T chunks
+  static constexpr int PSEG = NCHK * KC;  // prefix slots resident at once
+  uint16_t pk[NCHK][KC * D];  // prefix K chunks
+  uint16_t pv[NCHK][D * KC];  // prefix V^T chunks
   uint16_t ok[2][KC * D];     // own k^
   uint16_t ov[2][D * KC];     // own v^T
   __device__ int *words() { return reinterpret_cast<int *>(ok[0]); }
@@ -269,10 +271,12 @@ __device__ __forceinline__ void q_fragments(const uint16_t *qrow,
 // are left stale (their logits are masked by a select).  V^T columns past
 // the stored ones (up to the chunk end) are zeroed instead: masked keys
 // must multiply a finite value.  The store's pad columns [L, Lp) are zero.
-template <int WAVES>
+template <int WAVES, int NCHK>
 __device__ __forceinline__ void stage_prefix(const uint16_t *Kp,
                                              const uint16_t *VTp, int Lp,
-                                             int seg0, int n, Smem &sm) {
+                                             int seg0, int n,
+                                             Smem<NCHK> &sm) {
+  constexpr int PSEG = Smem<NCHK>::PSEG;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   // K: 1 KB block b = rows 4b..4b+3, lane -> (row, physical granule)
   const int kblocks = (n + 3) >> 2;
@@ -375,10 +379,10 @@ __device__ __forceinline__ void own_load(const AttnParams &P, const OwnStep &o,
 
 // k^ = RoPE(RMSNorm(k) * w) into sm.ok; v transposed into sm.ov.  Rows of
 // keys past the pair's end are zero.
-template <int WAVES>
+template <int WAVES, int NCHK>
 __device__ __forceinline__ void own_stage(const AttnParams &P,
-                                          const OwnRegs<WAVES> &r, Smem &sm,
-                                          int buf) {
+                                          const OwnRegs<WAVES> &r,
+                                          Smem<NCHK> &sm, int buf) {
   if (threadIdx.x >= 256 * (WAVES / 4)) return;
   const int t = threadIdx.x + opaque_zero();
   const int kk = (t >> 3) & 31, sub = t & 7;
@@ -586,13 +590,14 @@ __device__ __forceinline__ void attend(const uint16_t *kblk,
 // SMX fixed, so every loop below is straight-line code over one set of
 // accumulators.  Returns whether some row of this wave left the range the
 // fast modes guarantee (the unit is then recomputed in SAFE mode).
-template <int WAVES, int NQB, int SMX, bool SCORE>
-__device__ __forceinline__ bool run_unit(const AttnParams &P, Smem &sm,
+template <int WAVES, int NQB, int SMX, bool SCORE, int NCHK>
+__device__ __forceinline__ bool run_unit(const AttnParams &P, Smem<NCHK> &sm,
                                          const Frag &fo, int g, int row0,
                                          int row1, int L, int Lp,
                                          const uint16_t *Kp,
                                          const uint16_t *VTp, float B) {
   constexpr int PASS = WAVES * NQB * 32;
+  constexpr int PSEG = Smem<NCHK>::PSEG;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int lq = lane & 31, hf = lane >> 5;
   const int n_seg = (L + PSEG - 1) / PSEG;
@@ -661,7 +666,7 @@ __device__ __forceinline__ bool run_unit(const AttnParams &P, Smem &sm,
       const int n = L - seg0 < PSEG ? L - seg0 : PSEG;
       if (!resident) {
         __syncthreads();
-        stage_prefix<WAVES>(Kp, VTp, Lp, seg0, n, sm);
+        stage_prefix<WAVES, NCHK>(Kp, VTp, Lp, seg0, n, sm);
       }
       wait_vmem();
       __syncthreads();
@@ -685,7 +690,7 @@ __device__ __forceinline__ bool run_unit(const AttnParams &P, Smem &sm,
     // through the prefix products.)
     own_load<WAVES>(P, os, g, L, orr);
     __syncthreads();  // the previous pass's last own chunk is consumed
-    own_stage<WAVES>(P, orr, sm, 0);
+    own_stage<WAVES, NCHK>(P, orr, sm, 0);
     __syncthreads();
     int buf = 0;
     while (os.s <= s_hi) {
@@ -721,7 +726,7 @@ __device__ __forceinline__ bool run_unit(const AttnParams &P, Smem &sm,
       if (__any(need))  // wave-uniform: skip chunks no row of the wave sees
         attend<1, NQB, SMX>(sm.ok[buf], sm.ov[buf], fo, qf, acc, hf, B,
                             lim);
-      if (more) own_stage<WAVES>(P, orr, sm, buf ^ 1);
+      if (more) own_stage<WAVES, NCHK>(P, orr, sm, buf ^ 1);
       __syncthreads();
       buf ^= 1;
       os = nx;
@@ -800,10 +805,17 @@ __device__ __forceinline__ bool run_unit(const AttnParams &P, Smem &sm,
   return wave_bad;
 }
 
-template <int WAVES, int NQB, bool SAFE, bool SCORE>
-__global__ __launch_bounds__(WAVES * 64) __attribute__((
-    amdgpu_waves_per_eu(WAVES / 4, WAVES / 4))) void k_prefix_attn(AttnParams P) {
-  __shared__ __attribute__((aligned(16))) Smem sm;
+// Waves per SIMD: a block's waves spread over the CU's 4 SIMDs, and two
+// blocks share a CU when the LDS block fits in half of it (160 KB).
+constexpr int waves_per_simd(int waves, int nchk) {
+  return (waves / 4) * ((nchk + 2) * 2 * KC * D * 2 <= 81920 ? 2 : 1);
+}
+
+template <int WAVES, int NQB, bool SAFE, bool SCORE, int NCHK>
+__global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(
+    waves_per_simd(WAVES, NCHK),
+    waves_per_simd(WAVES, NCHK)))) void k_prefix_attn(AttnParams P) {
+  __shared__ __attribute__((aligned(16))) Smem<NCHK> sm;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int lq = lane & 31, hf = lane >> 5;
   const int queue = SAFE ? kFixQueue : (blockIdx.x & 7);
@@ -842,12 +854,12 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((
     const float kbound = fmaxf(
         P.kown[0], P.kmax[((int64_t)doc * P.n_layers + P.layer) * P.Hkv + g]);
     const float B = P.c * P.kown[1] * kbound * 1.001f;
-    const int n_seg = (L + PSEG - 1) / PSEG;
+    const int n_seg = (L + Smem<NCHK>::PSEG - 1) / Smem<NCHK>::PSEG;
     const bool resident = n_seg <= 1;
     if (!SAFE) {
       if (B <= kNoRefBound) {
-        if (resident && L > 0) stage_prefix<WAVES>(Kp, VTp, Lp, 0, L, sm);
-        wave_bad = run_unit<WAVES, NQB, 0, SCORE>(P, sm, fo, g, row0, row1, L, Lp,
+        if (resident && L > 0) stage_prefix<WAVES, NCHK>(Kp, VTp, Lp, 0, L, sm);
+        wave_bad = run_unit<WAVES, NQB, 0, SCORE, NCHK>(P, sm, fo, g, row0, row1, L, Lp,
                                            Kp, VTp, B) ||
                    P.flag_all;
       }
@@ -864,11 +876,11 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((
       }
       __syncthreads();
     } else {
-      if (resident && L > 0) stage_prefix<WAVES>(Kp, VTp, Lp, 0, L, sm);
+      if (resident && L > 0) stage_prefix<WAVES, NCHK>(Kp, VTp, Lp, 0, L, sm);
       // (self-check mode sends every unit to the exact mode)
       bool exact = !unscored || P.flag_all;
       if (!exact) {
-        wave_bad = run_unit<WAVES, NQB, 1, SCORE>(P, sm, fo, g, row0, row1, L, Lp,
+        wave_bad = run_unit<WAVES, NQB, 1, SCORE, NCHK>(P, sm, fo, g, row0, row1, L, Lp,
                                            Kp, VTp, B);
         __syncthreads();
         if (lane == 0) sm.words()[1 + wave] = wave_bad;
@@ -877,7 +889,7 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((
         __syncthreads();
       }
       if (exact)
-        run_unit<WAVES, NQB, 2, SCORE>(P, sm, fo, g, row0, row1, L, Lp, Kp, VTp, B);
+        run_unit<WAVES, NQB, 2, SCORE, NCHK>(P, sm, fo, g, row0, row1, L, Lp, Kp, VTp, B);
       __syncthreads();  // every wave is done with this item's LDS
     }
   }
@@ -919,7 +931,7 @@ __global__ __launch_bounds__(256) void k_queue_all(const int64_t *totals,
   if (blockIdx.x == 0 && threadIdx.x == 0) counters[kCntFix] = (int32_t)n;
 }
 
-template <int WAVES, int NQB, bool SAFE, bool SCORE>
+template <int WAVES, int NQB, bool SAFE, bool SCORE, int NCHK = 8>
 hipError_t launch_variant(const AttnParams &p, hipStream_t s, int max_grid) {
   int dev = 0, n_cu = 0, per_cu = 0;
   hipError_t e = hipGetDevice(&dev);
@@ -927,7 +939,7 @@ hipError_t launch_variant(const AttnParams &p, hipStream_t s, int max_grid) {
   e = hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev);
   if (e != hipSuccess) return e;
   e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
-      &per_cu, k_prefix_attn<WAVES, NQB, SAFE, SCORE>, WAVES * 64, 0);
+      &per_cu, k_prefix_attn<WAVES, NQB, SAFE, SCORE, NCHK>, WAVES * 64, 0);
   if (e != hipSuccess) return e;
   if (per_cu < 1) per_cu = 1;
   // Persistent grid, a multiple of 8 so block b always serves queue b % 8
@@ -935,7 +947,7 @@ hipError_t launch_variant(const AttnParams &p, hipStream_t s, int max_grid) {
   unsigned grid = (unsigned)(n_cu * per_cu);
   grid = (grid + 7) / 8 * 8;
   if (max_grid > 0 && grid > (unsigned)max_grid) grid = (unsigned)max_grid;
-  hipLaunchKernelGGL((k_prefix_attn<WAVES, NQB, SAFE, SCORE>), dim3(grid),
+  hipLaunchKernelGGL((k_prefix_attn<WAVES, NQB, SAFE, SCORE, NCHK>), dim3(grid),
                      dim3(WAVES * 64), 0, s, p);
   return hipGetLastError();
 }
@@ -991,16 +1003,27 @@ hipError_t launch_attention(const AttnCall &c, const Plan &pl,
     p.head_norm_w = static_cast<const uint16_t *>(c.head->norm_w);
     p.head_w = static_cast<const uint16_t *>(c.head->w_head);
   }
-  switch (score ? (a->kernel_variant == 4 ? 4 : 0) : a->kernel_variant) {
-    case 1:
-    case 5: e = launch_variant<4, 2, false, false>(p, s, 0); break;
+  // Tile shape.  Automatic: two 4-wave blocks per CU (80 KB of LDS each,
+  // 96 prefix slots resident) when every prefix fits or when only score
+  // rows are attended (one pass per unit, so nothing is restaged); else one
+  // 8-wave block per CU with 256 slots resident.
+  int shape_v = a->kernel_variant;
+  if (shape_v == 0 || shape_v == 5)
+    shape_v = score || st.max_len <= kSmallPrefix ? 6 : 2;
+  if (score && (shape_v == 1 || shape_v == 3)) shape_v = 6;
+  switch (shape_v) {
+    case 1: e = launch_variant<4, 2, false, false>(p, s, 0); break;
     case 3: e = launch_variant<4, 1, false, false>(p, s, 0); break;
+    case 6:
+      e = score ? launch_variant<4, 1, false, true, 3>(p, s, 0)
+                : launch_variant<4, 1, false, false, 3>(p, s, 0);
+      break;
     case 4:
       hipLaunchKernelGGL(k_queue_all, dim3(256), dim3(256), 0, s, p.totals,
                          p.items_cap, p.Hkv, p.counters, p.fix);
       e = hipGetLastError();
       break;
-    default:  // 0, 2 (score mode: every variant but 4)
+    default:  // 2
       e = score ? launch_variant<8, 1, false, true>(p, s, 0)
                 : launch_variant<8, 1, false, false>(p, s, 0);
       break;

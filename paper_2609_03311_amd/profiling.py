@@ -22,7 +22,10 @@ import sys
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 KERNEL_SOURCES = ("csrc/attn.hip", "csrc/internal.hpp")
-ATTN_KERNEL = r"k_prefix_attn<8, 1, false>|k_prefix_attn<8,1,false>"
+# the dominant kernel of each path on the Qwen3-8B-shaped workload: 8 waves,
+# 256 slots resident (full layer); two 4-wave blocks per CU (score rows)
+ATTN_KERNEL = r"k_prefix_attn<8, ?1, ?false, ?false, ?8>"
+SCORE_KERNEL = r"k_prefix_attn<4, ?1, ?false, ?true, ?3>"
 CALIB_KERNEL = r"bitwise_not"
 CALIB_BYTES = 1 << 30
 

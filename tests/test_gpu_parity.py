@@ -67,7 +67,7 @@ SWEEP = [
 ]
 
 
-@pytest.mark.parametrize("variant", [1, 2, 3, 4])
+@pytest.mark.parametrize("variant", [1, 2, 3, 4, 6])
 @pytest.mark.parametrize("i", range(len(SWEEP)))
 def test_shape_sweep(i, variant):
     Hq, Hkv, lens, P, Ts = SWEEP[i]
@@ -164,11 +164,12 @@ def test_deterministic_and_tiling_invariant():
     o1 = a.step.out.clone()
     run(a)
     assert torch.equal(o1, a.step.out)
-    b = setup(st, seed=2, kernel_variant=2)
-    run(b)
-    diff = (o1.float() - b.step.out.float()).abs().max().item()
-    assert torch.equal(o1, b.step.out), f"variants differ by {diff}"
-    assert torch.equal(a.step.score, b.step.score)
+    for vb in (2, 6):
+        b = setup(st, seed=2, kernel_variant=vb)
+        run(b)
+        diff = (o1.float() - b.step.out.float()).abs().max().item()
+        assert torch.equal(o1, b.step.out), f"variant {vb} differs by {diff}"
+        assert torch.equal(a.step.score, b.step.score)
     # permute pairs (and their token segments)
     perm = np.random.default_rng(3).permutation(st.n_pairs)
     cu = st.cu_seqlens

@@ -83,12 +83,13 @@ EDGE = [
 ]
 
 
-@pytest.mark.parametrize("variant", [0, 4, 5])
+@pytest.mark.parametrize("variant", [0, 2, 4, 5])
 @pytest.mark.parametrize("i", range(len(EDGE)))
 def test_score_edge_shapes(i, variant):
-    """Empty and non-resident-size prefixes (L = 0, L > 256), T = 1, GQA
-    ratios 1, 2, 4 and 16 heads per kv head, in the automatic, exact and
-    self-check variants."""
+    """Empty prefixes and prefixes longer than the resident segment (L = 0,
+    L > 96, L > 256), T = 1, GQA ratios 1, 4 and 16 q heads per kv head, in
+    the automatic shape (two blocks per CU), the 8-wave shape, and the exact
+    and self-check variants."""
     Hq, Hkv, lens, P, Ts = EDGE[i]
     rng = np.random.default_rng(300 + i)
     doc_ids = rng.integers(0, len(lens), P).astype(np.int32)
