@@ -10,6 +10,10 @@ synthetic tensors already resident in HBM when timing starts.
 Prints one JSON line: pairs/s per decoder layer (whole job), the attention
 kernel's achieved algorithmic HBM GB/s against the 8 TB/s peak, and the
 float64 CPU oracle timed on a bounded sample of the same workload.
+
+--path score measures last-layer scoring instead: only each pair's score
+token is attended (still over its whole prefix and all its own keys) and
+the score head is fused into the attention epilogue.
 """
 import argparse
 import ctypes
@@ -26,6 +30,8 @@ if ROOT not in sys.path:
 
 METRIC = ("query-doc pairs/sec per decoder layer; achieved HBM GB/s vs "
           "MI355X peak")
+METRIC_SCORE = ("query-doc pairs/sec for the last decoder layer (score-token "
+                "rows + fused score head); achieved HBM GB/s vs MI355X peak")
 PEAK_HBM_GBS = 8000.0
 PEAK_BF16_TFLOPS = 2500.0
 
@@ -107,13 +113,36 @@ def algorithmic_work(st):
                 score_bytes=score_bytes)
 
 
-def measured_traffic(config, variant):
+def algorithmic_work_score(st, rows):
+    """Last-layer scoring: each unique prefix once, every own key and value
+    once, the score token's q row, its output row when written (`rows`),
+    the head's partial sums (written, read back), the head weights and the
+    logits/score; flops of the score rows only."""
+    uniq = np.unique(st.doc_ids)
+    L = st.doc_len[uniq].astype(np.int64)
+    hkv, hq, D = st.n_kv_heads, st.n_q_heads, st.head_dim
+    P = st.n_pairs
+    prefix = int(L.sum()) * hkv * D * 2 * 2
+    kv = st.n_tokens * 2 * hkv * D * 2
+    q = P * hq * D * 2
+    out = P * hq * D * 2 + P * hq * 4 if rows else 0
+    head = P * hq * 3 * 4 * 2 + 3 * hq * D * 2 + P * 12
+    meta = P * 8 + len(uniq) * 12
+    T = st.seqlens.astype(np.int64)
+    Lp = st.doc_len[st.doc_ids].astype(np.int64)
+    flops = int(4 * hq * D * (Lp + T).sum())
+    return dict(prefix=prefix, qkv=kv + q, out=out + head, meta=meta,
+                total=prefix + kv + q + out + head + meta, flops=flops,
+                unique_docs=int(len(uniq)))
+
+
+def measured_traffic(config, variant, path_kind="full"):
     """HBM bytes per attention launch from the committed rocprofv3 counter
     summary of this workload, or None when there is none or the kernel's
     sources changed since the counters were taken."""
     from paper_2609_03311_amd import profiling
-    path = os.path.join(ROOT, "profiles",
-                        f"k_prefix_attn_{config}_traffic.txt")
+    tag = "k_prefix_attn_score" if path_kind == "score" else "k_prefix_attn"
+    path = os.path.join(ROOT, "profiles", f"{tag}_{config}_traffic.txt")
     vals = profiling.read_summary(path)
     if variant != 0 or "traffic_bytes_per_launch" not in vals:
         return None
@@ -130,9 +159,11 @@ def bits(t):
         np.uint16)
 
 
-def cpu_baseline(st, k_src, v_src, doc_off, online, prm, seconds):
+def cpu_baseline(st, k_src, v_src, doc_off, online, prm, seconds,
+                 last_only=False):
     """The float64 oracle on a bounded sample of the same workload's pairs
-    (deterministic order), on this host's cores."""
+    (deterministic order), on this host's cores.  last_only: the oracle of
+    last-layer scoring (score-token rows only)."""
     import torch
 
     import oracle
@@ -167,8 +198,9 @@ def cpu_baseline(st, k_src, v_src, doc_off, online, prm, seconds):
         nw, wh = bits(prm["norm_w"]), bits(prm["w_head"])
         t0 = time.perf_counter()
         out, _, _ = oracle.prefix_attn(*args, n_q_heads=st.n_q_heads,
-                                       n_kv_heads=st.n_kv_heads, L=L)
-        h = out[scu[1:] - 1].reshape(len(pairs), -1)
+                                       n_kv_heads=st.n_kv_heads,
+                                       last_only=last_only, L=L)
+        h = (out if last_only else out[scu[1:] - 1]).reshape(len(pairs), -1)
         oracle.score(h, nw, wh, L=L)
         return time.perf_counter() - t0
 
@@ -187,8 +219,9 @@ def cpu_baseline(st, k_src, v_src, doc_off, online, prm, seconds):
     return {"value": round(total_n / total_t, 3), "unit": "pairs/s",
             "cores": int(threads), "kind": "oracle",
             "sample": f"{total_n} of {st.n_pairs} pairs (seeded random "
-                      f"order), float64 C oracle incl. score head, "
-                      f"{total_t:.1f}s"}
+                      f"order), float64 C oracle"
+                      f"{' of the score-token rows' if last_only else ''} "
+                      f"incl. score head, {total_t:.1f}s"}
 
 
 def main():
@@ -199,6 +232,13 @@ def main():
     ap.add_argument("--config", default="qwen3_8b",
                     choices=sorted(DESCRIPTIONS))
     ap.add_argument("--variant", type=int, default=0)
+    ap.add_argument("--path", choices=["full", "score"], default="full",
+                    help="full: every online row of one layer (default); "
+                         "score: last-layer scoring (score-token rows, "
+                         "fused score head)")
+    ap.add_argument("--no-score-rows", action="store_true",
+                    help="with --path score: do not write the score rows "
+                         "(the fused head alone)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -228,11 +268,20 @@ def main():
     prm = workloads.params(st, dev, 6)
     store = pipeline.make_store(st.doc_len, st.n_kv_heads, k_src, v_src,
                                 device=dev)
-    step = pipeline.OnlineStep(store, n_pairs=st.n_pairs,
-                               n_q_heads=st.n_q_heads,
-                               total_tokens=st.n_tokens,
-                               max_tokens=int(st.seqlens.max()),
-                               kernel_variant=args.variant, device=dev)
+    score_path = args.path == "score"
+    if score_path:
+        step = pipeline.ScoreStep(store, n_pairs=st.n_pairs,
+                                  n_q_heads=st.n_q_heads,
+                                  total_tokens=st.n_tokens,
+                                  max_tokens=int(st.seqlens.max()),
+                                  kernel_variant=args.variant, device=dev,
+                                  with_rows=not args.no_score_rows)
+    else:
+        step = pipeline.OnlineStep(store, n_pairs=st.n_pairs,
+                                   n_q_heads=st.n_q_heads,
+                                   total_tokens=st.n_tokens,
+                                   max_tokens=int(st.seqlens.max()),
+                                   kernel_variant=args.variant, device=dev)
     doc_ids = torch.from_numpy(st.doc_ids).to(dev)
     cu = torch.from_numpy(st.cu_seqlens).to(dev)
     torch.cuda.synchronize()
@@ -253,6 +302,11 @@ def main():
 
     def one_step(i=None):
         timing = None if i is None else (ev.ev[2 * i], ev.ev[2 * i + 1])
+        if score_path:
+            step.run(0, doc_ids, cu, online["q"], online["k"], online["v"],
+                     prm["q_norm_w"], prm["k_norm_w"], prm["norm_w"],
+                     prm["w_head"], timing=timing)
+            return
         step.attention(0, doc_ids, cu, online["q"], online["k"],
                        online["v"], prm["q_norm_w"], prm["k_norm_w"],
                        timing=timing)
@@ -282,11 +336,14 @@ def main():
         f"attention kernel avg {attn_avg:.3f} ms "
         f"(min {min(attn_ms):.3f}, max {max(attn_ms):.3f})")
 
-    w = algorithmic_work(st)
+    w = (algorithmic_work_score(st, not args.no_score_rows) if score_path
+         else algorithmic_work(st))
     achieved = w["total"] / (attn_avg * 1e-3) / 1e9
-    traffic = measured_traffic(args.config, args.variant)
+    traffic = measured_traffic(args.config, args.variant, args.path)
+    if score_path and args.no_score_rows:
+        traffic = None
     result = {
-        "metric": METRIC,
+        "metric": METRIC_SCORE if score_path else METRIC,
         "value": round(st.n_pairs / (ms_step * 1e-3), 1),
         "unit": "pairs/s",
         "n_gpus": 1,
@@ -306,6 +363,9 @@ def main():
             "online_tokens": st.n_tokens,
             "unique_docs": w["unique_docs"],
             "kernel_variant": args.variant,
+            "path": ("last-layer scoring" + (", no score rows written"
+                                             if args.no_score_rows else "")
+                     if score_path else "full online layer"),
             "parallelism": "single GPU",
         },
         "attention_ms": round(attn_avg, 4),
@@ -325,7 +385,8 @@ def main():
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a bounded sample")
         result["cpu_baseline"] = cpu_baseline(st, k_src, v_src, doc_off,
-                                              online, prm, args.cpu_seconds)
+                                              online, prm, args.cpu_seconds,
+                                              last_only=score_path)
     print(json.dumps(result), flush=True)
 
 

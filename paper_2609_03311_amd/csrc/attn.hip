@@ -473,21 +473,16 @@ __device__ __forceinline__ Frag frag_offsets(int lq, int hf) {
   return f;
 }
 
-// One 32-key chunk for NQB query blocks: S^T = K Q^T, weights, O^T += V^T P^T.
-// MODE 0: no mask; MODE 1: key index (0..31 within the chunk) must be
-// <= lim[qb] (a per-row limit, < 0 hides every key of the chunk).
-// SMX 0: weights exp2(S); 1: exp2(S - m), m fixed at the first visible
-// chunk to min(B, max + 80); 2: exact running maximum.
-template <int MODE, int NQB, int SMX>
-__device__ __forceinline__ void attend(const uint16_t *kblk,
-                                       const uint16_t *vblk, const Frag &fo,
-                                       const bf16x8 (*qf)[8], Acc *acc,
-                                       int hf, float B, const int *lim) {
-  // K fragments are read RA at a time ahead of the QK products, and V^T
-  // fragments RA at a time ahead of the PV products, so LDS latency
-  // overlaps MFMA and VALU work (RA trades registers for latency hiding).
-  constexpr int RA = 4;
-  floatx16 S[NQB];
+// K fragments are read RA at a time ahead of the QK products, and V^T
+// fragments RA at a time ahead of the PV products, so LDS latency overlaps
+// MFMA and VALU work (RA trades registers for latency hiding).
+constexpr int RA = 4;
+
+// S^T = K Q^T for one 32-key chunk (logits in log2 units: q^ carries the
+// scale).
+template <int NQB>
+__device__ __forceinline__ void qk_part(const uint16_t *kblk, const Frag &fo,
+                                        const bf16x8 (*qf)[8], floatx16 *S) {
 #pragma unroll
   for (int qb = 0; qb < NQB; ++qb)
 #pragma unroll
@@ -505,15 +500,27 @@ __device__ __forceinline__ void attend(const uint16_t *kblk,
         S[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[s], qf[qb][s0 + s],
                                                         S[qb], 0, 0, 0);
   }
-  bf16x8 vf[RA];
-  auto vread = [&](int f0) {  // fragments f0..f0+RA-1, f = (db, t)
+}
+
+// V^T fragments f0 .. f0 + RA - 1 of a chunk, f = (db, t).
+__device__ __forceinline__ void v_read(const uint16_t *vblk, const Frag &fo,
+                                       int f0, bf16x8 *vf) {
 #pragma unroll
-    for (int f = f0; f < f0 + RA; ++f)
-      vf[f - f0] = *reinterpret_cast<const bf16x8 *>(
-          vblk + (f >> 1) * (32 * KC) + fo.v[f & 1]);
-  };
-  vread(0);
-  bf16x8 pb[NQB][2];
+  for (int f = f0; f < f0 + RA; ++f)
+    vf[f - f0] = *reinterpret_cast<const bf16x8 *>(
+        vblk + (f >> 1) * (32 * KC) + fo.v[f & 1]);
+}
+
+// Weights of one chunk's logits into pb (bf16), updating each row's
+// normaliser (and reference, rescaling O, in modes 1 and 2).
+// MODE 0: no mask; MODE 1: key index (0..31 within the chunk) must be
+// <= lim[qb] (a per-row limit, < 0 hides every key of the chunk).
+// SMX 0: weights exp2(S); 1: exp2(S - m), m fixed at the first visible
+// chunk to min(B, max + 80); 2: exact running maximum.
+template <int MODE, int NQB, int SMX>
+__device__ __forceinline__ void softmax_part(floatx16 *S, Acc *acc, int hf,
+                                             float B, const int *lim,
+                                             bf16x8 (*pb)[2]) {
 #pragma unroll
   for (int qb = 0; qb < NQB; ++qb) {
     if (MODE == 1) {
@@ -574,9 +581,16 @@ __device__ __forceinline__ void attend(const uint16_t *kblk,
                                             one, A.l, false);
     }
   }
+}
+
+// O^T += V^T P^T for one chunk; vf holds the first RA V^T fragments.
+template <int NQB>
+__device__ __forceinline__ void pv_part(const uint16_t *vblk, const Frag &fo,
+                                        bf16x8 *vf, Acc *acc,
+                                        const bf16x8 (*pb)[2]) {
 #pragma unroll
   for (int f0 = 0; f0 < 8; f0 += RA) {
-    if (f0 > 0) vread(f0);
+    if (f0 > 0) v_read(vblk, fo, f0, vf);
 #pragma unroll
     for (int f = f0; f < f0 + RA; ++f)
 #pragma unroll
@@ -584,6 +598,22 @@ __device__ __forceinline__ void attend(const uint16_t *kblk,
         acc[qb].o[f >> 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
             vf[f - f0], pb[qb][f & 1], acc[qb].o[f >> 1], 0, 0, 0);
   }
+}
+
+// One 32-key chunk for NQB query blocks: S^T = K Q^T, weights, O^T += V^T P^T
+// (the first V^T fragments are read before the weights are formed).
+template <int MODE, int NQB, int SMX>
+__device__ __forceinline__ void attend(const uint16_t *kblk,
+                                       const uint16_t *vblk, const Frag &fo,
+                                       const bf16x8 (*qf)[8], Acc *acc,
+                                       int hf, float B, const int *lim) {
+  floatx16 S[NQB];
+  qk_part<NQB>(kblk, fo, qf, S);
+  bf16x8 vf[RA];
+  v_read(vblk, fo, 0, vf);
+  bf16x8 pb[NQB][2];
+  softmax_part<MODE, NQB, SMX>(S, acc, hf, B, lim, pb);
+  pv_part<NQB>(vblk, fo, vf, acc, pb);
 }
 
 // The passes of one work unit (an item for one kv head) with softmax mode
