@@ -52,6 +52,9 @@ def _bind(lib):
         f64, f64, f64, P, P, P, i32]
     lib.dopr_oracle_score_attn.restype = ctypes.c_int
     lib.dopr_oracle_score_attn.argtypes = lib.dopr_oracle_prefix_attn.argtypes
+    lib.dopr_oracle_prefix_attn_f64.restype = ctypes.c_int
+    lib.dopr_oracle_prefix_attn_f64.argtypes = \
+        lib.dopr_oracle_prefix_attn.argtypes
     lib.dopr_oracle_score.restype = ctypes.c_int
     lib.dopr_oracle_score.argtypes = [i32, i32, P, P, P, f64, P, P]
     lib.dopr_oracle_group.restype = ctypes.c_int
@@ -110,9 +113,12 @@ def prefix_attn(doc_ids, cu_seqlens, doc_len, doc_off, prefix_k, prefix_v,
     doc_off = _c(doc_off, np.int64)
     pk = _c(prefix_k, np.uint16)
     pv = _c(prefix_v, np.uint16)
-    q = _c(q, np.uint16)
-    k = _c(k, np.uint16)
-    v = _c(v, np.uint16)
+    # float64 online projections (the decoder-layer oracle) or bf16 bits
+    f64 = np.asarray(q).dtype == np.float64
+    qkv_t = np.float64 if f64 else np.uint16
+    q = _c(q, qkv_t)
+    k = _c(k, qkv_t)
+    v = _c(v, qkv_t)
     wq = _c(q_norm_w, np.uint16)
     wk = _c(k_norm_w, np.uint16)
     D = q.shape[-1]
@@ -129,7 +135,12 @@ def prefix_attn(doc_ids, cu_seqlens, doc_len, doc_off, prefix_k, prefix_v,
     if pk.size == 0:  # keep valid pointers for documents with no slots
         pk = np.zeros((1, n_kv_heads, D), np.uint16)
         pv = np.zeros((1, n_kv_heads, D), np.uint16)
-    fn = L.dopr_oracle_score_attn if last_only else L.dopr_oracle_prefix_attn
+    if f64:
+        assert not last_only
+        fn = L.dopr_oracle_prefix_attn_f64
+    else:
+        fn = (L.dopr_oracle_score_attn if last_only
+              else L.dopr_oracle_prefix_attn)
     rc = fn(
         P, n_q_heads, n_kv_heads, D, _p(doc_ids), _p(cu), doc_len.shape[0],
         _p(doc_len), _p(doc_off), _p(pk), _p(pv), _p(q), _p(k), _p(v),
@@ -138,6 +149,67 @@ def prefix_attn(doc_ids, cu_seqlens, doc_len, doc_off, prefix_k, prefix_v,
     if rc != 0:
         raise RuntimeError(f"oracle prefix_attn failed: {rc}")
     return out, lse, status
+
+
+def bf16_bits_to_f64(u) -> np.ndarray:
+    """Exact widening of bf16 bit patterns (the top half of an fp32)."""
+    u = np.ascontiguousarray(u, dtype=np.uint16)
+    return (u.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
+def _rms_norm_rows(x, w, eps):
+    """RMSNorm over the last axis with a gain: w * x / sqrt(mean x^2 + eps)."""
+    return w * (x / np.sqrt(np.mean(x * x, axis=-1, keepdims=True) + eps))
+
+
+LAYER_WEIGHTS = ("attn_norm", "wq", "wk", "wv", "wo", "mlp_norm", "w_gate",
+                 "w_up", "w_down")
+
+
+def decoder_layer(x, doc_ids, cu_seqlens, doc_len, doc_off, prefix_k,
+                  prefix_v, weights, q_norm_w, k_norm_w, *, n_q_heads,
+                  n_kv_heads, rms_eps=1e-6, rope_theta=1e6,
+                  softmax_scale=None, threads=0, L=None):
+    """One decoder layer of the online pass, float64 throughout.
+
+    Online, only the query and score tokens run through the reranker while
+    every layer's attention also sees the document's stored prefix states
+    (Sec. 3.4, Sec. 3.2.2); the layer is the Qwen3 decoder layer the paper
+    builds on: pre-norm attention with a residual, then a pre-norm SwiGLU
+    MLP with a residual.  Linear maps follow the stored-weight convention
+    y = x W^T (W is [out, in]).
+
+    x: bf16 bits [Ntok, W] entering the layer; weights: dict of bf16 bits
+    attn_norm [W], wq [Hq*D, W], wk [Hkv*D, W], wv [Hkv*D, W],
+    wo [W, Hq*D], mlp_norm [W], w_gate [I, W], w_up [I, W], w_down [W, I].
+    Returns (y float64 [Ntok, W], attention rows float64 [Ntok, Hq, D],
+    status int32 [P]).
+    """
+    f = bf16_bits_to_f64
+    X = f(x)
+    ntok, W = X.shape
+    D = 128
+    w = {k: f(weights[k]) for k in LAYER_WEIGHTS}
+    # attention block: norm, projections, attention over [prefix ; own]
+    h = _rms_norm_rows(X, w["attn_norm"], rms_eps)
+    q = (h @ w["wq"].T).reshape(ntok, n_q_heads, D)
+    k = (h @ w["wk"].T).reshape(ntok, n_kv_heads, D)
+    v = (h @ w["wv"].T).reshape(ntok, n_kv_heads, D)
+    att, _, status = prefix_attn(doc_ids, cu_seqlens, doc_len, doc_off,
+                                 prefix_k, prefix_v, q, k, v, q_norm_w,
+                                 k_norm_w, n_q_heads=n_q_heads,
+                                 n_kv_heads=n_kv_heads, rms_eps=rms_eps,
+                                 rope_theta=rope_theta,
+                                 softmax_scale=softmax_scale, threads=threads,
+                                 L=L)
+    x2 = X + att.reshape(ntok, n_q_heads * D) @ w["wo"].T
+    # MLP block: norm, gate and up projections, SiLU(gate) * up, down
+    h2 = _rms_norm_rows(x2, w["mlp_norm"], rms_eps)
+    g = h2 @ w["w_gate"].T
+    u = h2 @ w["w_up"].T
+    a = g / (1.0 + np.exp(-g)) * u
+    y = x2 + a @ w["w_down"].T
+    return y, att, status
 
 
 def score(h, norm_w, w_head, rms_eps=1e-6, L=None):

@@ -85,17 +85,24 @@ static int doc_is_valid(int32_t doc, int64_t n_docs, const int32_t *doc_len) {
  *   its lse is -inf).
  * Returns 0, or a negative code for malformed arguments.
  */
+/* Element i of an online projection held either as bf16 bit patterns or as
+ * doubles (the decoder-layer oracle hands over its own float64 q, k, v). */
+static double online_elem(const void *a, int64_t i, int f64) {
+  return f64 ? ((const double *)a)[i] : bf16_to_double(((const uint16_t *)a)[i]);
+}
+
 /* last_only = 0: every online row, out/lse indexed by token.  last_only = 1:
  * only each pair's last row j = T_p - 1 (its score token), out/lse indexed
- * by pair; the own keys and values of all T_p tokens are still formed. */
+ * by pair; the own keys and values of all T_p tokens are still formed.
+ * qkv_f64: q, k, v are double arrays instead of bf16. */
 static int attention(
     int32_t n_pairs, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
     const int32_t *doc_ids, const int32_t *cu_seqlens, int64_t n_docs,
     const int32_t *doc_len, const int64_t *doc_off, const uint16_t *prefix_k,
-    const uint16_t *prefix_v, const uint16_t *q, const uint16_t *k,
-    const uint16_t *v, const uint16_t *q_norm_w, const uint16_t *k_norm_w,
-    double rms_eps, double rope_theta, double softmax_scale, double *out,
-    double *lse, int32_t *pair_status, int32_t n_threads, int last_only) {
+    const uint16_t *prefix_v, const void *q, const void *k, const void *v,
+    const uint16_t *q_norm_w, const uint16_t *k_norm_w, double rms_eps,
+    double rope_theta, double softmax_scale, double *out, double *lse,
+    int32_t *pair_status, int32_t n_threads, int last_only, int qkv_f64) {
   if (n_pairs < 0 || n_q_heads <= 0 || n_kv_heads <= 0 || head_dim <= 0 ||
       head_dim % 2 || n_q_heads % n_kv_heads)
     return ORACLE_ERR_ARG;
@@ -156,14 +163,14 @@ static int attention(
     /* Step 2: own keys k^ = RoPE_{L+j}(RMSNorm(k) * w_k); values as given. */
     for (int j = 0; j < T; ++j)
       for (int g = 0; g < Hkv; ++g) {
-        const uint16_t *src = k + ((tok0 + j) * Hkv + g) * D;
-        for (int i = 0; i < D; ++i) x[i] = bf16_to_double(src[i]);
+        const int64_t ks = ((tok0 + j) * Hkv + g) * D;
+        for (int i = 0; i < D; ++i) x[i] = online_elem(k, ks + i, qkv_f64);
         double *dst = khat + ((int64_t)j * Hkv + g) * D;
         rms_norm(x, wk, D, rms_eps, dst);
         rope(dst, D, (double)(L + j), rope_theta);
-        const uint16_t *vs = v + ((tok0 + j) * Hkv + g) * D;
+        const int64_t vs = ((tok0 + j) * Hkv + g) * D;
         double *vd = vown + ((int64_t)j * Hkv + g) * D;
-        for (int i = 0; i < D; ++i) vd[i] = bf16_to_double(vs[i]);
+        for (int i = 0; i < D; ++i) vd[i] = online_elem(v, vs + i, qkv_f64);
       }
 
     /* Step 3: every online token j of every q head h attends to all L
@@ -173,8 +180,8 @@ static int attention(
         const int j = jq;
         const int64_t orow = last_only ? p : tok0 + j;
         const int g = h / n_rep;
-        const uint16_t *src = q + ((tok0 + j) * Hq + h) * D;
-        for (int i = 0; i < D; ++i) x[i] = bf16_to_double(src[i]);
+        const int64_t qs = ((tok0 + j) * Hq + h) * D;
+        for (int i = 0; i < D; ++i) x[i] = online_elem(q, qs + i, qkv_f64);
         rms_norm(x, wq, D, rms_eps, qhat);
         rope(qhat, D, (double)(L + j), rope_theta);
 
@@ -230,7 +237,26 @@ int dopr_oracle_prefix_attn(
   return attention(n_pairs, n_q_heads, n_kv_heads, head_dim, doc_ids,
                    cu_seqlens, n_docs, doc_len, doc_off, prefix_k, prefix_v,
                    q, k, v, q_norm_w, k_norm_w, rms_eps, rope_theta,
-                   softmax_scale, out, lse, pair_status, n_threads, 0);
+                   softmax_scale, out, lse, pair_status, n_threads, 0, 0);
+}
+
+/*
+ * The same attention with the online projections q [Ntok, Hq, D] and k, v
+ * [Ntok, Hkv, D] given as doubles (the decoder-layer oracle forms them in
+ * float64 from its own projections).
+ */
+int dopr_oracle_prefix_attn_f64(
+    int32_t n_pairs, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
+    const int32_t *doc_ids, const int32_t *cu_seqlens, int64_t n_docs,
+    const int32_t *doc_len, const int64_t *doc_off, const uint16_t *prefix_k,
+    const uint16_t *prefix_v, const double *q, const double *k,
+    const double *v, const uint16_t *q_norm_w, const uint16_t *k_norm_w,
+    double rms_eps, double rope_theta, double softmax_scale, double *out,
+    double *lse, int32_t *pair_status, int32_t n_threads) {
+  return attention(n_pairs, n_q_heads, n_kv_heads, head_dim, doc_ids,
+                   cu_seqlens, n_docs, doc_len, doc_off, prefix_k, prefix_v,
+                   q, k, v, q_norm_w, k_norm_w, rms_eps, rope_theta,
+                   softmax_scale, out, lse, pair_status, n_threads, 0, 1);
 }
 
 /*
@@ -251,7 +277,7 @@ int dopr_oracle_score_attn(
   return attention(n_pairs, n_q_heads, n_kv_heads, head_dim, doc_ids,
                    cu_seqlens, n_docs, doc_len, doc_off, prefix_k, prefix_v,
                    q, k, v, q_norm_w, k_norm_w, rms_eps, rope_theta,
-                   softmax_scale, out, lse, pair_status, n_threads, 1);
+                   softmax_scale, out, lse, pair_status, n_threads, 1, 0);
 }
 
 /*

@@ -256,6 +256,85 @@ def pin_score_rows(L):
     assert np.abs(out[[0, 4]] - full[last[[0, 4]]]).max() < 1e-12
 
 
+def pin_decoder_layer(L):
+    """The decoder-layer oracle against Hugging Face's Qwen3DecoderLayer in
+    float64 with eager attention: each pair runs alone, its document's
+    prefix states injected as the layer's pre-filled cache and its online
+    tokens at positions L_d + j.  HF forms rotary angles from float32
+    inverse frequencies, hence the 1e-5 bound."""
+    import torch
+    from transformers import Qwen3Config
+    from transformers.cache_utils import DynamicCache
+    from transformers.models.qwen3.modeling_qwen3 import (
+        Qwen3DecoderLayer, Qwen3RotaryEmbedding)
+    cases = [dict(doc_len=[5, 0, 17], doc_ids=[0, 2, 1, 2], seqlens=[4, 1, 6, 3],
+                  n_q_heads=4, n_kv_heads=2),
+             dict(doc_len=[9, 3], doc_ids=[1, 0], seqlens=[5, 2],
+                  n_q_heads=8, n_kv_heads=2)]
+    W, I = 192, 320
+    for ci, c in enumerate(cases):
+        prob = make_problem(**c, seed=60 + ci)
+        st = workloads.custom(c["doc_len"], c["doc_ids"], c["seqlens"],
+                              c["n_q_heads"], c["n_kv_heads"])
+        b = refs.torch_bf16_to_bits
+        x = b(workloads.hidden_states(st, W, "cpu", 70 + ci))
+        wts = {k: b(t) for k, t in workloads.layer_weights(
+            st, W, I, "cpu", 80 + ci).items()}
+        y, _, status = oracle.decoder_layer(
+            x, prob["doc_ids"], prob["cu_seqlens"], prob["doc_len"],
+            prob["doc_off"], prob["prefix_k"], prob["prefix_v"], wts,
+            prob["q_norm_w"], prob["k_norm_w"], n_q_heads=c["n_q_heads"],
+            n_kv_heads=c["n_kv_heads"], L=L)
+        assert (status == 0).all()
+        Hq, Hkv = c["n_q_heads"], c["n_kv_heads"]
+        cfg = Qwen3Config(hidden_size=W, intermediate_size=I,
+                          num_attention_heads=Hq, num_key_value_heads=Hkv,
+                          head_dim=128, rope_theta=1e6, rms_norm_eps=1e-6,
+                          num_hidden_layers=1)
+        cfg._attn_implementation = "eager"
+        layer = Qwen3DecoderLayer(cfg, layer_idx=0).double().eval()
+        f = lambda a: torch.from_numpy(refs.bf16_bits_to_f64(a))
+        with torch.no_grad():
+            layer.input_layernorm.weight.copy_(f(wts["attn_norm"]))
+            layer.self_attn.q_proj.weight.copy_(f(wts["wq"]))
+            layer.self_attn.k_proj.weight.copy_(f(wts["wk"]))
+            layer.self_attn.v_proj.weight.copy_(f(wts["wv"]))
+            layer.self_attn.o_proj.weight.copy_(f(wts["wo"]))
+            layer.self_attn.q_norm.weight.copy_(f(prob["q_norm_w"]))
+            layer.self_attn.k_norm.weight.copy_(f(prob["k_norm_w"]))
+            layer.post_attention_layernorm.weight.copy_(f(wts["mlp_norm"]))
+            layer.mlp.gate_proj.weight.copy_(f(wts["w_gate"]))
+            layer.mlp.up_proj.weight.copy_(f(wts["w_up"]))
+            layer.mlp.down_proj.weight.copy_(f(wts["w_down"]))
+        rot = Qwen3RotaryEmbedding(cfg)
+        X = f(x)
+        pk = f(prob["prefix_k"])
+        pv = f(prob["prefix_v"])
+        cu = prob["cu_seqlens"]
+        for p in range(len(c["doc_ids"])):
+            d = int(prob["doc_ids"][p])
+            Ld, off = int(prob["doc_len"][d]), int(prob["doc_off"][d])
+            t0, T = int(cu[p]), int(cu[p + 1] - cu[p])
+            cache = DynamicCache()
+            if Ld > 0:
+                cache.update(pk[off:off + Ld].permute(1, 0, 2)[None].contiguous(),
+                             pv[off:off + Ld].permute(1, 0, 2)[None].contiguous(),
+                             0)
+            hs = X[t0:t0 + T][None]
+            pos = torch.arange(Ld, Ld + T)[None]
+            cos, sin = rot(hs, pos)
+            mask = torch.zeros(1, 1, T, Ld + T, dtype=torch.float64)
+            for j in range(T):
+                mask[0, 0, j, Ld + j + 1:] = -torch.inf
+            with torch.no_grad():
+                out = layer(hs, attention_mask=mask, position_ids=pos,
+                            past_key_values=cache if Ld > 0 else None,
+                            position_embeddings=(cos, sin))
+            out = out[0] if isinstance(out, tuple) else out
+            err = np.abs(out[0].numpy() - y[t0:t0 + T]).max()
+            assert err < 1e-5, f"case {ci} pair {p}: layer vs HF {err}"
+
+
 def pin_score(L):
     """Score head vs torch (F.rms_norm then a [2, W] linear map), the
     yes/no swap and the sigmoid/softmax identity."""
@@ -337,4 +416,5 @@ def pin_store_bytes(L):
 ALL_PINS = [pin_sdpa, pin_concat_fp64, pin_no_prefix_is_causal_self_attention,
             pin_uniform_logits, pin_ones_values, pin_single_key,
             pin_relative_positions, pin_invariances, pin_doc_range,
-            pin_score_rows, pin_score, pin_group, pin_store_bytes]
+            pin_score_rows, pin_decoder_layer, pin_score, pin_group,
+            pin_store_bytes]

@@ -94,3 +94,52 @@ def test_pins_catch_planted_mistake(mid, pattern, repl, tmp_path):
     assert "MISSED" not in r.stdout, f"{mid}: no pin failed\n{out[-2000:]}"
     # a crash (nonzero exit without CAUGHT) also counts as caught
     assert "CAUGHT" in r.stdout or r.returncode != 0, out[-2000:]
+
+
+# Mistakes planted in the Python decoder-layer oracle (oracle/__init__.py):
+# the pin battery runs against a copy of that module with one change.
+PY_SRC = os.path.join(ROOT, "oracle", "__init__.py")
+PY_MUTATIONS = [
+    ("layer_attn_residual_dropped", "x2 = X + att.reshape", "x2 = att.reshape"),
+    ("layer_mlp_residual_dropped", "y = x2 + a @", "y = a @"),
+    ("layer_silu_missing", "a = g / (1.0 + np.exp(-g)) * u", "a = g * u"),
+    ("layer_gate_is_up", 'g = h2 @ w["w_gate"].T', 'g = h2 @ w["w_up"].T'),
+    ("layer_norm_gain_missing", "return w * (x / np.sqrt(",
+     "return (x / np.sqrt("),
+    ("layer_mlp_norm_is_attn_norm", 'h2 = _rms_norm_rows(x2, w["mlp_norm"]',
+     'h2 = _rms_norm_rows(x2, w["attn_norm"]'),
+]
+
+PY_RUNNER = r"""
+import importlib.util, sys
+sys.path[:0] = [{root!r}, {tests!r}]
+import oracle as real
+spec = importlib.util.spec_from_file_location("oracle_mut", {path!r})
+mut = importlib.util.module_from_spec(spec)
+spec.loader.exec_module(mut)
+mut._lib = real.lib()
+import oracle_pins
+oracle_pins.oracle = mut
+try:
+    oracle_pins.pin_decoder_layer(real.lib())
+except Exception as e:
+    print("CAUGHT", type(e).__name__)
+    sys.exit(0)
+print("MISSED")
+"""
+
+
+@pytest.mark.parametrize("mid,pattern,repl", PY_MUTATIONS,
+                         ids=[m[0] for m in PY_MUTATIONS])
+def test_pins_catch_planted_layer_mistake(mid, pattern, repl, tmp_path):
+    src = open(PY_SRC).read()
+    assert src.count(pattern) == 1, f"{mid}: pattern must occur exactly once"
+    mutated = tmp_path / "oracle_mut.py"
+    mutated.write_text(src.replace(pattern, repl))
+    code = PY_RUNNER.format(root=ROOT, tests=os.path.dirname(__file__),
+                            path=str(mutated))
+    r = subprocess.run([sys.executable, "-c", code], capture_output=True,
+                       text=True, timeout=300)
+    out = r.stdout + r.stderr
+    assert "MISSED" not in r.stdout, f"{mid}: no pin failed\n{out[-2000:]}"
+    assert "CAUGHT" in r.stdout or r.returncode != 0, out[-2000:]

@@ -248,3 +248,49 @@ def params(st: Structure, device="cpu", seed: int = 6,
         "norm_w": _randn_bf16((W,), seed + 2, device, 0.1, 1.0),
         "w_head": _randn_bf16((2, W), seed + 3, device, 1.0 / np.sqrt(W)),
     }
+
+
+# Hidden and MLP widths of the Qwen3 decoder layers the workloads are shaped
+# after (a small pair for the tiny case).
+LAYER_DIMS = {
+    "tiny": (512, 1024),
+    "qwen3_0p6b": (1024, 3072),
+    "qwen3_4b": (2560, 9728),
+    "qwen3_8b": (4096, 12288),
+    "qwen3_8b_ragged": (4096, 12288),
+    "qwen3_8b_ragged_x8": (4096, 12288),
+}
+
+
+def layer_dims(st: Structure):
+    """(hidden, intermediate) of the decoder layer for a workload."""
+    base = st.name.split("_x")[0] if st.name.startswith("qwen3_8b") else \
+        st.name
+    return LAYER_DIMS.get(base, LAYER_DIMS["tiny"])
+
+
+def hidden_states(st: Structure, hidden: int, device="cpu",
+                  seed: int = 11):
+    """Hidden states of the online tokens entering a layer, N(0, 1)."""
+    return _randn_bf16((st.n_tokens, hidden), seed, device)
+
+
+def layer_weights(st: Structure, hidden: int, intermediate: int,
+                  device="cpu", seed: int = 21) -> Dict:
+    """One decoder layer's weights in the [out, in] convention: the two
+    norm gains 1 + 0.1 N(0,1); every projection N(0, 1/in), so activations
+    stay of order one through the layer."""
+    hq = st.n_q_heads * st.head_dim
+    hk = st.n_kv_heads * st.head_dim
+    W, I = hidden, intermediate
+    return {
+        "attn_norm": _randn_bf16((W,), seed, device, 0.1, 1.0),
+        "wq": _randn_bf16((hq, W), seed + 1, device, W ** -0.5),
+        "wk": _randn_bf16((hk, W), seed + 2, device, W ** -0.5),
+        "wv": _randn_bf16((hk, W), seed + 3, device, W ** -0.5),
+        "wo": _randn_bf16((W, hq), seed + 4, device, hq ** -0.5),
+        "mlp_norm": _randn_bf16((W,), seed + 5, device, 0.1, 1.0),
+        "w_gate": _randn_bf16((I, W), seed + 6, device, W ** -0.5),
+        "w_up": _randn_bf16((I, W), seed + 7, device, W ** -0.5),
+        "w_down": _randn_bf16((W, I), seed + 8, device, I ** -0.5),
+    }
