@@ -234,6 +234,47 @@ dopr_status_t dopr_prefix_attn_score(dopr_store_t st, int32_t layer,
                                      void *stream);
 
 /* ------------------------------------------------------------------------ */
+/* One decoder layer of the online pass (Sec. 3.4: only [q; t_score] runs
+ * through the reranker, every layer's attention also seeing the stored
+ * prefix states).  The layer is the Qwen3 decoder layer, in the stored-weight
+ * convention y = x W^T with W [out, in]:
+ *   h  = RMSNorm(x) * attn_norm_w
+ *   q, k, v = h w_q^T, h w_k^T, h w_v^T          (then as dopr_prefix_attn)
+ *   x2 = x + attention(q, k, v) w_o^T
+ *   h2 = RMSNorm(x2) * mlp_norm_w
+ *   y  = x2 + (SiLU(h2 w_gate^T) * (h2 w_up^T)) w_down^T
+ * RMSNorm is over the hidden width with epsilon rms_eps of the batch args.
+ * Projections accumulate in fp32 and every activation between steps is
+ * stored as bf16.  The batch is described by a dopr_attn_args_t whose q, k,
+ * v and out must be NULL (the layer forms them in its workspace); lse may be
+ * given ([Ntok, Hq]); workspace and workspace_bytes come from
+ * dopr_decoder_layer_workspace.  x and y may be the same buffer.           */
+typedef struct {
+  int32_t hidden;            /* W, multiple of 8                            */
+  int32_t intermediate;      /* I, multiple of 8                            */
+  const void *attn_norm_w;   /* dev bf16 [W]                                */
+  const void *w_q;           /* dev bf16 [Hq*D, W]                          */
+  const void *w_k;           /* dev bf16 [Hkv*D, W]                         */
+  const void *w_v;           /* dev bf16 [Hkv*D, W]                         */
+  const void *w_o;           /* dev bf16 [W, Hq*D]                          */
+  const void *mlp_norm_w;    /* dev bf16 [W]                                */
+  const void *w_gate;        /* dev bf16 [I, W]                             */
+  const void *w_up;          /* dev bf16 [I, W]                             */
+  const void *w_down;        /* dev bf16 [W, I]                             */
+  const void *x;             /* dev bf16 [Ntok, W] entering the layer       */
+  void *y;                   /* dev bf16 [Ntok, W] leaving it               */
+} dopr_layer_args_t;
+
+dopr_status_t dopr_decoder_layer_workspace(dopr_store_t st,
+                                           const dopr_attn_args_t *batch,
+                                           const dopr_layer_args_t *lw,
+                                           size_t *bytes);
+
+dopr_status_t dopr_decoder_layer(dopr_store_t st, int32_t layer,
+                                 const dopr_attn_args_t *batch,
+                                 const dopr_layer_args_t *lw, void *stream);
+
+/* ------------------------------------------------------------------------ */
 /* Exports used by the bit-exact tests of the integer steps.               */
 
 /* Doc-id grouping in canonical form: valid pairs (doc id in range and

@@ -62,6 +62,16 @@ class _ScoreArgs(ctypes.Structure):
                 ("logits", ctypes.c_void_p), ("score", ctypes.c_void_p)]
 
 
+class _LayerArgs(ctypes.Structure):
+    _fields_ = [("hidden", ctypes.c_int32), ("intermediate", ctypes.c_int32),
+                ("attn_norm_w", ctypes.c_void_p), ("w_q", ctypes.c_void_p),
+                ("w_k", ctypes.c_void_p), ("w_v", ctypes.c_void_p),
+                ("w_o", ctypes.c_void_p), ("mlp_norm_w", ctypes.c_void_p),
+                ("w_gate", ctypes.c_void_p), ("w_up", ctypes.c_void_p),
+                ("w_down", ctypes.c_void_p), ("x", ctypes.c_void_p),
+                ("y", ctypes.c_void_p)]
+
+
 class _ScoreHead(ctypes.Structure):
     _fields_ = [("norm_w", ctypes.c_void_p), ("w_head", ctypes.c_void_p),
                 ("rms_eps", ctypes.c_float), ("logits", ctypes.c_void_p),
@@ -87,6 +97,11 @@ EXPORTS = {
     "dopr_prefix_attn_score": ([ctypes.c_void_p, ctypes.c_int32,
                                 ctypes.c_void_p, ctypes.c_void_p,
                                 ctypes.c_void_p], ctypes.c_int),
+    "dopr_decoder_layer_workspace": ([ctypes.c_void_p, ctypes.c_void_p,
+                                      ctypes.c_void_p, ctypes.c_void_p],
+                                     ctypes.c_int),
+    "dopr_decoder_layer": ([ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p,
+                            ctypes.c_void_p, ctypes.c_void_p], ctypes.c_int),
     "dopr_group_pairs": ([ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p,
                           ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p,
                           ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
@@ -297,6 +312,50 @@ def dopr_prefix_attn_score(store: Store, layer: int, doc_ids, cu_seqlens, q,
                    _ptr(logits), _ptr(score))
     _check(lib().dopr_prefix_attn_score(store.handle, layer, ctypes.byref(a),
                                         ctypes.byref(h), _stream(stream)))
+
+
+_LAYER_FIELDS = ("attn_norm_w", "w_q", "w_k", "w_v", "w_o", "mlp_norm_w",
+                 "w_gate", "w_up", "w_down")
+
+
+def _layer_args(weights, x, y, hidden, intermediate):
+    """weights: dict with the _LAYER_FIELDS keys (device bf16 tensors)."""
+    return _LayerArgs(int(hidden), int(intermediate),
+                      *[_ptr(weights[k]) for k in _LAYER_FIELDS],
+                      _ptr(x), _ptr(y))
+
+
+def dopr_decoder_layer_workspace(store: Store, weights, *, n_pairs,
+                                 n_q_heads, max_tokens, total_tokens,
+                                 hidden, intermediate,
+                                 kernel_variant=0) -> int:
+    a = _shape_args(n_pairs, n_q_heads, max_tokens, total_tokens,
+                    kernel_variant)
+    la = _layer_args(weights, None, None, hidden, intermediate)
+    n = ctypes.c_size_t(0)
+    _check(lib().dopr_decoder_layer_workspace(
+        store.handle, ctypes.byref(a), ctypes.byref(la), ctypes.byref(n)))
+    return n.value
+
+
+def dopr_decoder_layer(store: Store, layer: int, doc_ids, cu_seqlens, x, y,
+                       weights, q_norm_w, k_norm_w, workspace, *, n_q_heads,
+                       max_tokens, hidden, intermediate, lse=None,
+                       rms_eps=1e-6, rope_theta=1e6, softmax_scale=None,
+                       kernel_variant=0, timing=None, stream=None):
+    """One decoder layer over the online tokens: x -> y ([Ntok, W] bf16)."""
+    if softmax_scale is None:
+        softmax_scale = 128 ** -0.5
+    ws_bytes = workspace.numel() * workspace.element_size()
+    a = _AttnArgs(doc_ids.numel(), int(n_q_heads), int(max_tokens),
+                  int(kernel_variant), int(x.shape[0]), _ptr(doc_ids),
+                  _ptr(cu_seqlens), None, None, None, _ptr(q_norm_w),
+                  _ptr(k_norm_w), float(rms_eps), float(rope_theta),
+                  float(softmax_scale), None, _ptr(lse), _ptr(workspace),
+                  ws_bytes, *(timing if timing is not None else (None, None)))
+    la = _layer_args(weights, x, y, hidden, intermediate)
+    _check(lib().dopr_decoder_layer(store.handle, layer, ctypes.byref(a),
+                                    ctypes.byref(la), _stream(stream)))
 
 
 def dopr_score_logits(h, norm_w, w_head, score, *, width=None,

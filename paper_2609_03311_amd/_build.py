@@ -17,7 +17,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libdopr.so")
-SOURCES = ["api.hip", "store.hip", "group.hip", "attn.hip", "score.hip"]
+SOURCES = ["api.hip", "store.hip", "group.hip", "attn.hip", "score.hip",
+           "layer.hip"]
 ARCH = "gfx950"
 
 FLAGS = [
@@ -54,7 +55,7 @@ def build(verbose: bool = False) -> str:
         objs = list(ex.map(_compile, SOURCES))
     tmp = LIB + ".tmp"
     cmd = [hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp,
-           *objs]
+           *objs, "-lhipblaslt"]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stderr}")

@@ -352,6 +352,113 @@ dopr_status_t dopr_prefix_attn_score(dopr_store_t st, int32_t layer,
   return run_attention(st, layer, args, head, stream);
 }
 
+}  // extern "C"
+
+namespace {
+
+// Shapes and checks of a decoder-layer call; on success *ls and *shape
+// describe the layer buffers and the attention plan.
+dopr_status_t check_layer(dopr_store_t st, const dopr_attn_args_t *b,
+                          const dopr_layer_args_t *l, LayerShape *ls,
+                          PlanShape *shape, int32_t *n_rep) {
+  dopr_status_t s = check_attn(st, b, shape, n_rep);
+  if (s != DOPR_OK) return s;
+  if (!l) return fail(DOPR_ERR_INVALID_ARG, "layer args are NULL");
+  if (l->hidden < 8 || l->hidden % 8 || l->intermediate < 8 ||
+      l->intermediate % 8)
+    return fail(DOPR_ERR_INVALID_ARG,
+                "hidden and intermediate must be multiples of 8, >= 8");
+  if (b->q || b->k || b->v || b->out)
+    return fail(DOPR_ERR_INVALID_ARG,
+                "q, k, v and out must be NULL: the layer forms them");
+  *ls = LayerShape{b->total_tokens, l->hidden, l->intermediate,
+                   b->n_q_heads, st->n_kv_heads};
+  return DOPR_OK;
+}
+
+size_t layer_bytes(const LayerShape &ls, const PlanShape &shape) {
+  return layer_carve(nullptr, ls).bytes + plan_bytes(shape);
+}
+
+}  // namespace
+
+extern "C" {
+
+dopr_status_t dopr_decoder_layer_workspace(dopr_store_t st,
+                                           const dopr_attn_args_t *batch,
+                                           const dopr_layer_args_t *lw,
+                                           size_t *bytes) {
+  if (!bytes) return fail(DOPR_ERR_INVALID_ARG, "bytes is NULL");
+  LayerShape ls;
+  PlanShape shape;
+  int32_t n_rep = 0;
+  dopr_status_t s = check_layer(st, batch, lw, &ls, &shape, &n_rep);
+  if (s != DOPR_OK) return s;
+  *bytes = layer_bytes(ls, shape);
+  return ok();
+}
+
+dopr_status_t dopr_decoder_layer(dopr_store_t st, int32_t layer,
+                                 const dopr_attn_args_t *b,
+                                 const dopr_layer_args_t *l, void *stream) {
+  LayerShape ls;
+  PlanShape shape;
+  int32_t n_rep = 0;
+  dopr_status_t s = check_layer(st, b, l, &ls, &shape, &n_rep);
+  if (s != DOPR_OK) return s;
+  if (layer < 0 || layer >= st->n_layers)
+    return fail(DOPR_ERR_INVALID_ARG, "layer out of range");
+  if (b->n_pairs == 0) return ok();
+  if (!b->doc_ids || !b->cu_seqlens || !b->q_norm_w || !b->k_norm_w ||
+      !b->workspace || !l->attn_norm_w || !l->w_q || !l->w_k || !l->w_v ||
+      !l->w_o || !l->mlp_norm_w || !l->w_gate || !l->w_up || !l->w_down ||
+      !l->x || !l->y)
+    return fail(DOPR_ERR_INVALID_ARG, "NULL buffer");
+  const void *al[] = {b->q_norm_w, b->k_norm_w, l->attn_norm_w, l->w_q,
+                      l->w_k,      l->w_v,      l->w_o,         l->mlp_norm_w,
+                      l->w_gate,   l->w_up,     l->w_down,      l->x,
+                      l->y};
+  for (const void *p : al)
+    if (!aligned16(p))
+      return fail(DOPR_ERR_INVALID_ARG,
+                  "weights, x and y must be 16-byte aligned");
+  if (reinterpret_cast<uintptr_t>(b->workspace) % kAlign)
+    return fail(DOPR_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+  const size_t need = layer_bytes(ls, shape);
+  if (b->workspace_bytes < need)
+    return fail(DOPR_ERR_WORKSPACE,
+                "workspace holds " + std::to_string(b->workspace_bytes) +
+                    " bytes, needs " + std::to_string(need));
+  s = check_device(st);
+  if (s != DOPR_OK) return s;
+  const LayerWs w = layer_carve(b->workspace, ls);
+  dopr_attn_args_t a = *b;  // the attention of this layer
+  a.q = w.q;
+  a.k = w.k;
+  a.v = w.v;
+  a.out = w.att;
+  a.workspace = w.plan;
+  a.workspace_bytes = plan_bytes(shape);
+  const Plan plan = plan_carve(w.plan, shape);
+  AttnCall call{st, layer, &a, n_rep};
+  hipStream_t hs = as_stream(stream);
+  int g = launch_layer_pre(ls, l, w, b->rms_eps, hs);
+  if (g != 0)
+    return g < 0 ? hip_fail(hipGetLastError(), "layer launch")
+                 : fail(DOPR_ERR_HIP, std::string("hipBLASLt: ") +
+                                          gemm_status_str(g));
+  hipError_t e = launch_plan(call, plan, shape, hs);
+  if (e != hipSuccess) return hip_fail(e, "scheduler launch");
+  e = launch_attention(call, plan, shape, hs);
+  if (e != hipSuccess) return hip_fail(e, "attention launch");
+  g = launch_layer_post(ls, l, w, b->rms_eps, hs);
+  if (g != 0)
+    return g < 0 ? hip_fail(hipGetLastError(), "layer launch")
+                 : fail(DOPR_ERR_HIP, std::string("hipBLASLt: ") +
+                                          gemm_status_str(g));
+  return ok();
+}
+
 dopr_status_t dopr_score_logits(const dopr_score_args_t *a, void *stream) {
   if (!a) return fail(DOPR_ERR_INVALID_ARG, "args is NULL");
   if (a->n_pairs < 0) return fail(DOPR_ERR_INVALID_ARG, "n_pairs < 0");

@@ -153,6 +153,39 @@ hipError_t launch_score(const dopr_score_args_t *a, hipStream_t s);
 hipError_t launch_score_reduce(const Plan &pl, int32_t n_pairs, int32_t n_q_heads,
                                const dopr_score_head_t *head, hipStream_t s);
 
+// ---------------------------------------------------------------------------
+// Decoder layer around the attention (layer.hip).
+constexpr int64_t kMlpChunk = 32768;               // MLP tokens per chunk
+constexpr size_t kGemmWorkspace = size_t(64) << 20;  // hipBLASLt workspace
+
+struct LayerShape {
+  int64_t ntok;
+  int32_t hidden, inter, hq, hkv;
+};
+
+struct LayerWs {
+  uint16_t *h;    // [Ntok][W]   RMSNorm(x), later RMSNorm(x2)
+  uint16_t *q;    // [Ntok][Hq][D]
+  uint16_t *k;    // [Ntok][Hkv][D]
+  uint16_t *v;    // [Ntok][Hkv][D]
+  uint16_t *att;  // [Ntok][Hq][D] attention rows
+  uint16_t *gu;   // [chunk][2I]  gate | up
+  uint16_t *act;  // [chunk][I]   SiLU(gate) * up
+  void *gemm_ws;
+  size_t gemm_ws_bytes;
+  int64_t chunk;
+  void *plan;     // the attention plan follows the layer's buffers
+  size_t bytes;   // layer buffers before the plan
+};
+
+LayerWs layer_carve(void *base, const LayerShape &s);
+// Return 0, -1 for a HIP launch error, or a hipBLASLt status.
+int launch_layer_pre(const LayerShape &s, const dopr_layer_args_t *l,
+                     const LayerWs &w, float eps, hipStream_t st);
+int launch_layer_post(const LayerShape &s, const dopr_layer_args_t *l,
+                      const LayerWs &w, float eps, hipStream_t st);
+const char *gemm_status_str(int s);
+
 // Record a deferred error code in a status word (first error wins).
 __device__ inline void raise_status(int32_t *status, int32_t code) {
   atomicCAS(status, 0, code);

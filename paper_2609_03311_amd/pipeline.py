@@ -7,7 +7,8 @@ from __future__ import annotations
 
 import numpy as np
 
-from . import (dopr_prefix_attn, dopr_prefix_attn_score,
+from . import (dopr_decoder_layer, dopr_decoder_layer_workspace,
+               dopr_prefix_attn, dopr_prefix_attn_score,
                dopr_prefix_attn_score_workspace, dopr_prefix_attn_workspace,
                dopr_score_logits, dopr_store_create, dopr_store_put)
 
@@ -122,3 +123,48 @@ class ScoreStep:
             max_tokens=self.max_tokens, logits=self.logits, lse=self.lse,
             total_tokens=self.total_tokens,
             kernel_variant=self.kernel_variant, stream=stream, **kw)
+
+
+# names of the layer weights in the generator's dict -> the C struct fields
+LAYER_KEYS = {"attn_norm": "attn_norm_w", "wq": "w_q", "wk": "w_k",
+              "wv": "w_v", "wo": "w_o", "mlp_norm": "mlp_norm_w",
+              "w_gate": "w_gate", "w_up": "w_up", "w_down": "w_down"}
+
+
+class LayerStep:
+    """Reusable buffers for one decoder layer over the online tokens:
+    x [Ntok, W] in, y [Ntok, W] out, the layer's intermediates in one
+    workspace."""
+
+    def __init__(self, store, weights, *, n_pairs, n_q_heads, total_tokens,
+                 max_tokens, hidden, intermediate, kernel_variant=0,
+                 device="cuda", with_lse=False):
+        import torch
+        self.store = store
+        self.weights = {LAYER_KEYS.get(k, k): v for k, v in weights.items()}
+        self.n_q_heads = n_q_heads
+        self.max_tokens = max_tokens
+        self.hidden = hidden
+        self.intermediate = intermediate
+        self.kernel_variant = kernel_variant
+        nbytes = dopr_decoder_layer_workspace(
+            store, self.weights, n_pairs=n_pairs, n_q_heads=n_q_heads,
+            max_tokens=max_tokens, total_tokens=total_tokens, hidden=hidden,
+            intermediate=intermediate, kernel_variant=kernel_variant)
+        self.workspace = torch.empty(max(nbytes, 256), dtype=torch.uint8,
+                                     device=device)
+        self.y = torch.empty((total_tokens, hidden), dtype=torch.bfloat16,
+                             device=device)
+        self.lse = (torch.empty((total_tokens, n_q_heads),
+                                dtype=torch.float32, device=device)
+                    if with_lse else None)
+
+    def run(self, layer, doc_ids, cu_seqlens, x, q_norm_w, k_norm_w,
+            stream=None, **kw):
+        dopr_decoder_layer(self.store, layer, doc_ids, cu_seqlens, x, self.y,
+                           self.weights, q_norm_w, k_norm_w, self.workspace,
+                           n_q_heads=self.n_q_heads,
+                           max_tokens=self.max_tokens, hidden=self.hidden,
+                           intermediate=self.intermediate, lse=self.lse,
+                           kernel_variant=self.kernel_variant, stream=stream,
+                           **kw)

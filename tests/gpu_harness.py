@@ -226,3 +226,107 @@ def compare_score(case: Case, sstep, pairs, tol=TOL):
     assert e_s <= tol, f"score max-abs {e_s} > {tol}"
     assert e_l <= tol, f"logit max-abs {e_l} > {tol}"
     return dict(out=e_out, score=e_s, lse=e_lse)
+
+
+# ---------------------------------------------------------------------------
+# One decoder layer around the attention.
+
+@dataclasses.dataclass
+class LayerCase:
+    base: Case
+    x: object          # device bf16 [Ntok, W]
+    weights: dict      # device bf16 tensors (generator names)
+    lstep: object
+    hidden: int
+    inter: int
+
+
+def setup_layer(case: Case, hidden=None, inter=None, seed=0,
+                kernel_variant=0):
+    from paper_2609_03311_amd import pipeline
+    st = case.st
+    W, I = workloads.layer_dims(st)
+    W, I = hidden or W, inter or I
+    dev = case.step.out.device
+    x = workloads.hidden_states(st, W, dev, seed * 100 + 11)
+    wts = workloads.layer_weights(st, W, I, dev, seed * 100 + 21)
+    max_t = int(st.seqlens.max()) if st.n_pairs else 1
+    lstep = pipeline.LayerStep(case.store, wts, n_pairs=st.n_pairs,
+                               n_q_heads=st.n_q_heads,
+                               total_tokens=st.n_tokens, max_tokens=max_t,
+                               hidden=W, intermediate=I,
+                               kernel_variant=kernel_variant, device=dev)
+    log(f"layer {st.name}: W={W} I={I} workspace "
+        f"{lstep.workspace.numel() / 2**20:.0f} MiB")
+    return LayerCase(case, x, wts, lstep, W, I)
+
+
+def run_layer(lc: LayerCase):
+    import torch
+    from paper_2609_03311_amd import dopr_check_status
+    c = lc.base
+    lc.lstep.run(0, c.doc_ids, c.cu, lc.x, c.prm["q_norm_w"],
+                 c.prm["k_norm_w"])
+    torch.cuda.synchronize()
+    return dopr_check_status(c.store)
+
+
+def oracle_layer_subset(lc: LayerCase, pairs):
+    """The float64 layer oracle on the tokens of a subset of pairs (every
+    projection is row-wise, so the subset is exact)."""
+    import torch
+    c = lc.base
+    st = c.st
+    pairs = np.asarray(pairs, np.int64)
+    cu = st.cu_seqlens.astype(np.int64)
+    docs = np.unique(st.doc_ids[pairs])
+    docs = docs[(docs >= 0) & (docs < st.n_docs)]
+    docs = docs[st.doc_len[docs] >= 0]
+    sub_off = np.full(st.n_docs, -1, np.int64)
+    rows, pos = [], 0
+    for d in docs:
+        L = int(st.doc_len[d])
+        sub_off[d] = pos
+        rows.append((int(c.doc_off[d]), L))
+        pos += L
+    idx = np.concatenate([np.arange(o, o + L) for o, L in rows]) if rows \
+        else np.zeros(0, np.int64)
+    dev = c.k_src.device
+    it = torch.from_numpy(idx).to(dev)
+    pk = refs.torch_bf16_to_bits(c.k_src.index_select(0, it))
+    pv = refs.torch_bf16_to_bits(c.v_src.index_select(0, it))
+    tok = np.concatenate([np.arange(cu[p], cu[p + 1]) for p in pairs])
+    tt = torch.from_numpy(tok).to(dev)
+    x = refs.torch_bf16_to_bits(lc.x.index_select(0, tt))
+    lens = (cu[pairs + 1] - cu[pairs]).astype(np.int64)
+    sub_cu = np.zeros(len(pairs) + 1, np.int64)
+    np.cumsum(lens, out=sub_cu[1:])
+    wts = {k: refs.torch_bf16_to_bits(v) for k, v in lc.weights.items()}
+    t0 = time.time()
+    y, _, status = oracle.decoder_layer(
+        x, st.doc_ids[pairs], sub_cu.astype(np.int32), st.doc_len, sub_off,
+        pk, pv, wts, refs.torch_bf16_to_bits(c.prm["q_norm_w"]),
+        refs.torch_bf16_to_bits(c.prm["k_norm_w"]), n_q_heads=st.n_q_heads,
+        n_kv_heads=st.n_kv_heads)
+    log(f"layer oracle on {len(pairs)} pairs ({len(tok)} tokens): "
+        f"{time.time() - t0:.1f}s")
+    return dict(tok=tok, y=y, status=status)
+
+
+def compare_layer(lc: LayerCase, pairs, atol, rtol):
+    """|y - y_ref| <= atol + rtol |y_ref| elementwise."""
+    import torch
+    ref = oracle_layer_subset(lc, pairs)
+    tt = torch.from_numpy(ref["tok"]).to(lc.lstep.y.device)
+    got = lc.lstep.y.index_select(0, tt).float().cpu().numpy()
+    err = np.abs(got - ref["y"])
+    bound = atol + rtol * np.abs(ref["y"])
+    worst = float((err / bound).max()) if err.size else 0.0
+    rel_rms = float(np.sqrt((err ** 2).mean() / (ref["y"] ** 2).mean())) \
+        if err.size else 0.0
+    log(f"{lc.base.st.name} layer: {len(pairs)} pairs max|dy|="
+        f"{err.max() if err.size else 0:.3e} rel-rms {rel_rms:.3e} "
+        f"max|y| {np.abs(ref['y']).max() if err.size else 0:.2f} "
+        f"worst err/bound {worst:.3f}")
+    assert worst <= 1.0, f"layer error exceeds atol {atol} + rtol {rtol}|y|"
+    return dict(max=float(err.max()) if err.size else 0.0, rel_rms=rel_rms)

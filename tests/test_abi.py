@@ -44,7 +44,8 @@ def test_struct_layouts_match_header(tmp_path):
     structs = {"dopr_store_desc_t": D._StoreDesc,
                "dopr_attn_args_t": D._AttnArgs,
                "dopr_score_args_t": D._ScoreArgs,
-               "dopr_score_head_t": D._ScoreHead}
+               "dopr_score_head_t": D._ScoreHead,
+               "dopr_layer_args_t": D._LayerArgs}
     lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "dopr.h"',
              "int main(void) {"]
     for cname, py in structs.items():
@@ -129,6 +130,13 @@ def test_host_validation_codes():
     assert "store is NULL" in D.dopr_last_error()
     assert L.dopr_prefix_attn_score_workspace(None, ctypes.byref(a),
                                               ctypes.byref(n)) == \
+        D.DOPR_ERR_INVALID_ARG
+    la = D._LayerArgs()
+    assert L.dopr_decoder_layer(None, 0, ctypes.byref(a), ctypes.byref(la),
+                                None) == D.DOPR_ERR_INVALID_ARG
+    assert L.dopr_decoder_layer_workspace(None, ctypes.byref(a),
+                                          ctypes.byref(la),
+                                          ctypes.byref(n)) == \
         D.DOPR_ERR_INVALID_ARG
     assert L.dopr_check_status(None, None) == D.DOPR_ERR_INVALID_ARG
     assert D.dopr_status_str(D.DOPR_ERR_DOC_RANGE) == "DOPR_ERR_DOC_RANGE"
