@@ -13,7 +13,9 @@ float64 CPU oracle timed on a bounded sample of the same workload.
 
 --path score measures last-layer scoring instead: only each pair's score
 token is attended (still over its whole prefix and all its own keys) and
-the score head is fused into the attention epilogue.
+the score head is fused into the attention epilogue.  --path layer measures
+one whole decoder layer over the online tokens (projections, norms, SwiGLU
+MLP and the prefix attention), MFMA-bound.
 """
 import argparse
 import ctypes
@@ -30,6 +32,9 @@ if ROOT not in sys.path:
 
 METRIC = ("query-doc pairs/sec per decoder layer; achieved HBM GB/s vs "
           "MI355X peak")
+METRIC_LAYER = ("query-doc pairs/sec per full decoder layer (projections, "
+                "prefix attention, SwiGLU MLP); achieved MFMA TFLOP/s vs "
+                "MI355X bf16 dense peak")
 METRIC_SCORE = ("query-doc pairs/sec for the last decoder layer (score-token "
                 "rows + fused score head); achieved HBM GB/s vs MI355X peak")
 PEAK_HBM_GBS = 8000.0
@@ -136,6 +141,66 @@ def algorithmic_work_score(st, rows):
                 unique_docs=int(len(uniq)))
 
 
+def layer_work(st, hidden, inter):
+    """Flops of one decoder layer over the online tokens: the projections
+    (q, k, v, o, gate, up, down) and the attention products."""
+    hq, hkv, D = st.n_q_heads, st.n_kv_heads, st.head_dim
+    n = st.n_tokens
+    proj = 2 * n * hidden * (hq + 2 * hkv) * D + 2 * n * hq * D * hidden
+    mlp = 2 * n * hidden * inter * 3
+    att = algorithmic_work(st)["flops"]
+    return dict(proj=proj, mlp=mlp, attention=att, total=proj + mlp + att)
+
+
+def cpu_baseline_layer(st, k_src, v_src, doc_off, x, wts, prm, seconds):
+    """The float64 layer oracle on a bounded sample of pairs."""
+    import torch
+
+    import oracle
+    L = oracle.lib()
+    threads = oracle.max_threads(L)
+    rng = np.random.default_rng(99)
+    order = rng.permutation(st.n_pairs)
+    cu = st.cu_seqlens.astype(np.int64)
+    dev = k_src.device
+    wb = {k: bits(v) for k, v in wts.items()}
+
+    def run(pairs):
+        docs = np.unique(st.doc_ids[pairs])
+        sub_off = np.full(st.n_docs, -1, np.int64)
+        idx, pos = [], 0
+        for d in docs:
+            n = int(st.doc_len[d])
+            sub_off[d] = pos
+            idx.append(np.arange(doc_off[d], doc_off[d] + n))
+            pos += n
+        it = torch.from_numpy(np.concatenate(idx)).to(dev)
+        tok = np.concatenate([np.arange(cu[p], cu[p + 1]) for p in pairs])
+        tt = torch.from_numpy(tok).to(dev)
+        lens = cu[pairs + 1] - cu[pairs]
+        scu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+        xs = bits(x.index_select(0, tt))
+        pk, pv = bits(k_src.index_select(0, it)), bits(v_src.index_select(0, it))
+        t0 = time.perf_counter()
+        oracle.decoder_layer(xs, st.doc_ids[pairs], scu, st.doc_len, sub_off,
+                             pk, pv, wb, bits(prm["q_norm_w"]),
+                             bits(prm["k_norm_w"]), n_q_heads=st.n_q_heads,
+                             n_kv_heads=st.n_kv_heads, L=L)
+        return time.perf_counter() - t0
+
+    total_t, total_n, i = 0.0, 0, 0
+    while total_t < seconds and i < st.n_pairs:
+        n = min(max(1, total_n), st.n_pairs - i)   # doubling batches
+        total_t += run(order[i:i + n])
+        total_n += n
+        i += n
+    return {"value": round(total_n / total_t, 3), "unit": "pairs/s",
+            "cores": int(threads), "kind": "oracle",
+            "sample": f"{total_n} of {st.n_pairs} pairs (seeded random "
+                      f"order), float64 decoder-layer oracle (numpy "
+                      f"projections, C attention), {total_t:.1f}s"}
+
+
 def measured_traffic(config, variant, path_kind="full"):
     """HBM bytes per attention launch from the committed rocprofv3 counter
     summary of this workload, or None when there is none or the kernel's
@@ -232,10 +297,12 @@ def main():
     ap.add_argument("--config", default="qwen3_8b",
                     choices=sorted(DESCRIPTIONS))
     ap.add_argument("--variant", type=int, default=0)
-    ap.add_argument("--path", choices=["full", "score"], default="full",
-                    help="full: every online row of one layer (default); "
-                         "score: last-layer scoring (score-token rows, "
-                         "fused score head)")
+    ap.add_argument("--path", choices=["full", "score", "layer"],
+                    default="full",
+                    help="full: every online row of one layer's attention "
+                         "(default); score: last-layer scoring (score-token "
+                         "rows, fused score head); layer: one whole decoder "
+                         "layer")
     ap.add_argument("--no-score-rows", action="store_true",
                     help="with --path score: do not write the score rows "
                          "(the fused head alone)")
@@ -264,12 +331,25 @@ def main():
     log(f"{args.config}: P={st.n_pairs} Ntok={st.n_tokens} "
         f"unique docs={len(np.unique(st.doc_ids))}")
     k_src, v_src, doc_off, _ = workloads.prefix_source(st, dev, 1)
-    online = workloads.online_inputs(st, dev, 3)
+    layer_path = args.path == "layer"
+    online = None if layer_path else workloads.online_inputs(st, dev, 3)
     prm = workloads.params(st, dev, 6)
     store = pipeline.make_store(st.doc_len, st.n_kv_heads, k_src, v_src,
                                 device=dev)
     score_path = args.path == "score"
-    if score_path:
+    if layer_path:
+        hidden, inter = workloads.layer_dims(st)
+        x = workloads.hidden_states(st, hidden, dev, 11)
+        wts = workloads.layer_weights(st, hidden, inter, dev, 21)
+        step = pipeline.LayerStep(store, wts, n_pairs=st.n_pairs,
+                                  n_q_heads=st.n_q_heads,
+                                  total_tokens=st.n_tokens,
+                                  max_tokens=int(st.seqlens.max()),
+                                  hidden=hidden, intermediate=inter,
+                                  kernel_variant=args.variant, device=dev)
+        log(f"layer W={hidden} I={inter}: workspace "
+            f"{step.workspace.numel() / 2**30:.1f} GiB")
+    elif score_path:
         step = pipeline.ScoreStep(store, n_pairs=st.n_pairs,
                                   n_q_heads=st.n_q_heads,
                                   total_tokens=st.n_tokens,
@@ -302,6 +382,10 @@ def main():
 
     def one_step(i=None):
         timing = None if i is None else (ev.ev[2 * i], ev.ev[2 * i + 1])
+        if layer_path:
+            step.run(0, doc_ids, cu, x, prm["q_norm_w"], prm["k_norm_w"],
+                     timing=timing)
+            return
         if score_path:
             step.run(0, doc_ids, cu, online["q"], online["k"], online["v"],
                      prm["q_norm_w"], prm["k_norm_w"], prm["norm_w"],
@@ -336,14 +420,23 @@ def main():
         f"attention kernel avg {attn_avg:.3f} ms "
         f"(min {min(attn_ms):.3f}, max {max(attn_ms):.3f})")
 
-    w = (algorithmic_work_score(st, not args.no_score_rows) if score_path
-         else algorithmic_work(st))
-    achieved = w["total"] / (attn_avg * 1e-3) / 1e9
-    traffic = measured_traffic(args.config, args.variant, args.path)
+    if layer_path:
+        lw = layer_work(st, hidden, inter)
+        w = dict(total=lw["total"], prefix=algorithmic_work(st)["prefix"],
+                 flops=lw["attention"],
+                 unique_docs=len(np.unique(st.doc_ids)))
+        achieved = lw["total"] / (ms_step * 1e-3) / 1e12
+        traffic = None
+    else:
+        w = (algorithmic_work_score(st, not args.no_score_rows) if score_path
+             else algorithmic_work(st))
+        achieved = w["total"] / (attn_avg * 1e-3) / 1e9
+        traffic = measured_traffic(args.config, args.variant, args.path)
     if score_path and args.no_score_rows:
         traffic = None
     result = {
-        "metric": METRIC_SCORE if score_path else METRIC,
+        "metric": (METRIC_LAYER if layer_path else
+                   METRIC_SCORE if score_path else METRIC),
         "value": round(st.n_pairs / (ms_step * 1e-3), 1),
         "unit": "pairs/s",
         "n_gpus": 1,
@@ -354,8 +447,11 @@ def main():
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16",
-        "data": "synthetic (seeded N(0,1) bf16 prefix states and online "
-                "q/k/v; no datasets or weights)",
+        "data": ("synthetic (seeded N(0,1) bf16 prefix states, hidden "
+                 "states and N(0, 1/fan-in) layer weights; no datasets or "
+                 "trained weights)" if layer_path else
+                 "synthetic (seeded N(0,1) bf16 prefix states and online "
+                 "q/k/v; no datasets or weights)"),
         "config": {
             "workload": DESCRIPTIONS[args.config],
             "name": args.config,
@@ -363,7 +459,9 @@ def main():
             "online_tokens": st.n_tokens,
             "unique_docs": w["unique_docs"],
             "kernel_variant": args.variant,
-            "path": ("last-layer scoring" + (", no score rows written"
+            "path": ("decoder layer (hidden %d, intermediate %d)" % (
+                hidden, inter) if layer_path else
+                     "last-layer scoring" + (", no score rows written"
                                              if args.no_score_rows else "")
                      if score_path else "full online layer"),
             "parallelism": "single GPU",
@@ -373,20 +471,36 @@ def main():
         "prefix_gb": round(w["prefix"] / 1e9, 4),
         "prefix_gbps": round(w["prefix"] / (attn_avg * 1e-3) / 1e9, 1),
         "attention_tflops": round(w["flops"] / (attn_avg * 1e-3) / 1e12, 1),
-        "roofline": {
+        "roofline": ({
+            "bound": "mfma",
+            "achieved": round(achieved, 1),
+            "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+            "traffic": None,
+        } if layer_path else {
             "bound": "hbm",
             "achieved": round(achieved, 1),
             "peak": PEAK_HBM_GBS,
             "unit": "GB/s",
             "frac": round(achieved / PEAK_HBM_GBS, 4),
             "traffic": traffic,
-        },
+        }),
     }
+    if layer_path:
+        result["algorithmic_gb"] = None   # MFMA-bound: flops, not bytes
+        result["layer_tflop"] = round(lw["total"] / 1e12, 3)
+        result["layer_split_tflop"] = {k: round(v / 1e12, 3)
+                                       for k, v in lw.items()}
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a bounded sample")
-        result["cpu_baseline"] = cpu_baseline(st, k_src, v_src, doc_off,
-                                              online, prm, args.cpu_seconds,
-                                              last_only=score_path)
+        if layer_path:
+            result["cpu_baseline"] = cpu_baseline_layer(
+                st, k_src, v_src, doc_off, x, wts, prm, args.cpu_seconds)
+        else:
+            result["cpu_baseline"] = cpu_baseline(
+                st, k_src, v_src, doc_off, online, prm, args.cpu_seconds,
+                last_only=score_path)
     print(json.dumps(result), flush=True)
 
 
