@@ -15,6 +15,11 @@ What is computed (see the C file for the step-by-step definition):
   * ``score`` -- s(q,d) from the score token's state (Sec. 3.2.3).
   * ``group`` -- canonical grouping of pairs by document.
   * ``store_payload_bytes`` -- document-side prefix memory (Tables 3, 9).
+  * ``decoder_layer`` -- the whole decoder layer around that attention
+    (numpy, float64, in this file).
+  * ``oracle.salience`` (own module, numpy float64) -- the offline salience
+    selection of Sec. 3.2.1: head-averaged causal attention, column top-p
+    means and the top-K positions of each document.
 """
 from __future__ import annotations
 
