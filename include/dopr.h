@@ -20,6 +20,9 @@
  *   dopr_prefix_attn_score
  *                      the last layer's share: only the score token's rows,
  *                      with the score head fused into the attention epilogue.
+ *   dopr_decoder_layer the whole decoder layer around that attention.
+ *   dopr_salience      offline: which document positions become prefix
+ *                      slots (Sec. 3.2.1 salience, top-K selection).
  *
  * Conventions shared by every call
  *   - All device buffers are allocated by the caller and passed as raw device
@@ -276,6 +279,76 @@ dopr_status_t dopr_decoder_layer(dopr_store_t st, int32_t layer,
 
 /* ------------------------------------------------------------------------ */
 /* Exports used by the bit-exact tests of the integer steps.               */
+
+/* ------------------------------------------------------------------------ */
+/* Offline salience selection (Sec. 3.2.1, applied offline in Sec. 3.3): for
+ * each document, independently encoded at positions 0..n_d-1, with the final
+ * layer's queries q^ and keys k^ as they enter the attention product (after
+ * any norm and rotary embedding), q head h reading kv head h / n_rep:
+ *   A_h[j, i] = softmax over i <= j of softmax_scale * q^_h[j] . k^_g[i]
+ *   Abar      = mean of A_h over the Hq query heads (row j attends,
+ *               column i is attended; zero above the diagonal)
+ *   u_i       = mean of the m = min(p, n_d - i) largest Abar[j, i] over the
+ *               visible rows j >= i (the paper's |T_p| = min(p, n - i + 1)
+ *               with 1-based i)
+ *   selected  = the K_d positions with the largest u, ties to the lower
+ *               position, written in ascending position order.
+ * The GPU computes logits in fp32 from the bf16 operands, probabilities
+ * with exp2 against each row's log-sum-exp, Abar and u in fp32.           */
+#define DOPR_SALIENCE_MAX_LEN 4096
+#define DOPR_SALIENCE_MAX_P 64
+
+typedef struct {
+  int32_t n_docs;            /* documents in the batch (>= 0)              */
+  int32_t max_doclen;        /* M: bound on every n_d, 1..4096             */
+  int32_t n_q_heads;         /* Hq, multiple of n_kv_heads                 */
+  int32_t n_kv_heads;        /* Hkv >= 1                                   */
+  int32_t top_p;             /* p, 1..64                                   */
+  float softmax_scale;       /* e.g. 1/sqrt(D)                             */
+  int64_t total_tokens;      /* Ntok = cu_doclens[n_docs]                  */
+  int64_t total_select;      /* cu_select[n_docs] (ignored if selected is
+                                NULL)                                      */
+  const int32_t *cu_doclens; /* dev int32 [n_docs+1]: document d owns token
+                                rows cu[d] .. cu[d+1]-1, 1 <= n_d <= M    */
+  const int32_t *cu_select;  /* dev int32 [n_docs+1]: K_d = cs[d+1]-cs[d],
+                                0 <= K_d <= n_d; or NULL with selected    */
+  const void *q;             /* dev bf16 [Ntok, Hq, D]                     */
+  const void *k;             /* dev bf16 [Ntok, Hkv, D]                    */
+  float *u;                  /* dev fp32 [Ntok]: salience of every token
+                                (output of dopr_salience, input of
+                                dopr_select_top_k)                         */
+  int32_t *selected;         /* dev int32 [total_select]: doc d's chosen
+                                positions (0-based within the document) at
+                                cs[d] .., ascending; or NULL (u only)     */
+  float *attn_mean;          /* optional dev fp32 [n_docs, M, M]: Abar of
+                                doc d at d*M*M + j*M + i; only i <= j < n_d
+                                is written.  NULL: kept in the workspace  */
+  int32_t *status;           /* optional dev int32, zeroed by the caller:
+                                receives DOPR_ERR_SEQLEN when cu_doclens or
+                                cu_select is malformed (the affected
+                                documents are skipped), else untouched    */
+  void *workspace;           /* dev scratch >= dopr_salience_workspace()   */
+  size_t workspace_bytes;
+} dopr_salience_args_t;
+
+/* Workspace bytes for these arguments (host): the row log-sum-exp of every
+ * (token, q head) and, unless attn_mean is given, Abar for as many documents
+ * at a time as fit in 1 GiB (at least one).  dopr_salience accepts any
+ * workspace that holds the row statistics plus one document's Abar
+ * (4 M^2 bytes) and processes as many documents per pass as fit. */
+dopr_status_t dopr_salience_workspace(const dopr_salience_args_t *args,
+                                      size_t *bytes);
+
+/* Salience u of every token and, if selected is not NULL, the top-K_d
+ * positions of every document.  Asynchronous on `stream`. */
+dopr_status_t dopr_salience(const dopr_salience_args_t *args, void *stream);
+
+/* The selection step alone, on u given by the caller: uses n_docs,
+ * max_doclen, total_tokens, total_select, cu_doclens, cu_select, u,
+ * selected and status; values order as IEEE-754 totalOrder (-0 < +0),
+ * ties to the lower position.  No workspace. */
+dopr_status_t dopr_select_top_k(const dopr_salience_args_t *args,
+                                void *stream);
 
 /* Doc-id grouping in canonical form: valid pairs (doc id in range and
  * resident) sorted by (doc id, pair index).  group_doc[G] ascending doc ids,

@@ -78,6 +78,20 @@ class _ScoreHead(ctypes.Structure):
                 ("score", ctypes.c_void_p)]
 
 
+class _SalienceArgs(ctypes.Structure):
+    _fields_ = [("n_docs", ctypes.c_int32), ("max_doclen", ctypes.c_int32),
+                ("n_q_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32),
+                ("top_p", ctypes.c_int32), ("softmax_scale", ctypes.c_float),
+                ("total_tokens", ctypes.c_int64),
+                ("total_select", ctypes.c_int64),
+                ("cu_doclens", ctypes.c_void_p), ("cu_select", ctypes.c_void_p),
+                ("q", ctypes.c_void_p), ("k", ctypes.c_void_p),
+                ("u", ctypes.c_void_p), ("selected", ctypes.c_void_p),
+                ("attn_mean", ctypes.c_void_p), ("status", ctypes.c_void_p),
+                ("workspace", ctypes.c_void_p),
+                ("workspace_bytes", ctypes.c_size_t)]
+
+
 EXPORTS = {
     "dopr_store_bytes": ([ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p],
                          ctypes.c_int),
@@ -109,6 +123,10 @@ EXPORTS = {
     "dopr_gather_prefix": ([ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
                             ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                             ctypes.c_void_p, ctypes.c_void_p], ctypes.c_int),
+    "dopr_salience_workspace": ([ctypes.c_void_p, ctypes.c_void_p],
+                                ctypes.c_int),
+    "dopr_salience": ([ctypes.c_void_p, ctypes.c_void_p], ctypes.c_int),
+    "dopr_select_top_k": ([ctypes.c_void_p, ctypes.c_void_p], ctypes.c_int),
     "dopr_check_status": ([ctypes.c_void_p, ctypes.c_void_p], ctypes.c_int),
     "dopr_status_str": ([ctypes.c_int], ctypes.c_char_p),
     "dopr_last_error": ([], ctypes.c_char_p),
@@ -396,6 +414,54 @@ def dopr_gather_prefix(store: Store, layer: int, doc_ids, out_cu_slots,
                                     _ptr(doc_ids), _ptr(out_cu_slots),
                                     _ptr(k_out), _ptr(v_out),
                                     _stream(stream)))
+
+
+def _salience_args(n_docs, max_doclen, n_q_heads, n_kv_heads, top_p,
+                   softmax_scale, total_tokens, total_select, cu_doclens,
+                   cu_select, q, k, u, selected, attn_mean, status, workspace):
+    return _SalienceArgs(
+        n_docs, max_doclen, n_q_heads, n_kv_heads, top_p, softmax_scale,
+        total_tokens, total_select, _ptr(cu_doclens), _ptr(cu_select),
+        _ptr(q), _ptr(k), _ptr(u), _ptr(selected), _ptr(attn_mean),
+        _ptr(status), _ptr(workspace),
+        0 if workspace is None else workspace.numel() * workspace.element_size())
+
+
+def dopr_salience_workspace(*, n_docs, max_doclen, n_q_heads, n_kv_heads,
+                            top_p, total_tokens, with_attention=False) -> int:
+    """Workspace bytes of dopr_salience (shape arguments only)."""
+    a = _salience_args(n_docs, max_doclen, n_q_heads, n_kv_heads, top_p,
+                       1.0, total_tokens, 0, None, None, None, None, None,
+                       None, None, None, None)
+    if with_attention:
+        a.attn_mean = 16  # any aligned non-NULL value: only its presence counts
+    n = ctypes.c_size_t(0)
+    _check(lib().dopr_salience_workspace(ctypes.byref(a), ctypes.byref(n)))
+    return n.value
+
+
+def dopr_salience(cu_doclens, q, k, u, *, max_doclen, top_p, softmax_scale,
+                  cu_select=None, selected=None, attn_mean=None, status=None,
+                  workspace=None, stream=None):
+    """Salience of every token (and the top-K positions of each document when
+    `selected` is given).  cu_doclens/cu_select: int32 device tensors;
+    q [Ntok, Hq, 128], k [Ntok, Hkv, 128] bf16; u fp32 [Ntok]."""
+    n_docs = cu_doclens.numel() - 1
+    total_select = 0 if selected is None else selected.numel()
+    a = _salience_args(n_docs, max_doclen, q.shape[1], k.shape[1], top_p,
+                       softmax_scale, q.shape[0], total_select, cu_doclens,
+                       cu_select, q, k, u, selected, attn_mean, status,
+                       workspace)
+    _check(lib().dopr_salience(ctypes.byref(a), _stream(stream)))
+
+
+def dopr_select_top_k(cu_doclens, cu_select, u, selected, *, max_doclen,
+                      status=None, stream=None):
+    """Top-K_d positions of each document on caller-given u."""
+    a = _salience_args(cu_doclens.numel() - 1, max_doclen, 1, 1, 1, 1.0,
+                       u.numel(), selected.numel(), cu_doclens, cu_select,
+                       None, None, u, selected, None, status, None)
+    _check(lib().dopr_select_top_k(ctypes.byref(a), _stream(stream)))
 
 
 def dopr_check_status(store: Store, stream=None) -> int:

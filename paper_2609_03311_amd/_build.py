@@ -18,7 +18,7 @@ CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libdopr.so")
 SOURCES = ["api.hip", "store.hip", "group.hip", "attn.hip", "score.hip",
-           "layer.hip"]
+           "layer.hip", "salience.hip"]
 ARCH = "gfx950"
 
 FLAGS = [

@@ -1,6 +1,7 @@
 // api.hip -- host side of the C ABI declared in include/dopr.h: argument
 // validation, store layout, workspace sizing and kernel launches.  Nothing
 // here allocates device memory; every device buffer comes from the caller.
+#include <algorithm>
 #include <cmath>
 #include <cstring>
 #include <string>
@@ -561,6 +562,166 @@ dopr_status_t dopr_gather_prefix(dopr_store_t st, int32_t layer, int32_t n,
                                static_cast<uint16_t *>(v_out),
                                as_stream(stream));
   if (e != hipSuccess) return hip_fail(e, "gather launch");
+  return ok();
+}
+
+}  // extern "C"
+
+namespace {
+
+// Host checks shared by the salience entry points; `full` adds those of the
+// attention part (heads, p, q, k); `ptrs` the buffer checks (not for a
+// workspace query).
+dopr_status_t check_salience(const dopr_salience_args_t *a, bool full,
+                             bool ptrs = true) {
+  if (!a) return fail(DOPR_ERR_INVALID_ARG, "args is NULL");
+  if (a->n_docs < 0) return fail(DOPR_ERR_INVALID_ARG, "n_docs < 0");
+  if (a->max_doclen < 1 || a->max_doclen > kSalienceMaxLen)
+    return fail(a->max_doclen > kSalienceMaxLen ? DOPR_ERR_UNSUPPORTED
+                                                : DOPR_ERR_INVALID_ARG,
+                "max_doclen must be in [1, 4096]");
+  if (a->total_tokens < 0 || a->total_tokens > INT32_MAX)
+    return fail(DOPR_ERR_INVALID_ARG, "total_tokens must be in [0, 2^31)");
+  if (a->selected && (a->total_select < 0 || a->total_select > INT32_MAX))
+    return fail(DOPR_ERR_INVALID_ARG, "total_select must be in [0, 2^31)");
+  if (full) {
+    if (a->n_q_heads < 1 || a->n_kv_heads < 1 ||
+        a->n_q_heads % a->n_kv_heads)
+      return fail(DOPR_ERR_INVALID_ARG,
+                  "n_q_heads must be a positive multiple of n_kv_heads");
+    if (a->top_p < 1 || a->top_p > kSalienceMaxP)
+      return fail(a->top_p > kSalienceMaxP ? DOPR_ERR_UNSUPPORTED
+                                           : DOPR_ERR_INVALID_ARG,
+                  "top_p must be in [1, 64]");
+    if (!std::isfinite(a->softmax_scale))
+      return fail(DOPR_ERR_INVALID_ARG, "softmax_scale must be finite");
+  }
+  if (a->n_docs == 0 || !ptrs) return ok();
+  if (!a->cu_doclens || !a->u)
+    return fail(DOPR_ERR_INVALID_ARG, "cu_doclens and u are required");
+  if (a->selected && !a->cu_select)
+    return fail(DOPR_ERR_INVALID_ARG, "selected needs cu_select");
+  if (full) {
+    if (!a->q || !a->k) return fail(DOPR_ERR_INVALID_ARG, "q and k are required");
+    if (!aligned16(a->q) || !aligned16(a->k))
+      return fail(DOPR_ERR_INVALID_ARG, "q and k must be 16-byte aligned");
+    if (a->attn_mean && (reinterpret_cast<uintptr_t>(a->attn_mean) & 15))
+      return fail(DOPR_ERR_INVALID_ARG, "attn_mean must be 16-byte aligned");
+  }
+  return ok();
+}
+
+struct SalienceWs {
+  size_t lse_bytes = 0, abar_bytes = 0, total = 0;
+  int32_t chunk = 0;  // documents per pass
+};
+
+SalienceWs salience_ws(const dopr_salience_args_t *a) {
+  SalienceWs w;
+  const size_t M = (size_t)a->max_doclen;
+  w.lse_bytes = align_up(sizeof(float) * (size_t)a->n_q_heads *
+                             (size_t)a->total_tokens, kAlign);
+  if (a->attn_mean) {
+    w.chunk = a->n_docs;
+  } else {
+    const size_t per = sizeof(float) * M * M;
+    size_t c = kSalienceAbarBudget / per;
+    if (c < 1) c = 1;
+    if (c > (size_t)a->n_docs) c = (size_t)a->n_docs;
+    w.chunk = (int32_t)c;
+    w.abar_bytes = align_up(per * c, kAlign);
+  }
+  w.total = w.lse_bytes + w.abar_bytes;
+  return w;
+}
+
+TopkParams topk_params(const dopr_salience_args_t *a) {
+  TopkParams t;
+  t.cu = a->cu_doclens;
+  t.cs = a->cu_select;
+  t.u = a->u;
+  t.selected = a->selected;
+  t.max_len = a->max_doclen;
+  t.total_tokens = a->total_tokens;
+  t.total_select = a->total_select;
+  t.status = a->status;
+  return t;
+}
+
+}  // namespace
+
+extern "C" {
+
+dopr_status_t dopr_salience_workspace(const dopr_salience_args_t *args,
+                                      size_t *bytes) {
+  if (!bytes) return fail(DOPR_ERR_INVALID_ARG, "bytes is NULL");
+  dopr_status_t s = check_salience(args, true, false);
+  if (s != DOPR_OK) return s;
+  *bytes = args->n_docs == 0 ? 0 : salience_ws(args).total;
+  return ok();
+}
+
+dopr_status_t dopr_salience(const dopr_salience_args_t *a, void *stream) {
+  dopr_status_t s = check_salience(a, true);
+  if (s != DOPR_OK) return s;
+  if (a->n_docs == 0) return ok();
+  SalienceWs w = salience_ws(a);
+  // the least workspace holds the row statistics and one document's Abar;
+  // more room lets more documents share a pass
+  const size_t per = sizeof(float) * (size_t)a->max_doclen * a->max_doclen;
+  const size_t least = w.lse_bytes + (a->attn_mean ? 0 : per);
+  if (!a->workspace || a->workspace_bytes < least)
+    return fail(DOPR_ERR_WORKSPACE,
+                "workspace needs at least " + std::to_string(least) +
+                    " bytes");
+  if (!a->attn_mean)
+    w.chunk = (int32_t)std::min<size_t>(
+        (size_t)a->n_docs, (a->workspace_bytes - w.lse_bytes) / per);
+  if (reinterpret_cast<uintptr_t>(a->workspace) % kAlign)
+    return fail(DOPR_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+  char *base = static_cast<char *>(a->workspace);
+  SalienceParams p;
+  p.q = static_cast<const uint16_t *>(a->q);
+  p.k = static_cast<const uint16_t *>(a->k);
+  p.cu = a->cu_doclens;
+  p.n_docs = a->n_docs;
+  p.d0 = 0;
+  p.hq = a->n_q_heads;
+  p.hkv = a->n_kv_heads;
+  p.n_rep = a->n_q_heads / a->n_kv_heads;
+  p.max_len = a->max_doclen;
+  p.top_p = a->top_p;
+  p.total_tokens = a->total_tokens;
+  p.c = a->softmax_scale * 1.4426950408889634f;
+  p.inv_hq = 1.0f / (float)a->n_q_heads;
+  p.lse2 = reinterpret_cast<float *>(base);
+  p.abar = a->attn_mean ? a->attn_mean
+                        : reinterpret_cast<float *>(base + w.lse_bytes);
+  p.abar_stride = (int64_t)a->max_doclen * a->max_doclen;
+  p.u = a->u;
+  p.status = a->status;
+  const int hr = p.n_rep % 4 == 0 ? 4 : p.n_rep % 2 == 0 ? 2 : 1;
+  const int pm = a->top_p <= 8 ? 8 : a->top_p <= 16 ? 16
+               : a->top_p <= 32 ? 32 : 64;
+  hipStream_t hs = as_stream(stream);
+  hipError_t e = launch_salience_check(p, hs);
+  for (int32_t d0 = 0; e == hipSuccess && d0 < a->n_docs; d0 += w.chunk) {
+    p.d0 = d0;
+    const int32_t nd = std::min(w.chunk, a->n_docs - d0);
+    e = launch_salience_chunk(p, nd, hr, pm, hs);
+  }
+  if (e == hipSuccess && a->selected)
+    e = launch_topk(topk_params(a), a->n_docs, hs);
+  if (e != hipSuccess) return hip_fail(e, "salience launch");
+  return ok();
+}
+
+dopr_status_t dopr_select_top_k(const dopr_salience_args_t *a, void *stream) {
+  dopr_status_t s = check_salience(a, false);
+  if (s != DOPR_OK) return s;
+  if (a->n_docs == 0 || !a->selected) return ok();
+  hipError_t e = launch_topk(topk_params(a), a->n_docs, as_stream(stream));
+  if (e != hipSuccess) return hip_fail(e, "top-k launch");
   return ok();
 }
 

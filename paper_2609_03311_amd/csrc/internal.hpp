@@ -186,6 +186,40 @@ int launch_layer_post(const LayerShape &s, const dopr_layer_args_t *l,
                       const LayerWs &w, float eps, hipStream_t st);
 const char *gemm_status_str(int s);
 
+// Offline salience selection (salience.hip).
+constexpr int kSalienceMaxLen = 4096;   // longest document (LDS sort bound)
+constexpr int kSalienceMaxP = 64;       // largest top-p (register list bound)
+constexpr size_t kSalienceAbarBudget = size_t(1) << 30;  // scratch bytes
+
+struct SalienceParams {
+  const uint16_t *q, *k;     // [Ntok, Hq, D], [Ntok, Hkv, D]
+  const int32_t *cu;         // [n_docs + 1]
+  int32_t n_docs, d0;        // all docs; first doc of this launch
+  int32_t hq, hkv, n_rep, max_len, top_p;
+  int64_t total_tokens;
+  float c;                   // softmax_scale * log2(e)
+  float inv_hq;
+  float *lse2;               // [Hq][Ntok] log2-domain row log-sum-exp
+  float *abar;               // doc d - d0 at (d - d0) * abar_stride
+  int64_t abar_stride;       // max_len * max_len
+  float *u;                  // [Ntok]
+  int32_t *status;           // deferred error word, or NULL
+};
+
+struct TopkParams {
+  const int32_t *cu, *cs;    // [n_docs + 1] token and selection offsets
+  const float *u;
+  int32_t *selected;
+  int32_t max_len;
+  int64_t total_tokens, total_select;
+  int32_t *status;
+};
+
+hipError_t launch_salience_check(const SalienceParams &p, hipStream_t s);
+hipError_t launch_salience_chunk(const SalienceParams &p, int32_t n_docs,
+                                 int hr, int pm, hipStream_t s);
+hipError_t launch_topk(const TopkParams &p, int32_t n_docs, hipStream_t s);
+
 // Record a deferred error code in a status word (first error wins).
 __device__ inline void raise_status(int32_t *status, int32_t code) {
   atomicCAS(status, 0, code);

@@ -1,0 +1,485 @@
+// salience.hip -- offline salience selection (Sec. 3.2.1, used by the
+// offline compression of Sec. 3.3).
+//
+// For one document of n tokens with final-layer queries q^ [n, Hq, D] and
+// keys k^ [n, Hkv, D] (as they enter the attention product):
+//   A_h[j, i] = softmax_i(scale * q^_h[j] . k^_g[i]),  i <= j,  g = h / n_rep
+//   Abar      = (1/Hq) sum_h A_h                     (rows attend, columns
+//                                                      are attended)
+//   u_i       = mean of the m = min(p, n - i) largest Abar[j, i], j >= i
+//   selected  = the K positions with the largest u (ties: lower position),
+//               written in ascending position order.
+//
+// Four kernels, each a plain pass over its data:
+//   k_row_lse     per (row block of 128, kv head): the log2-domain
+//                 log-sum-exp of every row of every q head of the group
+//                 (scaled logits; one flash-style sweep over the visible
+//                 keys with a running maximum).
+//   k_mean_attn   per (row block, key block) of 128 x 128 below the
+//                 diagonal: every head's probabilities exp2(S - lse2),
+//                 summed over heads in head order, times 1/Hq, stored as
+//                 fp32 row-major [n, n] (only i <= j is written).
+//   k_col_topp    per strip of 64 columns: each lane keeps the PM largest
+//                 values of its column in a sorted register list while four
+//                 waves stream interleaved rows; the lists are merged and
+//                 the top m averaged.
+//   k_topk        per document: bitonic sort of (u, position) keys in LDS,
+//                 then an ordered compaction of the chosen positions.
+//
+// Both attention kernels form S = K Q^T with the 32x32x16 bf16 MFMA in the
+// same operand layout and the same k order, so the logits they see are the
+// same fp32 values.  A-operand (key) rows are read in the order perm(m) so
+// that lane half hf's 16 accumulators hold 16 consecutive keys 16 hf + i
+// for the lane's query column.
+#include <cmath>
+
+#include "internal.hpp"
+
+namespace dopr {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+
+constexpr int D = kHeadDim;
+constexpr int kRowBlock = 128;   // rows per unit (4 waves x 32)
+constexpr int kKeyBlock = 128;   // keys per mean-attention unit
+constexpr int kStrip = 64;       // columns per top-p strip
+
+__device__ __forceinline__ int perm(int m) {
+  return ((m >> 2) & 1) * 16 + (m >> 3) * 4 + (m & 3);
+}
+// XOR swizzle of the 16-byte granules of a K row staged in LDS, so the rows
+// read together by a quarter wave fall on distinct bank groups.
+__device__ __forceinline__ int swz(int row) {
+  return (row & 3) | ((row >> 2) & 4) | ((row << 1) & 8);
+}
+
+struct Doc {
+  int64_t t0;
+  int32_t n;
+  bool ok;
+};
+
+__device__ __forceinline__ Doc doc_at(const SalienceParams &P, int d) {
+  Doc r;
+  const int32_t a = P.cu[d], b = P.cu[d + 1];
+  r.t0 = a;
+  r.n = b - a;
+  r.ok = a >= 0 && r.n >= 1 && r.n <= P.max_len && b <= P.total_tokens;
+  return r;
+}
+
+__device__ __forceinline__ bf16x8 ld8(const uint16_t *p) {
+  return *reinterpret_cast<const bf16x8 *>(p);
+}
+
+// ---------------------------------------------------------------------------
+// Row log-sum-exp.  grid (row blocks, Hkv, docs); each wave owns 32 rows and
+// the HR q heads of the group at a time (their Q fragments stay in
+// registers while the keys stream past).
+template <int HR>
+__global__ __launch_bounds__(256) void k_row_lse(SalienceParams P) {
+  const int d = P.d0 + blockIdx.z;
+  const Doc doc = doc_at(P, d);
+  if (!doc.ok) return;
+  const int rb = gridDim.x - 1 - blockIdx.x;  // longest rows first
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int hf = lane >> 5, lq = lane & 31;
+  const int row0 = rb * kRowBlock + wave * 32;
+  if (row0 >= doc.n) return;  // no barriers in this kernel
+  const int g = blockIdx.y;
+  const int j = row0 + lq;
+  const int jl = min(j, doc.n - 1);
+  const int kend = min(doc.n, row0 + 32);
+  const int64_t qrow = (doc.t0 + jl) * P.hq;
+  const int krow_lane = perm(lq);
+
+  for (int h0 = 0; h0 < P.n_rep; h0 += HR) {
+    const int hbase = g * P.n_rep + h0;
+    bf16x8 qf[HR][8];
+#pragma unroll
+    for (int r = 0; r < HR; ++r)
+#pragma unroll
+      for (int s = 0; s < 8; ++s)
+        qf[r][s] = ld8(P.q + (qrow + hbase + r) * D + 16 * s + 8 * hf);
+    float m[HR], l[HR];
+#pragma unroll
+    for (int r = 0; r < HR; ++r) {
+      m[r] = -INFINITY;
+      l[r] = 0.f;
+    }
+    for (int kb = 0; kb < kend; kb += 32) {
+      const int key = min(kb + krow_lane, doc.n - 1);
+      const uint16_t *kp = P.k + ((doc.t0 + key) * P.hkv + g) * D + 8 * hf;
+      bf16x8 kf[8];
+#pragma unroll
+      for (int s = 0; s < 8; ++s) kf[s] = ld8(kp + 16 * s);
+      const int lim = j - kb - 16 * hf;  // visible: i <= lim
+#pragma unroll
+      for (int r = 0; r < HR; ++r) {
+        floatx16 S;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) S[i] = 0.f;
+#pragma unroll
+        for (int s = 0; s < 8; ++s)
+          S = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[s], qf[r][s], S, 0,
+                                                      0, 0);
+        float x[16], mx = -INFINITY;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          x[i] = i <= lim ? S[i] * P.c : -INFINITY;
+          mx = fmaxf(mx, x[i]);
+        }
+        const float mn = fmaxf(m[r], mx);
+        if (mn > -INFINITY) {
+          float add = 0.f;
+#pragma unroll
+          for (int i = 0; i < 16; ++i)
+            add += __builtin_amdgcn_exp2f(x[i] - mn);
+          l[r] = l[r] * __builtin_amdgcn_exp2f(m[r] - mn) + add;
+          m[r] = mn;
+        }
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < HR; ++r) {
+      const float mo = __shfl_xor(m[r], 32, 64);
+      const float lo = __shfl_xor(l[r], 32, 64);
+      const float mn = fmaxf(m[r], mo);
+      // every row sees at least its own key, so mn is finite
+      const float tot = l[r] * __builtin_amdgcn_exp2f(m[r] - mn) +
+                        lo * __builtin_amdgcn_exp2f(mo - mn);
+      if (hf == 0 && j < doc.n)
+        P.lse2[(int64_t)(hbase + r) * P.total_tokens + doc.t0 + j] =
+            mn + log2f(tot);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Head-averaged attention.  grid (triangular tile index, docs); unit (rb, kb)
+// with kb <= rb covers rows rb*128 .. +127 and keys kb*128 .. +127.  Each
+// kv head's 128 key rows are staged in LDS and read by the 4 waves for the
+// group's q heads, HR heads per pass.
+constexpr int kLdsK = kKeyBlock * D;  // bf16 elements (swizzled rows)
+
+template <int HR>
+__global__ __launch_bounds__(256, 2) void k_mean_attn(SalienceParams P) {
+  __shared__ __attribute__((aligned(16))) uint16_t ks[kLdsK];
+  const int d = P.d0 + blockIdx.y;
+  const Doc doc = doc_at(P, d);
+  if (!doc.ok) return;
+  // tile t -> (rb, kb), t = rb (rb + 1) / 2 + kb
+  const int t = blockIdx.x;
+  int rb = (int)((sqrtf(8.f * t + 1.f) - 1.f) * 0.5f);
+  while ((rb + 1) * (rb + 2) / 2 <= t) ++rb;
+  while (rb * (rb + 1) / 2 > t) --rb;
+  const int kb = t - rb * (rb + 1) / 2;
+  if (rb * kRowBlock >= doc.n) return;  // block-uniform, before barriers
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int hf = lane >> 5, lq = lane & 31;
+  const int row0 = rb * kRowBlock + wave * 32;
+  const bool active = row0 < doc.n;
+  const int j = row0 + lq;
+  const int jl = min(j, doc.n - 1);
+  const int key0 = kb * kKeyBlock;
+  // key sub-tiles 0 .. nt-1 hold a key some row of this wave can see
+  const int last_row = min(row0 + 31, doc.n - 1);
+  const int nt = active ? min(4, (last_row - key0) / 32 + 1) : 0;
+  const bool diag = kb == rb;
+  const int64_t qrow = (doc.t0 + jl) * P.hq;
+
+  floatx16 acc[4];
+#pragma unroll
+  for (int s = 0; s < 4; ++s)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) acc[s][i] = 0.f;
+
+  const int kr = perm(lq);
+  for (int g = 0; g < P.hkv; ++g) {
+    __syncthreads();  // the previous head's keys are no longer read
+    // stage keys key0 .. key0+127 of kv head g (rows past n repeat row n-1)
+#pragma unroll
+    for (int c = 0; c < kKeyBlock * 16 / 256; ++c) {
+      const int id = c * 256 + threadIdx.x;
+      const int row = id >> 4, gr = id & 15;
+      const int key = min(key0 + row, doc.n - 1);
+      const uint4 v = *reinterpret_cast<const uint4 *>(
+          P.k + ((doc.t0 + key) * P.hkv + g) * D + gr * 8);
+      *reinterpret_cast<uint4 *>(ks + row * D + ((gr ^ swz(row)) << 3)) = v;
+    }
+    __syncthreads();
+    if (nt == 0) continue;
+    for (int h0 = 0; h0 < P.n_rep; h0 += HR) {
+      const int hbase = g * P.n_rep + h0;
+      bf16x8 qf[HR][8];
+      float L[HR];
+#pragma unroll
+      for (int r = 0; r < HR; ++r) {
+#pragma unroll
+        for (int s = 0; s < 8; ++s)
+          qf[r][s] = ld8(P.q + (qrow + hbase + r) * D + 16 * s + 8 * hf);
+        L[r] = P.lse2[(int64_t)(hbase + r) * P.total_tokens + doc.t0 + jl];
+      }
+      for (int st = 0; st < nt; ++st) {
+        const int row = 32 * st + kr;
+        bf16x8 kf[8];
+#pragma unroll
+        for (int s = 0; s < 8; ++s)
+          kf[s] = ld8(ks + row * D + (((2 * s + hf) ^ swz(row)) << 3));
+        const int lim = j - key0 - 32 * st - 16 * hf;  // visible: i <= lim
+#pragma unroll
+        for (int r = 0; r < HR; ++r) {
+          floatx16 S;
+#pragma unroll
+          for (int i = 0; i < 16; ++i) S[i] = 0.f;
+#pragma unroll
+          for (int s = 0; s < 8; ++s)
+            S = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[s], qf[r][s], S,
+                                                        0, 0, 0);
+          if (diag) {
+#pragma unroll
+            for (int i = 0; i < 16; ++i)
+              acc[st][i] += i <= lim ? __builtin_amdgcn_exp2f(
+                                           S[i] * P.c - L[r])
+                                     : 0.f;
+          } else {
+#pragma unroll
+            for (int i = 0; i < 16; ++i)
+              acc[st][i] += __builtin_amdgcn_exp2f(S[i] * P.c - L[r]);
+          }
+        }
+      }
+    }
+  }
+  if (!active || j >= doc.n) return;
+  float *out = P.abar + (int64_t)(d - P.d0) * P.abar_stride +
+               (int64_t)j * P.max_len;
+  const bool vec = (P.max_len & 3) == 0;  // rows 16-byte aligned
+#pragma unroll
+  for (int st = 0; st < 4; ++st) {
+    if (st >= nt) break;
+    const int i0 = key0 + 32 * st + 16 * hf;
+    float v[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) v[i] = acc[st][i] * P.inv_hq;
+    if (vec && i0 + 16 <= j + 1) {
+#pragma unroll
+      for (int c = 0; c < 4; ++c)
+        *reinterpret_cast<float4 *>(out + i0 + 4 * c) =
+            make_float4(v[4 * c], v[4 * c + 1], v[4 * c + 2], v[4 * c + 3]);
+    } else {
+#pragma unroll
+      for (int i = 0; i < 16; ++i)
+        if (i0 + i <= j) out[i0 + i] = v[i];
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Column top-p means.  grid (strips of 64 columns, docs); the 4 waves of a
+// block stream rows j = c0 + w, c0 + w + 4, ... of the strip; lane l keeps
+// the PM largest values of column c0 + l (descending, -1 = empty) and the
+// lists are merged through LDS at the end.
+template <int PM>
+__device__ __forceinline__ void insert(float (&L)[PM], float v) {
+#pragma unroll
+  for (int k = 0; k < PM; ++k) {
+    const float hi = fmaxf(L[k], v);
+    v = fminf(L[k], v);
+    L[k] = hi;
+  }
+}
+
+template <int PM>
+__global__ __launch_bounds__(256) void k_col_topp(SalienceParams P) {
+  __shared__ float merge[3][PM][kStrip];
+  const int d = P.d0 + blockIdx.y;
+  const Doc doc = doc_at(P, d);
+  if (!doc.ok) return;
+  const int c0 = blockIdx.x * kStrip;
+  if (c0 >= doc.n) return;  // block-uniform, before the barrier
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int c = c0 + lane;
+  const bool col = c < doc.n;
+  const float *base = P.abar + (int64_t)(d - P.d0) * P.abar_stride +
+                      (col ? c : c0);
+  float L[PM];
+#pragma unroll
+  for (int k = 0; k < PM; ++k) L[k] = -1.f;
+  constexpr int U = 8;
+  int j = c0 + wave;
+  for (; j + 4 * (U - 1) < doc.n; j += 4 * U) {
+    float v[U];
+#pragma unroll
+    for (int x = 0; x < U; ++x)
+      v[x] = base[(int64_t)(j + 4 * x) * P.max_len];
+#pragma unroll
+    for (int x = 0; x < U; ++x) {
+      const float w = (col && j + 4 * x >= c) ? v[x] : -1.f;
+      if (__any(w > L[PM - 1])) insert(L, w);
+    }
+  }
+  for (; j < doc.n; j += 4) {
+    const float v = base[(int64_t)j * P.max_len];
+    const float w = (col && j >= c) ? v : -1.f;
+    if (__any(w > L[PM - 1])) insert(L, w);
+  }
+  if (wave > 0) {
+#pragma unroll
+    for (int k = 0; k < PM; ++k) merge[wave - 1][k][lane] = L[k];
+  }
+  __syncthreads();
+  if (wave != 0 || !col) return;
+  for (int w = 0; w < 3; ++w)
+    for (int k = 0; k < PM; ++k) {
+      const float v = merge[w][k][lane];
+      if (__any(v > L[PM - 1])) insert(L, v);
+    }
+  const int m = min(P.top_p, doc.n - c);
+  float sum = 0.f;
+#pragma unroll
+  for (int k = 0; k < PM; ++k)
+    if (k < m) sum += L[k];
+  P.u[doc.t0 + c] = sum / (float)m;
+}
+
+// ---------------------------------------------------------------------------
+// Validation of the document and selection offsets (one thread per doc).
+__global__ __launch_bounds__(256) void k_check(SalienceParams P) {
+  const int d = blockIdx.x * 256 + threadIdx.x;
+  if (d >= P.n_docs) return;
+  if (!doc_at(P, d).ok || (d == P.n_docs - 1 &&
+                           P.cu[d + 1] != P.total_tokens))
+    raise_status(P.status, DOPR_ERR_SEQLEN);
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// Top-K selection.  One block per document; keys (orderable u bits << 32 |
+// ~position) sorted descending by a bitonic network in LDS, the first K
+// positions flagged and compacted in position order.
+namespace {
+
+constexpr int kTopkThreads = 1024;
+
+__device__ __forceinline__ uint32_t orderable(float f) {
+  const uint32_t b = __float_as_uint(f);
+  return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+}
+
+__global__ __launch_bounds__(kTopkThreads) void k_topk(TopkParams P) {
+  __shared__ uint64_t key[kSalienceMaxLen];
+  __shared__ uint8_t flag[kSalienceMaxLen];
+  __shared__ int32_t wsum[kTopkThreads / 64];
+  const int d = blockIdx.x;
+  const int32_t a = P.cu[d], b = P.cu[d + 1];
+  const int32_t n = b - a;
+  if (a < 0 || n < 1 || n > P.max_len || b > P.total_tokens) {
+    if (threadIdx.x == 0 && P.status) raise_status(P.status, DOPR_ERR_SEQLEN);
+    return;
+  }
+  const int32_t sa = P.cs[d], sb = P.cs[d + 1];
+  const int32_t K = sb - sa;
+  if (sa < 0 || K < 0 || K > n || sb > P.total_select) {
+    if (threadIdx.x == 0 && P.status) raise_status(P.status, DOPR_ERR_SEQLEN);
+    return;
+  }
+  if (K == 0) return;
+  int32_t *out = P.selected + sa;
+  if (K == n) {
+    for (int i = threadIdx.x; i < n; i += kTopkThreads) out[i] = i;
+    return;
+  }
+  int N2 = 1;
+  while (N2 < n) N2 <<= 1;
+  const float *u = P.u + a;
+  for (int i = threadIdx.x; i < N2; i += kTopkThreads)
+    key[i] = i < n ? ((uint64_t)orderable(u[i]) << 32) | (uint32_t)~i : 0ull;
+  __syncthreads();
+  for (int k = 2; k <= N2; k <<= 1)
+    for (int s = k >> 1; s > 0; s >>= 1) {
+      for (int i = threadIdx.x; i < N2; i += kTopkThreads) {
+        const int x = i ^ s;
+        if (x > i) {
+          const uint64_t p = key[i], q = key[x];
+          const bool desc = (i & k) == 0;
+          if (desc ? p < q : p > q) {
+            key[i] = q;
+            key[x] = p;
+          }
+        }
+      }
+      __syncthreads();
+    }
+  for (int i = threadIdx.x; i < n; i += kTopkThreads) flag[i] = 0;
+  __syncthreads();
+  for (int r = threadIdx.x; r < K; r += kTopkThreads)
+    flag[~(uint32_t)key[r]] = 1;
+  __syncthreads();
+  // ordered compaction: thread t owns positions [t*per, (t+1)*per)
+  const int per = (n + kTopkThreads - 1) / kTopkThreads;
+  const int p0 = threadIdx.x * per;
+  int cnt = 0;
+  for (int i = p0; i < min(p0 + per, n); ++i) cnt += flag[i];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int incl = cnt;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(incl, o, 64);
+    if (lane >= o) incl += y;
+  }
+  if (lane == 63) wsum[wave] = incl;
+  __syncthreads();
+  int before = incl - cnt;
+  for (int w = 0; w < wave; ++w) before += wsum[w];
+  for (int i = p0; i < min(p0 + per, n); ++i)
+    if (flag[i]) out[before++] = i;
+}
+
+}  // namespace
+
+hipError_t launch_salience_chunk(const SalienceParams &p, int32_t n_docs,
+                                 int hr, int pm, hipStream_t s) {
+  if (n_docs == 0) return hipSuccess;
+  const int nb = (p.max_len + kRowBlock - 1) / kRowBlock;
+  const dim3 g_lse(nb, p.hkv, n_docs);
+  const dim3 g_att(nb * (nb + 1) / 2, n_docs);
+  const dim3 g_col((p.max_len + kStrip - 1) / kStrip, n_docs);
+  if (hr == 4) {
+    hipLaunchKernelGGL(k_row_lse<4>, g_lse, dim3(256), 0, s, p);
+    hipLaunchKernelGGL(k_mean_attn<2>, g_att, dim3(256), 0, s, p);
+  } else if (hr == 2) {
+    hipLaunchKernelGGL(k_row_lse<2>, g_lse, dim3(256), 0, s, p);
+    hipLaunchKernelGGL(k_mean_attn<2>, g_att, dim3(256), 0, s, p);
+  } else {
+    hipLaunchKernelGGL(k_row_lse<1>, g_lse, dim3(256), 0, s, p);
+    hipLaunchKernelGGL(k_mean_attn<1>, g_att, dim3(256), 0, s, p);
+  }
+  if (pm == 8)
+    hipLaunchKernelGGL(k_col_topp<8>, g_col, dim3(256), 0, s, p);
+  else if (pm == 16)
+    hipLaunchKernelGGL(k_col_topp<16>, g_col, dim3(256), 0, s, p);
+  else if (pm == 32)
+    hipLaunchKernelGGL(k_col_topp<32>, g_col, dim3(256), 0, s, p);
+  else
+    hipLaunchKernelGGL(k_col_topp<64>, g_col, dim3(256), 0, s, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_salience_check(const SalienceParams &p, hipStream_t s) {
+  if (p.n_docs == 0 || !p.status) return hipSuccess;
+  hipLaunchKernelGGL(k_check, dim3((p.n_docs + 255) / 256), dim3(256), 0, s,
+                     p);
+  return hipGetLastError();
+}
+
+hipError_t launch_topk(const TopkParams &p, int32_t n_docs, hipStream_t s) {
+  if (n_docs == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_topk, dim3(n_docs), dim3(kTopkThreads), 0, s, p);
+  return hipGetLastError();
+}
+
+}  // namespace dopr

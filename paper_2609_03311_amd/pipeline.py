@@ -1,4 +1,5 @@
-"""One decoder layer's online DoPR step on an HBM prefix store.
+"""One decoder layer's online DoPR step on an HBM prefix store, and the
+offline salience selection that decides what the store holds.
 
 A thin convenience layer over the C ABI: it allocates device buffers with
 torch and issues the library calls; all computation runs in the HIP kernels.
@@ -10,7 +11,8 @@ import numpy as np
 from . import (dopr_decoder_layer, dopr_decoder_layer_workspace,
                dopr_prefix_attn, dopr_prefix_attn_score,
                dopr_prefix_attn_score_workspace, dopr_prefix_attn_workspace,
-               dopr_score_logits, dopr_store_create, dopr_store_put)
+               dopr_salience, dopr_salience_workspace, dopr_score_logits,
+               dopr_store_create, dopr_store_put)
 
 HEAD_DIM = 128
 
@@ -168,3 +170,50 @@ class LayerStep:
                            intermediate=self.intermediate, lse=self.lse,
                            kernel_variant=self.kernel_variant, stream=stream,
                            **kw)
+
+
+class SalienceStep:
+    """Reusable buffers for offline salience selection of a batch of
+    documents: salience u of every token and the top-K_d positions of each
+    document (K_d = n_d // ratio by default).  `with_attention` keeps the
+    head-averaged attention of every document ([n_docs, M, M] fp32)."""
+
+    def __init__(self, doc_lens, *, n_q_heads, n_kv_heads, top_p,
+                 n_select=None, ratio=8, max_doclen=None, device="cuda",
+                 with_attention=False):
+        import torch
+        lens = np.asarray(doc_lens, np.int64)
+        self.n_docs = int(lens.shape[0])
+        self.max_doclen = int(max_doclen or max(1, int(lens.max(initial=1))))
+        self.top_p = top_p
+        ks = (lens // ratio if n_select is None
+              else np.asarray(n_select, np.int64))
+        cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+        cs = np.concatenate([[0], np.cumsum(ks)]).astype(np.int32)
+        self.cu_host, self.cs_host = cu, cs
+        self.cu = torch.from_numpy(cu).to(device)
+        self.cs = torch.from_numpy(cs).to(device)
+        ntok = int(cu[-1])
+        self.u = torch.empty(ntok, dtype=torch.float32, device=device)
+        self.selected = torch.empty(max(int(cs[-1]), 1), dtype=torch.int32,
+                                    device=device)[:int(cs[-1])]
+        self.status = torch.zeros(1, dtype=torch.int32, device=device)
+        M = self.max_doclen
+        self.attn_mean = (torch.empty((self.n_docs, M, M), dtype=torch.float32,
+                                      device=device)
+                          if with_attention else None)
+        nbytes = dopr_salience_workspace(
+            n_docs=self.n_docs, max_doclen=M, n_q_heads=n_q_heads,
+            n_kv_heads=n_kv_heads, top_p=top_p, total_tokens=ntok,
+            with_attention=with_attention)
+        self.workspace = torch.empty(max(nbytes, 256), dtype=torch.uint8,
+                                     device=device)
+
+    def run(self, q, k, softmax_scale=HEAD_DIM ** -0.5, select=True,
+            stream=None):
+        dopr_salience(self.cu, q, k, self.u, max_doclen=self.max_doclen,
+                      top_p=self.top_p, softmax_scale=softmax_scale,
+                      cu_select=self.cs if select else None,
+                      selected=self.selected if select else None,
+                      attn_mean=self.attn_mean, status=self.status,
+                      workspace=self.workspace, stream=stream)

@@ -45,7 +45,8 @@ def test_struct_layouts_match_header(tmp_path):
                "dopr_attn_args_t": D._AttnArgs,
                "dopr_score_args_t": D._ScoreArgs,
                "dopr_score_head_t": D._ScoreHead,
-               "dopr_layer_args_t": D._LayerArgs}
+               "dopr_layer_args_t": D._LayerArgs,
+               "dopr_salience_args_t": D._SalienceArgs}
     lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "dopr.h"',
              "int main(void) {"]
     for cname, py in structs.items():
@@ -142,3 +143,56 @@ def test_host_validation_codes():
     assert D.dopr_status_str(D.DOPR_ERR_DOC_RANGE) == "DOPR_ERR_DOC_RANGE"
     assert D.dopr_status_str(D.DOPR_ERR_SEQLEN) == "DOPR_ERR_SEQLEN"
     assert L.dopr_store_destroy(None) == D.DOPR_OK
+
+
+def test_salience_host_validation_and_workspace():
+    """Salience argument checks and workspace sizes (host arithmetic only):
+    the row log-sum-exp of every (token, q head), plus the head-averaged
+    matrix of as many documents as fit in 1 GiB unless the caller keeps it."""
+    D = _D()
+    L = D.lib()
+    ws = D.dopr_salience_workspace(n_docs=64, max_doclen=2048, n_q_heads=32,
+                                   n_kv_heads=8, top_p=8,
+                                   total_tokens=64 * 2048)
+    lse = 4 * 32 * 64 * 2048
+    assert ws == lse + (1 << 30)          # 64 docs of 16 MiB in one pass
+    ws = D.dopr_salience_workspace(n_docs=3, max_doclen=2048, n_q_heads=32,
+                                   n_kv_heads=8, top_p=8, total_tokens=5000)
+    assert ws == -(-4 * 32 * 5000 // 256) * 256 + 3 * 2048 * 2048 * 4
+    ws = D.dopr_salience_workspace(n_docs=3, max_doclen=2048, n_q_heads=32,
+                                   n_kv_heads=8, top_p=8, total_tokens=5000,
+                                   with_attention=True)
+    assert ws == -(-4 * 32 * 5000 // 256) * 256
+    assert D.dopr_salience_workspace(n_docs=0, max_doclen=5, n_q_heads=2,
+                                     n_kv_heads=1, top_p=1,
+                                     total_tokens=0) == 0
+    bad = [dict(max_doclen=4097, code=D.DOPR_ERR_UNSUPPORTED),
+           dict(max_doclen=0, code=D.DOPR_ERR_INVALID_ARG),
+           dict(top_p=65, code=D.DOPR_ERR_UNSUPPORTED),
+           dict(top_p=0, code=D.DOPR_ERR_INVALID_ARG),
+           dict(n_q_heads=12, n_kv_heads=8, code=D.DOPR_ERR_INVALID_ARG),
+           dict(n_docs=-1, code=D.DOPR_ERR_INVALID_ARG)]
+    for b in bad:
+        kw = dict(n_docs=2, max_doclen=64, n_q_heads=16, n_kv_heads=8,
+                  top_p=8, total_tokens=100)
+        code = b.pop("code")
+        kw.update(b)
+        with pytest.raises(D.DoprError) as e:
+            D.dopr_salience_workspace(**kw)
+        assert e.value.status == code, b
+    a = D._SalienceArgs()
+    a.n_docs, a.max_doclen, a.n_q_heads, a.n_kv_heads = 2, 64, 16, 8
+    a.top_p, a.softmax_scale, a.total_tokens = 8, 0.088, 100
+    assert L.dopr_salience(ctypes.byref(a), None) == D.DOPR_ERR_INVALID_ARG
+    assert "cu_doclens and u" in D.dopr_last_error()
+    a.cu_doclens, a.u = 256, 256          # never dereferenced on the host
+    assert L.dopr_salience(ctypes.byref(a), None) == D.DOPR_ERR_INVALID_ARG
+    assert "q and k" in D.dopr_last_error()
+    a.q, a.k = 256, 256
+    assert L.dopr_salience(ctypes.byref(a), None) == D.DOPR_ERR_WORKSPACE
+    a.selected = 256
+    assert L.dopr_select_top_k(ctypes.byref(a), None) == \
+        D.DOPR_ERR_INVALID_ARG
+    assert "cu_select" in D.dopr_last_error()
+    a.n_docs = 0
+    assert L.dopr_select_top_k(ctypes.byref(a), None) == D.DOPR_OK

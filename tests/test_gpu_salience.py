@@ -1,0 +1,274 @@
+"""Offline salience selection (Sec. 3.2.1) vs the float64 oracle (GPU).
+
+Tolerances.  The GPU multiplies bf16 operands exactly and accumulates the
+128 products in fp32, so a logit carries an error of a few fp32 ulps of the
+dot product; in log2 units (|x| < 40 here) that is < 1e-5 absolute, which
+is the relative error of exp2(x - lse2) and of its mean over heads (the
+row log-sum-exp carries the same order).  Abar and u are therefore checked
+to |gpu - oracle| <= 1e-4 |oracle| + 1e-12 (ten times that bound; the
+absolute floor covers probabilities that fp32 flushes to zero).
+
+Selection is integer work decided by floating point, so it is checked in
+two parts: bit-exactly against a CPU top-K of the GPU's own u (stable
+lexsort: larger u first, ties to the lower position, output ascending), and
+for validity against the oracle's u: every chosen position is within the u
+tolerance of the K-th largest oracle value or above it, and every position
+left out is within it or below.
+"""
+import gc
+
+import numpy as np
+import pytest
+
+import workloads
+from gpu_harness import log
+from oracle import salience as sal_oracle
+
+pytestmark = pytest.mark.gpu
+
+D = 128
+RTOL, ATOL = 1e-4, 1e-12
+
+
+def _free():
+    import torch
+    gc.collect()
+    torch.cuda.empty_cache()
+
+
+def _bits(t):
+    import torch
+    return t.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+
+
+def run_case(lens, hq, hkv, p, *, n_select=None, seed=0, q_scale=1.0,
+             with_attention=True, max_doclen=None, q=None, k=None):
+    import torch
+    from paper_2609_03311_amd.pipeline import SalienceStep
+    log(f"salience lens={list(lens)[:8]}{'...' if len(lens) > 8 else ''} "
+        f"docs={len(lens)} Hq={hq} Hkv={hkv} p={p} seed={seed} "
+        f"q_scale={q_scale} attn={with_attention}")
+    if q is None:
+        q, k = workloads.salience_inputs(lens, hq, hkv, "cuda", seed, q_scale)
+    step = SalienceStep(lens, n_q_heads=hq, n_kv_heads=hkv, top_p=p,
+                        n_select=n_select, max_doclen=max_doclen,
+                        with_attention=with_attention)
+    step.run(q, k)
+    torch.cuda.synchronize()
+    assert step.status.item() == 0
+    return step, q, k
+
+
+def cpu_top_k(u32, k):
+    """Stable top-K of fp32 values: larger first, ties to the lower index,
+    returned ascending."""
+    n = len(u32)
+    order = np.lexsort((np.arange(n), -u32.astype(np.float64)))
+    return np.sort(order[:k])
+
+
+def check_doc(step, d, ora, with_attention=True):
+    cu, cs = step.cu_host, step.cs_host
+    t0, t1 = int(cu[d]), int(cu[d + 1])
+    n = t1 - t0
+    u = step.u[t0:t1].cpu().numpy()
+    uo = ora["u"][d]
+    err = np.abs(u - uo)
+    bound = RTOL * np.abs(uo) + ATOL
+    assert (err <= bound).all(), \
+        f"doc {d}: u off by {err.max():.3e} (worst {np.max(err / bound):.2f}x)"
+    if with_attention and d in ora["attention"]:
+        a = step.attn_mean[d, :n, :n].cpu().numpy().astype(np.float64)
+        ao = ora["attention"][d]
+        low = np.tril(np.ones((n, n), bool))
+        e = np.abs(a - ao)[low]
+        b = (RTOL * np.abs(ao) + ATOL)[low]
+        assert (e <= b).all(), \
+            f"doc {d}: attention off by {e.max():.3e} ({np.max(e / b):.2f}x)"
+    K = int(cs[d + 1] - cs[d])
+    sel = step.selected[int(cs[d]):int(cs[d + 1])].cpu().numpy()
+    assert np.array_equal(sel, cpu_top_k(u, K)), f"doc {d}: selection"
+    if 0 < K < n:
+        t = np.sort(uo)[::-1][K - 1]
+        tol = RTOL * t + ATOL
+        chosen = np.zeros(n, bool)
+        chosen[sel] = True
+        assert (uo[chosen] >= t - tol).all(), f"doc {d}: chose a low u"
+        assert (uo[~chosen] <= t + tol).all(), f"doc {d}: left out a high u"
+    return err.max()
+
+
+def oracle_for(step, q, k, p, docs, with_attention=True):
+    return sal_oracle.salience(_bits(q), _bits(k), step.cu_host, D ** -0.5, p,
+                               docs=docs, with_attention=with_attention)
+
+
+EDGE = [
+    # (lengths, Hq, Hkv, p)
+    ([1, 2, 31, 32, 33, 127, 128, 129, 300], 16, 8, 8),
+    ([5, 64, 257], 8, 8, 1),            # n_rep 1, p = 1 (column maximum)
+    ([17, 130, 96], 32, 8, 64),         # n_rep 4, p = 64 > most columns
+    ([200, 3, 131], 32, 4, 13),         # n_rep 8, odd p, M = 200
+    ([77, 1, 40], 12, 4, 3),            # n_rep 3
+]
+
+
+@pytest.mark.parametrize("i", range(len(EDGE)))
+def test_salience_parity_edges(i):
+    lens, hq, hkv, p = EDGE[i]
+    rng = np.random.default_rng(i)
+    ks = [int(rng.integers(0, n + 1)) for n in lens]
+    ks[0] = lens[0]                     # K = n
+    ks[-1] = 0                          # K = 0
+    step, q, k = run_case(lens, hq, hkv, p, n_select=ks, seed=10 + i,
+                          q_scale=1.0 + i)
+    ora = oracle_for(step, q, k, p, range(len(lens)))
+    worst = max(check_doc(step, d, ora) for d in range(len(lens)))
+    log(f"edge case {i}: max |du| {worst:.3e}")
+    del step
+    _free()
+
+
+def test_salience_uniform_closed_form():
+    """q = 0: Abar[j, i] = 1/(j+1) and u strictly decreasing, so the top-K
+    are the first K positions."""
+    import torch
+    lens, hq, hkv, p = [300, 45, 1], 16, 8, 8
+    _, k = workloads.salience_inputs(lens, hq, hkv, "cuda", 5)
+    q = torch.zeros((sum(lens), hq, D), dtype=torch.bfloat16, device="cuda")
+    step, _, _ = run_case(lens, hq, hkv, p, q=q, k=k,
+                          n_select=[37, 45, 1])
+    cu = step.cu_host
+    for d, n in enumerate(lens):
+        a = step.attn_mean[d, :n, :n].cpu().numpy().astype(np.float64)
+        want = np.tril(np.repeat(1.0 / np.arange(1, n + 1)[:, None], n, 1))
+        low = np.tril(np.ones((n, n), bool))
+        assert (np.abs(a - want)[low] <= RTOL * want[low]).all()
+        sel = step.selected[int(step.cs_host[d]):int(step.cs_host[d + 1])]
+        assert sel.cpu().tolist() == list(range(int(step.cs_host[d + 1] -
+                                                    step.cs_host[d])))
+        u = step.u[int(cu[d]):int(cu[d + 1])].cpu().numpy()
+        assert (np.diff(u) < 0).all()
+    del step
+    _free()
+
+
+@pytest.mark.parametrize("name", ["qwen3_0p6b_docs", "qwen3_4b_docs",
+                                  "qwen3_8b_docs"])
+def test_salience_batch_parity(name):
+    """The benchmarked batches (K = n/8, p = 8), attention kept in the
+    workspace, on a sample of documents the oracle recomputes."""
+    lens, hq, hkv = workloads.salience_batch(name)
+    step, q, k = run_case(lens, hq, hkv, workloads.SALIENCE_TOP_P,
+                          with_attention=False)
+    docs = [0, len(lens) // 2, len(lens) - 1]
+    ora = oracle_for(step, q, k, workloads.SALIENCE_TOP_P, docs,
+                     with_attention=False)
+    worst = max(check_doc(step, d, ora, False) for d in docs)
+    log(f"{name}: max |du| {worst:.3e} over docs {docs}")
+    # every document's selection is the exact top-K of its own u
+    u = step.u.cpu().numpy()
+    sel = step.selected.cpu().numpy()
+    cu, cs = step.cu_host, step.cs_host
+    for d in range(len(lens)):
+        got = sel[cs[d]:cs[d + 1]]
+        assert np.array_equal(got, cpu_top_k(u[cu[d]:cu[d + 1]],
+                                             int(cs[d + 1] - cs[d]))), d
+    del step
+    _free()
+
+
+def test_salience_longest_document():
+    """One document at the length limit (4096), GQA 8/2, p = 32."""
+    lens = [4096]
+    step, q, k = run_case(lens, 8, 2, 32, n_select=[512], seed=3,
+                          with_attention=False)
+    ora = oracle_for(step, q, k, 32, [0], with_attention=False)
+    log(f"n=4096: max |du| {check_doc(step, 0, ora, False):.3e}")
+    del step
+    _free()
+
+
+def test_salience_workspace_passes_and_repeat():
+    """Abar in the caller's buffer (one pass) and in the workspace (several
+    passes when the budget is small relative to M^2) give the same bits, and
+    a repeated call reproduces them."""
+    import torch
+    lens, hq, hkv = [513, 2048, 700, 64, 1999], 32, 8
+    q, k = workloads.salience_inputs(lens, hq, hkv, "cuda", 8)
+    a, _, _ = run_case(lens, hq, hkv, 8, q=q, k=k, with_attention=True)
+    b, _, _ = run_case(lens, hq, hkv, 8, q=q, k=k, with_attention=False)
+    # room for the row statistics and two documents: three passes
+    lse = -(-4 * hq * sum(lens) // 256) * 256
+    b.workspace = torch.empty(lse + 2 * 4 * 2048 * 2048 + 100,
+                              dtype=torch.uint8, device="cuda")
+    b.u.zero_()
+    b.selected.zero_()
+    b.run(q, k)
+    torch.cuda.synchronize()
+    assert torch.equal(a.u, b.u) and torch.equal(a.selected, b.selected)
+    u1 = b.u.clone()
+    b.run(q, k)
+    torch.cuda.synchronize()
+    assert torch.equal(u1, b.u)
+    del a, b
+    _free()
+
+
+def test_select_top_k_ties():
+    """The selection entry point alone on u with many exact ties, against
+    the CPU stable top-K, including K = 0, K = n, n = 1 and n = 4096."""
+    import torch
+    from paper_2609_03311_amd import dopr_select_top_k
+    rng = np.random.default_rng(0)
+    lens = [1, 7, 64, 1000, 4096, 333]
+    ks = [1, 0, 17, 999, 1234, 333]
+    u = np.concatenate([rng.integers(0, 5, n) / 4.0 for n in lens])
+    u = u.astype(np.float32)
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    cs = np.concatenate([[0], np.cumsum(ks)]).astype(np.int32)
+    dev = lambda a: torch.from_numpy(a).cuda()
+    sel = torch.full((int(cs[-1]),), -1, dtype=torch.int32, device="cuda")
+    status = torch.zeros(1, dtype=torch.int32, device="cuda")
+    dopr_select_top_k(dev(cu), dev(cs), dev(u), sel, max_doclen=4096,
+                      status=status)
+    torch.cuda.synchronize()
+    assert status.item() == 0
+    got = sel.cpu().numpy()
+    for d in range(len(lens)):
+        want = cpu_top_k(u[cu[d]:cu[d + 1]], ks[d])
+        assert np.array_equal(got[cs[d]:cs[d + 1]], want), d
+
+
+def test_salience_malformed_offsets():
+    """A document longer than max_doclen and a selection count above n_d
+    raise DOPR_ERR_SEQLEN in the status word; the well-formed documents are
+    still exact."""
+    import torch
+    from paper_2609_03311_amd import DOPR_ERR_SEQLEN, dopr_salience
+    lens, hq, hkv, p = [40, 90, 33], 16, 8, 4
+    from paper_2609_03311_amd.pipeline import SalienceStep
+    q, k = workloads.salience_inputs(lens, hq, hkv, "cuda", 12)
+    step = SalienceStep(lens, n_q_heads=hq, n_kv_heads=hkv, top_p=p,
+                        n_select=[4, 9, 3], max_doclen=64)
+    cs = torch.tensor([0, 4, 13, 60], dtype=torch.int32, device="cuda")
+    sel = torch.full((60,), -7, dtype=torch.int32, device="cuda")
+    step.u.fill_(-5.0)
+    dopr_salience(step.cu, q, k, step.u, max_doclen=64, top_p=p,
+                  softmax_scale=D ** -0.5, cu_select=cs, selected=sel,
+                  attn_mean=step.attn_mean, status=step.status,
+                  workspace=step.workspace)
+    torch.cuda.synchronize()
+    assert step.status.item() == DOPR_ERR_SEQLEN
+    u = step.u.cpu().numpy()
+    assert (u[40:130] == -5.0).all()          # doc 1 (90 > 64) skipped
+    ora = sal_oracle.salience(_bits(q), _bits(k), step.cu_host, D ** -0.5,
+                              p, n_select=[4, 9, 3], docs=[0, 2])
+    for d, (t0, t1) in ((0, (0, 40)), (2, (130, 163))):
+        assert (np.abs(u[t0:t1] - ora["u"][d]) <=
+                RTOL * np.abs(ora["u"][d]) + ATOL).all()
+    got = sel.cpu().numpy()
+    assert np.array_equal(got[:4], cpu_top_k(u[0:40], 4))
+    assert (got[13:] == -7).all()             # doc 2: K = 47 > 33 skipped
+    del step
+    _free()

@@ -294,3 +294,35 @@ def layer_weights(st: Structure, hidden: int, intermediate: int,
         "w_up": _randn_bf16((I, W), seed + 7, device, W ** -0.5),
         "w_down": _randn_bf16((W, I), seed + 8, device, I ** -0.5),
     }
+
+
+# ---------------------------------------------------------------------------
+# Offline salience selection: batches of documents encoded on their own.
+# Document lengths follow the paper's corpora at the three backbone sizes
+# (256-, 512- and 2048-token documents, K_infer = n / 8 slots kept, Table 8);
+# the final-layer queries and keys as they enter attention are standard
+# normal bf16 (an RMS-normed, rotated head vector has entries of order one),
+# so the scaled logits are N(0, q_scale^2).
+SALIENCE_BATCHES = {
+    # name: (document length, documents per batch, Hq, Hkv)
+    "qwen3_0p6b_docs": (256, 512, 16, 8),
+    "qwen3_4b_docs": (512, 256, 32, 8),
+    "qwen3_8b_docs": (2048, 64, 32, 8),
+}
+SALIENCE_TOP_P = 8          # the paper gives no value for p
+SALIENCE_RATIO = 8          # K_d = n_d / 8 (Table 8)
+
+
+def salience_batch(name: str):
+    """(doc_lens int32 [n_docs], Hq, Hkv) of a named salience batch."""
+    n, docs, hq, hkv = SALIENCE_BATCHES[name]
+    return np.full(docs, n, np.int32), hq, hkv
+
+
+def salience_inputs(doc_lens, n_q_heads, n_kv_heads, device="cpu",
+                    seed: int = 31, q_scale: float = 1.0):
+    """Final-layer queries [Ntok, Hq, D] and keys [Ntok, Hkv, D], bf16."""
+    ntok = int(np.asarray(doc_lens, np.int64).sum())
+    q = _randn_bf16((ntok, n_q_heads, HEAD_DIM), seed, device, q_scale)
+    k = _randn_bf16((ntok, n_kv_heads, HEAD_DIM), seed + 1, device)
+    return q, k
