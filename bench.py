@@ -15,7 +15,10 @@ float64 CPU oracle timed on a bounded sample of the same workload.
 token is attended (still over its whole prefix and all its own keys) and
 the score head is fused into the attention epilogue.  --path layer measures
 one whole decoder layer over the online tokens (projections, norms, SwiGLU
-MLP and the prefix attention), MFMA-bound.
+MLP and the prefix attention), MFMA-bound.  --path salience measures the
+offline side: salience selection of the prefix slots of a batch of whole
+documents (head-averaged attention, column top-p means, top-K), with
+--config one of the *_docs batches.
 """
 import argparse
 import ctypes
@@ -37,6 +40,9 @@ METRIC_LAYER = ("query-doc pairs/sec per full decoder layer (projections, "
                 "MI355X bf16 dense peak")
 METRIC_SCORE = ("query-doc pairs/sec for the last decoder layer (score-token "
                 "rows + fused score head); achieved HBM GB/s vs MI355X peak")
+METRIC_SALIENCE = ("documents/sec of offline salience selection (head-averaged "
+                   "causal attention, column top-p means, top-K); achieved "
+                   "MFMA TFLOP/s vs MI355X bf16 dense peak")
 PEAK_HBM_GBS = 8000.0
 PEAK_BF16_TFLOPS = 2500.0
 
@@ -55,6 +61,17 @@ DESCRIPTIONS = {
                        "(50% Zipf reuse), T=16..128+1",
     "qwen3_8b_ragged_x8": "as qwen3_8b_ragged with 8x longer (uncompressed) "
                           "prefixes, 64..2048 slots",
+}
+SALIENCE_DESCRIPTIONS = {
+    "qwen3_0p6b_docs": "salience selection, Qwen3-0.6B-shaped final layer: "
+                       "16q/8kv heads, D=128, 512 documents x 256 tokens, "
+                       "p=8, K=32 slots kept per document",
+    "qwen3_4b_docs": "salience selection, Qwen3-4B-shaped final layer: "
+                     "32q/8kv heads, D=128, 256 documents x 512 tokens, p=8, "
+                     "K=64 slots kept per document",
+    "qwen3_8b_docs": "salience selection, Qwen3-8B-shaped final layer: "
+                     "32q/8kv heads, D=128, 64 documents x 2048 tokens, p=8, "
+                     "K=256 slots kept per document",
 }
 
 
@@ -289,20 +306,125 @@ def cpu_baseline(st, k_src, v_src, doc_off, online, prm, seconds,
                       f"incl. score head, {total_t:.1f}s"}
 
 
+def salience_work(lens, hq, D=128):
+    """Flops of salience selection: the scaled logits of every head over the
+    causally visible keys, formed twice (once for each row's log-sum-exp,
+    once for the probabilities), and the exponentials of both sweeps."""
+    n = np.asarray(lens, np.int64)
+    visible = int((n * (n + 1) // 2).sum())
+    return dict(flops=2 * 2 * hq * D * visible, exps=2 * hq * visible)
+
+
+def cpu_baseline_salience(lens, q, k, p, seconds):
+    """The float64 salience oracle on a bounded sample of documents."""
+    import oracle
+    from oracle import salience as sal_oracle
+    threads = oracle.max_threads(oracle.lib())
+    rng = np.random.default_rng(99)
+    order = rng.permutation(len(lens))
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+    total_t, n_docs = 0.0, 0
+    for d in order:
+        t0, t1 = int(cu[d]), int(cu[d + 1])
+        qb, kb = bits(q[t0:t1]), bits(k[t0:t1])
+        c = time.perf_counter()
+        sal_oracle.salience(qb, kb, [0, t1 - t0], 128 ** -0.5, p,
+                            n_select=[(t1 - t0) // 8])
+        total_t += time.perf_counter() - c
+        n_docs += 1
+        if total_t >= seconds:
+            break
+    return {"value": round(n_docs / total_t, 3), "unit": "documents/s",
+            "cores": int(threads), "kind": "oracle",
+            "sample": f"{n_docs} of {len(lens)} documents (seeded random "
+                      f"order), float64 numpy salience oracle incl. top-K, "
+                      f"{total_t:.1f}s"}
+
+
+def bench_salience(args):
+    """Offline salience selection of a batch of documents: one step is one
+    dopr_salience call (row log-sum-exp, head-averaged attention, column
+    top-p means, top-K) over the whole batch, inputs resident in HBM."""
+    import torch
+
+    import workloads
+    from paper_2609_03311_amd.pipeline import SalienceStep
+    lens, hq, hkv = workloads.salience_batch(args.config)
+    p = workloads.SALIENCE_TOP_P
+    dev = "cuda"
+    q, k = workloads.salience_inputs(lens, hq, hkv, dev)
+    step = SalienceStep(lens, n_q_heads=hq, n_kv_heads=hkv, top_p=p,
+                        ratio=workloads.SALIENCE_RATIO, device=dev)
+    torch.cuda.synchronize()
+    log(f"{args.config}: {len(lens)} documents x {int(lens[0])} tokens, "
+        f"{hq}q/{hkv}kv heads; warming up")
+    for _ in range(args.warmup):
+        step.run(q, k)
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True),
+           torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for a, b in ev:
+        a.record()
+        step.run(q, k)
+        b.record()
+    t1.record()
+    torch.cuda.synchronize()
+    if int(step.status.item()) != 0:
+        raise SystemExit(f"device status {int(step.status.item())}")
+    ms_step = t0.elapsed_time(t1) / args.steps
+    call_ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
+    log(f"step {ms_step:.3f} ms, call avg {call_ms:.3f} ms")
+    w = salience_work(lens, hq)
+    achieved = w["flops"] / (call_ms * 1e-3) / 1e12
+    result = {
+        "metric": METRIC_SALIENCE,
+        "value": round(len(lens) / (ms_step * 1e-3), 1),
+        "unit": "documents/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1) bf16 final-layer queries and "
+                "keys; no datasets or weights)",
+        "config": {"workload": SALIENCE_DESCRIPTIONS[args.config],
+                   "name": args.config, "documents": int(len(lens)),
+                   "tokens": int(lens.sum()), "top_p": p,
+                   "path": "offline salience selection",
+                   "parallelism": "single GPU"},
+        "salience_ms": round(call_ms, 4),
+        "exps": w["exps"],
+        "roofline": {"bound": "mfma", "achieved": round(achieved, 1),
+                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                     "traffic": None,
+                     "scope": "the whole dopr_salience call (four kernels)"},
+    }
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle on a bounded sample")
+        result["cpu_baseline"] = cpu_baseline_salience(lens, q, k, p,
+                                                       args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="qwen3_8b",
-                    choices=sorted(DESCRIPTIONS))
+                    choices=sorted(DESCRIPTIONS) +
+                    sorted(SALIENCE_DESCRIPTIONS))
     ap.add_argument("--variant", type=int, default=0)
-    ap.add_argument("--path", choices=["full", "score", "layer"],
+    ap.add_argument("--path", choices=["full", "score", "layer", "salience"],
                     default="full",
                     help="full: every online row of one layer's attention "
                          "(default); score: last-layer scoring (score-token "
                          "rows, fused score head); layer: one whole decoder "
-                         "layer")
+                         "layer; salience: offline salience selection of "
+                         "a batch of documents (--config *_docs)")
     ap.add_argument("--no-score-rows", action="store_true",
                     help="with --path score: do not write the score rows "
                          "(the fused head alone)")
@@ -320,6 +442,13 @@ def main():
               "GPU serving its own shard of the prefix store). Run with "
               "--gpus 1.", file=sys.stderr)
         sys.exit(2)
+
+    if (args.path == "salience") != (args.config in SALIENCE_DESCRIPTIONS):
+        ap.error("--path salience goes with a *_docs --config, and a *_docs "
+                 "config with --path salience")
+    if args.path == "salience":
+        bench_salience(args)
+        return
 
     import torch
 
