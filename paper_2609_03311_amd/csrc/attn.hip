@@ -317,11 +317,29 @@ __device__ __forceinline__ void wait_vmem() {
 
 // One own-key chunk: 32 keys of one pair starting at key c0 (wave-uniform).
 struct OwnStep {
-  int s;     // sorted pair index
-  int c0;    // first own key of the chunk
-  int tok0;  // the pair's first batch token
-  int T;     // the pair's token count
+  int s;      // sorted pair index
+  int c0;     // first own key of the chunk
+  int tok0;   // the pair's first batch token
+  int T;      // the pair's token count
+  int srow0;  // the pair's first stacked row
 };
+
+// Sum over the 8 lanes 8k..8k+7 (every lane gets the same value): the two
+// quad butterflies, then the other quad through row_half_mirror (DPP, no
+// LDS round trip).  The additions pair the same values as a butterfly
+// over lane ^ 1, ^ 2, ^ 4.
+__device__ __forceinline__ float sum8_lanes(float x) {
+  x += __builtin_bit_cast(
+      float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), 0xB1, 0xF,
+                                      0xF, false));
+  x += __builtin_bit_cast(
+      float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), 0x4E, 0xF,
+                                      0xF, false));
+  x += __builtin_bit_cast(
+      float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), 0x141, 0xF,
+                                      0xF, false));
+  return x;
+}
 
 // Raw k/v rows and rotary factors of one own-key chunk, held in registers
 // between the prefetch and the LDS stage.  Thread t handles key
@@ -387,6 +405,9 @@ __device__ __forceinline__ void own_stage(const AttnParams &P,
   const int t = threadIdx.x + opaque_zero();
   const int kk = (t >> 3) & 31, sub = t & 7;
   if (key_role<WAVES>()) {
+    // the gains first: their load overlaps the norm's reduction
+    const uint4 g0 = *reinterpret_cast<const uint4 *>(P.kw + 8 * sub);
+    const uint4 g1 = *reinterpret_cast<const uint4 *>(P.kw + 64 + 8 * sub);
     float x[16];
     float ss = r.valid ? sumsq8(r.a1, sumsq8(r.a0, 0.f)) : 0.f;
     if (r.valid) {
@@ -396,15 +417,12 @@ __device__ __forceinline__ void own_stage(const AttnParams &P,
 #pragma unroll
       for (int e = 0; e < 16; ++e) x[e] = 0.f;
     }
-    ss += __shfl_xor(ss, 1, 64);
-    ss += __shfl_xor(ss, 2, 64);
-    ss += __shfl_xor(ss, 4, 64);
+    ss = sum8_lanes(ss);
     if (r.valid) {
       const float inv = rsqrtf(ss * (1.0f / D) + P.eps);
-      const uint16_t *kw = P.kw;
       float w0[8], w1[8];
-      unpack8(*reinterpret_cast<const uint4 *>(kw + 8 * sub), w0);
-      unpack8(*reinterpret_cast<const uint4 *>(kw + 64 + 8 * sub), w1);
+      unpack8(g0, w0);
+      unpack8(g1, w1);
       const float cs[16] = {r.r0.x, r.r0.y, r.r0.z, r.r0.w, r.r1.x, r.r1.y,
                             r.r1.z, r.r1.w, r.r2.x, r.r2.y, r.r2.z, r.r2.w,
                             r.r3.x, r.r3.y, r.r3.z, r.r3.w};
@@ -687,6 +705,7 @@ __device__ __forceinline__ bool run_unit(const AttnParams &P, Smem<NCHK> &sm,
       const int4 sp = P.spair[os.s];
       os.tok0 = sp.x;
       os.T = sp.y;
+      os.srow0 = sp.z;
     }
     OwnRegs<WAVES> orr;
 
@@ -700,6 +719,38 @@ __device__ __forceinline__ bool run_unit(const AttnParams &P, Smem<NCHK> &sm,
       }
       wait_vmem();
       __syncthreads();
+      if (WAVES == 8 && resident) {
+        // L2 warm-up while the prefix products run: one direct-to-LDS dword
+        // load per 128-byte line of the own k/v rows of the pass's first
+        // pair and of this lane's q row in the next pass, so the own-key
+        // steps and the next prologue find those lines in L2.  The dwords
+        // land in own buffer 1, which nothing reads or writes until the
+        // own-key phase; every wave drains them before that phase begins.
+        const int t = threadIdx.x;
+        uint16_t *junk = sm.ok[1] + wave * 512;
+        const int n_lines = os.T * 4;
+        for (int u2 = t, i = 0; i < 2; u2 += WAVES * 64, ++i) {
+          if (u2 < n_lines) {
+            const int tok = os.tok0 + (u2 >> 2);
+            const uint16_t *base = (u2 & 2) ? P.v : P.k;
+            __builtin_amdgcn_global_load_lds(
+                (const __attribute__((address_space(1))) void *)(
+                    base + ((int64_t)tok * P.Hkv + g) * D + (u2 & 1) * 64),
+                (__attribute__((address_space(3))) void *)(junk + i * 128),
+                4, 0, 0);
+          }
+        }
+        if (pass0 + PASS < row1) {
+          const int r = pass0 + PASS + wave * NQB * 32 + lq;
+          const int rc = r < row1 ? r : row1 - 1;
+          const int hd = g * P.n_rep + rc % P.n_rep;
+          __builtin_amdgcn_global_load_lds(
+              (const __attribute__((address_space(1))) void *)(
+                  P.q + ((int64_t)tj_next[0].x * P.Hq + hd) * D + hf * 64),
+              (__attribute__((address_space(3))) void *)(junk + 256), 4, 0,
+              0);
+        }
+      }
       const int n_full = live ? n >> 5 : 0;
       for (int ck = 0; ck < n_full; ++ck)
         attend<0, NQB, SMX>(sm.pk[ck], sm.pv[ck], fo, qf, acc, hf, B,
@@ -719,6 +770,7 @@ __device__ __forceinline__ bool run_unit(const AttnParams &P, Smem<NCHK> &sm,
     // (The first chunk is loaded only here: its registers are not held
     // through the prefix products.)
     own_load<WAVES>(P, os, g, L, orr);
+    wait_vmem();      // (also the warm-up loads into own buffer 1)
     __syncthreads();  // the previous pass's last own chunk is consumed
     own_stage<WAVES, NCHK>(P, orr, sm, 0);
     __syncthreads();
@@ -727,7 +779,7 @@ __device__ __forceinline__ bool run_unit(const AttnParams &P, Smem<NCHK> &sm,
       // next step: next chunk of this pair, else first chunk of the next.
       // Positions are stacked in descending order, so the pass's latest
       // position of this pair is at its first row in the pass.
-      const int srow0 = P.spair[os.s].z;
+      const int srow0 = os.srow0;
       const int lo_row = srow0 > pass0 ? srow0 : pass0;
       const int jmax = os.T - 1 - (lo_row - srow0) / P.n_rep;
       OwnStep nx = os;
@@ -740,6 +792,7 @@ __device__ __forceinline__ bool run_unit(const AttnParams &P, Smem<NCHK> &sm,
           const int4 sp = P.spair[nx.s];
           nx.tok0 = sp.x;
           nx.T = sp.y;
+          nx.srow0 = sp.z;
         }
       }
       const bool more = nx.s <= s_hi;
