@@ -18,7 +18,9 @@ one whole decoder layer over the online tokens (projections, norms, SwiGLU
 MLP and the prefix attention), MFMA-bound.  --path salience measures the
 offline side: salience selection of the prefix slots of a batch of whole
 documents (head-averaged attention, column top-p means, top-K), with
---config one of the *_docs batches.
+--config one of the *_docs batches.  --sweep-kinfer K1,K2,... times the
+full path on the same pairs at several inference prefix budgets (every
+document holds K slots) and prints one JSON line per budget.
 """
 import argparse
 import ctypes
@@ -409,6 +411,88 @@ def bench_salience(args):
     print(json.dumps(result), flush=True)
 
 
+def bench_kinfer(args):
+    """Same pairs, several inference prefix budgets K_infer (Sec. 4.5, the
+    memory and latency axes of the budget trade-off): the store holds K
+    slots per document; one JSON line per budget."""
+    import torch
+
+    import workloads
+    from paper_2609_03311_amd import dopr_check_status, pipeline
+    budgets = [int(k) for k in args.sweep_kinfer.split(",") if k]
+    base = workloads.make(args.config)
+    dev = "cuda"
+    online = workloads.online_inputs(base, dev, 3)
+    prm = workloads.params(base, dev, 6)
+    doc_ids = torch.from_numpy(base.doc_ids).to(dev)
+    cu = torch.from_numpy(base.cu_seqlens).to(dev)
+    n_layers_model = {1024: 28, 2560: 36, 4096: 36}.get(base.hidden, 1)
+    for K in budgets:
+        st = workloads.with_prefix_budget(base, K)
+        k_src, v_src, _, _ = workloads.prefix_source(st, dev, 1)
+        store = pipeline.make_store(st.doc_len, st.n_kv_heads, k_src, v_src,
+                                    device=dev)
+        del k_src, v_src
+        step = pipeline.OnlineStep(store, n_pairs=st.n_pairs,
+                                   n_q_heads=st.n_q_heads,
+                                   total_tokens=st.n_tokens,
+                                   max_tokens=int(st.seqlens.max()),
+                                   kernel_variant=args.variant, device=dev)
+        ev = HipEvents(2 * args.steps)
+        for _ in range(args.warmup):
+            step.attention(0, doc_ids, cu, online["q"], online["k"],
+                           online["v"], prm["q_norm_w"], prm["k_norm_w"])
+        torch.cuda.synchronize()
+        t0 = torch.cuda.Event(enable_timing=True)
+        t1 = torch.cuda.Event(enable_timing=True)
+        t0.record()
+        for i in range(args.steps):
+            step.attention(0, doc_ids, cu, online["q"], online["k"],
+                           online["v"], prm["q_norm_w"], prm["k_norm_w"],
+                           timing=(ev.ev[2 * i], ev.ev[2 * i + 1]))
+            step.score_head(cu, prm["norm_w"], prm["w_head"])
+        t1.record()
+        torch.cuda.synchronize()
+        ms_step = t0.elapsed_time(t1) / args.steps
+        attn = float(np.mean([ev.elapsed_ms(2 * i, 2 * i + 1)
+                              for i in range(args.steps)]))
+        ev.close()
+        if dopr_check_status(store) != 0:
+            raise SystemExit(f"device status error at K={K}")
+        w = algorithmic_work(st)
+        per_doc = K * st.n_kv_heads * st.head_dim * 2 * 2
+        achieved = w["total"] / (attn * 1e-3) / 1e9
+        res = {
+            "metric": METRIC, "value": round(st.n_pairs / (ms_step * 1e-3), 1),
+            "unit": "pairs/s", "n_gpus": 1, "steps": args.steps,
+            "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
+            "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+            "dtype": "bf16", "data": "synthetic",
+            "config": {"workload": DESCRIPTIONS[args.config] +
+                       f"; inference prefix budget K_infer={K} slots",
+                       "name": f"{args.config}_k{K}", "k_infer": K,
+                       "parallelism": "single GPU"},
+            "attention_ms": round(attn, 4),
+            "us_per_pair": round(ms_step * 1e3 / st.n_pairs, 4),
+            "store_gb_per_layer": round(per_doc * int((st.doc_len > 0).sum())
+                                        / 1e9, 3),
+            "doc_state_kb_all_layers": round(per_doc * n_layers_model / 1024,
+                                             1),
+            "algorithmic_gb": round(w["total"] / 1e9, 4),
+            "prefix_gb": round(w["prefix"] / 1e9, 4),
+            "attention_tflops": round(w["flops"] / (attn * 1e-3) / 1e12, 1),
+            "roofline": {"bound": "hbm", "achieved": round(achieved, 1),
+                         "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                         "frac": round(achieved / PEAK_HBM_GBS, 4),
+                         "traffic": None},
+        }
+        print(json.dumps(res), flush=True)
+        log(f"K_infer={K}: attention {attn:.3f} ms, step {ms_step:.3f} ms, "
+            f"{achieved:.0f} GB/s")
+        del step, store
+        torch.cuda.empty_cache()
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -428,6 +512,9 @@ def main():
     ap.add_argument("--no-score-rows", action="store_true",
                     help="with --path score: do not write the score rows "
                          "(the fused head alone)")
+    ap.add_argument("--sweep-kinfer", default="",
+                    help="comma-separated inference prefix budgets: time the "
+                         "full path on the same pairs at each budget")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -448,6 +535,9 @@ def main():
                  "config with --path salience")
     if args.path == "salience":
         bench_salience(args)
+        return
+    if args.sweep_kinfer:
+        bench_kinfer(args)
         return
 
     import torch

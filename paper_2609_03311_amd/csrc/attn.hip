@@ -719,38 +719,6 @@ __device__ __forceinline__ bool run_unit(const AttnParams &P, Smem<NCHK> &sm,
       }
       wait_vmem();
       __syncthreads();
-      if (WAVES == 8 && resident) {
-        // L2 warm-up while the prefix products run: one direct-to-LDS dword
-        // load per 128-byte line of the own k/v rows of the pass's first
-        // pair and of this lane's q row in the next pass, so the own-key
-        // steps and the next prologue find those lines in L2.  The dwords
-        // land in own buffer 1, which nothing reads or writes until the
-        // own-key phase; every wave drains them before that phase begins.
-        const int t = threadIdx.x;
-        uint16_t *junk = sm.ok[1] + wave * 512;
-        const int n_lines = os.T * 4;
-        for (int u2 = t, i = 0; i < 2; u2 += WAVES * 64, ++i) {
-          if (u2 < n_lines) {
-            const int tok = os.tok0 + (u2 >> 2);
-            const uint16_t *base = (u2 & 2) ? P.v : P.k;
-            __builtin_amdgcn_global_load_lds(
-                (const __attribute__((address_space(1))) void *)(
-                    base + ((int64_t)tok * P.Hkv + g) * D + (u2 & 1) * 64),
-                (__attribute__((address_space(3))) void *)(junk + i * 128),
-                4, 0, 0);
-          }
-        }
-        if (pass0 + PASS < row1) {
-          const int r = pass0 + PASS + wave * NQB * 32 + lq;
-          const int rc = r < row1 ? r : row1 - 1;
-          const int hd = g * P.n_rep + rc % P.n_rep;
-          __builtin_amdgcn_global_load_lds(
-              (const __attribute__((address_space(1))) void *)(
-                  P.q + ((int64_t)tj_next[0].x * P.Hq + hd) * D + hf * 64),
-              (__attribute__((address_space(3))) void *)(junk + 256), 4, 0,
-              0);
-        }
-      }
       const int n_full = live ? n >> 5 : 0;
       for (int ck = 0; ck < n_full; ++ck)
         attend<0, NQB, SMX>(sm.pk[ck], sm.pv[ck], fo, qf, acc, hf, B,
@@ -770,7 +738,6 @@ __device__ __forceinline__ bool run_unit(const AttnParams &P, Smem<NCHK> &sm,
     // (The first chunk is loaded only here: its registers are not held
     // through the prefix products.)
     own_load<WAVES>(P, os, g, L, orr);
-    wait_vmem();      // (also the warm-up loads into own buffer 1)
     __syncthreads();  // the previous pass's last own chunk is consumed
     own_stage<WAVES, NCHK>(P, orr, sm, 0);
     __syncthreads();

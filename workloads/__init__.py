@@ -157,6 +157,16 @@ def qwen3_8b_ragged(seed: int = 0, prefix_scale: int = 1) -> Structure:
     return Structure(name, 32, 8, 4096, doc_len, doc_ids, seqlens, seed=seed)
 
 
+def with_prefix_budget(st: Structure, k_infer: int) -> Structure:
+    """The same pairs with every resident document's prefix set to k_infer
+    slots: one inference prefix budget of a K_infer sweep (Sec. 4.5: the
+    budget is chosen at deployment without retraining)."""
+    doc_len = np.where(st.doc_len >= 0, k_infer, -1).astype(np.int32)
+    return Structure(f"{st.name}_k{k_infer}", st.n_q_heads, st.n_kv_heads,
+                     st.hidden, doc_len, st.doc_ids.copy(),
+                     st.seqlens.copy(), seed=st.seed)
+
+
 CONFIGS = {
     "tiny": tiny,
     "qwen3_0p6b": qwen3_0p6b,
