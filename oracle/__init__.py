@@ -54,7 +54,7 @@ def _bind(lib):
     lib.dopr_oracle_prefix_attn.restype = ctypes.c_int
     lib.dopr_oracle_prefix_attn.argtypes = [
         i32, i32, i32, i32, P, P, i64, P, P, P, P, P, P, P, P, P,
-        f64, f64, f64, P, P, P, i32]
+        f64, f64, P, f64, P, P, P, i32]
     lib.dopr_oracle_score_attn.restype = ctypes.c_int
     lib.dopr_oracle_score_attn.argtypes = lib.dopr_oracle_prefix_attn.argtypes
     lib.dopr_oracle_prefix_attn_f64.restype = ctypes.c_int
@@ -102,8 +102,12 @@ def max_threads(L=None) -> int:
 def prefix_attn(doc_ids, cu_seqlens, doc_len, doc_off, prefix_k, prefix_v,
                 q, k, v, q_norm_w, k_norm_w, *, n_q_heads, n_kv_heads,
                 rms_eps=1e-6, rope_theta=1e6, softmax_scale=None,
-                threads=0, last_only=False, L=None):
+                rope_inv_freq=None, threads=0, last_only=False, L=None):
     """Online prefix attention, float64.
+
+    q_norm_w, k_norm_w: bf16 gains of the per-head RMSNorm, or both None for
+    attention without QK-norm.  rope_inv_freq: float64 [D/2] rotation
+    frequencies, or None for theta^(-2i/D).
 
     prefix_k/prefix_v: uint16 [slots, Hkv, D]; document d's slots start at
     row doc_off[d].  q: uint16 [Ntok, Hq, D]; k, v: uint16 [Ntok, Hkv, D].
@@ -124,9 +128,13 @@ def prefix_attn(doc_ids, cu_seqlens, doc_len, doc_off, prefix_k, prefix_v,
     q = _c(q, qkv_t)
     k = _c(k, qkv_t)
     v = _c(v, qkv_t)
-    wq = _c(q_norm_w, np.uint16)
-    wk = _c(k_norm_w, np.uint16)
+    assert (q_norm_w is None) == (k_norm_w is None)
+    wq = None if q_norm_w is None else _c(q_norm_w, np.uint16)
+    wk = None if k_norm_w is None else _c(k_norm_w, np.uint16)
     D = q.shape[-1]
+    inv_freq = (None if rope_inv_freq is None
+                else _c(rope_inv_freq, np.float64))
+    assert inv_freq is None or inv_freq.shape == (D // 2,)
     ntok = int(cu[-1]) if cu.size else 0
     assert q.shape == (ntok, n_q_heads, D), (q.shape, ntok)
     assert k.shape == (ntok, n_kv_heads, D) and v.shape == k.shape
@@ -149,8 +157,10 @@ def prefix_attn(doc_ids, cu_seqlens, doc_len, doc_off, prefix_k, prefix_v,
     rc = fn(
         P, n_q_heads, n_kv_heads, D, _p(doc_ids), _p(cu), doc_len.shape[0],
         _p(doc_len), _p(doc_off), _p(pk), _p(pv), _p(q), _p(k), _p(v),
-        _p(wq), _p(wk), rms_eps, rope_theta, softmax_scale, _p(out), _p(lse),
-        _p(status), int(threads))
+        _p(wq) if wq is not None else None,
+        _p(wk) if wk is not None else None, rms_eps, rope_theta,
+        _p(inv_freq) if inv_freq is not None else None, softmax_scale,
+        _p(out), _p(lse), _p(status), int(threads))
     if rc != 0:
         raise RuntimeError(f"oracle prefix_attn failed: {rc}")
     return out, lse, status

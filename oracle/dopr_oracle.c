@@ -17,6 +17,9 @@
  * Qwen3 details the paper does not restate (it names only the Qwen3
  * backbone): per-head RMSNorm of q and k before rotate-half RoPE, GQA with
  * contiguous head groups, online positions continuing after the prefix.
+ * For the cross-family check (Llama; Appendix, "Generalization Across Model
+ * Families") the norm gains may be absent (no QK-norm) and the rotation
+ * frequencies may be given by the caller.
  *
  * Inputs are bf16 bit patterns (uint16) converted exactly to double; every
  * intermediate is double; no blocking, fusion or reordering.
@@ -53,11 +56,15 @@ static void rms_norm(const double *x, const double *w, int n, double eps,
 }
 
 /* Rotate-half rotary embedding at integer position `pos`: for i < D/2 the
- * pair (x_i, x_{i+D/2}) is rotated by angle pos * theta^(-2i/D). */
-static void rope(double *x, int d, double pos, double theta) {
+ * pair (x_i, x_{i+D/2}) is rotated by angle pos * omega_i, with
+ * omega_i = theta^(-2i/D), or inv_freq[i] when the caller gives the
+ * frequencies (model families that rescale them, e.g. Llama 3). */
+static void rope(double *x, int d, double pos, double theta,
+                 const double *inv_freq) {
   int half = d / 2;
   for (int i = 0; i < half; ++i) {
-    double freq = pow(theta, -2.0 * (double)i / (double)d);
+    double freq = inv_freq ? inv_freq[i]
+                           : pow(theta, -2.0 * (double)i / (double)d);
     double ang = pos * freq;
     double c = cos(ang), s = sin(ang);
     double a = x[i], b = x[i + half];
@@ -101,11 +108,16 @@ static int attention(
     const int32_t *doc_len, const int64_t *doc_off, const uint16_t *prefix_k,
     const uint16_t *prefix_v, const void *q, const void *k, const void *v,
     const uint16_t *q_norm_w, const uint16_t *k_norm_w, double rms_eps,
-    double rope_theta, double softmax_scale, double *out, double *lse,
-    int32_t *pair_status, int32_t n_threads, int last_only, int qkv_f64) {
+    double rope_theta, const double *rope_inv_freq, double softmax_scale,
+    double *out, double *lse, int32_t *pair_status, int32_t n_threads,
+    int last_only, int qkv_f64) {
   if (n_pairs < 0 || n_q_heads <= 0 || n_kv_heads <= 0 || head_dim <= 0 ||
       head_dim % 2 || n_q_heads % n_kv_heads)
     return ORACLE_ERR_ARG;
+  /* Both gains or neither: without them q and k enter RoPE as given (no
+   * per-head RMSNorm, as in attention families without QK-norm). */
+  if ((q_norm_w == NULL) != (k_norm_w == NULL)) return ORACLE_ERR_ARG;
+  const int qk_norm = q_norm_w != NULL;
   const int D = head_dim, Hq = n_q_heads, Hkv = n_kv_heads;
   const int n_rep = Hq / Hkv;
   for (int32_t p = 0; p < n_pairs; ++p)
@@ -115,8 +127,8 @@ static int attention(
   double *wk = (double *)malloc(sizeof(double) * D);
   if (!wq || !wk) { free(wq); free(wk); return ORACLE_ERR_NOMEM; }
   for (int i = 0; i < D; ++i) {
-    wq[i] = bf16_to_double(q_norm_w[i]);
-    wk[i] = bf16_to_double(k_norm_w[i]);
+    wq[i] = qk_norm ? bf16_to_double(q_norm_w[i]) : 1.0;
+    wk[i] = qk_norm ? bf16_to_double(k_norm_w[i]) : 1.0;
   }
 
   int failed = 0;
@@ -166,8 +178,11 @@ static int attention(
         const int64_t ks = ((tok0 + j) * Hkv + g) * D;
         for (int i = 0; i < D; ++i) x[i] = online_elem(k, ks + i, qkv_f64);
         double *dst = khat + ((int64_t)j * Hkv + g) * D;
-        rms_norm(x, wk, D, rms_eps, dst);
-        rope(dst, D, (double)(L + j), rope_theta);
+        if (qk_norm)
+          rms_norm(x, wk, D, rms_eps, dst);
+        else
+          for (int i = 0; i < D; ++i) dst[i] = x[i];
+        rope(dst, D, (double)(L + j), rope_theta, rope_inv_freq);
         const int64_t vs = ((tok0 + j) * Hkv + g) * D;
         double *vd = vown + ((int64_t)j * Hkv + g) * D;
         for (int i = 0; i < D; ++i) vd[i] = online_elem(v, vs + i, qkv_f64);
@@ -182,8 +197,11 @@ static int attention(
         const int g = h / n_rep;
         const int64_t qs = ((tok0 + j) * Hq + h) * D;
         for (int i = 0; i < D; ++i) x[i] = online_elem(q, qs + i, qkv_f64);
-        rms_norm(x, wq, D, rms_eps, qhat);
-        rope(qhat, D, (double)(L + j), rope_theta);
+        if (qk_norm)
+          rms_norm(x, wq, D, rms_eps, qhat);
+        else
+          for (int i = 0; i < D; ++i) qhat[i] = x[i];
+        rope(qhat, D, (double)(L + j), rope_theta, rope_inv_freq);
 
         const int n_keys = L + j + 1;
         for (int t = 0; t < L; ++t) {
@@ -232,12 +250,14 @@ int dopr_oracle_prefix_attn(
     const int32_t *doc_len, const int64_t *doc_off, const uint16_t *prefix_k,
     const uint16_t *prefix_v, const uint16_t *q, const uint16_t *k,
     const uint16_t *v, const uint16_t *q_norm_w, const uint16_t *k_norm_w,
-    double rms_eps, double rope_theta, double softmax_scale, double *out,
-    double *lse, int32_t *pair_status, int32_t n_threads) {
+    double rms_eps, double rope_theta, const double *rope_inv_freq,
+    double softmax_scale, double *out, double *lse, int32_t *pair_status,
+    int32_t n_threads) {
   return attention(n_pairs, n_q_heads, n_kv_heads, head_dim, doc_ids,
                    cu_seqlens, n_docs, doc_len, doc_off, prefix_k, prefix_v,
                    q, k, v, q_norm_w, k_norm_w, rms_eps, rope_theta,
-                   softmax_scale, out, lse, pair_status, n_threads, 0, 0);
+                   rope_inv_freq, softmax_scale, out, lse, pair_status,
+                   n_threads, 0, 0);
 }
 
 /*
@@ -251,12 +271,14 @@ int dopr_oracle_prefix_attn_f64(
     const int32_t *doc_len, const int64_t *doc_off, const uint16_t *prefix_k,
     const uint16_t *prefix_v, const double *q, const double *k,
     const double *v, const uint16_t *q_norm_w, const uint16_t *k_norm_w,
-    double rms_eps, double rope_theta, double softmax_scale, double *out,
-    double *lse, int32_t *pair_status, int32_t n_threads) {
+    double rms_eps, double rope_theta, const double *rope_inv_freq,
+    double softmax_scale, double *out, double *lse, int32_t *pair_status,
+    int32_t n_threads) {
   return attention(n_pairs, n_q_heads, n_kv_heads, head_dim, doc_ids,
                    cu_seqlens, n_docs, doc_len, doc_off, prefix_k, prefix_v,
                    q, k, v, q_norm_w, k_norm_w, rms_eps, rope_theta,
-                   softmax_scale, out, lse, pair_status, n_threads, 0, 1);
+                   rope_inv_freq, softmax_scale, out, lse, pair_status,
+                   n_threads, 0, 1);
 }
 
 /*
@@ -272,12 +294,14 @@ int dopr_oracle_score_attn(
     const int32_t *doc_len, const int64_t *doc_off, const uint16_t *prefix_k,
     const uint16_t *prefix_v, const uint16_t *q, const uint16_t *k,
     const uint16_t *v, const uint16_t *q_norm_w, const uint16_t *k_norm_w,
-    double rms_eps, double rope_theta, double softmax_scale, double *out,
-    double *lse, int32_t *pair_status, int32_t n_threads) {
+    double rms_eps, double rope_theta, const double *rope_inv_freq,
+    double softmax_scale, double *out, double *lse, int32_t *pair_status,
+    int32_t n_threads) {
   return attention(n_pairs, n_q_heads, n_kv_heads, head_dim, doc_ids,
                    cu_seqlens, n_docs, doc_len, doc_off, prefix_k, prefix_v,
                    q, k, v, q_norm_w, k_norm_w, rms_eps, rope_theta,
-                   softmax_scale, out, lse, pair_status, n_threads, 1, 0);
+                   rope_inv_freq, softmax_scale, out, lse, pair_status,
+                   n_threads, 1, 0);
 }
 
 /*

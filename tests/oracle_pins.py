@@ -11,6 +11,8 @@ raises AssertionError when the oracle disagrees with:
     relative-position property),
   * invariances (pair order, duplicated documents, bad ids),
   * the paper's printed memory figures (Tables 3, 9, 13, 14),
+  * Hugging Face's Llama rotary embedding + SDPA for attention without
+    QK-norm and with caller-given rotary frequencies (head sizes 128, 64),
   * Python's stable sort (grouping) and torch (score head).
 """
 from __future__ import annotations
@@ -413,8 +415,71 @@ def pin_store_bytes(L):
         1, 8, 128, np.array([-1, 0, 2], np.int32), L=L) == 2 * 4096
 
 
+def _bits(x):
+    """float -> bf16 bit patterns, round to nearest even (test-side)."""
+    f = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+    return ((f + (((f >> 16) & 1) + 0x7FFF)) >> 16).astype(np.uint16)
+
+
+def llama_config(n_q_heads, n_kv_heads, head_dim):
+    """Llama-3-family attention settings (rope_theta 5e5 and the Llama-3
+    rescaling of long rotary wavelengths, as in Llama-3.2-1B)."""
+    from transformers import LlamaConfig
+    return LlamaConfig(
+        hidden_size=n_q_heads * head_dim, num_attention_heads=n_q_heads,
+        num_key_value_heads=n_kv_heads, head_dim=head_dim,
+        rope_theta=500000.0, max_position_embeddings=131072,
+        rope_scaling={"rope_type": "llama3", "factor": 32.0,
+                      "low_freq_factor": 1.0, "high_freq_factor": 4.0,
+                      "original_max_position_embeddings": 8192})
+
+
+def make_problem_nonorm(doc_len, doc_ids, seqlens, n_q_heads, n_kv_heads,
+                        head_dim, seed):
+    """Seeded N(0,1) bf16 inputs at any head size, with no norm gains."""
+    rng = np.random.default_rng(seed)
+    doc_len = np.asarray(doc_len, np.int32)
+    cu = np.concatenate([[0], np.cumsum(seqlens)]).astype(np.int32)
+    doc_off = np.concatenate([[0], np.cumsum(doc_len)[:-1]]).astype(np.int64)
+    slots, ntok = int(doc_len.sum()), int(cu[-1])
+    g = lambda *shape: _bits(rng.standard_normal(shape))
+    return dict(
+        n_q_heads=n_q_heads, n_kv_heads=n_kv_heads, head_dim=head_dim,
+        doc_len=doc_len, doc_ids=np.asarray(doc_ids, np.int32),
+        cu_seqlens=cu, doc_off=doc_off,
+        prefix_k=g(max(slots, 1), n_kv_heads, head_dim)[:slots],
+        prefix_v=g(max(slots, 1), n_kv_heads, head_dim)[:slots],
+        q=g(ntok, n_q_heads, head_dim), k=g(ntok, n_kv_heads, head_dim),
+        v=g(ntok, n_kv_heads, head_dim), q_norm_w=None, k_norm_w=None)
+
+
+def pin_llama_family(L):
+    """Attention without QK-norm and with the caller's rotary frequencies
+    (Llama-3 family, head sizes 128 and 64): the oracle given Hugging Face's
+    Llama rotary module's inverse frequencies agrees with that module plus
+    SDPA (HF forms the angles in float32, hence 1e-5) and with the float64
+    brute force fed the same frequencies.  The Llama-3 frequencies differ
+    from theta^(-2i/D), so ignoring them cannot pass."""
+    for i, (D, hq, hkv) in enumerate([(128, 8, 2), (64, 4, 1)]):
+        prob = make_problem_nonorm([7, 0, 12], [2, 0, 1, 2], [5, 3, 1, 4],
+                                   hq, hkv, D, seed=91 + i)
+        ref, inv_freq = refs.attention_sdpa_llama(prob,
+                                                  llama_config(hq, hkv, D))
+        plain = 500000.0 ** (-np.arange(D // 2) * 2.0 / D)
+        assert np.abs(inv_freq / plain - 1).max() > 0.5
+        out, lse, st = run_oracle(prob, L, rope_theta=500000.0,
+                                  rope_inv_freq=inv_freq)
+        assert (st == 0).all()
+        err = np.abs(out - ref).max()
+        assert err < 1e-5, f"D={D}: oracle vs HF Llama rotary + SDPA {err}"
+        bf, bf_lse = refs.attention_concat_fp64(prob, rope_theta=500000.0,
+                                                inv_freq=inv_freq)
+        assert np.abs(out - bf).max() < 1e-10
+        assert np.abs(lse - bf_lse).max() < 1e-10
+
+
 ALL_PINS = [pin_sdpa, pin_concat_fp64, pin_no_prefix_is_causal_self_attention,
             pin_uniform_logits, pin_ones_values, pin_single_key,
             pin_relative_positions, pin_invariances, pin_doc_range,
             pin_score_rows, pin_decoder_layer, pin_score, pin_group,
-            pin_store_bytes]
+            pin_store_bytes, pin_llama_family]

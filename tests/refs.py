@@ -80,10 +80,48 @@ def attention_sdpa(prob, rms_eps=1e-6, rope_theta=1e6, scale=None):
     return out.numpy()
 
 
-def _rope_complex(x, pos, theta):
+def attention_sdpa_llama(prob, cfg):
+    """Library-routine reference for attention without QK-norm: the Hugging
+    Face Llama rotary embedding (its frequencies, including the Llama-3
+    rescaling of long wavelengths, come from the module's own init) and
+    SDPA with GQA over the masked [prefix ; online] sequence.  Returns
+    (out float64 [Ntok, Hq, D], the module's inverse frequencies float64)."""
+    import torch
+    import torch.nn.functional as F
+    from transformers.models.llama.modeling_llama import (
+        LlamaRotaryEmbedding, apply_rotary_pos_emb)
+
+    Hq, Hkv, D = prob["n_q_heads"], prob["n_kv_heads"], prob["head_dim"]
+    rot = LlamaRotaryEmbedding(cfg)
+    f = lambda a: torch.from_numpy(bf16_bits_to_f64(a))
+    pk, pv = f(prob["prefix_k"]), f(prob["prefix_v"])
+    Q, K, V = f(prob["q"]), f(prob["k"]), f(prob["v"])
+    out = torch.zeros(Q.shape, dtype=torch.float64)
+    for p in range(len(prob["doc_ids"])):
+        d, L, off, tok0, T = _pair_slices(prob, p)
+        q = Q[tok0:tok0 + T].permute(1, 0, 2)[None]
+        k = K[tok0:tok0 + T].permute(1, 0, 2)[None]
+        v = V[tok0:tok0 + T].permute(1, 0, 2)[None]
+        pos = torch.arange(L, L + T)[None]
+        cos, sin = rot(q, pos)
+        qr, kr = apply_rotary_pos_emb(q, k, cos, sin)
+        kp = pk[off:off + L].permute(1, 0, 2)[None]
+        vp = pv[off:off + L].permute(1, 0, 2)[None]
+        keys = torch.cat([kp, kr], dim=2)
+        vals = torch.cat([vp, v], dim=2)
+        mask = torch.ones(T, L + T, dtype=torch.bool)
+        mask[:, L:] = torch.tril(torch.ones(T, T, dtype=torch.bool))
+        o = F.scaled_dot_product_attention(qr, keys, vals, attn_mask=mask,
+                                           scale=D ** -0.5, enable_gqa=True)
+        out[tok0:tok0 + T] = o[0].permute(1, 0, 2)
+    return out.numpy(), rot.inv_freq.double().numpy()
+
+
+def _rope_complex(x, pos, theta, freq=None):
     D = x.shape[-1]
     half = D // 2
-    freq = theta ** (-np.arange(half, dtype=np.float64) * 2.0 / D)
+    if freq is None:
+        freq = theta ** (-np.arange(half, dtype=np.float64) * 2.0 / D)
     z = (x[..., :half] + 1j * x[..., half:]) * np.exp(
         1j * np.multiply.outer(pos, freq))[:, None, :]
     return np.concatenate([z.real, z.imag], axis=-1)
@@ -93,8 +131,11 @@ def _rms(x, w, eps):
     return x / np.sqrt(np.mean(x * x, axis=-1, keepdims=True) + eps) * w
 
 
-def attention_concat_fp64(prob, rms_eps=1e-6, rope_theta=1e6, scale=None):
-    """Returns (out [Ntok,Hq,D], lse [Ntok,Hq]) in float64."""
+def attention_concat_fp64(prob, rms_eps=1e-6, rope_theta=1e6, scale=None,
+                          inv_freq=None):
+    """Returns (out [Ntok,Hq,D], lse [Ntok,Hq]) in float64.  Without norm
+    gains in prob (q_norm_w None) q and k are rotated as given; inv_freq
+    overrides theta^(-2i/D)."""
     from scipy.special import logsumexp
     Hq, Hkv, D = prob["n_q_heads"], prob["n_kv_heads"], prob["head_dim"]
     rep = Hq // Hkv
@@ -102,16 +143,19 @@ def attention_concat_fp64(prob, rms_eps=1e-6, rope_theta=1e6, scale=None):
     f = bf16_bits_to_f64
     pk, pv = f(prob["prefix_k"]), f(prob["prefix_v"])
     Q, K, V = f(prob["q"]), f(prob["k"]), f(prob["v"])
-    wq, wk = f(prob["q_norm_w"]), f(prob["k_norm_w"])
+    norm = prob.get("q_norm_w") is not None
+    if norm:
+        wq, wk = f(prob["q_norm_w"]), f(prob["k_norm_w"])
     out = np.zeros(Q.shape)
     lse = np.zeros(Q.shape[:2])
     for p in range(len(prob["doc_ids"])):
         d, L, off, tok0, T = _pair_slices(prob, p)
         pos = np.arange(L, L + T, dtype=np.float64)
-        qh = _rope_complex(_rms(Q[tok0:tok0 + T], wq, rms_eps), pos,
-                           rope_theta)                       # [T,Hq,D]
-        kh = _rope_complex(_rms(K[tok0:tok0 + T], wk, rms_eps), pos,
-                           rope_theta)                       # [T,Hkv,D]
+        qs, ks = Q[tok0:tok0 + T], K[tok0:tok0 + T]
+        if norm:
+            qs, ks = _rms(qs, wq, rms_eps), _rms(ks, wk, rms_eps)
+        qh = _rope_complex(qs, pos, rope_theta, inv_freq)    # [T,Hq,D]
+        kh = _rope_complex(ks, pos, rope_theta, inv_freq)    # [T,Hkv,D]
         keys = np.concatenate([pk[off:off + L], kh], axis=0)  # [S,Hkv,D]
         vals = np.concatenate([pv[off:off + L], V[tok0:tok0 + T]], axis=0)
         S = L + T

@@ -30,10 +30,20 @@ MUTATIONS = [
     ("rmsnorm_no_weight", "y[i] = w[i] * (x[i] * inv);",
      "y[i] = (x[i] * inv);"),
     ("rmsnorm_sum_not_mean", "sqrt(ss / (double)n + eps)", "sqrt(ss + eps)"),
-    ("q_position_not_offset", "rope(qhat, D, (double)(L + j), rope_theta);",
-     "rope(qhat, D, (double)(j), rope_theta);"),
-    ("k_position_not_offset", "rope(dst, D, (double)(L + j), rope_theta);",
-     "rope(dst, D, (double)(j), rope_theta);"),
+    ("q_position_not_offset",
+     "rope(qhat, D, (double)(L + j), rope_theta, rope_inv_freq);",
+     "rope(qhat, D, (double)(j), rope_theta, rope_inv_freq);"),
+    ("k_position_not_offset",
+     "rope(dst, D, (double)(L + j), rope_theta, rope_inv_freq);",
+     "rope(dst, D, (double)(j), rope_theta, rope_inv_freq);"),
+    ("rope_ignores_given_freqs", "double freq = inv_freq ? inv_freq[i]",
+     "double freq = 0 ? inv_freq[i]"),
+    ("q_normed_without_gains",
+     "if (qk_norm)\n          rms_norm(x, wq, D, rms_eps, qhat);",
+     "if (1)\n          rms_norm(x, wq, D, rms_eps, qhat);"),
+    ("k_normed_without_gains",
+     "if (qk_norm)\n          rms_norm(x, wk, D, rms_eps, dst);",
+     "if (1)\n          rms_norm(x, wk, D, rms_eps, dst);"),
     ("gqa_interleaved", "const int g = h / n_rep;", "const int g = h % Hkv;"),
     ("self_key_dropped", "const int n_keys = L + j + 1;",
      "const int n_keys = L + j;"),
