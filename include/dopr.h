@@ -123,8 +123,12 @@ dopr_status_t dopr_store_destroy(dopr_store_t st);
  *   keys   = [ K_d[g, 0..L_d-1] ; k^[0..j, g] ]
  *   values = [ V_d[g, 0..L_d-1] ;  v[0..j, g] ]
  *   out[j,h] = softmax(softmax_scale * q^ . keys) . values
- * RoPE is the rotate-half form with base rope_theta; RMSNorm is per head over
- * D with epsilon rms_eps.  Online positions continue after the prefix.      */
+ * RoPE is the rotate-half form: the pair (x_i, x_{i+D/2}) turns by
+ * position * omega_i with omega_i = rope_theta^(-2i/D), or rope_inv_freq[i]
+ * when given.  RMSNorm is per head over D with epsilon rms_eps; with both
+ * norm gains NULL there is no RMSNorm (q^ = RoPE(q), k^ = RoPE(k), as in
+ * attention families without QK-norm such as Llama).  Online positions
+ * continue after the prefix.                                               */
 typedef struct {
   int32_t n_pairs;          /* P >= 0                                       */
   int32_t n_q_heads;        /* Hq, multiple of the store's Hkv              */
@@ -146,8 +150,9 @@ typedef struct {
   const void *q;            /* dev bf16 [Ntok, Hq, D]   raw (pre-norm)      */
   const void *k;            /* dev bf16 [Ntok, Hkv, D]  raw (pre-norm)      */
   const void *v;            /* dev bf16 [Ntok, Hkv, D]                      */
-  const void *q_norm_w;     /* dev bf16 [D]                                 */
-  const void *k_norm_w;     /* dev bf16 [D]                                 */
+  const void *q_norm_w;     /* dev bf16 [D], or NULL with k_norm_w NULL:
+                               no per-head RMSNorm                          */
+  const void *k_norm_w;     /* dev bf16 [D], or NULL (see q_norm_w)         */
   float rms_eps;            /* e.g. 1e-6                                    */
   float rope_theta;         /* e.g. 1e6                                     */
   float softmax_scale;      /* e.g. 1/sqrt(D)                               */
@@ -160,6 +165,9 @@ typedef struct {
                                right before the attention kernel, or NULL  */
   void *timing_end;         /* optional hipEvent_t recorded right after it,
                                or NULL (profiling of the dominant kernel)   */
+  const float *rope_inv_freq; /* dev fp32 [D/2] rotation frequencies
+                               omega_i (e.g. a family's rescaled ones), or
+                               NULL for rope_theta^(-2i/D); 4-byte aligned */
 } dopr_attn_args_t;
 
 /* Workspace bytes needed by dopr_prefix_attn for these arguments (host). */

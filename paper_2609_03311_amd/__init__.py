@@ -50,7 +50,8 @@ class _AttnArgs(ctypes.Structure):
                 ("lse", ctypes.c_void_p), ("workspace", ctypes.c_void_p),
                 ("workspace_bytes", ctypes.c_size_t),
                 ("timing_begin", ctypes.c_void_p),
-                ("timing_end", ctypes.c_void_p)]
+                ("timing_end", ctypes.c_void_p),
+                ("rope_inv_freq", ctypes.c_void_p)]
 
 
 class _ScoreArgs(ctypes.Structure):
@@ -244,7 +245,7 @@ def dopr_store_destroy(store: Store):
 def _attn_args(store, doc_ids, cu_seqlens, q, k, v, q_norm_w, k_norm_w, out,
                lse, workspace, *, max_tokens, total_tokens=None,
                rms_eps=1e-6, rope_theta=1e6, softmax_scale=None,
-               kernel_variant=0, timing=None):
+               kernel_variant=0, timing=None, rope_inv_freq=None):
     n_q_heads = q.shape[1] if q is not None else store.n_kv_heads
     if total_tokens is None:
         total_tokens = q.shape[0]
@@ -258,7 +259,8 @@ def _attn_args(store, doc_ids, cu_seqlens, q, k, v, q_norm_w, k_norm_w, out,
                      _ptr(q_norm_w), _ptr(k_norm_w), float(rms_eps),
                      float(rope_theta), float(softmax_scale), _ptr(out),
                      _ptr(lse), _ptr(workspace), ws_bytes,
-                     *(timing if timing is not None else (None, None)))
+                     *(timing if timing is not None else (None, None)),
+                     _ptr(rope_inv_freq))
 
 
 def _shape_args(n_pairs, n_q_heads, max_tokens, total_tokens,
@@ -299,14 +301,17 @@ def dopr_prefix_attn(store: Store, layer: int, doc_ids, cu_seqlens, q, k, v,
                      q_norm_w, k_norm_w, out, workspace, *, max_tokens,
                      lse=None, total_tokens=None, rms_eps=1e-6,
                      rope_theta=1e6, softmax_scale=None, kernel_variant=0,
-                     timing=None, stream=None):
+                     timing=None, rope_inv_freq=None, stream=None):
     """`timing` is an optional (begin, end) pair of raw hipEvent_t handles
-    recorded around the attention kernel."""
+    recorded around the attention kernel.  q_norm_w and k_norm_w may both
+    be None (no QK-norm); rope_inv_freq is an optional fp32 [D/2] device
+    tensor of rotation frequencies."""
     a = _attn_args(store, doc_ids, cu_seqlens, q, k, v, q_norm_w, k_norm_w,
                    out, lse, workspace, max_tokens=max_tokens,
                    total_tokens=total_tokens, rms_eps=rms_eps,
                    rope_theta=rope_theta, softmax_scale=softmax_scale,
-                   kernel_variant=kernel_variant, timing=timing)
+                   kernel_variant=kernel_variant, timing=timing,
+                   rope_inv_freq=rope_inv_freq)
     _check(lib().dopr_prefix_attn(store.handle, layer, ctypes.byref(a),
                                   _stream(stream)))
 
@@ -317,7 +322,7 @@ def dopr_prefix_attn_score(store: Store, layer: int, doc_ids, cu_seqlens, q,
                            lse=None, total_tokens=None, rms_eps=1e-6,
                            head_rms_eps=1e-6, rope_theta=1e6,
                            softmax_scale=None, kernel_variant=0, timing=None,
-                           stream=None):
+                           rope_inv_freq=None, stream=None):
     """Last-layer scoring: the score token's attention rows (out [P, Hq, D]
     or None, lse [P, Hq] or None) with the score head fused (score [P],
     logits [P, 2] or None)."""
@@ -325,7 +330,8 @@ def dopr_prefix_attn_score(store: Store, layer: int, doc_ids, cu_seqlens, q,
                    out, lse, workspace, max_tokens=max_tokens,
                    total_tokens=total_tokens, rms_eps=rms_eps,
                    rope_theta=rope_theta, softmax_scale=softmax_scale,
-                   kernel_variant=kernel_variant, timing=timing)
+                   kernel_variant=kernel_variant, timing=timing,
+                   rope_inv_freq=rope_inv_freq)
     h = _ScoreHead(_ptr(norm_w), _ptr(w_head), float(head_rms_eps),
                    _ptr(logits), _ptr(score))
     _check(lib().dopr_prefix_attn_score(store.handle, layer, ctypes.byref(a),

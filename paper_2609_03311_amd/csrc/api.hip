@@ -292,12 +292,17 @@ dopr_status_t run_attention(dopr_store_t st, int32_t layer,
   }
   if (a->n_pairs == 0) return ok();
   if (!a->doc_ids || !a->cu_seqlens || !a->q || !a->k || !a->v ||
-      !a->q_norm_w || !a->k_norm_w || (!a->out && !score) || !a->workspace)
+      (!a->out && !score) || !a->workspace)
     return fail(DOPR_ERR_INVALID_ARG, "NULL buffer");
+  if (!a->q_norm_w != !a->k_norm_w)
+    return fail(DOPR_ERR_INVALID_ARG,
+                "q_norm_w and k_norm_w must both be given or both be NULL");
   if (!aligned16(a->q) || !aligned16(a->k) || !aligned16(a->v) ||
       !aligned16(a->out) || !aligned16(a->q_norm_w) || !aligned16(a->k_norm_w))
     return fail(DOPR_ERR_INVALID_ARG,
                 "q, k, v, out and norm weights must be 16-byte aligned");
+  if (reinterpret_cast<uintptr_t>(a->rope_inv_freq) % 4)
+    return fail(DOPR_ERR_INVALID_ARG, "rope_inv_freq must be 4-byte aligned");
   if (score) {
     if (!head->norm_w || !head->w_head || !head->score)
       return fail(DOPR_ERR_INVALID_ARG, "NULL score-head buffer");

@@ -105,6 +105,7 @@ struct AttnParams {
   const uint16_t *head_norm_w, *head_w;
   int32_t items_cap, Hq, Hkv, n_rep, layer, n_layers;
   int32_t flag_all;  // queue every unit for the SAFE pass (self-check mode)
+  int32_t norm;      // per-head RMSNorm of q and k (0: no QK-norm, unit gains)
   float eps, c;      // c = softmax_scale * log2(e)
 };
 
@@ -213,7 +214,8 @@ __device__ __forceinline__ int find_pair(const AttnParams &P, int r) {
 __device__ __forceinline__ void q_fragments(const uint16_t *qrow,
                                             const uint16_t *w,
                                             const float2 *rope_row, int hf,
-                                            float eps, float c, bf16x8 *qf) {
+                                            float eps, float c, bool norm,
+                                            bf16x8 *qf) {
   // every load is issued up front (one round trip to memory): the raw row,
   // the gains (packed) and this lane's 32 (cos, sin) pairs
   uint4 raw[8], wr[8];
@@ -237,7 +239,7 @@ __device__ __forceinline__ void q_fragments(const uint16_t *qrow,
 #pragma unroll
   for (int s = 0; s < 8; ++s) ss = sumsq8(raw[s], ss);
   ss += __shfl_xor(ss, 32, 64);
-  const float inv = c * rsqrtf(ss * (1.0f / D) + eps);
+  const float inv = norm ? c * rsqrtf(ss * (1.0f / D) + eps) : c;
 #pragma unroll
   for (int s = 0; s < 4; ++s) {
     float x0[8], x1[8], w0[8], w1[8];
@@ -419,7 +421,7 @@ __device__ __forceinline__ void own_stage(const AttnParams &P,
     }
     ss = sum8_lanes(ss);
     if (r.valid) {
-      const float inv = rsqrtf(ss * (1.0f / D) + P.eps);
+      const float inv = P.norm ? rsqrtf(ss * (1.0f / D) + P.eps) : 1.f;
       float w0[8], w1[8];
       unpack8(g0, w0);
       unpack8(g1, w1);
@@ -682,7 +684,7 @@ __device__ __forceinline__ bool run_unit(const AttnParams &P, Smem<NCHK> &sm,
       if (live)
         q_fragments(P.q + ((int64_t)tokq[qb] * P.Hq + head[qb]) * D, P.qw,
                     P.rope + (int64_t)(L + tj.y) * kRopeHalf, hf, P.eps,
-                    P.c, qf[qb]);
+                    P.c, P.norm != 0, qf[qb]);
       acc[qb].m = SMX == 2 ? -INFINITY : (SMX == 1 ? INFINITY : 0.f);
       acc[qb].l = 0.f;
 #pragma unroll
@@ -900,7 +902,11 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(
     const int64_t blk = P.doc_off[doc];
     const uint16_t *Kp = P.payload + k_offset(blk, L, P.Hkv, P.layer, g);
     const uint16_t *VTp = P.payload + vt_offset(blk, L, P.Hkv, P.layer, g);
-    // every logit of this unit lies in [-B, B] (log2 units)
+    // every logit of this unit lies in [-B, B] (log2 units).  Without
+    // QK-norm no bound is known (kown = 0, so B = 0): the unit runs the
+    // no-reference mode anyway, and a row whose normaliser leaves the range
+    // that mode serves exactly is caught by the check after the pass and
+    // recomputed by the exact pass.
     const float kbound = fmaxf(
         P.kown[0], P.kmax[((int64_t)doc * P.n_layers + P.layer) * P.Hkv + g]);
     const float B = P.c * P.kown[1] * kbound * 1.001f;
@@ -1012,8 +1018,9 @@ hipError_t launch_attention(const AttnCall &c, const Plan &pl,
   p.q = static_cast<const uint16_t *>(a->q);
   p.k = static_cast<const uint16_t *>(a->k);
   p.v = static_cast<const uint16_t *>(a->v);
-  p.qw = static_cast<const uint16_t *>(a->q_norm_w);
-  p.kw = static_cast<const uint16_t *>(a->k_norm_w);
+  p.norm = a->q_norm_w != nullptr;
+  p.qw = p.norm ? static_cast<const uint16_t *>(a->q_norm_w) : pl.unit_w;
+  p.kw = p.norm ? static_cast<const uint16_t *>(a->k_norm_w) : pl.unit_w;
   p.doc_len = st.d_len;
   p.doc_off = st.d_off;
   p.kmax = st.d_kmax;

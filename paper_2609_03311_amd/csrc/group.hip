@@ -301,10 +301,14 @@ __global__ __launch_bounds__(kThreads) void k_token_table(Plan pl, PlanArgs a,
 // form RoPE(RMSNorm(x) * w): an RMS-normed vector has norm <= sqrt(D), the
 // gain scales it by at most max|w|, rotation keeps it, and bf16 rounding
 // adds at most 2^-8.  bound[0] is for keys (w_k), bound[1] for queries.
+// Without QK-norm (no gains) no bound is known: both are written as 0 and
+// unit_w gets the unit gains the attention kernel multiplies by.
 __global__ __launch_bounds__(128) void k_norm_bound(const uint16_t *kw,
                                                     const uint16_t *qw,
-                                                    float *bound) {
+                                                    float *bound,
+                                                    uint16_t *unit_w) {
   __shared__ float red[2][2];
+  if (!kw) unit_w[threadIdx.x] = 0x3F80;  // bf16 1.0
   float a = 0.f, b = 0.f;
   if (kw) a = fabsf(__uint_as_float((uint32_t)kw[threadIdx.x] << 16));
   if (qw) b = fabsf(__uint_as_float((uint32_t)qw[threadIdx.x] << 16));
@@ -323,15 +327,18 @@ __global__ __launch_bounds__(128) void k_norm_bound(const uint16_t *kw,
                          sqrtf((float)kHeadDim) * 1.01f;
 }
 
-// Step 6: rotary table, (cos, sin)(pos * theta^(-2i/D)) in double, stored
-// as float.
+// Step 6: rotary table, (cos, sin)(pos * omega_i) in double, stored as
+// float; omega_i = theta^(-2i/D), or the caller's inv_freq[i].
 __global__ __launch_bounds__(kThreads) void k_rope_table(float2 *tab,
                                                          int32_t n_pos,
-                                                         double log_theta) {
+                                                         double log_theta,
+                                                         const float *inv_freq) {
   const int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x;
   if (e >= (int64_t)n_pos * kRopeHalf) return;
   const int32_t pos = (int32_t)(e / kRopeHalf), i = (int32_t)(e % kRopeHalf);
-  const double freq = exp(-2.0 * (double)i / (double)kHeadDim * log_theta);
+  const double freq =
+      inv_freq ? (double)inv_freq[i]
+               : exp(-2.0 * (double)i / (double)kHeadDim * log_theta);
   double sn, cs;
   sincos((double)pos * freq, &sn, &cs);
   tab[e] = make_float2((float)cs, (float)sn);
@@ -385,6 +392,7 @@ Plan carve(void *ws, const PlanShape &s, size_t *bytes) {
   pl.part = s.score_only ? c.take<float>(P * s.n_rep * s.n_kv_heads * 3)
                          : nullptr;
   pl.kown = c.take<float>(2);
+  pl.unit_w = c.take<uint16_t>(kHeadDim);
   pl.rope_pos = s.max_len + s.max_tokens;
   pl.rope = c.take<float2>((int64_t)pl.rope_pos * kRopeHalf);
   *bytes = c.off;
@@ -450,12 +458,14 @@ hipError_t launch_plan(const AttnCall &c, const Plan &pl,
                        dim3(kThreads), 0, s, pl, pa, totals);
   hipLaunchKernelGGL(k_norm_bound, dim3(1), dim3(kHeadDim), 0, s,
                      static_cast<const uint16_t *>(a->k_norm_w),
-                     static_cast<const uint16_t *>(a->q_norm_w), pl.kown);
+                     static_cast<const uint16_t *>(a->q_norm_w), pl.kown,
+                     pl.unit_w);
   const double log_theta = std::log((double)a->rope_theta);
   hipLaunchKernelGGL(k_rope_table,
                      dim3(blocks_for((int64_t)pl.rope_pos * kRopeHalf,
                                      kThreads)),
-                     dim3(kThreads), 0, s, pl.rope, pl.rope_pos, log_theta);
+                     dim3(kThreads), 0, s, pl.rope, pl.rope_pos, log_theta,
+                     a->rope_inv_freq);
   return hipGetLastError();
 }
 

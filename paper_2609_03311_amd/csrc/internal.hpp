@@ -110,6 +110,8 @@ struct Plan {
   int2 *utok;           // [stacked tokens] (batch token, position)
   float *part;          // [P][Hq][3] score-head partial sums (score mode)
   float *kown;          // [2] bounds on |k^| (own keys) and |q^|: sqrt(D) max|w|
+                        // (0 when there is no QK-norm: no bound is known)
+  uint16_t *unit_w;     // [D] bf16 ones: the gains when there is no QK-norm
   float2 *rope;         // [rope_pos][64] (cos, sin)
   int32_t items_cap;
   int32_t blk_cap;
