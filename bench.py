@@ -63,7 +63,43 @@ DESCRIPTIONS = {
                        "(50% Zipf reuse), T=16..128+1",
     "qwen3_8b_ragged_x8": "as qwen3_8b_ragged with 8x longer (uncompressed) "
                           "prefixes, 64..2048 slots",
+    "llama3_8b": "Llama-3-8B-shaped attention (no QK-norm, rope_theta 5e5 "
+                 "with Llama-3 frequency rescaling): 32q/8kv heads, D=128, "
+                 "the qwen3_8b pairs (20k docs x 256 slots, 256 queries x "
+                 "100 docs, T=128+1)",
 }
+# attention families: QK-norm on (Qwen3) or off with given frequencies
+LLAMA_ROPE_THETA = 500000.0
+
+
+def llama3_rope_inv_freq(head_dim=128, theta=LLAMA_ROPE_THETA, factor=32.0,
+                         low_freq_factor=1.0, high_freq_factor=4.0,
+                         original_max_position=8192):
+    """Rotation frequencies of the Llama-3 family: theta^(-2i/D), with
+    wavelengths longer than original_max_position / low_freq_factor slowed
+    down by `factor`, those shorter than original_max_position /
+    high_freq_factor kept, and a linear blend (in original_max_position /
+    wavelength) in between.  float32 [D/2], as the models compute them."""
+    inv = theta ** (-np.arange(0, head_dim, 2, dtype=np.float64) / head_dim)
+    inv = inv.astype(np.float32).astype(np.float64)
+    wavelen = 2.0 * np.pi / inv
+    blend = ((original_max_position / wavelen - low_freq_factor) /
+             (high_freq_factor - low_freq_factor))
+    mid = (1.0 - blend) * inv / factor + blend * inv
+    out = np.where(wavelen > original_max_position / low_freq_factor,
+                   inv / factor, inv)
+    in_band = ((wavelen >= original_max_position / high_freq_factor) &
+               (wavelen <= original_max_position / low_freq_factor))
+    return np.where(in_band, mid, out).astype(np.float32)
+
+
+def family_args(config, dev):
+    """(gains_enabled, extra keyword arguments of the attention calls)."""
+    if not config.startswith("llama"):
+        return True, {}
+    import torch
+    inv = torch.from_numpy(llama3_rope_inv_freq()).to(dev)
+    return False, {"rope_theta": LLAMA_ROPE_THETA, "rope_inv_freq": inv}
 SALIENCE_DESCRIPTIONS = {
     "qwen3_0p6b_docs": "salience selection, Qwen3-0.6B-shaped final layer: "
                        "16q/8kv heads, D=128, 512 documents x 256 tokens, "
@@ -244,7 +280,7 @@ def bits(t):
 
 
 def cpu_baseline(st, k_src, v_src, doc_off, online, prm, seconds,
-                 last_only=False):
+                 last_only=False, family=None):
     """The float64 oracle on a bounded sample of the same workload's pairs
     (deterministic order), on this host's cores.  last_only: the oracle of
     last-layer scoring (score-token rows only)."""
@@ -278,12 +314,18 @@ def cpu_baseline(st, k_src, v_src, doc_off, online, prm, seconds,
                 bits(online["q"].index_select(0, tt)),
                 bits(online["k"].index_select(0, tt)),
                 bits(online["v"].index_select(0, tt)),
-                bits(prm["q_norm_w"]), bits(prm["k_norm_w"]))
+                None if prm["q_norm_w"] is None else bits(prm["q_norm_w"]),
+                None if prm["k_norm_w"] is None else bits(prm["k_norm_w"]))
         nw, wh = bits(prm["norm_w"]), bits(prm["w_head"])
+        fam = {}
+        if family:
+            fam = {"rope_theta": family["rope_theta"],
+                   "rope_inv_freq": family["rope_inv_freq"].double().cpu()
+                   .numpy()}
         t0 = time.perf_counter()
         out, _, _ = oracle.prefix_attn(*args, n_q_heads=st.n_q_heads,
                                        n_kv_heads=st.n_kv_heads,
-                                       last_only=last_only, L=L)
+                                       last_only=last_only, L=L, **fam)
         h = (out if last_only else out[scu[1:] - 1]).reshape(len(pairs), -1)
         oracle.score(h, nw, wh, L=L)
         return time.perf_counter() - t0
@@ -547,12 +589,17 @@ def main():
 
     st = workloads.make(args.config)
     dev = "cuda"
+    norm_on, fam = family_args(args.config, dev)
+    if not norm_on and args.path == "layer":
+        ap.error("--path layer builds the Qwen3 decoder layer (QK-norm on)")
     log(f"{args.config}: P={st.n_pairs} Ntok={st.n_tokens} "
         f"unique docs={len(np.unique(st.doc_ids))}")
     k_src, v_src, doc_off, _ = workloads.prefix_source(st, dev, 1)
     layer_path = args.path == "layer"
     online = None if layer_path else workloads.online_inputs(st, dev, 3)
     prm = workloads.params(st, dev, 6)
+    if not norm_on:
+        prm["q_norm_w"] = prm["k_norm_w"] = None
     store = pipeline.make_store(st.doc_len, st.n_kv_heads, k_src, v_src,
                                 device=dev)
     score_path = args.path == "score"
@@ -608,11 +655,11 @@ def main():
         if score_path:
             step.run(0, doc_ids, cu, online["q"], online["k"], online["v"],
                      prm["q_norm_w"], prm["k_norm_w"], prm["norm_w"],
-                     prm["w_head"], timing=timing)
+                     prm["w_head"], timing=timing, **fam)
             return
         step.attention(0, doc_ids, cu, online["q"], online["k"],
                        online["v"], prm["q_norm_w"], prm["k_norm_w"],
-                       timing=timing)
+                       timing=timing, **fam)
         step.score_head(cu, prm["norm_w"], prm["w_head"])
 
     for _ in range(args.warmup):
@@ -719,7 +766,7 @@ def main():
         else:
             result["cpu_baseline"] = cpu_baseline(
                 st, k_src, v_src, doc_off, online, prm, args.cpu_seconds,
-                last_only=score_path)
+                last_only=score_path, family=fam)
     print(json.dumps(result), flush=True)
 
 

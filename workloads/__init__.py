@@ -133,6 +133,15 @@ def qwen3_8b(seed: int = 0) -> Structure:
                      seed=seed)
 
 
+def llama3_8b(seed: int = 0) -> Structure:
+    """Llama-3-8B-shaped attention (hidden 4096, 32q/8kv, head size 128, no
+    QK-norm): the pair structure of qwen3_8b (the cross-family check runs
+    the same batch through the other family's attention)."""
+    st = qwen3_8b(seed)
+    st.name = "llama3_8b"
+    return st
+
+
 def qwen3_8b_ragged(seed: int = 0, prefix_scale: int = 1) -> Structure:
     """Qwen3-8B-shaped layer, ragged: prefix lengths uniform 8..256 slots
     over a 1M-id space; 16384 pairs, half Zipf(1.1) reuse and half distinct
@@ -174,6 +183,7 @@ CONFIGS = {
     "qwen3_8b": qwen3_8b,
     "qwen3_8b_ragged": qwen3_8b_ragged,
     "qwen3_8b_ragged_x8": lambda seed=0: qwen3_8b_ragged(seed, 8),
+    "llama3_8b": llama3_8b,
 }
 
 
