@@ -18,7 +18,9 @@ one whole decoder layer over the online tokens (projections, norms, SwiGLU
 MLP and the prefix attention), MFMA-bound.  --path salience measures the
 offline side: salience selection of the prefix slots of a batch of whole
 documents (head-averaged attention, column top-p means, top-K), with
---config one of the *_docs batches.  --sweep-kinfer K1,K2,... times the
+--config one of the *_docs batches.  --path ingest times filling the
+workload's prefix store (dopr_store_put) and repacking it to the documents
+the batch references (dopr_store_copy_docs).  --sweep-kinfer K1,K2,... times the
 full path on the same pairs at several inference prefix budgets (every
 document holds K slots) and prints one JSON line per budget.
 """
@@ -453,6 +455,83 @@ def bench_salience(args):
     print(json.dumps(result), flush=True)
 
 
+def bench_ingest(args):
+    """Store ingest at scale: dopr_store_put of every resident document of
+    the workload's store (the offline fill, Sec. 3.3), then a repack with
+    dopr_store_copy_docs into a store that keeps only the documents the
+    batch references.  Both are streaming copies: HBM-bound; one JSON line
+    each."""
+    import torch
+
+    import workloads
+    from paper_2609_03311_amd import (dopr_check_status, dopr_store_copy_docs,
+                                      dopr_store_create, dopr_store_put)
+    st = workloads.make(args.config)
+    dev = "cuda"
+    k_src, v_src, _, cu = workloads.prefix_source(st, dev, 1)
+    res = st.resident_docs().astype(np.int32)
+    ids = torch.from_numpy(res).to(dev)
+    cu_t = torch.from_numpy(cu.astype(np.int64)).to(dev)
+    store = dopr_store_create(1, st.n_kv_heads, st.head_dim, st.doc_len)
+    kept = np.full(st.n_docs, -1, np.int32)
+    used = np.unique(st.doc_ids)
+    kept[used] = st.doc_len[used]
+    packed = dopr_store_create(1, st.n_kv_heads, st.head_dim, kept)
+
+    def timed(fn):
+        for _ in range(args.warmup):
+            fn()
+        torch.cuda.synchronize()
+        ev = [(torch.cuda.Event(enable_timing=True),
+               torch.cuda.Event(enable_timing=True))
+              for _ in range(args.steps)]
+        for a, b in ev:
+            a.record()
+            fn()
+            b.record()
+        torch.cuda.synchronize()
+        return float(np.mean([a.elapsed_time(b) for a, b in ev]))
+
+    def block_bytes(lens):
+        lens = lens.astype(np.int64)
+        return int(((lens + (lens + 7) // 8 * 8) * st.n_kv_heads *
+                    st.head_dim * 2).sum())
+
+    put_ms = timed(lambda: dopr_store_put(store, 0, ids, cu_t, k_src, v_src))
+    copy_ms = timed(lambda: dopr_store_copy_docs(packed, store))
+    assert dopr_check_status(store) == 0 and dopr_check_status(packed) == 0
+    lens = st.doc_len[res]
+    src_bytes = int(lens.astype(np.int64).sum()) * st.n_kv_heads * \
+        st.head_dim * 2 * 2
+    put_bytes = src_bytes + block_bytes(lens)
+    copy_bytes = 2 * block_bytes(st.doc_len[used])
+    for kind, ms, nbytes, ndocs, what in (
+            ("put", put_ms, put_bytes, len(res),
+             "dopr_store_put of every resident document (read canonical "
+             "[slots, Hkv, D] states, write K rows and transposed V)"),
+            ("repack", copy_ms, copy_bytes, len(used),
+             "dopr_store_copy_docs into a store keeping only the documents "
+             "the batch references")):
+        gbs = nbytes / (ms * 1e-3) / 1e9
+        print(json.dumps({
+            "metric": "prefix-store ingest: documents/s; achieved HBM GB/s "
+                      "vs MI355X peak",
+            "value": round(ndocs / (ms * 1e-3), 1), "unit": "documents/s",
+            "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+            "ms_per_step": round(ms, 4), "higher_is_better": True,
+            "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+            "data": "synthetic",
+            "config": {"workload": DESCRIPTIONS[args.config] + "; " + what,
+                       "name": f"{args.config}_{kind}", "documents": ndocs,
+                       "parallelism": "single GPU"},
+            "bytes_moved_gb": round(nbytes / 1e9, 3),
+            "roofline": {"bound": "hbm", "achieved": round(gbs, 1),
+                         "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                         "frac": round(gbs / PEAK_HBM_GBS, 4),
+                         "traffic": None}}), flush=True)
+        log(f"{kind}: {ms:.3f} ms, {nbytes / 1e9:.2f} GB, {gbs:.0f} GB/s")
+
+
 def bench_kinfer(args):
     """Same pairs, several inference prefix budgets K_infer (Sec. 4.5, the
     memory and latency axes of the budget trade-off): the store holds K
@@ -544,7 +623,8 @@ def main():
                     choices=sorted(DESCRIPTIONS) +
                     sorted(SALIENCE_DESCRIPTIONS))
     ap.add_argument("--variant", type=int, default=0)
-    ap.add_argument("--path", choices=["full", "score", "layer", "salience"],
+    ap.add_argument("--path", choices=["full", "score", "layer", "salience",
+                                       "ingest"],
                     default="full",
                     help="full: every online row of one layer's attention "
                          "(default); score: last-layer scoring (score-token "
@@ -580,6 +660,9 @@ def main():
         return
     if args.sweep_kinfer:
         bench_kinfer(args)
+        return
+    if args.path == "ingest":
+        bench_ingest(args)
         return
 
     import torch

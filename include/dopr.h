@@ -114,6 +114,22 @@ dopr_status_t dopr_store_put(dopr_store_t st, int32_t layer, int64_t n,
 
 dopr_status_t dopr_store_destroy(dopr_store_t st);
 
+/* Carry documents over from one store to another (store maintenance: the
+ * prefix states are built once per document offline and kept for reuse,
+ * Sec. 3.3-3.4, so a collection that grows or shrinks is served by a new
+ * store holding the kept documents).  For every document id resident in
+ * both stores with the same slot count, dst receives src's states for all
+ * layers and kv heads (and their key-norm bounds); ids resident only in dst
+ * keep their contents (fill them with dopr_store_put), ids resident only in
+ * src are dropped.  So a store with more resident ids appends documents,
+ * and one with fewer repacks the kept ones densely.  Both stores must have
+ * the same n_docs (id space), n_layers and n_kv_heads and distinct,
+ * non-overlapping pools (INVALID_ARG otherwise).  A document resident in
+ * both with different slot counts is skipped and reported as a deferred
+ * DOC_RANGE on dst.  Asynchronous on `stream`.                             */
+dopr_status_t dopr_store_copy_docs(dopr_store_t dst, dopr_store_t src,
+                                   void *stream);
+
 /* ------------------------------------------------------------------------ */
 /* Online prefix attention (Sec. 3.4): for every pair p with document
  * d = doc_ids[p] and online tokens j = 0..T_p-1 (query tokens, then the

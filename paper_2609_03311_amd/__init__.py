@@ -102,6 +102,8 @@ EXPORTS = {
                         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                         ctypes.c_void_p, ctypes.c_void_p], ctypes.c_int),
     "dopr_store_destroy": ([ctypes.c_void_p], ctypes.c_int),
+    "dopr_store_copy_docs": ([ctypes.c_void_p, ctypes.c_void_p,
+                              ctypes.c_void_p], ctypes.c_int),
     "dopr_prefix_attn_workspace": ([ctypes.c_void_p, ctypes.c_void_p,
                                     ctypes.c_void_p], ctypes.c_int),
     "dopr_prefix_attn": ([ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p,
@@ -240,6 +242,13 @@ def dopr_store_put(store: Store, layer: int, doc_ids, src_cu_slots, k_src,
 
 def dopr_store_destroy(store: Store):
     store.close()
+
+
+def dopr_store_copy_docs(dst: Store, src: Store, stream=None):
+    """Copy the documents resident in both stores (same slot counts) from
+    src to dst: all layers, heads and key-norm bounds."""
+    _check(lib().dopr_store_copy_docs(dst.handle, src.handle,
+                                      _stream(stream)))
 
 
 def _attn_args(store, doc_ids, cu_seqlens, q, k, v, q_norm_w, k_norm_w, out,

@@ -252,6 +252,25 @@ dopr_status_t dopr_store_put(dopr_store_t st, int32_t layer, int64_t n,
   return ok();
 }
 
+dopr_status_t dopr_store_copy_docs(dopr_store_t dst, dopr_store_t src,
+                                   void *stream) {
+  if (!dst || !src) return fail(DOPR_ERR_INVALID_ARG, "store is NULL");
+  if (dst->n_docs != src->n_docs || dst->n_layers != src->n_layers ||
+      dst->n_kv_heads != src->n_kv_heads)
+    return fail(DOPR_ERR_INVALID_ARG,
+                "stores differ in n_docs, n_layers or n_kv_heads");
+  if (dst->pool < src->pool + src->pool_bytes &&
+      src->pool < dst->pool + dst->pool_bytes)
+    return fail(DOPR_ERR_INVALID_ARG, "store pools overlap");
+  if (dst->device != src->device)
+    return fail(DOPR_ERR_INVALID_ARG, "stores live on different devices");
+  dopr_status_t s = check_device(dst);
+  if (s != DOPR_OK) return s;
+  hipError_t e = launch_store_copy(*dst, *src, as_stream(stream));
+  if (e != hipSuccess) return hip_fail(e, "store_copy launch");
+  return ok();
+}
+
 dopr_status_t dopr_store_destroy(dopr_store_t st) {
   delete st;
   return ok();

@@ -139,6 +139,8 @@ hipError_t launch_store_put(const dopr_store &st, int32_t layer, int64_t n,
 hipError_t launch_gather(const dopr_store &st, int32_t layer, int32_t n,
                          const int32_t *doc_ids, const int64_t *out_cu,
                          uint16_t *k, uint16_t *v, hipStream_t s);
+hipError_t launch_store_copy(const dopr_store &dst, const dopr_store &src,
+                             hipStream_t s);
 
 struct AttnCall {
   const dopr_store *st;

@@ -120,7 +120,53 @@ __global__ __launch_bounds__(kThreads) void k_gather(
   }
 }
 
+// Copy every document resident in both stores with the same prefix length:
+// its whole payload block (all layers and kv heads, laid out identically
+// in both pools) and its key-norm bounds.  Documents resident in only one
+// store are left alone; one resident in both with different lengths raises
+// DOC_RANGE on dst and is skipped.  Grid-strided over documents, one
+// workgroup per document at a time, four 16-byte moves in flight per lane.
+__global__ __launch_bounds__(kThreads) void k_store_copy(StoreView dst,
+                                                         int32_t *dst_status,
+                                                         StoreView src) {
+  const int64_t nk = (int64_t)dst.n_layers * dst.n_kv_heads;
+  for (int64_t d = blockIdx.x; d < dst.n_docs; d += gridDim.x) {
+    const int32_t L = dst.doc_len[d], Ls = src.doc_len[d];
+    if (L < 0 || Ls < 0) continue;
+    if (L != Ls) {
+      if (threadIdx.x == 0) raise_status(dst_status, DOPR_ERR_DOC_RANGE);
+      continue;
+    }
+    const int64_t n16 =
+        (int64_t)dst.n_layers * layer_block_elems(L, dst.n_kv_heads) / 8;
+    const uint4 *s = reinterpret_cast<const uint4 *>(src.payload +
+                                                     src.doc_off[d]);
+    uint4 *t = reinterpret_cast<uint4 *>(dst.payload + dst.doc_off[d]);
+    int64_t e = threadIdx.x;
+    for (; e + 3 * kThreads < n16; e += 4 * kThreads) {
+      const uint4 a = s[e], b = s[e + kThreads], c = s[e + 2 * kThreads],
+                  f = s[e + 3 * kThreads];
+      t[e] = a;
+      t[e + kThreads] = b;
+      t[e + 2 * kThreads] = c;
+      t[e + 3 * kThreads] = f;
+    }
+    for (; e < n16; e += kThreads) t[e] = s[e];
+    for (int64_t k = threadIdx.x; k < nk; k += kThreads)
+      dst.kmax[d * nk + k] = src.kmax[d * nk + k];
+  }
+}
+
 }  // namespace
+
+hipError_t launch_store_copy(const dopr_store &dst, const dopr_store &src,
+                             hipStream_t s) {
+  if (dst.n_docs == 0) return hipSuccess;
+  const int64_t grid = dst.n_docs < 4096 ? dst.n_docs : 4096;
+  hipLaunchKernelGGL(k_store_copy, dim3((unsigned)grid), dim3(kThreads), 0,
+                     s, dst.view(), dst.d_status, src.view());
+  return hipGetLastError();
+}
 
 hipError_t launch_store_put(const dopr_store &st, int32_t layer, int64_t n,
                             const int32_t *doc_ids, const int64_t *src_cu,

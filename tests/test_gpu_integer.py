@@ -132,3 +132,99 @@ def test_score_head_parity(W, P, mode):
     el = np.abs(logits.cpu().numpy() - rl).max()
     log(f"score W={W} P={P} {mode}: max|ds|={e:.2e} max|dlogit|={el:.2e}")
     assert e < 2e-2 and el < 2e-2
+
+
+def _put_layers(store, doc_len, docs, n_layers, seed):
+    """Fill `docs` (ascending ids) of every layer from seeded canonical
+    states; returns {(layer, doc): (k, v)} bf16 tensors [L, Hkv, D]."""
+    import torch
+    from paper_2609_03311_amd import dopr_store_put
+    ref = {}
+    lens = doc_len[docs].astype(np.int64)
+    cu = np.concatenate([[0], np.cumsum(lens)])
+    g = torch.Generator(device="cuda")
+    for layer in range(n_layers):
+        g.manual_seed(seed + layer)
+        shape = (max(int(cu[-1]), 1), 8, 128)
+        k = torch.randn(shape, generator=g, device="cuda").to(torch.bfloat16)
+        v = torch.randn(shape, generator=g, device="cuda").to(torch.bfloat16)
+        dopr_store_put(store, layer, torch.from_numpy(docs).cuda(),
+                       torch.from_numpy(cu).cuda(), k, v)
+        for i, d in enumerate(docs):
+            ref[(layer, int(d))] = (k[cu[i]:cu[i + 1]], v[cu[i]:cu[i + 1]])
+    return ref
+
+
+def test_store_copy_appends_and_repacks():
+    """dopr_store_copy_docs carries every document resident in both stores
+    (all layers, bit-exact), leaves dst-only documents to dopr_store_put,
+    drops src-only ones, and reports a slot-count mismatch as DOC_RANGE
+    without touching that document."""
+    import torch
+    from paper_2609_03311_amd import (DOPR_ERR_DOC_RANGE, DOPR_ERR_INVALID_ARG,
+                                      DoprError, dopr_check_status,
+                                      dopr_gather_prefix, dopr_store_copy_docs,
+                                      dopr_store_create)
+    rng = np.random.default_rng(7)
+    n_docs, n_layers = 60, 2
+    len_a = rng.integers(0, 70, n_docs).astype(np.int32)
+    len_a[rng.random(n_docs) < 0.2] = -1
+    len_b = len_a.copy()
+    len_b[rng.random(n_docs) < 0.3] = -1                 # dropped (repack)
+    new = (len_a < 0) & (rng.random(n_docs) < 0.5)
+    len_b[new] = rng.integers(1, 300, new.sum())          # appended
+    both = np.nonzero((len_a >= 0) & (len_b >= 0))[0]
+    mismatch = int(both[3])
+    len_b[mismatch] = len_a[mismatch] + 5
+    a = dopr_store_create(n_layers, 8, 128, len_a)
+    b = dopr_store_create(n_layers, 8, 128, len_b)
+    res_a = np.nonzero(len_a >= 0)[0].astype(np.int32)
+    ref_a = _put_layers(a, len_a, res_a, n_layers, seed=100)
+    dopr_store_copy_docs(b, a)
+    only_b = np.nonzero((len_b >= 0) & ((len_a < 0) |
+                                        (np.arange(n_docs) == mismatch)))[0]
+    assert dopr_check_status(b) == DOPR_ERR_DOC_RANGE    # the mismatch
+    ref_b = _put_layers(b, len_b, only_b.astype(np.int32), n_layers,
+                        seed=200)
+    assert dopr_check_status(a) == 0 and dopr_check_status(b) == 0
+    res_b = np.nonzero(len_b >= 0)[0].astype(np.int32)
+    cu = np.concatenate([[0], np.cumsum(len_b[res_b].astype(np.int64))])
+    for layer in range(n_layers):
+        ko = torch.empty((max(int(cu[-1]), 1), 8, 128), dtype=torch.bfloat16,
+                         device="cuda")
+        vo = torch.empty_like(ko)
+        dopr_gather_prefix(b, layer, torch.from_numpy(res_b).cuda(),
+                           torch.from_numpy(cu).cuda(), ko, vo)
+        assert dopr_check_status(b) == 0
+        for i, d in enumerate(res_b):
+            k_want, v_want = (ref_b if d in set(only_b.tolist())
+                              else ref_a)[(layer, int(d))]
+            got_k, got_v = ko[cu[i]:cu[i + 1]], vo[cu[i]:cu[i + 1]]
+            assert torch.equal(got_k.view(torch.int16),
+                               k_want.view(torch.int16)), (layer, d)
+            assert torch.equal(got_v.view(torch.int16),
+                               v_want.view(torch.int16)), (layer, d)
+    log(f"store copy: {len(res_b)} docs in dst, "
+        f"{len(res_b) - len(only_b)} carried, {len(only_b)} put")
+    # attention over carried documents is identical in both stores (the
+    # payload and the key-norm bounds travelled together)
+    from paper_2609_03311_amd import pipeline
+    carried = np.array([d for d in res_b if d not in set(only_b.tolist())
+                        and len_b[d] > 0], np.int32)[:12]
+    st = workloads.custom(len_b, carried, np.full(len(carried), 9), 32, 8)
+    on = workloads.online_inputs(st, "cuda", 5)
+    prm = workloads.params(st, "cuda", 6)
+    outs = []
+    for store in (a, b):
+        step = pipeline.OnlineStep(store, n_pairs=st.n_pairs, n_q_heads=32,
+                                   total_tokens=st.n_tokens, max_tokens=9)
+        step.attention(1, torch.from_numpy(st.doc_ids).cuda(),
+                       torch.from_numpy(st.cu_seqlens).cuda(), on["q"],
+                       on["k"], on["v"], prm["q_norm_w"], prm["k_norm_w"])
+        torch.cuda.synchronize()
+        outs.append(step.out.clone())
+    assert torch.equal(outs[0], outs[1])
+    c = dopr_store_create(1, 8, 128, len_b)
+    with pytest.raises(DoprError) as e:
+        dopr_store_copy_docs(c, a)
+    assert e.value.status == DOPR_ERR_INVALID_ARG
