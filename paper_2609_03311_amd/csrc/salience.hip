@@ -75,70 +75,121 @@ __device__ __forceinline__ bf16x8 ld8(const uint16_t *p) {
 }
 
 // ---------------------------------------------------------------------------
-// Row log-sum-exp.  grid (row blocks, Hkv, docs); each wave owns 32 rows and
-// the HR q heads of the group at a time (their Q fragments stay in
-// registers while the keys stream past).
+// Keys are staged in LDS in blocks of 128 rows (32 KB), double-buffered so a
+// block's direct global->LDS loads overlap the products on the previous one.
+constexpr int kLdsK = kKeyBlock * D;  // bf16 elements (swizzled rows)
+
+// Keys key0 .. key0+127 of kv head g into `dst`: each lane writes 16 bytes of
+// a 1 KB block (4 key rows), fetching the global granule that the swizzled
+// layout puts in its slot, so slot p of row r holds granule p ^ swz(r).
+// Rows past the document's end repeat row n-1 (masked by the causal test).
+__device__ __forceinline__ void stage_keys(const SalienceParams &P,
+                                           const Doc &doc, int key0, int g,
+                                           uint16_t *dst) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int b = wave; b < kKeyBlock / 4; b += 4) {
+    const int row = 4 * b + (lane >> 4), p = lane & 15;
+    const int key = min(key0 + row, doc.n - 1);
+    __builtin_amdgcn_global_load_lds(
+        (const __attribute__((address_space(1))) void *)(
+            P.k + ((doc.t0 + key) * P.hkv + g) * D + ((p ^ swz(row)) << 3)),
+        (__attribute__((address_space(3))) void *)(dst + b * 512), 16, 0, 0);
+  }
+}
+
+__device__ __forceinline__ void wait_vmem() {
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+}
+
+// ---------------------------------------------------------------------------
+// Row log-sum-exp.  grid (row blocks of 128, kv head, docs); each wave owns
+// 32 rows and keeps the HR q heads of the group in registers while the
+// document's keys 0 .. (last row of the block) stream through LDS, one
+// 128-key block at a time, shared by the block's four waves.  Per row and
+// head: a running maximum and sum over the visible keys (scaled logits in
+// log2 units), combined across the two lane halves at the end.
 template <int HR>
-__global__ __launch_bounds__(256) void k_row_lse(SalienceParams P) {
+__global__ __launch_bounds__(256, 2) void k_row_lse(SalienceParams P) {
+  __shared__ __attribute__((aligned(16))) uint16_t ks[2][kLdsK];
   const int d = P.d0 + blockIdx.z;
   const Doc doc = doc_at(P, d);
   if (!doc.ok) return;
   const int rb = gridDim.x - 1 - blockIdx.x;  // longest rows first
+  if (rb * kRowBlock >= doc.n) return;        // block-uniform, before barriers
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int hf = lane >> 5, lq = lane & 31;
   const int row0 = rb * kRowBlock + wave * 32;
-  if (row0 >= doc.n) return;  // no barriers in this kernel
+  const bool active = row0 < doc.n;
   const int g = blockIdx.y;
   const int j = row0 + lq;
   const int jl = min(j, doc.n - 1);
-  const int kend = min(doc.n, row0 + 32);
+  const int last = min(row0 + 31, doc.n - 1);
   const int64_t qrow = (doc.t0 + jl) * P.hq;
-  const int krow_lane = perm(lq);
+  const int kr = perm(lq);
+  const int n_kb = rb + 1;  // key blocks 0 .. rb
 
   for (int h0 = 0; h0 < P.n_rep; h0 += HR) {
     const int hbase = g * P.n_rep + h0;
     bf16x8 qf[HR][8];
-#pragma unroll
-    for (int r = 0; r < HR; ++r)
-#pragma unroll
-      for (int s = 0; s < 8; ++s)
-        qf[r][s] = ld8(P.q + (qrow + hbase + r) * D + 16 * s + 8 * hf);
     float m[HR], l[HR];
 #pragma unroll
     for (int r = 0; r < HR; ++r) {
       m[r] = -INFINITY;
       l[r] = 0.f;
-    }
-    for (int kb = 0; kb < kend; kb += 32) {
-      const int key = min(kb + krow_lane, doc.n - 1);
-      const uint16_t *kp = P.k + ((doc.t0 + key) * P.hkv + g) * D + 8 * hf;
-      bf16x8 kf[8];
-#pragma unroll
-      for (int s = 0; s < 8; ++s) kf[s] = ld8(kp + 16 * s);
-      const int lim = j - kb - 16 * hf;  // visible: i <= lim
-#pragma unroll
-      for (int r = 0; r < HR; ++r) {
-        floatx16 S;
-#pragma unroll
-        for (int i = 0; i < 16; ++i) S[i] = 0.f;
+      if (active) {
 #pragma unroll
         for (int s = 0; s < 8; ++s)
-          S = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[s], qf[r][s], S, 0,
-                                                      0, 0);
-        float x[16], mx = -INFINITY;
+          qf[r][s] = ld8(P.q + (qrow + hbase + r) * D + 16 * s + 8 * hf);
+      }
+    }
+    if (h0 > 0) __syncthreads();  // the previous heads are done with ks[0]
+    stage_keys(P, doc, 0, g, ks[0]);
+    for (int kb = 0; kb < n_kb; ++kb) {
+      wait_vmem();
+      __syncthreads();  // block kb staged; every wave done with the other
+      if (kb + 1 < n_kb)
+        stage_keys(P, doc, (kb + 1) * kKeyBlock, g, ks[(kb + 1) & 1]);
+      if (!active) continue;
+      const uint16_t *kbuf = ks[kb & 1];
+      const int key0 = kb * kKeyBlock;
+      const int nt = min(4, (last - key0) / 32 + 1);
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          x[i] = i <= lim ? S[i] * P.c : -INFINITY;
-          mx = fmaxf(mx, x[i]);
-        }
-        const float mn = fmaxf(m[r], mx);
-        if (mn > -INFINITY) {
-          float add = 0.f;
+      for (int st = 0; st < 4; ++st) {
+        if (st >= nt) break;
+        const int row = 32 * st + kr;
+        bf16x8 kf[8];
 #pragma unroll
-          for (int i = 0; i < 16; ++i)
-            add += __builtin_amdgcn_exp2f(x[i] - mn);
-          l[r] = l[r] * __builtin_amdgcn_exp2f(m[r] - mn) + add;
-          m[r] = mn;
+        for (int s = 0; s < 8; ++s)
+          kf[s] = ld8(kbuf + row * D + (((2 * s + hf) ^ swz(row)) << 3));
+        // keys of this sub-tile past the wave's first row need the mask
+        const bool masked = key0 + 32 * st + 31 > row0;
+        const int lim = j - key0 - 32 * st - 16 * hf;  // visible: i <= lim
+#pragma unroll
+        for (int r = 0; r < HR; ++r) {
+          floatx16 S;
+#pragma unroll
+          for (int i = 0; i < 16; ++i) S[i] = 0.f;
+#pragma unroll
+          for (int s = 0; s < 8; ++s)
+            S = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[s], qf[r][s], S,
+                                                        0, 0, 0);
+          float x[16], mx = -INFINITY;
+#pragma unroll
+          for (int i = 0; i < 16; ++i) {
+            x[i] = S[i] * P.c;
+            if (masked && i > lim) x[i] = -INFINITY;
+            mx = fmaxf(mx, x[i]);
+          }
+          const float mn = fmaxf(m[r], mx);
+          if (mn > -INFINITY) {
+            float add = 0.f;
+#pragma unroll
+            for (int i = 0; i < 16; ++i)
+              add += __builtin_amdgcn_exp2f(x[i] - mn);
+            l[r] = l[r] * __builtin_amdgcn_exp2f(m[r] - mn) + add;
+            m[r] = mn;
+          }
         }
       }
     }
@@ -150,7 +201,7 @@ __global__ __launch_bounds__(256) void k_row_lse(SalienceParams P) {
       // every row sees at least its own key, so mn is finite
       const float tot = l[r] * __builtin_amdgcn_exp2f(m[r] - mn) +
                         lo * __builtin_amdgcn_exp2f(mo - mn);
-      if (hf == 0 && j < doc.n)
+      if (active && hf == 0 && j < doc.n)
         P.lse2[(int64_t)(hbase + r) * P.total_tokens + doc.t0 + j] =
             mn + log2f(tot);
     }
@@ -160,13 +211,17 @@ __global__ __launch_bounds__(256) void k_row_lse(SalienceParams P) {
 // ---------------------------------------------------------------------------
 // Head-averaged attention.  grid (triangular tile index, docs); unit (rb, kb)
 // with kb <= rb covers rows rb*128 .. +127 and keys kb*128 .. +127.  Each
-// kv head's 128 key rows are staged in LDS and read by the 4 waves for the
-// group's q heads, HR heads per pass.
-constexpr int kLdsK = kKeyBlock * D;  // bf16 elements (swizzled rows)
+// kv head's 128 key rows are staged in LDS with direct global->LDS loads,
+// double-buffered so the next kv head's keys arrive while the current one
+// is used; each wave walks the q heads one at a time with the next head's
+// q fragments and row log-sum-exp loaded one head ahead.
+struct HeadQ {
+  bf16x8 f[8];
+  float L;
+};
 
-template <int HR>
 __global__ __launch_bounds__(256, 2) void k_mean_attn(SalienceParams P) {
-  __shared__ __attribute__((aligned(16))) uint16_t ks[kLdsK];
+  __shared__ __attribute__((aligned(16))) uint16_t ks[2][kLdsK];
   const int d = P.d0 + blockIdx.y;
   const Doc doc = doc_at(P, d);
   if (!doc.ok) return;
@@ -196,62 +251,62 @@ __global__ __launch_bounds__(256, 2) void k_mean_attn(SalienceParams P) {
 #pragma unroll
     for (int i = 0; i < 16; ++i) acc[s][i] = 0.f;
 
+  auto load_head = [&](int h, HeadQ &q) {
+#pragma unroll
+    for (int s = 0; s < 8; ++s)
+      q.f[s] = ld8(P.q + (qrow + h) * D + 16 * s + 8 * hf);
+    q.L = P.lse2[(int64_t)h * P.total_tokens + doc.t0 + jl];
+  };
   const int kr = perm(lq);
-  for (int g = 0; g < P.hkv; ++g) {
-    __syncthreads();  // the previous head's keys are no longer read
-    // stage keys key0 .. key0+127 of kv head g (rows past n repeat row n-1)
-#pragma unroll
-    for (int c = 0; c < kKeyBlock * 16 / 256; ++c) {
-      const int id = c * 256 + threadIdx.x;
-      const int row = id >> 4, gr = id & 15;
-      const int key = min(key0 + row, doc.n - 1);
-      const uint4 v = *reinterpret_cast<const uint4 *>(
-          P.k + ((doc.t0 + key) * P.hkv + g) * D + gr * 8);
-      *reinterpret_cast<uint4 *>(ks + row * D + ((gr ^ swz(row)) << 3)) = v;
+  // Head h: on a new kv head, wait for its keys (and for every wave to be
+  // done with the other buffer), then start the next kv head's keys; issue
+  // the next head's q loads; then this head's products and probabilities.
+  int g_cur = -1;
+  auto head = [&](int h, const HeadQ &cur, HeadQ &nxt) {
+    const int g = h / P.n_rep;
+    if (g != g_cur) {
+      wait_vmem();
+      __syncthreads();
+      if (g + 1 < P.hkv) stage_keys(P, doc, key0, g + 1, ks[(g + 1) & 1]);
+      g_cur = g;
     }
-    __syncthreads();
-    if (nt == 0) continue;
-    for (int h0 = 0; h0 < P.n_rep; h0 += HR) {
-      const int hbase = g * P.n_rep + h0;
-      bf16x8 qf[HR][8];
-      float L[HR];
+    if (active && h + 1 < P.hq) load_head(h + 1, nxt);
+    const uint16_t *kbuf = ks[g & 1];
 #pragma unroll
-      for (int r = 0; r < HR; ++r) {
+    for (int st = 0; st < 4; ++st) {
+      if (st >= nt) break;
+      const int row = 32 * st + kr;
+      bf16x8 kf[8];
 #pragma unroll
-        for (int s = 0; s < 8; ++s)
-          qf[r][s] = ld8(P.q + (qrow + hbase + r) * D + 16 * s + 8 * hf);
-        L[r] = P.lse2[(int64_t)(hbase + r) * P.total_tokens + doc.t0 + jl];
-      }
-      for (int st = 0; st < nt; ++st) {
-        const int row = 32 * st + kr;
-        bf16x8 kf[8];
+      for (int s = 0; s < 8; ++s)
+        kf[s] = ld8(kbuf + row * D + (((2 * s + hf) ^ swz(row)) << 3));
+      floatx16 S;
 #pragma unroll
-        for (int s = 0; s < 8; ++s)
-          kf[s] = ld8(ks + row * D + (((2 * s + hf) ^ swz(row)) << 3));
-        const int lim = j - key0 - 32 * st - 16 * hf;  // visible: i <= lim
+      for (int i = 0; i < 16; ++i) S[i] = 0.f;
 #pragma unroll
-        for (int r = 0; r < HR; ++r) {
-          floatx16 S;
+      for (int s = 0; s < 8; ++s)
+        S = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[s], cur.f[s], S, 0, 0,
+                                                    0);
+      const int lim = j - key0 - 32 * st - 16 * hf;  // visible: i <= lim
+      if (diag) {
 #pragma unroll
-          for (int i = 0; i < 16; ++i) S[i] = 0.f;
+        for (int i = 0; i < 16; ++i)
+          acc[st][i] += i <= lim ? __builtin_amdgcn_exp2f(
+                                       fmaf(S[i], P.c, -cur.L))
+                                 : 0.f;
+      } else {
 #pragma unroll
-          for (int s = 0; s < 8; ++s)
-            S = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[s], qf[r][s], S,
-                                                        0, 0, 0);
-          if (diag) {
-#pragma unroll
-            for (int i = 0; i < 16; ++i)
-              acc[st][i] += i <= lim ? __builtin_amdgcn_exp2f(
-                                           S[i] * P.c - L[r])
-                                     : 0.f;
-          } else {
-#pragma unroll
-            for (int i = 0; i < 16; ++i)
-              acc[st][i] += __builtin_amdgcn_exp2f(S[i] * P.c - L[r]);
-          }
-        }
+        for (int i = 0; i < 16; ++i)
+          acc[st][i] += __builtin_amdgcn_exp2f(fmaf(S[i], P.c, -cur.L));
       }
     }
+  };
+  stage_keys(P, doc, key0, 0, ks[0]);
+  HeadQ qa, qb;
+  if (active) load_head(0, qa);
+  for (int h = 0; h < P.hq; h += 2) {
+    head(h, qa, qb);
+    if (h + 1 < P.hq) head(h + 1, qb, qa);
   }
   if (!active || j >= doc.n) return;
   float *out = P.abar + (int64_t)(d - P.d0) * P.abar_stride +
@@ -450,14 +505,12 @@ hipError_t launch_salience_chunk(const SalienceParams &p, int32_t n_docs,
   const dim3 g_col((p.max_len + kStrip - 1) / kStrip, n_docs);
   if (hr == 4) {
     hipLaunchKernelGGL(k_row_lse<4>, g_lse, dim3(256), 0, s, p);
-    hipLaunchKernelGGL(k_mean_attn<2>, g_att, dim3(256), 0, s, p);
   } else if (hr == 2) {
     hipLaunchKernelGGL(k_row_lse<2>, g_lse, dim3(256), 0, s, p);
-    hipLaunchKernelGGL(k_mean_attn<2>, g_att, dim3(256), 0, s, p);
   } else {
     hipLaunchKernelGGL(k_row_lse<1>, g_lse, dim3(256), 0, s, p);
-    hipLaunchKernelGGL(k_mean_attn<1>, g_att, dim3(256), 0, s, p);
   }
+  hipLaunchKernelGGL(k_mean_attn, g_att, dim3(256), 0, s, p);
   if (pm == 8)
     hipLaunchKernelGGL(k_col_topp<8>, g_col, dim3(256), 0, s, p);
   else if (pm == 16)
