@@ -69,6 +69,10 @@ DESCRIPTIONS = {
                  "with Llama-3 frequency rescaling): 32q/8kv heads, D=128, "
                  "the qwen3_8b pairs (20k docs x 256 slots, 256 queries x "
                  "100 docs, T=128+1)",
+    "llama3_2_1b": "Llama-3.2-1B-shaped attention (no QK-norm, rope_theta "
+                   "5e5 with Llama-3 frequency rescaling): 32q/8kv heads, "
+                   "D=64, the qwen3_8b pairs (20k docs x 256 slots, 256 "
+                   "queries x 100 docs, T=128+1)",
 }
 # attention families: QK-norm on (Qwen3) or off with given frequencies
 LLAMA_ROPE_THETA = 500000.0
@@ -95,12 +99,12 @@ def llama3_rope_inv_freq(head_dim=128, theta=LLAMA_ROPE_THETA, factor=32.0,
     return np.where(in_band, mid, out).astype(np.float32)
 
 
-def family_args(config, dev):
+def family_args(config, dev, head_dim=128):
     """(gains_enabled, extra keyword arguments of the attention calls)."""
     if not config.startswith("llama"):
         return True, {}
     import torch
-    inv = torch.from_numpy(llama3_rope_inv_freq()).to(dev)
+    inv = torch.from_numpy(llama3_rope_inv_freq(head_dim)).to(dev)
     return False, {"rope_theta": LLAMA_ROPE_THETA, "rope_inv_freq": inv}
 SALIENCE_DESCRIPTIONS = {
     "qwen3_0p6b_docs": "salience selection, Qwen3-0.6B-shaped final layer: "
@@ -672,7 +676,7 @@ def main():
 
     st = workloads.make(args.config)
     dev = "cuda"
-    norm_on, fam = family_args(args.config, dev)
+    norm_on, fam = family_args(args.config, dev, st.head_dim)
     if not norm_on and args.path == "layer":
         ap.error("--path layer builds the Qwen3 decoder layer (QK-norm on)")
     log(f"{args.config}: P={st.n_pairs} Ntok={st.n_tokens} "

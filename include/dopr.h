@@ -31,8 +31,10 @@
  *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
  *     Every call is asynchronous on that stream unless stated otherwise.
  *   - bf16 means IEEE bfloat16 bit patterns (uint16); fp32 means IEEE float.
- *   - head_dim D must be 128.  n_q_heads must be a multiple of n_kv_heads;
- *     q head h reads kv head h / (n_q_heads / n_kv_heads).
+ *   - head_dim D is 128 (Qwen3, Llama 3) or 64 (Llama 3.2 1B, the model of
+ *     the cross-family check in the Appendix); the decoder layer and the
+ *     salience selection take D = 128 only.  n_q_heads must be a multiple
+ *     of n_kv_heads; q head h reads kv head h / (n_q_heads / n_kv_heads).
  *   - Every call returns a dopr_status_t.  Host-checkable argument errors are
  *     returned before anything is launched.  Errors found on the device (a
  *     doc id that is out of range or not resident, malformed cu_seqlens) are
@@ -55,7 +57,7 @@ extern "C" {
 typedef enum {
   DOPR_OK = 0,
   DOPR_ERR_INVALID_ARG = -1, /* null pointer, bad size, bad shape          */
-  DOPR_ERR_UNSUPPORTED = -2, /* valid but not implemented (e.g. D != 128)  */
+  DOPR_ERR_UNSUPPORTED = -2, /* valid but not implemented (e.g. D = 96)    */
   DOPR_ERR_DOC_RANGE = -3,   /* doc id outside [0,n_docs) or not resident  */
   DOPR_ERR_WORKSPACE = -4,   /* workspace or pool smaller than required    */
   DOPR_ERR_HIP = -5,         /* a HIP runtime call failed                  */
@@ -74,7 +76,7 @@ typedef struct dopr_store *dopr_store_t;
 typedef struct {
   int32_t n_layers;       /* decoder layers held per document (>= 1)        */
   int32_t n_kv_heads;     /* Hkv (>= 1)                                     */
-  int32_t head_dim;       /* D; must be 128                                 */
+  int32_t head_dim;       /* D; 128 or 64 (UNSUPPORTED otherwise)           */
   int64_t n_docs;         /* size of the doc-id space [0, n_docs)           */
   const int32_t *doc_len; /* HOST [n_docs]: prefix slots L_d of doc d.
                              0 is allowed (no prefix); -1 = not resident
@@ -229,7 +231,7 @@ dopr_status_t dopr_score_logits(const dopr_score_args_t *args, void *stream);
  * exactly the rows dopr_prefix_attn computes for those tokens (same keys:
  * all L_d prefix slots and all T_p own keys, so every own key and value is
  * still read and every own key is normed and rotated), and feeds them to
- * the score head of dopr_score_logits with width W = n_q_heads * 128:
+ * the score head of dopr_score_logits with width W = n_q_heads * D:
  *   h = out[p] viewed as [W] (bf16-rounded attention output),
  *   h^ = RMSNorm(h) * norm_w;  l_yes = w_yes . h^;  l_no = w_no . h^;
  *   s = l_yes - l_no.
@@ -244,7 +246,7 @@ dopr_status_t dopr_score_logits(const dopr_score_args_t *args, void *stream);
  * bad doc id gets zero rows, lse -inf, logits and score 0, and a deferred
  * DOC_RANGE status.  All buffers are caller-owned.                         */
 typedef struct {
-  const void *norm_w;       /* dev bf16 [W], W = n_q_heads * 128            */
+  const void *norm_w;       /* dev bf16 [W], W = n_q_heads * D              */
   const void *w_head;       /* dev bf16 [2, W]: row 0 = yes, row 1 = no    */
   float rms_eps;            /* >= 0, finite                                 */
   float *logits;            /* dev fp32 [P, 2] (l_yes, l_no), or NULL      */

@@ -197,11 +197,13 @@ def dopr_store_bytes(n_layers: int, n_kv_heads: int, head_dim: int,
 class Store:
     """Handle of a prefix store laid out in a caller-owned device pool."""
 
-    def __init__(self, handle, pool, n_layers, n_kv_heads, doc_len):
+    def __init__(self, handle, pool, n_layers, n_kv_heads, doc_len,
+                 head_dim=128):
         self.handle = handle
         self.pool = pool  # keeps the device memory alive
         self.n_layers = n_layers
         self.n_kv_heads = n_kv_heads
+        self.head_dim = head_dim
         self.doc_len = doc_len
 
     def close(self):
@@ -230,7 +232,8 @@ def dopr_store_create(n_layers: int, n_kv_heads: int, head_dim: int,
     _check(lib().dopr_store_create(ctypes.byref(d), pool.data_ptr(),
                                    pool.numel() * pool.element_size(),
                                    _stream(stream), ctypes.byref(h)))
-    return Store(h.value, pool, n_layers, n_kv_heads, keep.copy())
+    return Store(h.value, pool, n_layers, n_kv_heads, keep.copy(),
+                 head_dim=head_dim)
 
 
 def dopr_store_put(store: Store, layer: int, doc_ids, src_cu_slots, k_src,
@@ -259,7 +262,7 @@ def _attn_args(store, doc_ids, cu_seqlens, q, k, v, q_norm_w, k_norm_w, out,
     if total_tokens is None:
         total_tokens = q.shape[0]
     if softmax_scale is None:
-        softmax_scale = 128 ** -0.5
+        softmax_scale = store.head_dim ** -0.5
     ws_bytes = 0 if workspace is None else (
         workspace.numel() * workspace.element_size())
     return _AttnArgs(doc_ids.numel(), n_q_heads, int(max_tokens),

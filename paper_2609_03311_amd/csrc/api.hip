@@ -51,8 +51,8 @@ dopr_status_t layout_store(const dopr_store_desc_t *d, StoreLayout *lay,
     return fail(DOPR_ERR_INVALID_ARG, "doc_len is NULL");
   if (d->n_layers < 1 || d->n_kv_heads < 1)
     return fail(DOPR_ERR_INVALID_ARG, "n_layers and n_kv_heads must be >= 1");
-  if (d->head_dim != kHeadDim)
-    return fail(DOPR_ERR_UNSUPPORTED, "head_dim must be 128");
+  if (d->head_dim != 128 && d->head_dim != 64)
+    return fail(DOPR_ERR_UNSUPPORTED, "head_dim must be 128 or 64");
   size_t off = align_up(sizeof(int32_t) * kStatusWords, kAlign);
   lay->len_off = off;
   off = align_up(off + sizeof(int32_t) * (size_t)d->n_docs, kAlign);
@@ -74,8 +74,9 @@ dopr_status_t layout_store(const dopr_store_desc_t *d, StoreLayout *lay,
                   "doc_len entries must be >= 0, or -1 (not resident)");
     if (L < 0) continue;
     if (doc_off) (*doc_off)[i] = elems;
-    elems += (int64_t)d->n_layers * layer_block_elems(L, d->n_kv_heads);
-    canon += (size_t)L * d->n_layers * d->n_kv_heads * kHeadDim * 2 * 2;
+    elems += (int64_t)d->n_layers *
+             layer_block_elems(L, d->n_kv_heads, d->head_dim);
+    canon += (size_t)L * d->n_layers * d->n_kv_heads * d->head_dim * 2 * 2;
     if (L > max_len) max_len = L;
   }
   lay->total = off + sizeof(uint16_t) * (size_t)elems;
@@ -126,6 +127,7 @@ dopr_status_t check_attn(const dopr_store *st, const dopr_attn_args_t *a,
   shape->total_tokens = a->total_tokens;
   shape->max_len = st->max_len;
   shape->n_kv_heads = st->n_kv_heads;
+  shape->head_dim = st->head_dim;
   shape->score_only = score_only;
   return DOPR_OK;
 }
@@ -256,9 +258,9 @@ dopr_status_t dopr_store_copy_docs(dopr_store_t dst, dopr_store_t src,
                                    void *stream) {
   if (!dst || !src) return fail(DOPR_ERR_INVALID_ARG, "store is NULL");
   if (dst->n_docs != src->n_docs || dst->n_layers != src->n_layers ||
-      dst->n_kv_heads != src->n_kv_heads)
+      dst->n_kv_heads != src->n_kv_heads || dst->head_dim != src->head_dim)
     return fail(DOPR_ERR_INVALID_ARG,
-                "stores differ in n_docs, n_layers or n_kv_heads");
+                "stores differ in n_docs, n_layers, n_kv_heads or head_dim");
   if (dst->pool < src->pool + src->pool_bytes &&
       src->pool < dst->pool + dst->pool_bytes)
     return fail(DOPR_ERR_INVALID_ARG, "store pools overlap");
@@ -389,6 +391,9 @@ dopr_status_t check_layer(dopr_store_t st, const dopr_attn_args_t *b,
   dopr_status_t s = check_attn(st, b, shape, n_rep);
   if (s != DOPR_OK) return s;
   if (!l) return fail(DOPR_ERR_INVALID_ARG, "layer args are NULL");
+  if (st->head_dim != kHeadDim)
+    return fail(DOPR_ERR_UNSUPPORTED,
+                "the decoder layer is built for head_dim 128");
   if (l->hidden < 8 || l->hidden % 8 || l->intermediate < 8 ||
       l->intermediate % 8)
     return fail(DOPR_ERR_INVALID_ARG,

@@ -64,7 +64,6 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 
-constexpr int D = kHeadDim;
 constexpr int KC = 32;      // keys per MFMA chunk
 constexpr int kTotItems = 2;
 constexpr int kFixQueue = 8;  // cursor slot of the fixup pass
@@ -77,8 +76,11 @@ constexpr float kNoRefBound = 64.f;  // |logit| <= 64: weights exp2(logit)
 // computed by the fast pass (its logit bound exceeds kNoRefBound); those
 // run the bounded-reference mode first, the others the exact mode.
 constexpr int32_t kFixUnscored = 1 << 30;
-// Largest prefix the two-blocks-per-CU shape keeps resident (3 chunks).
-constexpr int32_t kSmallPrefix = 3 * KC;
+// Prefix chunks resident in LDS per head size: the one-block-per-CU shape
+// fills the CU's LDS (D = 128: 8 chunks, 256 slots; D = 64: 16 chunks),
+// the two-blocks-per-CU shape holds 3 (resp. 6) chunks.
+constexpr int big_chunks(int d) { return d == 128 ? 8 : 16; }
+constexpr int small_chunks(int d) { return d == 128 ? 3 : 6; }
 
 struct AttnParams {
   const uint16_t *q, *k, *v, *qw, *kw;
@@ -109,13 +111,13 @@ struct AttnParams {
   float eps, c;      // c = softmax_scale * log2(e)
 };
 
-// 160 KB: the whole LDS of a CU.  Keys and values live in 32-key chunk
-// blocks of 8 KB -- K [32 keys][D] and V^T [D][32 keys], 16-byte granules
-// XOR-swizzled -- so prefix chunks and own-key chunks share one layout and
-// one set of per-lane read offsets.  The own-key chunk is double-buffered;
-// at item boundaries (no own chunk in flight) its first words carry the
-// work index broadcast and the per-wave overflow flags.
-template <int NCHK>
+// Up to 160 KB: the whole LDS of a CU.  Keys and values live in 32-key
+// chunk blocks of 64*D bytes -- K [32 keys][D] and V^T [D][32 keys], 16-byte
+// granules XOR-swizzled -- so prefix chunks and own-key chunks share one
+// layout and one set of per-lane read offsets.  The own-key chunk is
+// double-buffered; at item boundaries (no own chunk in flight) its first
+// words carry the work index broadcast and the per-wave overflow flags.
+template <int D, int NCHK>
 struct Smem {
   static constexpr int PSEG = NCHK * KC;  // prefix slots resident at once
   uint16_t pk[NCHK][KC * D];  // prefix K chunks
@@ -130,16 +132,23 @@ __device__ __forceinline__ int perm32(int m) {
 }
 // XOR swizzles of 16-byte granules: the 16 rows read together by a quarter
 // wave (perm32 of lanes 0..15 or 16..31) land on 16 distinct bank groups.
+// A K row is 256 B at D = 128 (16 granules) and 128 B at D = 64 (8, so two
+// rows share a 256-byte bank line).
+template <int D>
 __device__ __forceinline__ int swz(int row) {
-  return (row & 3) | ((row >> 2) & 4) | ((row << 1) & 8);
+  if constexpr (D == 128)
+    return (row & 3) | ((row >> 2) & 4) | ((row << 1) & 8);
+  else
+    return ((row >> 1) & 1) | ((row >> 1) & 2) | ((row >> 2) & 4);
 }
 __device__ __forceinline__ int swz_v(int row) {
   return ((row >> 2) & 1) | ((row >> 3) & 2);
 }
 // Element offsets inside a chunk block: K row `key` (0..31), granule gr
-// (0..15); V^T row d (0..127), granule g (0..3, keys 8g..8g+7).
+// (0..D/8-1); V^T row d (0..D-1), granule g (0..3, keys 8g..8g+7).
+template <int D>
 __device__ __forceinline__ int kc_off(int key, int gr) {
-  return key * D + ((gr ^ swz(key)) << 3);
+  return key * D + ((gr ^ swz<D>(key)) << 3);
 }
 __device__ __forceinline__ int vc_off(int d, int g) {
   return d * KC + ((g ^ swz_v(d)) << 3);
@@ -206,29 +215,31 @@ __device__ __forceinline__ int find_pair(const AttnParams &P, int r) {
 
 // c * q^ with q^ = RoPE_pos(RMSNorm(q) * w), in the B-operand layout: lane
 // half hf holds head dims 16*s + 8*hf + e of its query column (k-step
-// s = 0..7); the rotate-half partner of dim i < 64 is dim i + 64 = k-step
-// s + 4, same lane.  c = softmax_scale * log2(e).  The raw row stays
-// packed until the norm is known; the rotation then runs one k-step pair at
-// a time, each finished fragment pinned in place so the compiler does not
-// keep the step's inputs alive until the first product.
+// s = 0..D/16-1); the rotate-half partner of dim i < D/2 is dim i + D/2 =
+// k-step s + D/32, same lane.  c = softmax_scale * log2(e).  The raw row
+// stays packed until the norm is known; the rotation then runs one k-step
+// pair at a time, each finished fragment pinned in place so the compiler
+// does not keep the step's inputs alive until the first product.
+template <int D>
 __device__ __forceinline__ void q_fragments(const uint16_t *qrow,
                                             const uint16_t *w,
                                             const float2 *rope_row, int hf,
                                             float eps, float c, bool norm,
                                             bf16x8 *qf) {
+  constexpr int NS = D / 16, HS = NS / 2;
   // every load is issued up front (one round trip to memory): the raw row,
-  // the gains (packed) and this lane's 32 (cos, sin) pairs
-  uint4 raw[8], wr[8];
-  float4 cs[16];
+  // the gains (packed) and this lane's D/4 (cos, sin) pairs
+  uint4 raw[NS], wr[NS];
+  float4 cs[4 * HS];
 #pragma unroll
-  for (int s = 0; s < 8; ++s)
+  for (int s = 0; s < NS; ++s)
     raw[s] = *reinterpret_cast<const uint4 *>(qrow + 16 * s + 8 * hf);
   w += opaque_zero();
 #pragma unroll
-  for (int s = 0; s < 8; ++s)
+  for (int s = 0; s < NS; ++s)
     wr[s] = *reinterpret_cast<const uint4 *>(w + 16 * s + 8 * hf);
 #pragma unroll
-  for (int s = 0; s < 4; ++s)
+  for (int s = 0; s < HS; ++s)
 #pragma unroll
     for (int e2 = 0; e2 < 4; ++e2)
       cs[4 * s + e2] =
@@ -237,16 +248,16 @@ __device__ __forceinline__ void q_fragments(const uint16_t *qrow,
   // unpacked row is not kept alive until the rotation
   float ss = 0.f;
 #pragma unroll
-  for (int s = 0; s < 8; ++s) ss = sumsq8(raw[s], ss);
+  for (int s = 0; s < NS; ++s) ss = sumsq8(raw[s], ss);
   ss += __shfl_xor(ss, 32, 64);
   const float inv = norm ? c * rsqrtf(ss * (1.0f / D) + eps) : c;
 #pragma unroll
-  for (int s = 0; s < 4; ++s) {
+  for (int s = 0; s < HS; ++s) {
     float x0[8], x1[8], w0[8], w1[8];
     unpack8(raw[s], x0);
-    unpack8(raw[s + 4], x1);
+    unpack8(raw[s + HS], x1);
     unpack8(wr[s], w0);
-    unpack8(wr[s + 4], w1);
+    unpack8(wr[s + HS], w1);
 #pragma unroll
     for (int e2 = 0; e2 < 4; ++e2) {
       const float4 t = cs[4 * s + e2];  // (cos, sin) of dims 2e2, 2e2 + 1
@@ -260,9 +271,9 @@ __device__ __forceinline__ void q_fragments(const uint16_t *qrow,
       x1[e + 1] = fmaf(b, t.z, a * t.w);
     }
     qf[s] = to_bf16x8(x0);
-    qf[s + 4] = to_bf16x8(x1);
+    qf[s + HS] = to_bf16x8(x1);
     pin(qf[s]);
-    pin(qf[s + 4]);
+    pin(qf[s + HS]);
   }
 }
 
@@ -273,34 +284,38 @@ __device__ __forceinline__ void q_fragments(const uint16_t *qrow,
 // are left stale (their logits are masked by a select).  V^T columns past
 // the stored ones (up to the chunk end) are zeroed instead: masked keys
 // must multiply a finite value.  The store's pad columns [L, Lp) are zero.
-template <int WAVES, int NCHK>
+template <int WAVES, int D, int NCHK>
 __device__ __forceinline__ void stage_prefix(const uint16_t *Kp,
                                              const uint16_t *VTp, int Lp,
                                              int seg0, int n,
-                                             Smem<NCHK> &sm) {
-  constexpr int PSEG = Smem<NCHK>::PSEG;
+                                             Smem<D, NCHK> &sm) {
+  constexpr int PSEG = Smem<D, NCHK>::PSEG;
+  constexpr int G = D / 8;       // granules per K row
+  constexpr int RPB = 64 / G;    // K rows per 1 KB block
+  constexpr int VB = D / 16;     // 1 KB V^T blocks per chunk
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  // K: 1 KB block b = rows 4b..4b+3, lane -> (row, physical granule)
-  const int kblocks = (n + 3) >> 2;
+  // K: 1 KB block b = rows RPB*b .. RPB*b + RPB-1, lane -> (row, physical
+  // granule)
+  const int kblocks = (unsigned)(n + RPB - 1) / RPB;
   uint16_t *pk = sm.pk[0];
   for (int b = wave; b < kblocks; b += WAVES) {
-    const int r = 4 * b + (lane >> 4), p = lane & 15;
+    const int r = RPB * b + (unsigned)lane / G, p = (unsigned)lane % G;
     if (r < n) {
-      const int gr = p ^ swz(r & 31);
+      const int gr = p ^ swz<D>(r & 31);
       __builtin_amdgcn_global_load_lds(
           (const __attribute__((address_space(1))) void *)(
               Kp + (int64_t)(seg0 + r) * D + gr * 8),
           (__attribute__((address_space(3))) void *)(pk + b * 512), 16, 0, 0);
     }
   }
-  // V^T: 1 KB block b = chunk b / 8, rows d = 16 (b % 8) .. + 15, four
+  // V^T: 1 KB block b = chunk b / VB, rows d = 16 (b % VB) .. + 15, four
   // granules of 8 keys each
   const int lp = Lp - seg0 < PSEG ? Lp - seg0 : PSEG;  // stored columns
-  const int vblocks = ((n + KC - 1) / KC) * 8;
+  const int vblocks = ((n + KC - 1) / KC) * VB;
   uint16_t *pv = sm.pv[0];
   for (int b = wave; b < vblocks; b += WAVES) {
-    const int d = 16 * (b & 7) + (lane >> 2), p = lane & 3;
-    const int key = KC * (b >> 3) + 8 * (p ^ swz_v(d));
+    const int d = 16 * ((unsigned)b % VB) + (lane >> 2), p = lane & 3;
+    const int key = KC * ((unsigned)b / VB) + 8 * (p ^ swz_v(d));
     if (key < lp)
       __builtin_amdgcn_global_load_lds(
           (const __attribute__((address_space(1))) void *)(
@@ -326,90 +341,104 @@ struct OwnStep {
   int srow0;  // the pair's first stacked row
 };
 
-// Sum over the 8 lanes 8k..8k+7 (every lane gets the same value): the two
-// quad butterflies, then the other quad through row_half_mirror (DPP, no
-// LDS round trip).  The additions pair the same values as a butterfly
-// over lane ^ 1, ^ 2, ^ 4.
-__device__ __forceinline__ float sum8_lanes(float x) {
+// Sum over the N = 4 or 8 lanes Nk..Nk+N-1 (every lane gets the same
+// value): the two quad butterflies, then for N = 8 the other quad through
+// row_half_mirror (DPP, no LDS round trip).  The additions pair the same
+// values as a butterfly over lane ^ 1, ^ 2 (, ^ 4).
+template <int N>
+__device__ __forceinline__ float sum_lanes(float x) {
   x += __builtin_bit_cast(
       float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), 0xB1, 0xF,
                                       0xF, false));
   x += __builtin_bit_cast(
       float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), 0x4E, 0xF,
                                       0xF, false));
-  x += __builtin_bit_cast(
-      float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), 0x141, 0xF,
-                                      0xF, false));
+  if constexpr (N == 8)
+    x += __builtin_bit_cast(
+        float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), 0x141,
+                                        0xF, 0xF, false));
   return x;
 }
 
 // Raw k/v rows and rotary factors of one own-key chunk, held in registers
-// between the prefetch and the LDS stage.  Thread t handles key
-// kk = (t / 8) % 32, head dims 8*sub..8*sub+7 (sub = t % 8) and their
-// rotate-half partners 64+8*sub..64+8*sub+7.  With 8 waves the first 256
-// threads stage k^ and the other 256 stage v (one register set, two
-// roles); with 4 waves every thread stages both.
-template <int WAVES>
+// between the prefetch and the LDS stage.  NSUB = D/16 threads share a key:
+// thread t handles key kk = (t / NSUB) % 32, head dims 8*sub..8*sub+7
+// (sub = t % NSUB) and their rotate-half partners D/2+8*sub..D/2+8*sub+7,
+// so a role takes 2*D threads.  When the block has 4*D threads or more the
+// first 2*D stage k^ and the next 2*D stage v (one register set, two
+// roles); otherwise (4 waves at D = 128) each of the first 2*D threads
+// stages both.
+template <int WAVES, int D>
+struct OwnGeo {
+  static constexpr int NSUB = D / 16;
+  static constexpr int ROLE = 2 * D;
+  static constexpr bool SPLIT = WAVES * 64 >= 2 * ROLE;
+  static constexpr int ACTIVE = SPLIT ? 2 * ROLE : ROLE;
+};
+
 struct OwnRegs {
   uint4 a0, a1;            // k (or v in the value role)
-  uint4 b0, b1;            // v when one thread has both roles (4 waves)
+  uint4 b0, b1;            // v when one thread has both roles
   float4 r0, r1, r2, r3;   // (cos, sin) of the key's position
   bool valid;
 };
 
-template <int WAVES>
+template <int WAVES, int D>
 __device__ __forceinline__ bool key_role() {
-  return WAVES == 4 || threadIdx.x < 256;
+  return !OwnGeo<WAVES, D>::SPLIT || threadIdx.x < OwnGeo<WAVES, D>::ROLE;
 }
-template <int WAVES>
+template <int WAVES, int D>
 __device__ __forceinline__ bool value_role() {
-  return WAVES == 4 || threadIdx.x >= 256;
+  return !OwnGeo<WAVES, D>::SPLIT || threadIdx.x >= OwnGeo<WAVES, D>::ROLE;
 }
 
-template <int WAVES>
+template <int WAVES, int D>
 __device__ __forceinline__ void own_load(const AttnParams &P, const OwnStep &o,
-                                         int g, int L, OwnRegs<WAVES> &r) {
+                                         int g, int L, OwnRegs &r) {
+  using Geo = OwnGeo<WAVES, D>;
   // thread indices are recomputed here (opaque offset) rather than hoisted
   // out of the kernel's loops with their derived addresses
   const int t = threadIdx.x + opaque_zero();
-  const int kk = (t >> 3) & 31, sub = t & 7;
+  const int kk = ((unsigned)t / Geo::NSUB) & 31, sub = (unsigned)t % Geo::NSUB;
   const int jk = o.c0 + kk;
-  r.valid = t < 256 * (WAVES / 4) && jk < o.T;
+  r.valid = t < Geo::ACTIVE && jk < o.T;
   if (r.valid) {
     const int64_t off = ((int64_t)(o.tok0 + jk) * P.Hkv + g) * D;
-    if (key_role<WAVES>()) {
+    if (key_role<WAVES, D>()) {
       r.a0 = *reinterpret_cast<const uint4 *>(P.k + off + 8 * sub);
-      r.a1 = *reinterpret_cast<const uint4 *>(P.k + off + 64 + 8 * sub);
+      r.a1 = *reinterpret_cast<const uint4 *>(P.k + off + D / 2 + 8 * sub);
       const float4 *cq = reinterpret_cast<const float4 *>(
-          P.rope + (int64_t)(L + jk) * kRopeHalf + 8 * sub);
+          P.rope + (int64_t)(L + jk) * (D / 2) + 8 * sub);
       r.r0 = cq[0];
       r.r1 = cq[1];
       r.r2 = cq[2];
       r.r3 = cq[3];
     }
-    if (WAVES == 4) {
+    if (!Geo::SPLIT) {
       r.b0 = *reinterpret_cast<const uint4 *>(P.v + off + 8 * sub);
-      r.b1 = *reinterpret_cast<const uint4 *>(P.v + off + 64 + 8 * sub);
-    } else if (value_role<WAVES>()) {
+      r.b1 = *reinterpret_cast<const uint4 *>(P.v + off + D / 2 + 8 * sub);
+    } else if (value_role<WAVES, D>()) {
       r.a0 = *reinterpret_cast<const uint4 *>(P.v + off + 8 * sub);
-      r.a1 = *reinterpret_cast<const uint4 *>(P.v + off + 64 + 8 * sub);
+      r.a1 = *reinterpret_cast<const uint4 *>(P.v + off + D / 2 + 8 * sub);
     }
   }
 }
 
 // k^ = RoPE(RMSNorm(k) * w) into sm.ok; v transposed into sm.ov.  Rows of
 // keys past the pair's end are zero.
-template <int WAVES, int NCHK>
+template <int WAVES, int D, int NCHK>
 __device__ __forceinline__ void own_stage(const AttnParams &P,
-                                          const OwnRegs<WAVES> &r,
-                                          Smem<NCHK> &sm, int buf) {
-  if (threadIdx.x >= 256 * (WAVES / 4)) return;
+                                          const OwnRegs &r,
+                                          Smem<D, NCHK> &sm, int buf) {
+  using Geo = OwnGeo<WAVES, D>;
+  if (threadIdx.x >= Geo::ACTIVE) return;
   const int t = threadIdx.x + opaque_zero();
-  const int kk = (t >> 3) & 31, sub = t & 7;
-  if (key_role<WAVES>()) {
+  const int kk = ((unsigned)t / Geo::NSUB) & 31, sub = (unsigned)t % Geo::NSUB;
+  if (key_role<WAVES, D>()) {
     // the gains first: their load overlaps the norm's reduction
     const uint4 g0 = *reinterpret_cast<const uint4 *>(P.kw + 8 * sub);
-    const uint4 g1 = *reinterpret_cast<const uint4 *>(P.kw + 64 + 8 * sub);
+    const uint4 g1 =
+        *reinterpret_cast<const uint4 *>(P.kw + D / 2 + 8 * sub);
     float x[16];
     float ss = r.valid ? sumsq8(r.a1, sumsq8(r.a0, 0.f)) : 0.f;
     if (r.valid) {
@@ -419,7 +448,7 @@ __device__ __forceinline__ void own_stage(const AttnParams &P,
 #pragma unroll
       for (int e = 0; e < 16; ++e) x[e] = 0.f;
     }
-    ss = sum8_lanes(ss);
+    ss = sum_lanes<Geo::NSUB>(ss);
     if (r.valid) {
       const float inv = P.norm ? rsqrtf(ss * (1.0f / D) + P.eps) : 1.f;
       float w0[8], w1[8];
@@ -436,23 +465,23 @@ __device__ __forceinline__ void own_stage(const AttnParams &P,
         x[8 + e] = fmaf(b, co, a * si);
       }
     }
-    *reinterpret_cast<uint4 *>(sm.ok[buf] + kc_off(kk, sub)) =
+    *reinterpret_cast<uint4 *>(sm.ok[buf] + kc_off<D>(kk, sub)) =
         as_uint4(to_bf16x8(x));
-    *reinterpret_cast<uint4 *>(sm.ok[buf] + kc_off(kk, sub + 8)) =
+    *reinterpret_cast<uint4 *>(sm.ok[buf] + kc_off<D>(kk, sub + Geo::NSUB)) =
         as_uint4(to_bf16x8(x + 8));
   }
-  if (value_role<WAVES>()) {
+  if (value_role<WAVES, D>()) {
     // a pure transpose: the bf16 halves are stored as they are (keys past
     // the pair's end are written as zeros)
-    const uint4 &v0 = WAVES == 4 ? r.b0 : r.a0;
-    const uint4 &v1 = WAVES == 4 ? r.b1 : r.a1;
+    const uint4 &v0 = Geo::SPLIT ? r.a0 : r.b0;
+    const uint4 &v1 = Geo::SPLIT ? r.a1 : r.b1;
     const uint32_t h[8] = {r.valid ? v0.x : 0u, r.valid ? v0.y : 0u,
                            r.valid ? v0.z : 0u, r.valid ? v0.w : 0u,
                            r.valid ? v1.x : 0u, r.valid ? v1.y : 0u,
                            r.valid ? v1.z : 0u, r.valid ? v1.w : 0u};
-    // rows d = 8*sub + e and 64 + 8*sub + e, column kk: the swizzle of row
-    // d depends only on e >= 4 and sub, so two base addresses serve all 16
-    // stores (the rest are constant offsets)
+    // rows d = 8*sub + e and D/2 + 8*sub + e, column kk: the swizzle of
+    // row d depends only on e >= 4 and sub (not on adding D/2), so two base
+    // addresses serve all 16 stores (the rest are constant offsets)
     const int gr = kk >> 3, in = kk & 7;
     uint16_t *ov = sm.ov[buf];
     const int b0 = vc_off(8 * sub, gr) + in, b1 = vc_off(8 * sub + 4, gr) + in;
@@ -461,7 +490,7 @@ __device__ __forceinline__ void own_stage(const AttnParams &P,
       const int base = (e < 4 ? b0 + e * KC : b1 + (e - 4) * KC);
       const uint32_t lo = h[e >> 1], hi = h[4 + (e >> 1)];
       ov[base] = (uint16_t)((e & 1) ? lo >> 16 : lo);
-      ov[base + 64 * KC] = (uint16_t)((e & 1) ? hi >> 16 : hi);
+      ov[base + (D / 2) * KC] = (uint16_t)((e & 1) ? hi >> 16 : hi);
     }
   }
 }
@@ -470,8 +499,9 @@ __device__ __forceinline__ void own_stage(const AttnParams &P,
 // units.  m is the reference subtracted from the logits: 0 in mode 0; in
 // mode 1 fixed at the first visible chunk (+inf before); in mode 2 (SAFE)
 // the running maximum (-inf before).
+template <int D>
 struct Acc {
-  floatx16 o[4];
+  floatx16 o[D / 32];
   float m, l;
 };
 
@@ -480,14 +510,16 @@ struct Acc {
 // 16s + 8hf .. + 7 of key row perm32(lq)) and V^T fragment f = (db, t)
 // (head-dim row 32db + perm32(lq), keys 16hf + 8t .. + 7).  The V^T
 // offsets differ by whole rows across db, so two registers hold them.
+template <int D>
 struct Frag {
-  int k[8], v[2];
+  int k[D / 16], v[2];
 };
-__device__ __forceinline__ Frag frag_offsets(int lq, int hf) {
-  Frag f;
+template <int D>
+__device__ __forceinline__ Frag<D> frag_offsets(int lq, int hf) {
+  Frag<D> f;
   const int row = perm32(lq);
 #pragma unroll
-  for (int s = 0; s < 8; ++s) f.k[s] = kc_off(row, 2 * s + hf);
+  for (int s = 0; s < D / 16; ++s) f.k[s] = kc_off<D>(row, 2 * s + hf);
   f.v[0] = vc_off(row, 2 * hf);
   f.v[1] = vc_off(row, 2 * hf + 1);
   return f;
@@ -500,15 +532,17 @@ constexpr int RA = 4;
 
 // S^T = K Q^T for one 32-key chunk (logits in log2 units: q^ carries the
 // scale).
-template <int NQB>
-__device__ __forceinline__ void qk_part(const uint16_t *kblk, const Frag &fo,
-                                        const bf16x8 (*qf)[8], floatx16 *S) {
+template <int NQB, int D>
+__device__ __forceinline__ void qk_part(const uint16_t *kblk,
+                                        const Frag<D> &fo,
+                                        const bf16x8 (*qf)[D / 16],
+                                        floatx16 *S) {
 #pragma unroll
   for (int qb = 0; qb < NQB; ++qb)
 #pragma unroll
     for (int i = 0; i < 16; ++i) S[qb][i] = 0.f;
 #pragma unroll
-  for (int s0 = 0; s0 < 8; s0 += RA) {
+  for (int s0 = 0; s0 < D / 16; s0 += RA) {
     bf16x8 kf[RA];
 #pragma unroll
     for (int s = 0; s < RA; ++s)
@@ -523,8 +557,10 @@ __device__ __forceinline__ void qk_part(const uint16_t *kblk, const Frag &fo,
 }
 
 // V^T fragments f0 .. f0 + RA - 1 of a chunk, f = (db, t).
-__device__ __forceinline__ void v_read(const uint16_t *vblk, const Frag &fo,
-                                       int f0, bf16x8 *vf) {
+template <int D>
+__device__ __forceinline__ void v_read(const uint16_t *vblk,
+                                       const Frag<D> &fo, int f0,
+                                       bf16x8 *vf) {
 #pragma unroll
   for (int f = f0; f < f0 + RA; ++f)
     vf[f - f0] = *reinterpret_cast<const bf16x8 *>(
@@ -537,8 +573,8 @@ __device__ __forceinline__ void v_read(const uint16_t *vblk, const Frag &fo,
 // <= lim[qb] (a per-row limit, < 0 hides every key of the chunk).
 // SMX 0: weights exp2(S); 1: exp2(S - m), m fixed at the first visible
 // chunk to min(B, max + 80); 2: exact running maximum.
-template <int MODE, int NQB, int SMX>
-__device__ __forceinline__ void softmax_part(floatx16 *S, Acc *acc, int hf,
+template <int MODE, int NQB, int SMX, int D>
+__device__ __forceinline__ void softmax_part(floatx16 *S, Acc<D> *acc, int hf,
                                              float B, const int *lim,
                                              bf16x8 (*pb)[2]) {
 #pragma unroll
@@ -548,7 +584,7 @@ __device__ __forceinline__ void softmax_part(floatx16 *S, Acc *acc, int hf,
       for (int i = 0; i < 16; ++i)
         S[qb][i] = 16 * hf + i <= lim[qb] ? S[qb][i] : -INFINITY;
     }
-    Acc &A = acc[qb];
+    Acc<D> &A = acc[qb];
     if (SMX == 2) {
       float mx = -INFINITY;
 #pragma unroll
@@ -561,7 +597,7 @@ __device__ __forceinline__ void softmax_part(floatx16 *S, Acc *acc, int hf,
       A.m = mnew;
       if (__any(need)) {
 #pragma unroll
-        for (int db = 0; db < 4; ++db)
+        for (int db = 0; db < D / 32; ++db)
 #pragma unroll
           for (int i = 0; i < 16; ++i) A.o[db][i] *= alpha;
       }
@@ -604,12 +640,12 @@ __device__ __forceinline__ void softmax_part(floatx16 *S, Acc *acc, int hf,
 }
 
 // O^T += V^T P^T for one chunk; vf holds the first RA V^T fragments.
-template <int NQB>
-__device__ __forceinline__ void pv_part(const uint16_t *vblk, const Frag &fo,
-                                        bf16x8 *vf, Acc *acc,
-                                        const bf16x8 (*pb)[2]) {
+template <int NQB, int D>
+__device__ __forceinline__ void pv_part(const uint16_t *vblk,
+                                        const Frag<D> &fo, bf16x8 *vf,
+                                        Acc<D> *acc, const bf16x8 (*pb)[2]) {
 #pragma unroll
-  for (int f0 = 0; f0 < 8; f0 += RA) {
+  for (int f0 = 0; f0 < D / 16; f0 += RA) {
     if (f0 > 0) v_read(vblk, fo, f0, vf);
 #pragma unroll
     for (int f = f0; f < f0 + RA; ++f)
@@ -622,32 +658,34 @@ __device__ __forceinline__ void pv_part(const uint16_t *vblk, const Frag &fo,
 
 // One 32-key chunk for NQB query blocks: S^T = K Q^T, weights, O^T += V^T P^T
 // (the first V^T fragments are read before the weights are formed).
-template <int MODE, int NQB, int SMX>
+template <int MODE, int NQB, int SMX, int D>
 __device__ __forceinline__ void attend(const uint16_t *kblk,
-                                       const uint16_t *vblk, const Frag &fo,
-                                       const bf16x8 (*qf)[8], Acc *acc,
-                                       int hf, float B, const int *lim) {
+                                       const uint16_t *vblk,
+                                       const Frag<D> &fo,
+                                       const bf16x8 (*qf)[D / 16],
+                                       Acc<D> *acc, int hf, float B,
+                                       const int *lim) {
   floatx16 S[NQB];
-  qk_part<NQB>(kblk, fo, qf, S);
+  qk_part<NQB, D>(kblk, fo, qf, S);
   bf16x8 vf[RA];
-  v_read(vblk, fo, 0, vf);
+  v_read<D>(vblk, fo, 0, vf);
   bf16x8 pb[NQB][2];
-  softmax_part<MODE, NQB, SMX>(S, acc, hf, B, lim, pb);
-  pv_part<NQB>(vblk, fo, vf, acc, pb);
+  softmax_part<MODE, NQB, SMX, D>(S, acc, hf, B, lim, pb);
+  pv_part<NQB, D>(vblk, fo, vf, acc, pb);
 }
 
 // The passes of one work unit (an item for one kv head) with softmax mode
 // SMX fixed, so every loop below is straight-line code over one set of
 // accumulators.  Returns whether some row of this wave left the range the
 // fast modes guarantee (the unit is then recomputed in SAFE mode).
-template <int WAVES, int NQB, int SMX, bool SCORE, int NCHK>
-__device__ __forceinline__ bool run_unit(const AttnParams &P, Smem<NCHK> &sm,
-                                         const Frag &fo, int g, int row0,
-                                         int row1, int L, int Lp,
-                                         const uint16_t *Kp,
+template <int WAVES, int NQB, int SMX, bool SCORE, int D, int NCHK>
+__device__ __forceinline__ bool run_unit(const AttnParams &P,
+                                         Smem<D, NCHK> &sm, const Frag<D> &fo,
+                                         int g, int row0, int row1, int L,
+                                         int Lp, const uint16_t *Kp,
                                          const uint16_t *VTp, float B) {
   constexpr int PASS = WAVES * NQB * 32;
-  constexpr int PSEG = Smem<NCHK>::PSEG;
+  constexpr int PSEG = Smem<D, NCHK>::PSEG;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int lq = lane & 31, hf = lane >> 5;
   const int n_seg = (L + PSEG - 1) / PSEG;
@@ -667,8 +705,8 @@ __device__ __forceinline__ bool run_unit(const AttnParams &P, Smem<NCHK> &sm,
     // Rows of this lane: batch token, position in the pair, q head.
     int tokq[NQB], head[NQB];
     bool valid[NQB];
-    bf16x8 qf[NQB][8];
-    Acc acc[NQB];
+    bf16x8 qf[NQB][D / 16];
+    Acc<D> acc[NQB];
     // a wave whose rows all lie past the item's end (the tail pass of an
     // item) computes nothing; it still stages and meets the barriers
     const bool live = pass0 + wave * NQB * 32 < row1;
@@ -682,13 +720,13 @@ __device__ __forceinline__ bool run_unit(const AttnParams &P, Smem<NCHK> &sm,
       tokq[qb] = tj.x;
       head[qb] = g * P.n_rep + (rc - u * P.n_rep);
       if (live)
-        q_fragments(P.q + ((int64_t)tokq[qb] * P.Hq + head[qb]) * D, P.qw,
-                    P.rope + (int64_t)(L + tj.y) * kRopeHalf, hf, P.eps,
-                    P.c, P.norm != 0, qf[qb]);
+        q_fragments<D>(P.q + ((int64_t)tokq[qb] * P.Hq + head[qb]) * D,
+                       P.qw, P.rope + (int64_t)(L + tj.y) * (D / 2), hf,
+                       P.eps, P.c, P.norm != 0, qf[qb]);
       acc[qb].m = SMX == 2 ? -INFINITY : (SMX == 1 ? INFINITY : 0.f);
       acc[qb].l = 0.f;
 #pragma unroll
-      for (int db = 0; db < 4; ++db)
+      for (int db = 0; db < D / 32; ++db)
 #pragma unroll
         for (int i = 0; i < 16; ++i) acc[qb].o[db][i] = 0.f;
     }
@@ -709,7 +747,7 @@ __device__ __forceinline__ bool run_unit(const AttnParams &P, Smem<NCHK> &sm,
       os.T = sp.y;
       os.srow0 = sp.z;
     }
-    OwnRegs<WAVES> orr;
+    OwnRegs orr;
 
     // Document prefix: every row sees all L slots.
     for (int sg = 0; sg < n_seg; ++sg) {
@@ -717,20 +755,20 @@ __device__ __forceinline__ bool run_unit(const AttnParams &P, Smem<NCHK> &sm,
       const int n = L - seg0 < PSEG ? L - seg0 : PSEG;
       if (!resident) {
         __syncthreads();
-        stage_prefix<WAVES, NCHK>(Kp, VTp, Lp, seg0, n, sm);
+        stage_prefix<WAVES, D, NCHK>(Kp, VTp, Lp, seg0, n, sm);
       }
       wait_vmem();
       __syncthreads();
       const int n_full = live ? n >> 5 : 0;
       for (int ck = 0; ck < n_full; ++ck)
-        attend<0, NQB, SMX>(sm.pk[ck], sm.pv[ck], fo, qf, acc, hf, B,
-                            nullptr);
+        attend<0, NQB, SMX, D>(sm.pk[ck], sm.pv[ck], fo, qf, acc, hf, B,
+                               nullptr);
       if (live && (n & 31)) {
         int lim[NQB];
 #pragma unroll
         for (int qb = 0; qb < NQB; ++qb) lim[qb] = (n & 31) - 1;
-        attend<1, NQB, SMX>(sm.pk[n_full], sm.pv[n_full], fo, qf, acc, hf,
-                            B, lim);
+        attend<1, NQB, SMX, D>(sm.pk[n_full], sm.pv[n_full], fo, qf, acc,
+                               hf, B, lim);
       }
     }
 
@@ -739,9 +777,9 @@ __device__ __forceinline__ bool run_unit(const AttnParams &P, Smem<NCHK> &sm,
     // then normed/rotated into the other buffer; one barrier per chunk.
     // (The first chunk is loaded only here: its registers are not held
     // through the prefix products.)
-    own_load<WAVES>(P, os, g, L, orr);
+    own_load<WAVES, D>(P, os, g, L, orr);
     __syncthreads();  // the previous pass's last own chunk is consumed
-    own_stage<WAVES, NCHK>(P, orr, sm, 0);
+    own_stage<WAVES, D, NCHK>(P, orr, sm, 0);
     __syncthreads();
     int buf = 0;
     while (os.s <= s_hi) {
@@ -765,7 +803,7 @@ __device__ __forceinline__ bool run_unit(const AttnParams &P, Smem<NCHK> &sm,
         }
       }
       const bool more = nx.s <= s_hi;
-      if (more) own_load<WAVES>(P, nx, g, L, orr);
+      if (more) own_load<WAVES, D>(P, nx, g, L, orr);
       // per row: last visible key of this chunk (same pair, key <= row)
       int lim[NQB];
       bool need = false;
@@ -776,9 +814,9 @@ __device__ __forceinline__ bool run_unit(const AttnParams &P, Smem<NCHK> &sm,
         need = need || (valid[qb] && lim[qb] >= 0);
       }
       if (__any(need))  // wave-uniform: skip chunks no row of the wave sees
-        attend<1, NQB, SMX>(sm.ok[buf], sm.ov[buf], fo, qf, acc, hf, B,
-                            lim);
-      if (more) own_stage<WAVES, NCHK>(P, orr, sm, buf ^ 1);
+        attend<1, NQB, SMX, D>(sm.ok[buf], sm.ov[buf], fo, qf, acc, hf, B,
+                               lim);
+      if (more) own_stage<WAVES, D, NCHK>(P, orr, sm, buf ^ 1);
       __syncthreads();
       buf ^= 1;
       os = nx;
@@ -801,7 +839,7 @@ __device__ __forceinline__ bool run_unit(const AttnParams &P, Smem<NCHK> &sm,
       uint16_t *op = P.out + orow * D;
       float ss = 0.f, sy = 0.f, sn = 0.f;
 #pragma unroll
-      for (int db = 0; db < 4; ++db) {
+      for (int db = 0; db < D / 32; ++db) {
         float o[16];
 #pragma unroll
         for (int i = 0; i < 16; ++i) o[i] = acc[qb].o[db][i] * inv;
@@ -859,15 +897,15 @@ __device__ __forceinline__ bool run_unit(const AttnParams &P, Smem<NCHK> &sm,
 
 // Waves per SIMD: a block's waves spread over the CU's 4 SIMDs, and two
 // blocks share a CU when the LDS block fits in half of it (160 KB).
-constexpr int waves_per_simd(int waves, int nchk) {
-  return (waves / 4) * ((nchk + 2) * 2 * KC * D * 2 <= 81920 ? 2 : 1);
+constexpr int waves_per_simd(int waves, int d, int nchk) {
+  return (waves / 4) * ((nchk + 2) * 2 * KC * d * 2 <= 81920 ? 2 : 1);
 }
 
-template <int WAVES, int NQB, bool SAFE, bool SCORE, int NCHK>
+template <int WAVES, int NQB, bool SAFE, bool SCORE, int D, int NCHK>
 __global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(
-    waves_per_simd(WAVES, NCHK),
-    waves_per_simd(WAVES, NCHK)))) void k_prefix_attn(AttnParams P) {
-  __shared__ __attribute__((aligned(16))) Smem<NCHK> sm;
+    waves_per_simd(WAVES, D, NCHK),
+    waves_per_simd(WAVES, D, NCHK)))) void k_prefix_attn(AttnParams P) {
+  __shared__ __attribute__((aligned(16))) Smem<D, NCHK> sm;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int lq = lane & 31, hf = lane >> 5;
   const int queue = SAFE ? kFixQueue : (blockIdx.x & 7);
@@ -879,7 +917,7 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(
     if (n_items > P.items_cap) n_items = P.items_cap;
     n_work = n_items * P.Hkv;
   }
-  const Frag fo = frag_offsets(lq, hf);
+  const Frag<D> fo = frag_offsets<D>(lq, hf);
 
   for (;;) {
     if (threadIdx.x == 0) sm.words()[0] = atomicAdd(&P.next[queue], 1);
@@ -900,8 +938,9 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(
     const int doc = P.group_doc[it.x];
     const int L = P.doc_len[doc], Lp = pad8(L);
     const int64_t blk = P.doc_off[doc];
-    const uint16_t *Kp = P.payload + k_offset(blk, L, P.Hkv, P.layer, g);
-    const uint16_t *VTp = P.payload + vt_offset(blk, L, P.Hkv, P.layer, g);
+    const uint16_t *Kp = P.payload + k_offset(blk, L, P.Hkv, P.layer, g, D);
+    const uint16_t *VTp =
+        P.payload + vt_offset(blk, L, P.Hkv, P.layer, g, D);
     // every logit of this unit lies in [-B, B] (log2 units).  Without
     // QK-norm no bound is known (kown = 0, so B = 0): the unit runs the
     // no-reference mode anyway, and a row whose normaliser leaves the range
@@ -910,13 +949,14 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(
     const float kbound = fmaxf(
         P.kown[0], P.kmax[((int64_t)doc * P.n_layers + P.layer) * P.Hkv + g]);
     const float B = P.c * P.kown[1] * kbound * 1.001f;
-    const int n_seg = (L + Smem<NCHK>::PSEG - 1) / Smem<NCHK>::PSEG;
+    const int n_seg = (L + Smem<D, NCHK>::PSEG - 1) / Smem<D, NCHK>::PSEG;
     const bool resident = n_seg <= 1;
     if (!SAFE) {
       if (B <= kNoRefBound) {
-        if (resident && L > 0) stage_prefix<WAVES, NCHK>(Kp, VTp, Lp, 0, L, sm);
-        wave_bad = run_unit<WAVES, NQB, 0, SCORE, NCHK>(P, sm, fo, g, row0, row1, L, Lp,
-                                           Kp, VTp, B) ||
+        if (resident && L > 0)
+          stage_prefix<WAVES, D, NCHK>(Kp, VTp, Lp, 0, L, sm);
+        wave_bad = run_unit<WAVES, NQB, 0, SCORE, D, NCHK>(
+                       P, sm, fo, g, row0, row1, L, Lp, Kp, VTp, B) ||
                    P.flag_all;
       }
       __syncthreads();  // every wave is done with this item's LDS
@@ -932,12 +972,13 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(
       }
       __syncthreads();
     } else {
-      if (resident && L > 0) stage_prefix<WAVES, NCHK>(Kp, VTp, Lp, 0, L, sm);
+      if (resident && L > 0)
+        stage_prefix<WAVES, D, NCHK>(Kp, VTp, Lp, 0, L, sm);
       // (self-check mode sends every unit to the exact mode)
       bool exact = !unscored || P.flag_all;
       if (!exact) {
-        wave_bad = run_unit<WAVES, NQB, 1, SCORE, NCHK>(P, sm, fo, g, row0, row1, L, Lp,
-                                           Kp, VTp, B);
+        wave_bad = run_unit<WAVES, NQB, 1, SCORE, D, NCHK>(
+            P, sm, fo, g, row0, row1, L, Lp, Kp, VTp, B);
         __syncthreads();
         if (lane == 0) sm.words()[1 + wave] = wave_bad;
         __syncthreads();
@@ -945,7 +986,8 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(
         __syncthreads();
       }
       if (exact)
-        run_unit<WAVES, NQB, 2, SCORE, NCHK>(P, sm, fo, g, row0, row1, L, Lp, Kp, VTp, B);
+        run_unit<WAVES, NQB, 2, SCORE, D, NCHK>(P, sm, fo, g, row0, row1, L,
+                                                Lp, Kp, VTp, B);
       __syncthreads();  // every wave is done with this item's LDS
     }
   }
@@ -956,7 +998,7 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(
 // token ranges (score mode) pair p owns row p; out may then be NULL.
 __global__ __launch_bounds__(256) void k_zero_invalid(
     const int32_t *counters, const int32_t *invalid, const int32_t *cu,
-    int32_t Hq, uint16_t *out, float *lse) {
+    int32_t Hq, int32_t D, uint16_t *out, float *lse) {
   const int32_t n_inv = counters[kCntInvalid];
   for (int32_t idx = blockIdx.x; idx < n_inv; idx += gridDim.x) {
     const int32_t p = invalid[idx];
@@ -987,7 +1029,8 @@ __global__ __launch_bounds__(256) void k_queue_all(const int64_t *totals,
   if (blockIdx.x == 0 && threadIdx.x == 0) counters[kCntFix] = (int32_t)n;
 }
 
-template <int WAVES, int NQB, bool SAFE, bool SCORE, int NCHK = 8>
+template <int WAVES, int NQB, bool SAFE, bool SCORE, int D,
+          int NCHK = big_chunks(D)>
 hipError_t launch_variant(const AttnParams &p, hipStream_t s, int max_grid) {
   int dev = 0, n_cu = 0, per_cu = 0;
   hipError_t e = hipGetDevice(&dev);
@@ -995,7 +1038,8 @@ hipError_t launch_variant(const AttnParams &p, hipStream_t s, int max_grid) {
   e = hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev);
   if (e != hipSuccess) return e;
   e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
-      &per_cu, k_prefix_attn<WAVES, NQB, SAFE, SCORE, NCHK>, WAVES * 64, 0);
+      &per_cu, k_prefix_attn<WAVES, NQB, SAFE, SCORE, D, NCHK>, WAVES * 64,
+      0);
   if (e != hipSuccess) return e;
   if (per_cu < 1) per_cu = 1;
   // Persistent grid, a multiple of 8 so block b always serves queue b % 8
@@ -1003,9 +1047,40 @@ hipError_t launch_variant(const AttnParams &p, hipStream_t s, int max_grid) {
   unsigned grid = (unsigned)(n_cu * per_cu);
   grid = (grid + 7) / 8 * 8;
   if (max_grid > 0 && grid > (unsigned)max_grid) grid = (unsigned)max_grid;
-  hipLaunchKernelGGL((k_prefix_attn<WAVES, NQB, SAFE, SCORE, NCHK>), dim3(grid),
-                     dim3(WAVES * 64), 0, s, p);
+  hipLaunchKernelGGL((k_prefix_attn<WAVES, NQB, SAFE, SCORE, D, NCHK>),
+                     dim3(grid), dim3(WAVES * 64), 0, s, p);
   return hipGetLastError();
+}
+
+// The fast pass in tile shape shape_v (1, 2, 3, 6; 4 queues every unit
+// for the exact pass instead), then the exact pass over the queued units.
+template <int D>
+hipError_t launch_passes(const AttnParams &p, int shape_v, bool score,
+                         hipStream_t s) {
+  hipError_t e;
+  switch (shape_v) {
+    case 1: e = launch_variant<4, 2, false, false, D>(p, s, 0); break;
+    case 3: e = launch_variant<4, 1, false, false, D>(p, s, 0); break;
+    case 6:
+      e = score ? launch_variant<4, 1, false, true, D, small_chunks(D)>(p, s, 0)
+                : launch_variant<4, 1, false, false, D, small_chunks(D)>(p, s,
+                                                                         0);
+      break;
+    case 4:
+      hipLaunchKernelGGL(k_queue_all, dim3(256), dim3(256), 0, s, p.totals,
+                         p.items_cap, p.Hkv, p.counters, p.fix);
+      e = hipGetLastError();
+      break;
+    default:  // 2
+      e = score ? launch_variant<8, 1, false, true, D>(p, s, 0)
+                : launch_variant<8, 1, false, false, D>(p, s, 0);
+      break;
+  }
+  if (e != hipSuccess) return e;
+  // Work units the fast pass flagged or left unscored (normally none) are
+  // computed here; in exact mode that is every unit.
+  return score ? launch_variant<4, 1, true, true, D>(p, s, 0)
+               : launch_variant<4, 1, true, false, D>(p, s, 0);
 }
 
 }  // namespace
@@ -1060,36 +1135,18 @@ hipError_t launch_attention(const AttnCall &c, const Plan &pl,
     p.head_norm_w = static_cast<const uint16_t *>(c.head->norm_w);
     p.head_w = static_cast<const uint16_t *>(c.head->w_head);
   }
-  // Tile shape.  Automatic: two 4-wave blocks per CU (80 KB of LDS each,
-  // 96 prefix slots resident) when every prefix fits or when only score
-  // rows are attended (one pass per unit, so nothing is restaged); else one
-  // 8-wave block per CU with 256 slots resident.
+  // Tile shape.  Automatic: two 4-wave blocks per CU (half the LDS each:
+  // 96 prefix slots resident at D = 128, 192 at D = 64) when every prefix
+  // fits or when only score rows are attended (one pass per unit, so
+  // nothing is restaged); else one 8-wave block per CU with 256 (512) slots
+  // resident.
+  const int D = st.head_dim;
   int shape_v = a->kernel_variant;
   if (shape_v == 0 || shape_v == 5)
-    shape_v = score || st.max_len <= kSmallPrefix ? 6 : 2;
+    shape_v = score || st.max_len <= small_chunks(D) * KC ? 6 : 2;
   if (score && (shape_v == 1 || shape_v == 3)) shape_v = 6;
-  switch (shape_v) {
-    case 1: e = launch_variant<4, 2, false, false>(p, s, 0); break;
-    case 3: e = launch_variant<4, 1, false, false>(p, s, 0); break;
-    case 6:
-      e = score ? launch_variant<4, 1, false, true, 3>(p, s, 0)
-                : launch_variant<4, 1, false, false, 3>(p, s, 0);
-      break;
-    case 4:
-      hipLaunchKernelGGL(k_queue_all, dim3(256), dim3(256), 0, s, p.totals,
-                         p.items_cap, p.Hkv, p.counters, p.fix);
-      e = hipGetLastError();
-      break;
-    default:  // 2
-      e = score ? launch_variant<8, 1, false, true>(p, s, 0)
-                : launch_variant<8, 1, false, false>(p, s, 0);
-      break;
-  }
-  if (e != hipSuccess) return e;
-  // Work units the fast pass flagged or left unscored (normally none) are
-  // computed here; in exact mode that is every unit.
-  e = score ? launch_variant<4, 1, true, true>(p, s, 0)
-            : launch_variant<4, 1, true, false>(p, s, 0);
+  e = D == 128 ? launch_passes<128>(p, shape_v, score, s)
+               : launch_passes<64>(p, shape_v, score, s);
   if (e != hipSuccess) return e;
   if (a->timing_end) {
     e = hipEventRecord(static_cast<hipEvent_t>(a->timing_end), s);
@@ -1099,11 +1156,12 @@ hipError_t launch_attention(const AttnCall &c, const Plan &pl,
       (unsigned)(a->n_pairs < 1024 ? (a->n_pairs > 0 ? a->n_pairs : 1) : 1024);
   hipLaunchKernelGGL(k_zero_invalid, dim3(zgrid), dim3(256), 0, s,
                      pl.counters, pl.invalid, score ? nullptr : a->cu_seqlens,
-                     a->n_q_heads, p.out, a->lse);
+                     a->n_q_heads, D, p.out, a->lse);
   if (score) {
     e = hipGetLastError();
     if (e != hipSuccess) return e;
-    return launch_score_reduce(pl, a->n_pairs, a->n_q_heads, c.head, s);
+    return launch_score_reduce(pl, a->n_pairs, a->n_q_heads,
+                               a->n_q_heads * D, c.head, s);
   }
   (void)shape;
   return hipGetLastError();

@@ -302,7 +302,8 @@ __global__ __launch_bounds__(kThreads) void k_token_table(Plan pl, PlanArgs a,
 // gain scales it by at most max|w|, rotation keeps it, and bf16 rounding
 // adds at most 2^-8.  bound[0] is for keys (w_k), bound[1] for queries.
 // Without QK-norm (no gains) no bound is known: both are written as 0 and
-// unit_w gets the unit gains the attention kernel multiplies by.
+// unit_w gets the unit gains the attention kernel multiplies by.  One
+// thread per head dim (blockDim.x = D, 64 or 128).
 __global__ __launch_bounds__(128) void k_norm_bound(const uint16_t *kw,
                                                     const uint16_t *qw,
                                                     float *bound,
@@ -322,23 +323,28 @@ __global__ __launch_bounds__(128) void k_norm_bound(const uint16_t *kw,
     red[1][threadIdx.x >> 6] = b;
   }
   __syncthreads();
-  if (threadIdx.x < 2)
-    bound[threadIdx.x] = fmaxf(red[threadIdx.x][0], red[threadIdx.x][1]) *
-                         sqrtf((float)kHeadDim) * 1.01f;
+  if (threadIdx.x < 2) {
+    const float m = blockDim.x > 64
+                        ? fmaxf(red[threadIdx.x][0], red[threadIdx.x][1])
+                        : red[threadIdx.x][0];
+    bound[threadIdx.x] = m * sqrtf((float)blockDim.x) * 1.01f;
+  }
 }
 
-// Step 6: rotary table, (cos, sin)(pos * omega_i) in double, stored as
-// float; omega_i = theta^(-2i/D), or the caller's inv_freq[i].
+// Step 6: rotary table, (cos, sin)(pos * omega_i) for i < half = D/2, in
+// double, stored as float; omega_i = theta^(-2i/D), or the caller's
+// inv_freq[i].
 __global__ __launch_bounds__(kThreads) void k_rope_table(float2 *tab,
                                                          int32_t n_pos,
+                                                         int32_t half,
                                                          double log_theta,
                                                          const float *inv_freq) {
   const int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-  if (e >= (int64_t)n_pos * kRopeHalf) return;
-  const int32_t pos = (int32_t)(e / kRopeHalf), i = (int32_t)(e % kRopeHalf);
+  if (e >= (int64_t)n_pos * half) return;
+  const int32_t pos = (int32_t)(e / half), i = (int32_t)(e % half);
   const double freq =
       inv_freq ? (double)inv_freq[i]
-               : exp(-2.0 * (double)i / (double)kHeadDim * log_theta);
+               : exp(-(double)i / (double)half * log_theta);
   double sn, cs;
   sincos((double)pos * freq, &sn, &cs);
   tab[e] = make_float2((float)cs, (float)sn);
@@ -394,7 +400,7 @@ Plan carve(void *ws, const PlanShape &s, size_t *bytes) {
   pl.kown = c.take<float>(2);
   pl.unit_w = c.take<uint16_t>(kHeadDim);
   pl.rope_pos = s.max_len + s.max_tokens;
-  pl.rope = c.take<float2>((int64_t)pl.rope_pos * kRopeHalf);
+  pl.rope = c.take<float2>((int64_t)pl.rope_pos * (s.head_dim / 2));
   *bytes = c.off;
   return pl;
 }
@@ -456,16 +462,17 @@ hipError_t launch_plan(const AttnCall &c, const Plan &pl,
   if (a->cu_seqlens)
     hipLaunchKernelGGL(k_token_table, dim3((unsigned)(P + 1)),
                        dim3(kThreads), 0, s, pl, pa, totals);
-  hipLaunchKernelGGL(k_norm_bound, dim3(1), dim3(kHeadDim), 0, s,
+  const int32_t D = c.st->head_dim;
+  hipLaunchKernelGGL(k_norm_bound, dim3(1), dim3(D), 0, s,
                      static_cast<const uint16_t *>(a->k_norm_w),
                      static_cast<const uint16_t *>(a->q_norm_w), pl.kown,
                      pl.unit_w);
   const double log_theta = std::log((double)a->rope_theta);
   hipLaunchKernelGGL(k_rope_table,
-                     dim3(blocks_for((int64_t)pl.rope_pos * kRopeHalf,
+                     dim3(blocks_for((int64_t)pl.rope_pos * (D / 2),
                                      kThreads)),
-                     dim3(kThreads), 0, s, pl.rope, pl.rope_pos, log_theta,
-                     a->rope_inv_freq);
+                     dim3(kThreads), 0, s, pl.rope, pl.rope_pos, D / 2,
+                     log_theta, a->rope_inv_freq);
   return hipGetLastError();
 }
 

@@ -11,9 +11,10 @@
 
 namespace dopr {
 
+// Head sizes: 128 (Qwen3, Llama 3) and 64 (Llama 3.2 1B).  Everything sized
+// for the largest uses kHeadDim; per-call code takes the store's head_dim.
 constexpr int kHeadDim = 128;
 constexpr int kAlign = 256;
-constexpr int kRopeHalf = kHeadDim / 2;
 
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 __host__ __device__ inline int32_t pad8(int32_t n) { return (n + 7) & ~7; }
@@ -39,21 +40,23 @@ struct StoreView {
   float *kmax;             // [n_docs][n_layers][Hkv] key-norm bound
   uint16_t *payload;
   int64_t n_docs;
-  int32_t n_layers, n_kv_heads;
+  int32_t n_layers, n_kv_heads, head_dim;
 };
 
-__host__ __device__ inline int64_t layer_block_elems(int32_t L, int32_t hkv) {
-  return (int64_t)hkv * kHeadDim * ((int64_t)L + pad8(L));
+__host__ __device__ inline int64_t layer_block_elems(int32_t L, int32_t hkv,
+                                                     int32_t D) {
+  return (int64_t)hkv * D * ((int64_t)L + pad8(L));
 }
 __host__ __device__ inline int64_t k_offset(int64_t blk, int32_t L, int32_t hkv,
-                                            int32_t layer, int32_t g) {
-  return blk + layer * layer_block_elems(L, hkv) + (int64_t)g * L * kHeadDim;
+                                            int32_t layer, int32_t g,
+                                            int32_t D) {
+  return blk + layer * layer_block_elems(L, hkv, D) + (int64_t)g * L * D;
 }
 __host__ __device__ inline int64_t vt_offset(int64_t blk, int32_t L,
                                              int32_t hkv, int32_t layer,
-                                             int32_t g) {
-  return blk + layer * layer_block_elems(L, hkv) +
-         (int64_t)hkv * L * kHeadDim + (int64_t)g * kHeadDim * pad8(L);
+                                             int32_t g, int32_t D) {
+  return blk + layer * layer_block_elems(L, hkv, D) + (int64_t)hkv * L * D +
+         (int64_t)g * D * pad8(L);
 }
 
 }  // namespace dopr
@@ -71,7 +74,8 @@ struct dopr_store {
   int32_t max_len;  // largest L over resident documents
   int device;
   dopr::StoreView view() const {
-    return {d_len, d_off, d_kmax, d_payload, n_docs, n_layers, n_kv_heads};
+    return {d_len, d_off, d_kmax, d_payload, n_docs, n_layers, n_kv_heads,
+            head_dim};
   }
 };
 
@@ -112,7 +116,7 @@ struct Plan {
   float *kown;          // [2] bounds on |k^| (own keys) and |q^|: sqrt(D) max|w|
                         // (0 when there is no QK-norm: no bound is known)
   uint16_t *unit_w;     // [D] bf16 ones: the gains when there is no QK-norm
-  float2 *rope;         // [rope_pos][64] (cos, sin)
+  float2 *rope;         // [rope_pos][D/2] (cos, sin)
   int32_t items_cap;
   int32_t blk_cap;
   int32_t rope_pos;
@@ -125,6 +129,7 @@ struct PlanShape {
   int32_t n_pairs, n_rep, max_tokens, rows_per_item;
   int64_t n_docs, total_tokens;
   int32_t max_len, n_kv_heads;
+  int32_t head_dim = kHeadDim;
   bool score_only = false;
 };
 
@@ -154,8 +159,10 @@ hipError_t launch_plan(const AttnCall &c, const Plan &plan,
 hipError_t launch_attention(const AttnCall &c, const Plan &plan,
                             const PlanShape &shape, hipStream_t s);
 hipError_t launch_score(const dopr_score_args_t *a, hipStream_t s);
+// width: the score head's input width, n_q_heads * head_dim.
 hipError_t launch_score_reduce(const Plan &pl, int32_t n_pairs, int32_t n_q_heads,
-                               const dopr_score_head_t *head, hipStream_t s);
+                               int32_t width, const dopr_score_head_t *head,
+                               hipStream_t s);
 
 // ---------------------------------------------------------------------------
 // Decoder layer around the attention (layer.hip).

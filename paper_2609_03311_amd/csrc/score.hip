@@ -116,13 +116,13 @@ __global__ __launch_bounds__(kThreads) void k_score_reduce(
 }  // namespace
 
 hipError_t launch_score_reduce(const Plan &pl, int32_t n_pairs,
-                               int32_t n_q_heads,
+                               int32_t n_q_heads, int32_t width,
                                const dopr_score_head_t *head, hipStream_t s) {
   if (n_pairs == 0) return hipSuccess;
   const unsigned grid = (unsigned)((n_pairs + kThreads - 1) / kThreads);
   hipLaunchKernelGGL(k_score_reduce, dim3(grid), dim3(kThreads), 0, s,
                      pl.part, pl.pair_flag, n_pairs, n_q_heads,
-                     (float)n_q_heads * kHeadDim, head->rms_eps, head->logits,
+                     (float)width, head->rms_eps, head->logits,
                      head->score);
   return hipGetLastError();
 }

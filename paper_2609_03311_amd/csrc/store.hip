@@ -30,20 +30,21 @@ __global__ __launch_bounds__(kThreads) void k_store_put(
     return;
   }
   const int32_t L = sv.doc_len[d], Lp = pad8(L);
+  const int D = sv.head_dim, G = D / 8;  // 16-byte granules per row
   const int64_t blk = sv.doc_off[d];
-  uint16_t *K = sv.payload + k_offset(blk, L, hkv, layer, g);
-  uint16_t *VT = sv.payload + vt_offset(blk, L, hkv, layer, g);
+  uint16_t *K = sv.payload + k_offset(blk, L, hkv, layer, g, D);
+  uint16_t *VT = sv.payload + vt_offset(blk, L, hkv, layer, g, D);
 
-  // Copy K and track the largest key norm of the slice (16 lanes per row;
-  // rows are 16-lane aligned so a row's lanes run the loop together).
+  // Copy K and track the largest key norm of the slice (G lanes per row, a
+  // power of two dividing 64, so a row's lanes run the loop together).
   float norm2_max = 0.f;
-  for (int64_t gi = threadIdx.x; gi < (int64_t)L * 16; gi += kThreads) {
-    const int64_t row = gi >> 4;
-    const int c = gi & 15;
+  for (int64_t gi = threadIdx.x; gi < (int64_t)L * G; gi += kThreads) {
+    const int64_t row = gi / G;
+    const int c = gi % G;
     const uint4 *src = reinterpret_cast<const uint4 *>(
-        ksrc + ((s0 + row) * hkv + g) * kHeadDim);
+        ksrc + ((s0 + row) * hkv + g) * D);
     const uint4 u = src[c];
-    reinterpret_cast<uint4 *>(K + row * kHeadDim)[c] = u;
+    reinterpret_cast<uint4 *>(K + row * D)[c] = u;
     const uint32_t w[4] = {u.x, u.y, u.z, u.w};
     float ss = 0.f;
 #pragma unroll
@@ -53,8 +54,7 @@ __global__ __launch_bounds__(kThreads) void k_store_put(
       ss = fmaf(lo, lo, ss);
       ss = fmaf(hi, hi, ss);
     }
-#pragma unroll
-    for (int off = 1; off < 16; off <<= 1) ss += __shfl_xor(ss, off, 64);
+    for (int off = 1; off < G; off <<= 1) ss += __shfl_xor(ss, off, 64);
     norm2_max = fmaxf(norm2_max, ss);
   }
   __shared__ float red[kThreads / 64];
@@ -73,17 +73,17 @@ __global__ __launch_bounds__(kThreads) void k_store_put(
 
   __shared__ uint16_t tile[kTile][kHeadDim + 2];
   for (int t0 = 0; t0 < Lp; t0 += kTile) {
-    for (int gi = threadIdx.x; gi < kTile * 16; gi += kThreads) {
-      const int r = gi >> 4, c = gi & 15, slot = t0 + r;
+    for (int gi = threadIdx.x; gi < kTile * G; gi += kThreads) {
+      const int r = gi / G, c = gi % G, slot = t0 + r;
       uint4 val = make_uint4(0, 0, 0, 0);
       if (slot < L)
         val = reinterpret_cast<const uint4 *>(
-            vsrc + ((s0 + slot) * hkv + g) * kHeadDim)[c];
+            vsrc + ((s0 + slot) * hkv + g) * D)[c];
       uint32_t *dst = reinterpret_cast<uint32_t *>(&tile[r][c * 8]);
       dst[0] = val.x; dst[1] = val.y; dst[2] = val.z; dst[3] = val.w;
     }
     __syncthreads();
-    for (int e = threadIdx.x; e < kHeadDim * kTile; e += kThreads) {
+    for (int e = threadIdx.x; e < D * kTile; e += kThreads) {
       const int dd = e / kTile, r = e % kTile, slot = t0 + r;
       if (slot < Lp) VT[(int64_t)dd * Lp + slot] = tile[r][dd];
     }
@@ -104,19 +104,20 @@ __global__ __launch_bounds__(kThreads) void k_gather(
     return;
   }
   const int32_t L = sv.doc_len[d], Lp = pad8(L);
+  const int D = sv.head_dim, G = D / 8;
   const int64_t blk = sv.doc_off[d];
-  const uint16_t *K = sv.payload + k_offset(blk, L, hkv, layer, g);
-  const uint16_t *VT = sv.payload + vt_offset(blk, L, hkv, layer, g);
-  for (int64_t gi = threadIdx.x; gi < (int64_t)L * 16; gi += kThreads) {
-    const int64_t row = gi >> 4;
-    const int c = gi & 15;
-    reinterpret_cast<uint4 *>(kout + ((o0 + row) * hkv + g) * kHeadDim)[c] =
-        reinterpret_cast<const uint4 *>(K + row * kHeadDim)[c];
+  const uint16_t *K = sv.payload + k_offset(blk, L, hkv, layer, g, D);
+  const uint16_t *VT = sv.payload + vt_offset(blk, L, hkv, layer, g, D);
+  for (int64_t gi = threadIdx.x; gi < (int64_t)L * G; gi += kThreads) {
+    const int64_t row = gi / G;
+    const int c = gi % G;
+    reinterpret_cast<uint4 *>(kout + ((o0 + row) * hkv + g) * D)[c] =
+        reinterpret_cast<const uint4 *>(K + row * D)[c];
   }
-  for (int64_t e = threadIdx.x; e < (int64_t)L * kHeadDim; e += kThreads) {
-    const int64_t slot = e / kHeadDim;
-    const int dd = e % kHeadDim;
-    vout[((o0 + slot) * hkv + g) * kHeadDim + dd] = VT[(int64_t)dd * Lp + slot];
+  for (int64_t e = threadIdx.x; e < (int64_t)L * D; e += kThreads) {
+    const int64_t slot = e / D;
+    const int dd = e % D;
+    vout[((o0 + slot) * hkv + g) * D + dd] = VT[(int64_t)dd * Lp + slot];
   }
 }
 
@@ -138,7 +139,8 @@ __global__ __launch_bounds__(kThreads) void k_store_copy(StoreView dst,
       continue;
     }
     const int64_t n16 =
-        (int64_t)dst.n_layers * layer_block_elems(L, dst.n_kv_heads) / 8;
+        (int64_t)dst.n_layers *
+        layer_block_elems(L, dst.n_kv_heads, dst.head_dim) / 8;
     const uint4 *s = reinterpret_cast<const uint4 *>(src.payload +
                                                      src.doc_off[d]);
     uint4 *t = reinterpret_cast<uint4 *>(dst.payload + dst.doc_off[d]);

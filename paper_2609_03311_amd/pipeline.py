@@ -20,12 +20,12 @@ HEAD_DIM = 128
 def make_store(doc_len, n_kv_heads, k_src, v_src, *, n_layers=1, layer=0,
                device="cuda", stream=None):
     """Create a store for `doc_len` and fill `layer` from canonical prefix
-    states k_src/v_src [slots, Hkv, D] (bf16, device) holding the resident
-    documents' slots in ascending doc-id order."""
+    states k_src/v_src [slots, Hkv, D] (bf16, device; D = 128 or 64) holding
+    the resident documents' slots in ascending doc-id order."""
     import torch
     doc_len = np.ascontiguousarray(doc_len, np.int32)
-    store = dopr_store_create(n_layers, n_kv_heads, HEAD_DIM, doc_len,
-                              device=device, stream=stream)
+    store = dopr_store_create(n_layers, n_kv_heads, int(k_src.shape[-1]),
+                              doc_len, device=device, stream=stream)
     res = np.nonzero(doc_len >= 0)[0].astype(np.int32)
     if res.size:
         cu = np.zeros(res.size + 1, np.int64)
@@ -55,7 +55,7 @@ class OnlineStep:
             kernel_variant=kernel_variant)
         self.workspace = torch.empty(max(nbytes, 256), dtype=torch.uint8,
                                      device=device)
-        self.out = torch.empty((total_tokens, n_q_heads, HEAD_DIM),
+        self.out = torch.empty((total_tokens, n_q_heads, store.head_dim),
                                dtype=torch.bfloat16, device=device)
         self.lse = (torch.empty((total_tokens, n_q_heads), dtype=torch.float32,
                                 device=device) if with_lse else None)
@@ -74,7 +74,7 @@ class OnlineStep:
 
     def score_head(self, cu_seqlens, norm_w, w_head, stream=None,
                    rms_eps=1e-6):
-        width = self.n_q_heads * HEAD_DIM
+        width = self.n_q_heads * self.store.head_dim
         dopr_score_logits(self.out, norm_w, w_head, self.score, width=width,
                           h_row_stride=width, cu_seqlens=cu_seqlens,
                           logits=self.logits, rms_eps=rms_eps,
@@ -108,7 +108,7 @@ class ScoreStep:
             kernel_variant=kernel_variant)
         self.workspace = torch.empty(max(nbytes, 256), dtype=torch.uint8,
                                      device=device)
-        self.out = (torch.empty((n_pairs, n_q_heads, HEAD_DIM),
+        self.out = (torch.empty((n_pairs, n_q_heads, store.head_dim),
                                 dtype=torch.bfloat16, device=device)
                     if with_rows else None)
         self.lse = (torch.empty((n_pairs, n_q_heads), dtype=torch.float32,

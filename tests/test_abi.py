@@ -91,9 +91,15 @@ def test_store_bytes_closed_form():
 
 def test_host_validation_codes():
     D = _D()
-    with pytest.raises(D.DoprError) as e:
-        D.dopr_store_bytes(1, 8, 64, [4])
-    assert e.value.status == D.DOPR_ERR_UNSUPPORTED
+    for bad_d in (96, 32, 256):
+        with pytest.raises(D.DoprError) as e:
+            D.dopr_store_bytes(1, 8, bad_d, [4])
+        assert e.value.status == D.DOPR_ERR_UNSUPPORTED
+    # head size 64 (Llama 3.2 1B) is laid out like 128, at half the bytes
+    _, p64 = D.dopr_store_bytes(2, 8, 64, [4, 0, 13])
+    _, p128 = D.dopr_store_bytes(2, 8, 128, [4, 0, 13])
+    assert p64 == oracle.store_payload_bytes(2, 8, 64, np.array([4, 0, 13]))
+    assert 2 * p64 == p128
     with pytest.raises(D.DoprError) as e:
         D.dopr_store_bytes(1, 8, 128, [4, -2])
     assert e.value.status == D.DOPR_ERR_INVALID_ARG

@@ -2,9 +2,11 @@
 Llama family used for the paper's cross-family check; Appendix,
 "Generalization Across Model Families"), GPU vs the float64 oracle.
 
-Shapes are Llama-3-8B-like (32 q / 8 kv heads, head size 128, rope_theta
-5e5 with the Llama-3 rescaling of long wavelengths); the frequencies come
-from Hugging Face's Llama rotary module and reach both sides as inputs.
+Shapes are Llama-3-8B-like (32 q / 8 kv heads, head size 128) and
+Llama-3.2-1B-like (the same heads at head size 64, the model the paper
+checks), rope_theta 5e5 with the Llama-3 rescaling of long wavelengths; the
+frequencies come from Hugging Face's Llama rotary module and reach both
+sides as inputs.
 Without QK-norm no logit bound is known in advance, so every work unit runs
 the reference-free softmax and rows it cannot serve are recomputed by the
 exact pass: the large-query case checks that hand-off against exact mode.
@@ -23,27 +25,29 @@ from oracle_pins import llama_config
 pytestmark = pytest.mark.gpu
 
 TOL = 2e-2
-D = 128
+HEAD_SIZES = [128, 64]
 
 
-def _inv_freq(hq, hkv):
+def _inv_freq(hq, hkv, d):
     from transformers.models.llama.modeling_llama import LlamaRotaryEmbedding
-    return LlamaRotaryEmbedding(llama_config(hq, hkv, D)).inv_freq.float()
+    return LlamaRotaryEmbedding(llama_config(hq, hkv, d)).inv_freq.float()
 
 
 def _case(name, doc_len, doc_ids, seqlens, hq=32, hkv=8, q_scale=1.0,
-          seed=0):
+          seed=0, d=128):
     import torch
     from paper_2609_03311_amd import pipeline
-    st = workloads.custom(doc_len, doc_ids, seqlens, hq, hkv, name=name)
-    log(f"setup {name}: P={st.n_pairs} Ntok={st.n_tokens} q_scale={q_scale}")
+    st = workloads.custom(doc_len, doc_ids, seqlens, hq, hkv, name=name,
+                          head_dim=d)
+    log(f"setup {name}: D={d} P={st.n_pairs} Ntok={st.n_tokens} "
+        f"q_scale={q_scale}")
     k_src, v_src, doc_off, _ = workloads.prefix_source(st, "cuda",
                                                        seed * 100 + 1)
     on = workloads.online_inputs(st, "cuda", seed * 100 + 3)
     if q_scale != 1.0:
         on["q"] = (on["q"].float() * q_scale).to(torch.bfloat16)
     store = pipeline.make_store(st.doc_len, hkv, k_src, v_src)
-    inv = _inv_freq(hq, hkv)
+    inv = _inv_freq(hq, hkv, d)
     return dict(st=st, k_src=k_src, v_src=v_src, doc_off=doc_off, on=on,
                 store=store, inv=inv, inv_dev=inv.cuda(),
                 doc_ids=torch.from_numpy(st.doc_ids).cuda(),
@@ -87,16 +91,17 @@ CASES = [
 ]
 
 
+@pytest.mark.parametrize("d", HEAD_SIZES)
 @pytest.mark.parametrize("name,doc_len,doc_ids,seqlens", CASES,
                          ids=[c[0] for c in CASES])
-def test_no_qk_norm_parity(name, doc_len, doc_ids, seqlens):
-    c = _case(name, doc_len, doc_ids, seqlens)
+def test_no_qk_norm_parity(name, doc_len, doc_ids, seqlens, d):
+    c = _case(name, doc_len, doc_ids, seqlens, d=d)
     out, lse = _gpu(c)
     ref, ref_lse, status = _oracle(c)
     assert (status == 0).all()
     e = float(np.abs(out - ref).max())
     el = float(np.abs(lse - ref_lse).max())
-    log(f"{name}: max|dO|={e:.3e} max|dlse|={el:.3e}")
+    log(f"{name} D={d}: max|dO|={e:.3e} max|dlse|={el:.3e}")
     assert e <= TOL and el <= TOL
     # the frequencies matter: with theta^(-2i/D) the outputs move by more
     # than the tolerance (the Llama-3 rescaling only touches the long
@@ -112,11 +117,12 @@ def test_no_qk_norm_parity(name, doc_len, doc_ids, seqlens):
     assert float(np.abs(plain - ref).max()) > 2 * TOL
 
 
-def test_no_qk_norm_score_rows():
+@pytest.mark.parametrize("d", HEAD_SIZES)
+def test_no_qk_norm_score_rows(d):
     """Last-layer scoring without QK-norm: the score-token rows."""
     import torch
     from paper_2609_03311_amd import dopr_check_status, pipeline
-    c = _case("llama_score", *CASES[0][1:])
+    c = _case("llama_score", *CASES[0][1:], d=d)
     st = c["st"]
     prm = workloads.params(st, "cuda", 6)
     ss = pipeline.ScoreStep(c["store"], n_pairs=st.n_pairs,
@@ -135,11 +141,12 @@ def test_no_qk_norm_score_rows():
                         refs.torch_bf16_to_bits(prm["norm_w"]),
                         refs.torch_bf16_to_bits(prm["w_head"]))
     es = float(np.abs(ss.score.cpu().numpy() - s).max())
-    log(f"llama score rows: max|dO|={e:.3e} max|ds|={es:.3e}")
+    log(f"llama score rows D={d}: max|dO|={e:.3e} max|ds|={es:.3e}")
     assert (status == 0).all() and e <= TOL and es <= TOL
 
 
-def test_no_qk_norm_large_queries_take_exact_pass():
+@pytest.mark.parametrize("d", HEAD_SIZES)
+def test_no_qk_norm_large_queries_take_exact_pass(d):
     """Queries scaled x40 push the largest logits of many rows past what the
     reference-free mode represents (2^|logit| overflows): those units must be
     recomputed by the exact pass.  With |q| ~ 450 the bf16 rounding of q^
@@ -147,7 +154,7 @@ def test_no_qk_norm_large_queries_take_exact_pass():
     (same operands) and for finiteness rather than against float64."""
     import torch
     c = _case("llama_large_q", [96, 200], [0, 1, 0], [20, 9, 33],
-              q_scale=40.0, seed=5)
+              q_scale=40.0, seed=5, d=d)
     fast, fast_lse = _gpu(c, variant=0)
     exact, exact_lse = _gpu(c, variant=4)
     assert np.isfinite(fast).all() and np.isfinite(fast_lse).all()
@@ -168,7 +175,7 @@ def test_one_norm_gain_is_rejected():
     from paper_2609_03311_amd import pipeline
     step = pipeline.OnlineStep(c["store"], n_pairs=1, n_q_heads=32,
                                total_tokens=st.n_tokens, max_tokens=4)
-    w = torch.ones(D, dtype=torch.bfloat16, device="cuda")
+    w = torch.ones(128, dtype=torch.bfloat16, device="cuda")
     with pytest.raises(DoprError) as e:
         step.attention(0, c["doc_ids"], c["cu"], c["on"]["q"], c["on"]["k"],
                        c["on"]["v"], w, None)

@@ -142,6 +142,17 @@ def llama3_8b(seed: int = 0) -> Structure:
     return st
 
 
+def llama3_2_1b(seed: int = 0) -> Structure:
+    """Llama-3.2-1B-shaped attention (hidden 2048, 32q/8kv, head size 64,
+    no QK-norm; the model of the paper's cross-family check): the pair
+    structure of qwen3_8b."""
+    st = qwen3_8b(seed)
+    st.name = "llama3_2_1b"
+    st.hidden = 2048
+    st.head_dim = 64
+    return st
+
+
 def qwen3_8b_ragged(seed: int = 0, prefix_scale: int = 1) -> Structure:
     """Qwen3-8B-shaped layer, ragged: prefix lengths uniform 8..256 slots
     over a 1M-id space; 16384 pairs, half Zipf(1.1) reuse and half distinct
@@ -184,6 +195,7 @@ CONFIGS = {
     "qwen3_8b_ragged": qwen3_8b_ragged,
     "qwen3_8b_ragged_x8": lambda seed=0: qwen3_8b_ragged(seed, 8),
     "llama3_8b": llama3_8b,
+    "llama3_2_1b": llama3_2_1b,
 }
 
 
@@ -192,13 +204,13 @@ def make(name: str, seed: int = 0) -> Structure:
 
 
 def custom(doc_len, doc_ids, seqlens, n_q_heads=16, n_kv_heads=8,
-           name="custom") -> Structure:
+           name="custom", head_dim=HEAD_DIM) -> Structure:
     """A hand-shaped structure (edge cases, sweeps)."""
     return Structure(name, int(n_q_heads), int(n_kv_heads),
-                     int(n_q_heads) * HEAD_DIM,
+                     int(n_q_heads) * int(head_dim),
                      np.asarray(doc_len, np.int32),
                      np.asarray(doc_ids, np.int32),
-                     np.asarray(seqlens, np.int32))
+                     np.asarray(seqlens, np.int32), head_dim=int(head_dim))
 
 
 # ---------------------------------------------------------------------------
