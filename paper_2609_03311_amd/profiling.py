@@ -22,10 +22,13 @@ import sys
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 KERNEL_SOURCES = ("csrc/attn.hip", "csrc/internal.hpp")
-# the dominant kernel of each path on the Qwen3-8B-shaped workload: 8 waves,
-# 256 slots resident (full layer); two 4-wave blocks per CU (score rows)
-ATTN_KERNEL = r"k_prefix_attn<8, ?1, ?false, ?false, ?8>"
-SCORE_KERNEL = r"k_prefix_attn<4, ?1, ?false, ?true, ?3>"
+# the dominant kernel of each path on the Qwen3-8B-shaped workload (head
+# size 128): 8 waves, 256 slots resident (full layer); two 4-wave blocks per
+# CU (score rows).  At head size 64 the same shapes hold 512 and 192 slots.
+ATTN_KERNEL = r"k_prefix_attn<8, ?1, ?false, ?false, ?128, ?8>"
+SCORE_KERNEL = r"k_prefix_attn<4, ?1, ?false, ?true, ?128, ?3>"
+ATTN_KERNEL_D64 = r"k_prefix_attn<8, ?1, ?false, ?false, ?64, ?16>"
+SCORE_KERNEL_D64 = r"k_prefix_attn<4, ?1, ?false, ?true, ?64, ?6>"
 CALIB_KERNEL = r"bitwise_not"
 CALIB_BYTES = 1 << 30
 
