@@ -78,9 +78,12 @@ constexpr float kNoRefBound = 64.f;  // |logit| <= 64: weights exp2(logit)
 constexpr int32_t kFixUnscored = 1 << 30;
 // Prefix chunks resident in LDS per head size: the one-block-per-CU shape
 // fills the CU's LDS (D = 128: 8 chunks, 256 slots; D = 64: 16 chunks),
-// the two-blocks-per-CU shape holds 3 (resp. 6) chunks.
+// the two-blocks-per-CU shape half of it (3 chunks at D = 128; at D = 64
+// 8 chunks, so a 256-slot prefix stays resident in both blocks and the
+// two blocks' independent barriers let one's memory waits overlap the
+// other's products).
 constexpr int big_chunks(int d) { return d == 128 ? 8 : 16; }
-constexpr int small_chunks(int d) { return d == 128 ? 3 : 6; }
+constexpr int small_chunks(int d) { return d == 128 ? 3 : 8; }
 
 struct AttnParams {
   const uint16_t *q, *k, *v, *qw, *kw;
@@ -1136,7 +1139,7 @@ hipError_t launch_attention(const AttnCall &c, const Plan &pl,
     p.head_w = static_cast<const uint16_t *>(c.head->w_head);
   }
   // Tile shape.  Automatic: two 4-wave blocks per CU (half the LDS each:
-  // 96 prefix slots resident at D = 128, 192 at D = 64) when every prefix
+  // 96 prefix slots resident at D = 128, 256 at D = 64) when every prefix
   // fits or when only score rows are attended (one pass per unit, so
   // nothing is restaged); else one 8-wave block per CU with 256 (512) slots
   // resident.

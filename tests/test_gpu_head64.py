@@ -5,8 +5,8 @@ QK-norm gains as well as without, in every tile shape, with prefixes longer
 than the LDS-resident segment, and the store's put/gather at D = 64.
 
 At D = 64 a 32-key chunk block is 4 KB, so the one-block-per-CU shape keeps
-512 prefix slots resident (16 chunks) and the two-blocks-per-CU shape 192
-(6 chunks); the 700- and 513-slot prefixes below are streamed in segments
+512 prefix slots resident (16 chunks) and the two-blocks-per-CU shape 256
+(8 chunks); the 700- and 513-slot prefixes below are streamed in segments
 by every shape.  Tolerance: max-abs 2e-2 on O, LSE, logits and score, as at
 D = 128 (bf16 operands, fp32 accumulation over half as many products).
 Integer work (store put/gather) is compared bit for bit.
@@ -41,8 +41,8 @@ def _structure(seed, lens, n_pairs, t_choices, name, hq=32, hkv=8):
                             head_dim=D)
 
 
-# prefixes 0..256 (two 4-wave blocks per CU hold 192: 256 streams there),
-# T from 1 (score token only) to 70 (several own-key chunks)
+# prefixes 0..256 (resident in every shape), T from 1 (score token only) to
+# 70 (several own-key chunks)
 RAGGED = dict(lens=[256, 0, 33, 100, 7, 192, 65, 1], n_pairs=24,
               t_choices=[1, 2, 31, 33, 70])
 # prefixes past the 512 slots the one-block-per-CU shape keeps resident
