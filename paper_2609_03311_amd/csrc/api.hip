@@ -85,9 +85,16 @@ dopr_status_t layout_store(const dopr_store_desc_t *d, StoreLayout *lay,
   return DOPR_OK;
 }
 
-int32_t default_rows_per_item(int32_t variant) {
-  (void)variant;
-  return 2048;
+// Rows per work item: long items for the block-wide kernels (a document's
+// prefix is staged once per item), 32 for the one-wave-per-unit score
+// kernel that the automatic choice takes when every prefix is at most
+// kScoreRowsMaxLen slots.
+int32_t default_rows_per_item(int32_t variant, bool score_only,
+                              int32_t max_len) {
+  return score_only && (variant == 0 || variant == 5) &&
+                 max_len <= kScoreRowsMaxLen
+             ? 32
+             : 2048;
 }
 
 // Validation shared by the workspace query and the attention call.
@@ -122,7 +129,8 @@ dopr_status_t check_attn(const dopr_store *st, const dopr_attn_args_t *a,
   shape->n_pairs = a->n_pairs;
   shape->n_rep = *n_rep;
   shape->max_tokens = a->max_tokens;
-  shape->rows_per_item = default_rows_per_item(a->kernel_variant);
+  shape->rows_per_item =
+      default_rows_per_item(a->kernel_variant, score_only, st->max_len);
   shape->n_docs = st->n_docs;
   shape->total_tokens = a->total_tokens;
   shape->max_len = st->max_len;
@@ -537,7 +545,7 @@ dopr_status_t dopr_group_pairs(dopr_store_t st, int32_t n_pairs,
   a.cu_seqlens = nullptr;
   a.rope_theta = 1e6f;
   a.softmax_scale = 1.f;
-  PlanShape shape{n_pairs,     1,          1, default_rows_per_item(0),
+  PlanShape shape{n_pairs,     1,          1, default_rows_per_item(0, false, 0),
                   st->n_docs,  (int64_t)n_pairs, st->max_len,
                   st->n_kv_heads};
   const size_t need = plan_bytes(shape);

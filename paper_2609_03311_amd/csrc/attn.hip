@@ -996,6 +996,358 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(
   }
 }
 
+// ---------------------------------------------------------------------------
+// Last-layer scoring with one wave per work unit.  A score work unit holds
+// the score-token rows of the pairs of one document for one kv head, a few
+// rows (n_rep per pair), so a block-wide unit leaves most of the block idle
+// behind barriers while the prefix is staged.  Here every wave takes its own
+// unit (items of at most 32 rows) and streams it with no block barrier, so
+// a CU has eight units in flight and their memory waits overlap:
+//   - prefix K and V^T fragments are loaded straight from the store into
+//     MFMA operand registers (the store keeps V transposed, so both are
+//     16-byte runs per lane);
+//   - own keys are normed and rotated in registers by the lane that holds
+//     the key's fragments, with the arithmetic of own_stage;
+//   - own values are transposed through the wave's own 8 KB LDS slice in
+//     the chunk-block layout, then read as V^T fragments.
+// The chunk sequence and every operand value equal those of the full path,
+// so a score row comes out bit-identical to the full path's row.
+
+// k^ = RoPE(RMSNorm(k) * w) of key row `krow` in the A-operand layout: lane
+// half hf holds the head-dim groups sub = 2 s' + hf (s' < D/32) and their
+// rotate-half partners, as kf[s'] and kf[s' + D/32].  The norm's sum of
+// squares is formed per group and added in the order of own_stage's lane
+// reduction, so the values equal the staged ones bit for bit.  Invalid keys
+// give zero rows.  The gains come from the block's LDS copy `kw`; the
+// rotary factors are loaded for half of the groups at a time.
+template <int D>
+__device__ __forceinline__ void k_group(const uint4 &a0, const uint4 &a1,
+                                        const uint16_t *kw, const float4 *cs,
+                                        float inv, int sub, bool valid,
+                                        bf16x8 &lo, bf16x8 &hi) {
+  float x[16];
+  if (valid) {
+    unpack8(a0, x);
+    unpack8(a1, x + 8);
+    float w0[8], w1[8];
+    unpack8(*reinterpret_cast<const uint4 *>(kw + 8 * sub), w0);
+    unpack8(*reinterpret_cast<const uint4 *>(kw + D / 2 + 8 * sub), w1);
+    const float c[16] = {cs[0].x, cs[0].y, cs[0].z, cs[0].w,
+                         cs[1].x, cs[1].y, cs[1].z, cs[1].w,
+                         cs[2].x, cs[2].y, cs[2].z, cs[2].w,
+                         cs[3].x, cs[3].y, cs[3].z, cs[3].w};
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float a = x[e] * inv * w0[e], b = x[8 + e] * inv * w1[e];
+      const float co = c[2 * e], si = c[2 * e + 1];
+      x[e] = fmaf(a, co, -b * si);
+      x[8 + e] = fmaf(b, co, a * si);
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < 16; ++e) x[e] = 0.f;
+  }
+  lo = to_bf16x8(x);
+  hi = to_bf16x8(x + 8);
+}
+
+template <int D>
+__device__ __forceinline__ void own_k_fragments(const AttnParams &P,
+                                                const uint16_t *krow,
+                                                const float2 *rope_row,
+                                                const uint16_t *kw,
+                                                bool valid, int hf,
+                                                bf16x8 *kf) {
+  constexpr int NG = D / 32;  // groups per lane half
+  constexpr int NH = NG / 2;  // groups per rotary-factor batch
+  uint4 a0[NG], a1[NG];
+  float4 cs[NH][4];
+  if (valid) {
+#pragma unroll
+    for (int s = 0; s < NG; ++s) {
+      const int sub = 2 * s + hf;
+      a0[s] = *reinterpret_cast<const uint4 *>(krow + 8 * sub);
+      a1[s] = *reinterpret_cast<const uint4 *>(krow + D / 2 + 8 * sub);
+    }
+#pragma unroll
+    for (int s = 0; s < NH; ++s)
+#pragma unroll
+      for (int e2 = 0; e2 < 4; ++e2)
+        cs[s][e2] =
+            reinterpret_cast<const float4 *>(rope_row + 8 * (2 * s + hf))[e2];
+  }
+  // group sums, then pairs of adjacent groups (this half's group 2s' with
+  // the other half's 2s' + 1), then the pair sums in a balanced tree
+  float y[NG];
+#pragma unroll
+  for (int s = 0; s < NG; ++s) {
+    const float own = valid ? sumsq8(a1[s], sumsq8(a0[s], 0.f)) : 0.f;
+    y[s] = own + __shfl_xor(own, 32, 64);
+  }
+  float ss;
+  if constexpr (NG == 4)
+    ss = (y[0] + y[1]) + (y[2] + y[3]);
+  else
+    ss = y[0] + y[1];
+  const float inv = P.norm ? rsqrtf(ss * (1.0f / D) + P.eps) : 1.f;
+#pragma unroll
+  for (int s = 0; s < NH; ++s)
+    k_group<D>(a0[s], a1[s], kw, cs[s], inv, 2 * s + hf, valid, kf[s],
+               kf[s + NG]);
+  // second batch of rotary factors (the first batch's registers are free)
+  if (valid) {
+    const float2 *rr = rope_row + opaque_zero();
+#pragma unroll
+    for (int s = 0; s < NH; ++s)
+#pragma unroll
+      for (int e2 = 0; e2 < 4; ++e2)
+        cs[s][e2] = reinterpret_cast<const float4 *>(
+            rr + 8 * (2 * (s + NH) + hf))[e2];
+  }
+#pragma unroll
+  for (int s = NH; s < NG; ++s)
+    k_group<D>(a0[s], a1[s], kw, cs[s - NH], inv, 2 * s + hf, valid, kf[s],
+               kf[s + NG]);
+}
+
+// v of own keys c0 .. c0 + 31 of a pair, transposed into the wave's V^T
+// chunk block: lane i takes keys 4m .. 4m + 3 (m = i % 8) and head dims
+// D/8 * (i / 8) .. + D/8 - 1, and writes four keys of one head dim per
+// 8-byte store.  Keys past the pair's end are written as zeros.
+template <int D>
+__device__ __forceinline__ void own_v_transpose(const AttnParams &P,
+                                                const uint16_t *v0, int64_t
+                                                key_stride, int nvalid,
+                                                uint16_t *ov) {
+  constexpr int DL = D / 8;  // head dims per lane
+  const int lane = threadIdx.x & 63;
+  const int m = lane & 7, d0 = DL * (lane >> 3);
+  uint4 r[4][DL / 8];
+#pragma unroll
+  for (int k = 0; k < 4; ++k)
+#pragma unroll
+    for (int h = 0; h < DL / 8; ++h)
+      r[k][h] = 4 * m + k < nvalid
+                    ? *reinterpret_cast<const uint4 *>(
+                          v0 + (int64_t)(4 * m + k) * key_stride + d0 + 8 * h)
+                    : make_uint4(0, 0, 0, 0);
+#pragma unroll
+  for (int h = 0; h < DL / 8; ++h) {
+    const uint32_t w[4][4] = {{r[0][h].x, r[0][h].y, r[0][h].z, r[0][h].w},
+                              {r[1][h].x, r[1][h].y, r[1][h].z, r[1][h].w},
+                              {r[2][h].x, r[2][h].y, r[2][h].z, r[2][h].w},
+                              {r[3][h].x, r[3][h].y, r[3][h].z, r[3][h].w}};
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int d = d0 + 8 * h + e;
+      uint32_t k4[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+        k4[k] = (e & 1) ? w[k][e >> 1] >> 16 : w[k][e >> 1] & 0xffffu;
+      const uint2 pk = make_uint2(k4[0] | (k4[1] << 16), k4[2] | (k4[3] << 16));
+      *reinterpret_cast<uint2 *>(ov + vc_off(d, m >> 1) + 4 * (m & 1)) = pk;
+    }
+  }
+}
+
+// One 32-key chunk from operand registers: S^T = K Q^T, weights, O^T +=
+// V^T P^T, in the order of attend (k-steps, then V^T fragments).
+template <int MODE, int D>
+__device__ __forceinline__ void attend_regs(const bf16x8 *kf,
+                                            const bf16x8 *vf,
+                                            const bf16x8 (*qf)[D / 16],
+                                            Acc<D> *acc, int hf,
+                                            const int *lim) {
+  floatx16 S[1];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) S[0][i] = 0.f;
+#pragma unroll
+  for (int s = 0; s < D / 16; ++s)
+    S[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[s], qf[0][s], S[0], 0,
+                                                   0, 0);
+  bf16x8 pb[1][2];
+  softmax_part<MODE, 1, 0, D>(S, acc, hf, 0.f, lim, pb);
+#pragma unroll
+  for (int f = 0; f < D / 16; ++f)
+    acc[0].o[f >> 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+        vf[f], pb[0][f & 1], acc[0].o[f >> 1], 0, 0, 0);
+}
+
+template <int D>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(
+    2, 2))) void k_score_rows(AttnParams P) {
+  __shared__ __attribute__((aligned(16))) uint16_t sov[4][D * KC];
+  __shared__ __attribute__((aligned(16))) uint16_t skw[D];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lq = lane & 31, hf = lane >> 5, prow = perm32(lq);
+  // the k gains, once per block (the block's only barrier)
+  if (threadIdx.x < D / 8)
+    reinterpret_cast<uint4 *>(skw)[threadIdx.x] =
+        reinterpret_cast<const uint4 *>(P.kw)[threadIdx.x];
+  __syncthreads();
+  const int queue = blockIdx.x & 7;
+  int64_t n_items = P.totals[kTotItems];
+  if (n_items > P.items_cap) n_items = P.items_cap;
+  const int64_t n_work = n_items * P.Hkv;
+  const Frag<D> fo = frag_offsets<D>(lq, hf);
+  uint16_t *ov = sov[wave];
+
+  for (;;) {
+    int slot = 0;
+    if (lane == 0) slot = atomicAdd(&P.next[queue], 1);
+    slot = __builtin_amdgcn_readfirstlane(slot);
+    const int64_t w = queue + 8 * (int64_t)slot;
+    if (w >= n_work) break;
+    const int item = (int)(w / P.Hkv), g = (int)(w % P.Hkv);
+    const int4 it = P.items[item];
+    const int doc = P.group_doc[it.x];
+    const int L = P.doc_len[doc], Lp = pad8(L);
+    const int64_t blk = P.doc_off[doc];
+    const uint16_t *Kp = P.payload + k_offset(blk, L, P.Hkv, P.layer, g, D);
+    const uint16_t *VTp =
+        P.payload + vt_offset(blk, L, P.Hkv, P.layer, g, D);
+    const float kbound = fmaxf(
+        P.kown[0], P.kmax[((int64_t)doc * P.n_layers + P.layer) * P.Hkv + g]);
+    const float B = P.c * P.kown[1] * kbound * 1.001f;
+    if (B > kNoRefBound) {  // the exact pass computes the unit
+      if (lane == 0)
+        P.fix[atomicAdd(&P.counters[kCntFix], 1)] = (int32_t)w | kFixUnscored;
+      continue;
+    }
+    bool bad = false;
+    for (int t0 = it.y; t0 < it.z; t0 += 32) {
+      const int t1 = t0 + 32 < it.z ? t0 + 32 : it.z;
+      // this lane's row: stacked token u is the sorted pair
+      const int r = t0 + lq;
+      const bool valid = r < t1;
+      const int rc = valid ? r : t1 - 1;
+      const int u = rc / P.n_rep;
+      const int head = g * P.n_rep + (rc - u * P.n_rep);
+      const int2 tj = P.utok[u];
+      bf16x8 qf[1][D / 16];
+      q_fragments<D>(P.q + ((int64_t)tj.x * P.Hq + head) * D, P.qw,
+                     P.rope + (int64_t)(L + tj.y) * (D / 2), hf, P.eps, P.c,
+                     P.norm != 0, qf[0]);
+      Acc<D> acc[1];
+      acc[0].m = 0.f;
+      acc[0].l = 0.f;
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) acc[0].o[db][i] = 0.f;
+
+      // prefix chunks: K rows past L are clamped (their logits are masked),
+      // V^T granules past the stored columns are zero
+      for (int c0 = 0; c0 < L; c0 += KC) {
+        bf16x8 kf[D / 16], vf[D / 16];
+        const int krow = c0 + prow < L ? c0 + prow : L - 1;
+#pragma unroll
+        for (int s = 0; s < D / 16; ++s)
+          kf[s] = *reinterpret_cast<const bf16x8 *>(
+              Kp + (int64_t)krow * D + 16 * s + 8 * hf);
+#pragma unroll
+        for (int f = 0; f < D / 16; ++f) {
+          const int key = c0 + 16 * hf + 8 * (f & 1);
+          vf[f] = key < Lp ? *reinterpret_cast<const bf16x8 *>(
+                                 VTp + (int64_t)(32 * (f >> 1) + prow) * Lp +
+                                 key)
+                           : bf16x8{};
+        }
+        if (c0 + KC <= L) {
+          attend_regs<0, D>(kf, vf, qf, acc, hf, nullptr);
+        } else {
+          const int lim[1] = {L - c0 - 1};
+          attend_regs<1, D>(kf, vf, qf, acc, hf, lim);
+        }
+      }
+
+      // own keys, pair by pair: a score row sees every own key of its pair
+      const int s_lo = t0 / P.n_rep, s_hi = (t1 - 1) / P.n_rep;
+      for (int s = s_lo; s <= s_hi; ++s) {
+        const int4 sp = P.spair[s];
+        const int tok0 = sp.x, T = sp.y;
+        for (int c0 = 0; c0 < T; c0 += KC) {
+          const int lim[1] = {valid && u == s ? T - 1 - c0 : -1};
+          const int jk = c0 + prow;
+          bf16x8 kf[D / 16], vf[D / 16];
+          own_k_fragments<D>(
+              P, P.k + ((int64_t)(tok0 + (jk < T ? jk : T - 1)) * P.Hkv + g) * D,
+              P.rope + (int64_t)(L + jk) * (D / 2), skw, jk < T, hf, kf);
+          own_v_transpose<D>(P, P.v + ((int64_t)(tok0 + c0) * P.Hkv + g) * D,
+                             (int64_t)P.Hkv * D, T - c0, ov);
+          // the slice's stores land before the fragment reads (one wave)
+          asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+#pragma unroll
+          for (int f = 0; f < D / 16; ++f)
+            vf[f] = *reinterpret_cast<const bf16x8 *>(
+                ov + (f >> 1) * (32 * KC) + fo.v[f & 1]);
+          attend_regs<1, D>(kf, vf, qf, acc, hf, lim);
+          // every fragment read has returned before the next transpose
+          asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        }
+      }
+
+      // Normalise; O (bf16) if requested, the head's partial sums, LSE.
+      const float lt = acc[0].l + __shfl_xor(acc[0].l, 32, 64);
+      if (valid) {
+        bad = bad || !(lt >= kLoOk && lt <= kHiOk);
+        const float inv = 1.0f / lt;
+        const int64_t orow = (int64_t)P.pair_order[u] * P.Hq + head;
+        uint16_t *op = P.out ? P.out + orow * D : nullptr;
+        float ss = 0.f, sy = 0.f, sn = 0.f;
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db) {
+          float o[16];
+#pragma unroll
+          for (int i = 0; i < 16; ++i) o[i] = acc[0].o[db][i] * inv;
+          const uint4 h0 = as_uint4(to_bf16x8(o)),
+                      h1 = as_uint4(to_bf16x8(o + 8));
+          if (op) {
+            uint4 *dst = reinterpret_cast<uint4 *>(op + 32 * db + 16 * hf);
+            dst[0] = h0;
+            dst[1] = h1;
+          }
+          // (the opaque offset keeps each slice's weight loads in its own
+          // iteration instead of all of them in flight at once)
+          const int64_t c0 =
+              (int64_t)head * D + 32 * db + 16 * hf + opaque_zero();
+          const int64_t W = (int64_t)P.Hq * D;
+#pragma unroll
+          for (int half = 0; half < 2; ++half) {
+            float hv[8], gv[8], yv[8], nv[8];
+            unpack8(half ? h1 : h0, hv);
+            unpack8(*reinterpret_cast<const uint4 *>(P.head_norm_w + c0 +
+                                                     8 * half), gv);
+            unpack8(*reinterpret_cast<const uint4 *>(P.head_w + c0 +
+                                                     8 * half), yv);
+            unpack8(*reinterpret_cast<const uint4 *>(P.head_w + W + c0 +
+                                                     8 * half), nv);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+              ss = fmaf(hv[e], hv[e], ss);
+              const float gh = gv[e] * hv[e];
+              sy = fmaf(gh, yv[e], sy);
+              sn = fmaf(gh, nv[e], sn);
+            }
+          }
+        }
+        ss += __shfl_xor(ss, 32, 64);
+        sy += __shfl_xor(sy, 32, 64);
+        sn += __shfl_xor(sn, 32, 64);
+        if (hf == 0) {
+          float *pp = P.part + orow * 3;
+          pp[0] = ss;
+          pp[1] = sy;
+          pp[2] = sn;
+          if (P.lse) P.lse[orow] = (acc[0].m + __log2f(lt)) * kLn2;
+        }
+      }
+    }
+    if ((__any(bad) || P.flag_all) && lane == 0)
+      P.fix[atomicAdd(&P.counters[kCntFix], 1)] = (int32_t)w;
+  }
+}
+
 // Pairs whose document is out of range or not resident: zero outputs and
 // -inf LSE (their token range was validated by the scheduler).  With no
 // token ranges (score mode) pair p owns row p; out may then be NULL.
@@ -1055,13 +1407,33 @@ hipError_t launch_variant(const AttnParams &p, hipStream_t s, int max_grid) {
   return hipGetLastError();
 }
 
-// The fast pass in tile shape shape_v (1, 2, 3, 6; 4 queues every unit
-// for the exact pass instead), then the exact pass over the queued units.
+// One-wave-per-unit score kernel: a persistent grid of 4-wave blocks, as
+// many as fit (two per CU), a multiple of 8 so block b serves queue b % 8.
+template <int D>
+hipError_t launch_score_rows(const AttnParams &p, hipStream_t s) {
+  int dev = 0, n_cu = 0, per_cu = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  e = hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess) return e;
+  e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_score_rows<D>,
+                                                   256, 0);
+  if (e != hipSuccess) return e;
+  if (per_cu < 1) per_cu = 1;
+  const unsigned grid = (unsigned)((n_cu * per_cu + 7) / 8 * 8);
+  hipLaunchKernelGGL(k_score_rows<D>, dim3(grid), dim3(256), 0, s, p);
+  return hipGetLastError();
+}
+
+// The fast pass in tile shape shape_v (1, 2, 3, 6; 7 the one-wave-per-unit
+// score kernel; 4 queues every unit for the exact pass instead), then the
+// exact pass over the queued units.
 template <int D>
 hipError_t launch_passes(const AttnParams &p, int shape_v, bool score,
                          hipStream_t s) {
   hipError_t e;
   switch (shape_v) {
+    case 7: e = launch_score_rows<D>(p, s); break;
     case 1: e = launch_variant<4, 2, false, false, D>(p, s, 0); break;
     case 3: e = launch_variant<4, 1, false, false, D>(p, s, 0); break;
     case 6:
@@ -1138,15 +1510,19 @@ hipError_t launch_attention(const AttnCall &c, const Plan &pl,
     p.head_norm_w = static_cast<const uint16_t *>(c.head->norm_w);
     p.head_w = static_cast<const uint16_t *>(c.head->w_head);
   }
-  // Tile shape.  Automatic: two 4-wave blocks per CU (half the LDS each:
-  // 96 prefix slots resident at D = 128, 256 at D = 64) when every prefix
-  // fits or when only score rows are attended (one pass per unit, so
-  // nothing is restaged); else one 8-wave block per CU with 256 (512) slots
-  // resident.
+  // Tile shape.  Automatic: for score rows, one wave per work unit (shape
+  // 7) unless some prefix is longer than kScoreRowsMaxLen (each 32-row unit
+  // streams its whole prefix, so long prefixes shared by many pairs are
+  // cheaper staged once per item by shape 6); else two 4-wave blocks per CU
+  // (half the LDS each: 96 prefix slots resident at D = 128, 256 at
+  // D = 64) when every prefix fits, and one 8-wave block per CU with 256
+  // (512) slots resident otherwise.  Variants 2 and 6 keep the block-wide
+  // kernels for score rows (1 and 3 map to 6).
   const int D = st.head_dim;
   int shape_v = a->kernel_variant;
   if (shape_v == 0 || shape_v == 5)
-    shape_v = score || st.max_len <= small_chunks(D) * KC ? 6 : 2;
+    shape_v = score ? (st.max_len <= kScoreRowsMaxLen ? 7 : 6)
+                    : st.max_len <= small_chunks(D) * KC ? 6 : 2;
   if (score && (shape_v == 1 || shape_v == 3)) shape_v = 6;
   e = D == 128 ? launch_passes<128>(p, shape_v, score, s)
                : launch_passes<64>(p, shape_v, score, s);

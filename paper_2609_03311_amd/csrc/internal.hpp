@@ -15,6 +15,9 @@ namespace dopr {
 // for the largest uses kHeadDim; per-call code takes the store's head_dim.
 constexpr int kHeadDim = 128;
 constexpr int kAlign = 256;
+// Longest prefix for which last-layer scoring runs one wave per 32-row work
+// unit (the kernel variant and the planner's item size both follow it).
+constexpr int32_t kScoreRowsMaxLen = 512;
 
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 __host__ __device__ inline int32_t pad8(int32_t n) { return (n + 7) & ~7; }
