@@ -289,10 +289,11 @@ __device__ __forceinline__ void q_fragments(const uint16_t *qrow,
 // must multiply a finite value.  The store's pad columns [L, Lp) are zero.
 template <int WAVES, int D, int NCHK>
 __device__ __forceinline__ void stage_prefix(const uint16_t *Kp,
-                                             const uint16_t *VTp, int Lp,
+                                             const uint16_t *VTp, int L,
                                              int seg0, int n,
                                              Smem<D, NCHK> &sm) {
   constexpr int PSEG = Smem<D, NCHK>::PSEG;
+  const int Lp = pad8(L);
   constexpr int G = D / 8;       // granules per K row
   constexpr int RPB = 64 / G;    // K rows per 1 KB block
   constexpr int VB = D / 16;     // 1 KB V^T blocks per chunk
@@ -758,7 +759,7 @@ __device__ __forceinline__ bool run_unit(const AttnParams &P,
       const int n = L - seg0 < PSEG ? L - seg0 : PSEG;
       if (!resident) {
         __syncthreads();
-        stage_prefix<WAVES, D, NCHK>(Kp, VTp, Lp, seg0, n, sm);
+        stage_prefix<WAVES, D, NCHK>(Kp, VTp, L, seg0, n, sm);
       }
       wait_vmem();
       __syncthreads();
@@ -957,7 +958,7 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(
     if (!SAFE) {
       if (B <= kNoRefBound) {
         if (resident && L > 0)
-          stage_prefix<WAVES, D, NCHK>(Kp, VTp, Lp, 0, L, sm);
+          stage_prefix<WAVES, D, NCHK>(Kp, VTp, L, 0, L, sm);
         wave_bad = run_unit<WAVES, NQB, 0, SCORE, D, NCHK>(
                        P, sm, fo, g, row0, row1, L, Lp, Kp, VTp, B) ||
                    P.flag_all;
@@ -976,7 +977,7 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(
       __syncthreads();
     } else {
       if (resident && L > 0)
-        stage_prefix<WAVES, D, NCHK>(Kp, VTp, Lp, 0, L, sm);
+        stage_prefix<WAVES, D, NCHK>(Kp, VTp, L, 0, L, sm);
       // (self-check mode sends every unit to the exact mode)
       bool exact = !unscored || P.flag_all;
       if (!exact) {
@@ -1150,8 +1151,34 @@ __device__ __forceinline__ void own_v_transpose(const AttnParams &P,
   }
 }
 
-// One 32-key chunk from operand registers: S^T = K Q^T, weights, O^T +=
-// V^T P^T, in the order of attend (k-steps, then V^T fragments).
+// One 32-key chunk from operand registers, in the order of attend: S^T =
+// K Q^T over the k-steps (qk_regs), then the weights and O^T += V^T P^T over
+// the V^T fragments (pv_regs).  Split so that a caller can free the K
+// fragments before it gathers the V^T ones.
+template <int D>
+__device__ __forceinline__ void qk_regs(const bf16x8 *kf,
+                                        const bf16x8 (*qf)[D / 16],
+                                        floatx16 *S) {
+#pragma unroll
+  for (int i = 0; i < 16; ++i) S[0][i] = 0.f;
+#pragma unroll
+  for (int s = 0; s < D / 16; ++s)
+    S[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[s], qf[0][s], S[0], 0,
+                                                   0, 0);
+}
+
+template <int MODE, int D>
+__device__ __forceinline__ void pv_regs(floatx16 *S, const bf16x8 *vf,
+                                        Acc<D> *acc, int hf,
+                                        const int *lim) {
+  bf16x8 pb[1][2];
+  softmax_part<MODE, 1, 0, D>(S, acc, hf, 0.f, lim, pb);
+#pragma unroll
+  for (int f = 0; f < D / 16; ++f)
+    acc[0].o[f >> 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+        vf[f], pb[0][f & 1], acc[0].o[f >> 1], 0, 0, 0);
+}
+
 template <int MODE, int D>
 __device__ __forceinline__ void attend_regs(const bf16x8 *kf,
                                             const bf16x8 *vf,
@@ -1159,18 +1186,8 @@ __device__ __forceinline__ void attend_regs(const bf16x8 *kf,
                                             Acc<D> *acc, int hf,
                                             const int *lim) {
   floatx16 S[1];
-#pragma unroll
-  for (int i = 0; i < 16; ++i) S[0][i] = 0.f;
-#pragma unroll
-  for (int s = 0; s < D / 16; ++s)
-    S[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[s], qf[0][s], S[0], 0,
-                                                   0, 0);
-  bf16x8 pb[1][2];
-  softmax_part<MODE, 1, 0, D>(S, acc, hf, 0.f, lim, pb);
-#pragma unroll
-  for (int f = 0; f < D / 16; ++f)
-    acc[0].o[f >> 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-        vf[f], pb[0][f & 1], acc[0].o[f >> 1], 0, 0, 0);
+  qk_regs<D>(kf, qf, S);
+  pv_regs<MODE, D>(S, vf, acc, hf, lim);
 }
 
 template <int D>
@@ -1269,19 +1286,25 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(
         for (int c0 = 0; c0 < T; c0 += KC) {
           const int lim[1] = {valid && u == s ? T - 1 - c0 : -1};
           const int jk = c0 + prow;
-          bf16x8 kf[D / 16], vf[D / 16];
-          own_k_fragments<D>(
-              P, P.k + ((int64_t)(tok0 + (jk < T ? jk : T - 1)) * P.Hkv + g) * D,
-              P.rope + (int64_t)(L + jk) * (D / 2), skw, jk < T, hf, kf);
+          floatx16 S[1];
+          {
+            bf16x8 kf[D / 16];
+            own_k_fragments<D>(
+                P,
+                P.k + ((int64_t)(tok0 + (jk < T ? jk : T - 1)) * P.Hkv + g) * D,
+                P.rope + (int64_t)(L + jk) * (D / 2), skw, jk < T, hf, kf);
+            qk_regs<D>(kf, qf, S);
+          }
           own_v_transpose<D>(P, P.v + ((int64_t)(tok0 + c0) * P.Hkv + g) * D,
                              (int64_t)P.Hkv * D, T - c0, ov);
           // the slice's stores land before the fragment reads (one wave)
           asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+          bf16x8 vf[D / 16];
 #pragma unroll
           for (int f = 0; f < D / 16; ++f)
             vf[f] = *reinterpret_cast<const bf16x8 *>(
                 ov + (f >> 1) * (32 * KC) + fo.v[f & 1]);
-          attend_regs<1, D>(kf, vf, qf, acc, hf, lim);
+          pv_regs<1, D>(S, vf, acc, hf, lim);
           // every fragment read has returned before the next transpose
           asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
         }
