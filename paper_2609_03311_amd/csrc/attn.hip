@@ -1153,7 +1153,7 @@ __device__ __forceinline__ void own_v_transpose(const AttnParams &P,
 
 // One 32-key chunk from operand registers, in the order of attend: S^T =
 // K Q^T over the k-steps (qk_regs), then the weights and O^T += V^T P^T over
-// the V^T fragments (pv_regs).  Split so that a caller can free the K
+// the V^T fragments (pv_regs).  Two calls, so that a caller can free the K
 // fragments before it gathers the V^T ones.
 template <int D>
 __device__ __forceinline__ void qk_regs(const bf16x8 *kf,
@@ -1177,17 +1177,6 @@ __device__ __forceinline__ void pv_regs(floatx16 *S, const bf16x8 *vf,
   for (int f = 0; f < D / 16; ++f)
     acc[0].o[f >> 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
         vf[f], pb[0][f & 1], acc[0].o[f >> 1], 0, 0, 0);
-}
-
-template <int MODE, int D>
-__device__ __forceinline__ void attend_regs(const bf16x8 *kf,
-                                            const bf16x8 *vf,
-                                            const bf16x8 (*qf)[D / 16],
-                                            Acc<D> *acc, int hf,
-                                            const int *lim) {
-  floatx16 S[1];
-  qk_regs<D>(kf, qf, S);
-  pv_regs<MODE, D>(S, vf, acc, hf, lim);
 }
 
 template <int D>
@@ -1226,13 +1215,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(
     const float kbound = fmaxf(
         P.kown[0], P.kmax[((int64_t)doc * P.n_layers + P.layer) * P.Hkv + g]);
     const float B = P.c * P.kown[1] * kbound * 1.001f;
-    if (B > kNoRefBound) {  // the exact pass computes the unit
-      if (lane == 0)
-        P.fix[atomicAdd(&P.counters[kCntFix], 1)] = (int32_t)w | kFixUnscored;
-      continue;
-    }
+    // a unit over the bound is left to the exact pass.  Every lane runs the
+    // same path to the end of the unit (no early continue: the unit loop
+    // must leave the queue with the whole wave, and the one queue push is
+    // made by lane 0 after a wave-wide vote)
+    const bool unscored = B > kNoRefBound;
     bool bad = false;
-    for (int t0 = it.y; t0 < it.z; t0 += 32) {
+    for (int t0 = it.y; !unscored && t0 < it.z; t0 += 32) {
       const int t1 = t0 + 32 < it.z ? t0 + 32 : it.z;
       // this lane's row: stacked token u is the sorted pair
       const int r = t0 + lq;
@@ -1255,13 +1244,17 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(
 
       // prefix chunks: K rows past L are clamped (their logits are masked),
       // V^T granules past the stored columns are zero
+      // (at D = 128 the V^T fragments are gathered after the QK products,
+      // so the K fragments' registers are free again: fewer spills)
       for (int c0 = 0; c0 < L; c0 += KC) {
+        floatx16 S[1];
         bf16x8 kf[D / 16], vf[D / 16];
         const int krow = c0 + prow < L ? c0 + prow : L - 1;
 #pragma unroll
         for (int s = 0; s < D / 16; ++s)
           kf[s] = *reinterpret_cast<const bf16x8 *>(
               Kp + (int64_t)krow * D + 16 * s + 8 * hf);
+        if constexpr (D == 128) qk_regs<D>(kf, qf, S);
 #pragma unroll
         for (int f = 0; f < D / 16; ++f) {
           const int key = c0 + 16 * hf + 8 * (f & 1);
@@ -1270,11 +1263,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(
                                  key)
                            : bf16x8{};
         }
+        if constexpr (D != 128) qk_regs<D>(kf, qf, S);
         if (c0 + KC <= L) {
-          attend_regs<0, D>(kf, vf, qf, acc, hf, nullptr);
+          pv_regs<0, D>(S, vf, acc, hf, nullptr);
         } else {
           const int lim[1] = {L - c0 - 1};
-          attend_regs<1, D>(kf, vf, qf, acc, hf, lim);
+          pv_regs<1, D>(S, vf, acc, hf, lim);
         }
       }
 
@@ -1366,8 +1360,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(
         }
       }
     }
-    if ((__any(bad) || P.flag_all) && lane == 0)
-      P.fix[atomicAdd(&P.counters[kCntFix], 1)] = (int32_t)w;
+    const bool push = unscored || P.flag_all || __any(bad);
+    if (push && lane == 0)
+      P.fix[atomicAdd(&P.counters[kCntFix], 1)] =
+          (int32_t)w | (unscored ? kFixUnscored : 0);
   }
 }
 

@@ -88,8 +88,9 @@ EDGE = [
 def test_score_edge_shapes(i, variant):
     """Empty prefixes and prefixes longer than the resident segment (L = 0,
     L > 96, L > 256), T = 1, GQA ratios 1, 4 and 16 q heads per kv head, in
-    the automatic shape (two blocks per CU), the 8-wave shape, and the exact
-    and self-check variants."""
+    the automatic shape (one wave per 32-row unit while every prefix is at
+    most 512 slots, else two 4-wave blocks per CU), the 8-wave shape, and
+    the exact and self-check variants."""
     Hq, Hkv, lens, P, Ts = EDGE[i]
     rng = np.random.default_rng(300 + i)
     doc_ids = rng.integers(0, len(lens), P).astype(np.int32)
@@ -142,4 +143,74 @@ def test_score_without_rows_and_repeat():
     assert run_score(case, b) == 0
     assert torch.equal(s1, b.score)
     del case, a, b
+    _free()
+
+
+def _score_rows(case, variant, **kw):
+    import torch
+    ss = setup_score(case, kernel_variant=variant)
+    o, p = case.online, case.prm
+    ss.run(0, case.doc_ids, case.cu, o["q"], o["k"], o["v"], p["q_norm_w"],
+           p["k_norm_w"], p["norm_w"], p["w_head"], **kw)
+    torch.cuda.synchronize()
+    return ss.out.float().clone(), ss.lse.clone(), ss.score.clone()
+
+
+def test_score_units_over_the_logit_bound_take_exact_pass():
+    """Score rows whose document keys are ~10^3 times larger than N(0,1)
+    exceed the logit bound of the reference-free softmax: the one-wave
+    score kernel must leave those units to the exact pass (and compute the
+    other document's units itself).  Checked against exact mode on the same
+    operands (bf16 operand error is too large for the float64 oracle at
+    these norms) and, for the untouched document, against the oracle."""
+    import torch
+    from paper_2609_03311_amd import dopr_check_status, pipeline
+    st = workloads.custom([96, 40], [0, 1, 0, 1], [20, 9, 5, 33], 32, 8,
+                          name="score_extreme")
+    case = setup(st, seed=13)
+    k = case.k_src.float()
+    kstar = k[40].clone()
+    sign = torch.tensor([(-1.0) ** t for t in range(64)],
+                        device=k.device)[:, None, None]
+    k[0:32] = 0.0
+    k[32:96] = 1000.0 * sign * kstar[None]
+    case.k_src.copy_(k.to(torch.bfloat16))
+    case.store = pipeline.make_store(st.doc_len, st.n_kv_heads, case.k_src,
+                                     case.v_src)
+    fast, fast_lse, _ = _score_rows(case, 0)
+    exact, exact_lse, _ = _score_rows(case, 4)
+    assert dopr_check_status(case.store) == 0
+    assert torch.isfinite(fast).all() and torch.isfinite(fast_lse).all()
+    d = (fast - exact).abs().max().item()
+    dl = (fast_lse - exact_lse).abs().max().item()
+    log(f"score extreme: fast vs exact max diff O {d:.3e} lse {dl:.3e}")
+    assert d < 2e-2 and dl <= 1e-3 * exact_lse.abs().max().item() + 2e-2
+    ss = setup_score(case)
+    assert run_score(case, ss) == 0
+    compare_score(case, ss, np.array([1, 3]))
+    _free()
+
+
+def test_score_rows_out_of_range_are_recomputed():
+    """Without QK-norm no logit bound is known, so the one-wave kernel runs
+    every unit reference-free; queries scaled x40 push some rows' largest
+    logits past what that mode represents, and those units must be flagged
+    by the range check and recomputed exactly.  Compared with exact mode."""
+    import torch
+    from paper_2609_03311_amd import dopr_check_status
+    st = workloads.custom([96, 200, 0], [0, 1, 0, 2, 1], [20, 9, 33, 4, 1],
+                          32, 8, name="score_large_q")
+    case = setup(st, seed=5)
+    case.online["q"] = (case.online["q"].float() * 40.0).to(torch.bfloat16)
+    case.prm["q_norm_w"] = case.prm["k_norm_w"] = None
+    fast, fast_lse, fs = _score_rows(case, 0, rope_theta=5e5)
+    exact, exact_lse, es = _score_rows(case, 4, rope_theta=5e5)
+    assert dopr_check_status(case.store) == 0
+    assert torch.isfinite(fast).all() and torch.isfinite(fast_lse).all()
+    d = (fast - exact).abs().max().item()
+    dl = (fast_lse - exact_lse).abs().max().item()
+    ds = (fs - es).abs().max().item()
+    log(f"score large q: fast vs exact O {d:.3e} lse {dl:.3e} s {ds:.3e}")
+    assert d < 2e-2 and ds < 2e-2
+    assert dl <= 1e-3 * exact_lse.abs().max().item() + 2e-2
     _free()
