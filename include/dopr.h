@@ -155,9 +155,10 @@ typedef struct {
                                shape (identical results; for tuning
                                sweeps): 1 = 4 waves x 64 rows, 2 = 8 waves
                                x 32 rows, 3 = 4 waves x 32 rows (each one
-                               block per CU, 256 prefix slots resident),
-                               6 = 4 waves x 32 rows, two blocks per CU,
-                               96 slots resident;
+                               block per CU, 256 prefix slots resident;
+                               512 at D = 64), 6 = 4 waves x 32 rows, two
+                               blocks per CU, 96 slots resident (256 at
+                               D = 64);
                                4 = exact running-max softmax for every row
                                (slower; the reference for the fast path);
                                5 = self-check: the fast pass queues every
@@ -242,9 +243,12 @@ dopr_status_t dopr_score_logits(const dopr_score_args_t *args, void *stream);
  *   out  dev bf16 [P, Hq, D]: the score rows, or NULL (not written);
  *   lse  dev fp32 [P, Hq], or NULL;
  * and the workspace comes from dopr_prefix_attn_score_workspace.
- * kernel_variant 1 and 3 select shape 6 here (2 and 6 as above).  A pair with a
- * bad doc id gets zero rows, lse -inf, logits and score 0, and a deferred
- * DOC_RANGE status.  All buffers are caller-owned.                         */
+ * kernel_variant 0 (automatic) runs one wave per work unit of at most 32
+ * score rows while every resident prefix is at most 512 slots (one 4-wave
+ * block per 4 units, no block barrier), else shape 6; 1 and 3 select
+ * shape 6 here (2 and 6 as above; identical results in every case).  A
+ * pair with a bad doc id gets zero rows, lse -inf, logits and score 0, and
+ * a deferred DOC_RANGE status.  All buffers are caller-owned.              */
 typedef struct {
   const void *norm_w;       /* dev bf16 [W], W = n_q_heads * D              */
   const void *w_head;       /* dev bf16 [2, W]: row 0 = yes, row 1 = no    */
