@@ -214,3 +214,34 @@ def test_score_rows_out_of_range_are_recomputed():
     assert d < 2e-2 and ds < 2e-2
     assert dl <= 1e-3 * exact_lse.abs().max().item() + 2e-2
     _free()
+
+
+@pytest.mark.parametrize("d", [128, 64])
+@pytest.mark.parametrize("norm", [True, False], ids=["qknorm", "nonorm"])
+def test_score_rows_equal_full_rows_any_head_size(d, norm):
+    """The one-wave score kernel norms and rotates own keys in registers
+    with the staging arithmetic of the block kernels (its sum of squares is
+    added in the same order, which differs between head sizes 128 and 64):
+    its rows equal the full layer's rows bit for bit at both head sizes,
+    with and without QK-norm, over ragged prefixes (0..256) and T = 1..70."""
+    import torch
+    rng = np.random.default_rng(77)
+    lens = np.array([256, 0, 33, 100, 7, 192, 65, 1], np.int32)
+    doc_ids = rng.integers(0, len(lens), 24).astype(np.int32)
+    seqlens = rng.choice(np.array([1, 2, 31, 33, 70]), 24).astype(np.int32)
+    st = workloads.custom(lens, doc_ids, seqlens, 32, 8,
+                          name=f"score_eq_d{d}", head_dim=d)
+    case = setup(st, seed=8)
+    if not norm:
+        case.prm["q_norm_w"] = case.prm["k_norm_w"] = None
+    assert run(case) == 0
+    ss = setup_score(case)
+    assert run_score(case, ss) == 0
+    last = torch.from_numpy(st.cu_seqlens[1:].astype(np.int64) - 1).cuda()
+    full_o = case.step.out.index_select(0, last)
+    full_lse = case.step.lse.index_select(0, last)
+    diff = (full_o.float() - ss.out.float()).abs().max().item()
+    log(f"D={d} norm={norm}: score rows vs full rows max diff {diff:.3e}")
+    assert torch.equal(full_o, ss.out), f"rows differ by {diff}"
+    assert torch.equal(full_lse, ss.lse)
+    _free()
