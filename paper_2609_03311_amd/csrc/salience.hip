@@ -174,19 +174,20 @@ __global__ __launch_bounds__(256, 2) void k_row_lse(SalienceParams P) {
           for (int s = 0; s < 8; ++s)
             S = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[s], qf[r][s], S,
                                                         0, 0, 0);
+          // the scale c > 0 commutes with the max, so it is applied once
+          // to the chunk's max and fused into each exponent's argument
           float x[16], mx = -INFINITY;
 #pragma unroll
           for (int i = 0; i < 16; ++i) {
-            x[i] = S[i] * P.c;
-            if (masked && i > lim) x[i] = -INFINITY;
+            x[i] = masked && i > lim ? -INFINITY : S[i];
             mx = fmaxf(mx, x[i]);
           }
-          const float mn = fmaxf(m[r], mx);
+          const float mn = fmaxf(m[r], mx * P.c);
           if (mn > -INFINITY) {
             float add = 0.f;
 #pragma unroll
             for (int i = 0; i < 16; ++i)
-              add += __builtin_amdgcn_exp2f(x[i] - mn);
+              add += __builtin_amdgcn_exp2f(fmaf(x[i], P.c, -mn));
             l[r] = l[r] * __builtin_amdgcn_exp2f(m[r] - mn) + add;
             m[r] = mn;
           }
