@@ -1002,8 +1002,10 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(
 // the score-token rows of the pairs of one document for one kv head, a few
 // rows (n_rep per pair), so a block-wide unit leaves most of the block idle
 // behind barriers while the prefix is staged.  Here every wave takes its own
-// unit (items of at most 32 rows) and streams it with no block barrier, so
-// a CU has eight units in flight and their memory waits overlap:
+// unit (items cut at about 32 rows; the planner's 32-row-aligned cut can
+// leave an item empty or up to 63 rows long, which the wave then walks as
+// 32-row tiles) and streams it with no block barrier, so a CU has eight
+// units in flight and their memory waits overlap:
 //   - prefix K and V^T fragments are loaded straight from the store into
 //     MFMA operand registers (the store keeps V transposed, so both are
 //     16-byte runs per lane);
