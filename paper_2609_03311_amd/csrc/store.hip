@@ -83,9 +83,20 @@ __global__ __launch_bounds__(kThreads) void k_store_put(
       dst[0] = val.x; dst[1] = val.y; dst[2] = val.z; dst[3] = val.w;
     }
     __syncthreads();
-    for (int e = threadIdx.x; e < D * kTile; e += kThreads) {
-      const int dd = e / kTile, r = e % kTile, slot = t0 + r;
-      if (slot < Lp) VT[(int64_t)dd * Lp + slot] = tile[r][dd];
+    // eight slots of one head dim per thread, one 16-byte store (t0 and
+    // Lp are multiples of 8, so a run is wholly inside or past the row)
+    for (int e = threadIdx.x; e < D * (kTile / 8); e += kThreads) {
+      const int dd = e / (kTile / 8), r = 8 * (e % (kTile / 8)),
+                slot = t0 + r;
+      if (slot < Lp) {
+        uint32_t w[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          w[i] = (uint32_t)tile[r + 2 * i][dd] |
+                 ((uint32_t)tile[r + 2 * i + 1][dd] << 16);
+        *reinterpret_cast<uint4 *>(VT + (int64_t)dd * Lp + slot) =
+            make_uint4(w[0], w[1], w[2], w[3]);
+      }
     }
     __syncthreads();
   }
