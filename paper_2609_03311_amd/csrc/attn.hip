@@ -1016,6 +1016,16 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(
 // The chunk sequence and every operand value equal those of the full path,
 // so a score row comes out bit-identical to the full path's row.
 
+// x of lane ^ 32, through the lane-swap instruction (no LDS round trip):
+// the swap of a value with itself leaves the lower half's values in [0]
+// and the upper half's in [1], each in both halves.
+__device__ __forceinline__ float xor32(float x, int hf) {
+  const auto r = __builtin_amdgcn_permlane32_swap(
+      __builtin_bit_cast(unsigned, x), __builtin_bit_cast(unsigned, x), false,
+      false);
+  return __builtin_bit_cast(float, hf ? r[0] : r[1]);
+}
+
 // k^ = RoPE(RMSNorm(k) * w) of key row `krow` in the A-operand layout: lane
 // half hf holds the head-dim groups sub = 2 s' + hf (s' < D/32) and their
 // rotate-half partners, as kf[s'] and kf[s' + D/32].  The norm's sum of
@@ -1085,7 +1095,7 @@ __device__ __forceinline__ void own_k_fragments(const AttnParams &P,
 #pragma unroll
   for (int s = 0; s < NG; ++s) {
     const float own = valid ? sumsq8(a1[s], sumsq8(a0[s], 0.f)) : 0.f;
-    y[s] = own + __shfl_xor(own, 32, 64);
+    y[s] = own + xor32(own, hf);
   }
   float ss;
   if constexpr (NG == 4)
@@ -1307,7 +1317,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(
       }
 
       // Normalise; O (bf16) if requested, the head's partial sums, LSE.
-      const float lt = acc[0].l + __shfl_xor(acc[0].l, 32, 64);
+      const float lt = acc[0].l + xor32(acc[0].l, hf);
       if (valid) {
         bad = bad || !(lt >= kLoOk && lt <= kHiOk);
         const float inv = 1.0f / lt;
@@ -1350,9 +1360,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(
             }
           }
         }
-        ss += __shfl_xor(ss, 32, 64);
-        sy += __shfl_xor(sy, 32, 64);
-        sn += __shfl_xor(sn, 32, 64);
+        ss += xor32(ss, hf);
+        sy += xor32(sy, hf);
+        sn += xor32(sn, hf);
         if (hf == 0) {
           float *pp = P.part + orow * 3;
           pp[0] = ss;
