@@ -17,8 +17,11 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libdopr.so")
-SOURCES = ["api.hip", "store.hip", "group.hip", "attn.hip", "score.hip",
-           "layer.hip", "salience.hip"]
+SOURCES = ["api.hip", "store.hip", "group.hip", "attn.hip", "stream.hip",
+           "score.hip", "layer.hip", "salience.hip"]
+# per-file flags: the streaming kernel's cursor must stay in scalar
+# registers (common-code sinking would move it to scratch memory)
+EXTRA = {"stream.hip": ["-mllvm", "-simplifycfg-sink-common=false"]}
 ARCH = "gfx950"
 
 FLAGS = [
@@ -42,7 +45,8 @@ def hipcc() -> str:
 
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
-    cmd = [hipcc(), *FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [hipcc(), *FLAGS, *EXTRA.get(src, []), "-c", os.path.join(CSRC, src),
+           "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed for {src}:\n{r.stderr}")

@@ -85,16 +85,30 @@ dopr_status_t layout_store(const dopr_store_desc_t *d, StoreLayout *lay,
   return DOPR_OK;
 }
 
+bool uses_stream_kernel(int32_t variant);
+
 // Rows per work item: long items for the block-wide kernels (a document's
 // prefix is staged once per item), 32 for the one-wave-per-unit score
 // kernel that the automatic choice takes when every prefix is at most
-// kScoreRowsMaxLen slots.
+// kScoreRowsMaxLen slots, and one pass (256 rows; at most 64 pairs) for the
+// streaming kernel: a document's items then sit next to each other in one XCD's
+// queue, neighbouring CUs take them at the same time, and its prefix and
+// own-key chunks are fetched from HBM once and read from that XCD's L2 by
+// the others.
 int32_t default_rows_per_item(int32_t variant, bool score_only,
-                              int32_t max_len) {
-  return score_only && (variant == 0 || variant == 5) &&
-                 max_len <= kScoreRowsMaxLen
-             ? 32
-             : 2048;
+                              int32_t max_len, int32_t n_rep) {
+  if (score_only)
+    return (variant == 0 || variant == 5) && max_len <= kScoreRowsMaxLen
+               ? 32
+               : 2048;
+  (void)n_rep;
+  return 2048;
+}
+
+// The full layer runs the streaming kernel in the automatic choice, the
+// self-check mode and variant 8 (its plan then holds k^ of every token).
+bool uses_stream_kernel(int32_t variant) {
+  return variant == 0 || variant == 5 || variant == 8;
 }
 
 // Validation shared by the workspace query and the attention call.
@@ -118,8 +132,9 @@ dopr_status_t check_attn(const dopr_store *st, const dopr_attn_args_t *a,
     return fail(DOPR_ERR_UNSUPPORTED,
                 "stacked rows (tokens, or pairs in score mode) * n_rep must "
                 "be < 2^31");
-  if (a->kernel_variant < 0 || a->kernel_variant > 6)
-    return fail(DOPR_ERR_INVALID_ARG, "kernel_variant must be in 0..6");
+  if (a->kernel_variant < 0 || a->kernel_variant > 8 ||
+      a->kernel_variant == 7)
+    return fail(DOPR_ERR_INVALID_ARG, "kernel_variant must be in 0..6 or 8");
   if (!(a->softmax_scale > 0.f) || !std::isfinite(a->softmax_scale))
     return fail(DOPR_ERR_INVALID_ARG, "softmax_scale must be finite and > 0");
   if (!(a->rope_theta > 1.f) || !std::isfinite(a->rope_theta))
@@ -130,13 +145,15 @@ dopr_status_t check_attn(const dopr_store *st, const dopr_attn_args_t *a,
   shape->n_rep = *n_rep;
   shape->max_tokens = a->max_tokens;
   shape->rows_per_item =
-      default_rows_per_item(a->kernel_variant, score_only, st->max_len);
+      default_rows_per_item(a->kernel_variant, score_only, st->max_len,
+                            *n_rep);
   shape->n_docs = st->n_docs;
   shape->total_tokens = a->total_tokens;
   shape->max_len = st->max_len;
   shape->n_kv_heads = st->n_kv_heads;
   shape->head_dim = st->head_dim;
   shape->score_only = score_only;
+  shape->stream = !score_only && uses_stream_kernel(a->kernel_variant);
   return DOPR_OK;
 }
 
@@ -545,7 +562,7 @@ dopr_status_t dopr_group_pairs(dopr_store_t st, int32_t n_pairs,
   a.cu_seqlens = nullptr;
   a.rope_theta = 1e6f;
   a.softmax_scale = 1.f;
-  PlanShape shape{n_pairs,     1,          1, default_rows_per_item(0, false, 0),
+  PlanShape shape{n_pairs,     1,          1, 2048,
                   st->n_docs,  (int64_t)n_pairs, st->max_len,
                   st->n_kv_heads};
   const size_t need = plan_bytes(shape);

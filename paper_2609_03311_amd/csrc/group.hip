@@ -127,6 +127,7 @@ struct PlanArgs {
   int32_t n_pairs, n_rep, max_tokens, rows_per_item;
   int32_t *status;
   bool score_only;
+  bool exact_items;
 };
 
 __global__ __launch_bounds__(kThreads) void k_plan_init(Plan pl, int64_t n_docs,
@@ -138,6 +139,7 @@ __global__ __launch_bounds__(kThreads) void k_plan_init(Plan pl, int64_t n_docs,
     pl.fill[i] = 0;
   }
   if (i < kCounters) pl.counters[i] = 0;
+  if (i < 64) reinterpret_cast<int32_t *>(pl.zero)[i] = 0;
   if (i < kTotals) totals[i] = 0;
   if (i < kNextQueues) next[i] = 0;
 }
@@ -233,8 +235,11 @@ __global__ __launch_bounds__(kThreads) void k_items_count(Plan pl, PlanArgs a,
   pl.item_scan[g] = (rows + a.rows_per_item - 1) / a.rows_per_item;
 }
 
-// Step 5b: split a group's rows into near-equal items, boundaries on
-// multiples of 32 rows.
+// Step 5b: split a group's rows into items, boundaries on multiples of 32
+// rows: near-equal items (the block kernels, which walk an item in passes),
+// or, with exact_items, items of exactly rows_per_item rows and a shorter
+// last one (the streaming kernel serves an item in one pass, so no item
+// may exceed it).
 __global__ __launch_bounds__(kThreads) void k_items_emit(Plan pl, PlanArgs a,
                                                          const int64_t *totals) {
   const int32_t g = blockIdx.x * kThreads + threadIdx.x;
@@ -249,11 +254,22 @@ __global__ __launch_bounds__(kThreads) void k_items_emit(Plan pl, PlanArgs a,
   for (int64_t it = 0; it < n_it; ++it) {
     const int64_t idx = first + it;
     if (idx >= pl.items_cap) break;
-    const int64_t b0 = base + ((it * R / n_it) & ~(int64_t)31);
+    const int64_t b0 =
+        a.exact_items ? base + it * a.rows_per_item
+                      : base + ((it * R / n_it) & ~(int64_t)31);
     const int64_t b1 =
-        it + 1 < n_it ? base + (((it + 1) * R / n_it) & ~(int64_t)31)
-                      : base + R;
-    pl.items[idx] = make_int4(g, (int32_t)b0, (int32_t)b1, 0);
+        it + 1 < n_it
+            ? (a.exact_items ? base + (it + 1) * a.rows_per_item
+                             : base + (((it + 1) * R / n_it) & ~(int64_t)31))
+            : base + R;
+    // the item's first sorted pair: the last of the group's pairs whose
+    // stacked rows start at or before b0
+    int32_t lo = pl.group_ptr[g], hi = pl.group_ptr[g + 1] - 1;
+    while (lo < hi) {
+      const int32_t mid = (lo + hi + 1) >> 1;
+      if (pl.prow[mid] <= b0) lo = mid; else hi = mid - 1;
+    }
+    pl.items[idx] = make_int4(g, (int32_t)b0, (int32_t)b1, lo);
   }
 }
 
@@ -331,6 +347,36 @@ __global__ __launch_bounds__(128) void k_norm_bound(const uint16_t *kw,
   }
 }
 
+// Work units of the pass kernel, one per (item, kv head): the item's rows
+// and first pair, the document's prefix length and the element offsets of
+// its K and V^T slices for this layer and head; a unit whose logits the
+// norm bounds cannot keep within the reference-free range (the kernels'
+// kNoRefBound) is marked with L = -1 and left to the exact pass.
+__global__ __launch_bounds__(kThreads) void k_unit_table(
+    Plan pl, StoreView sv, int32_t layer, float c, float no_ref_bound,
+    const int64_t *totals) {
+  const int64_t w = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  const int64_t n_items = totals[kTotItems] < pl.items_cap
+                              ? totals[kTotItems]
+                              : pl.items_cap;
+  if (w >= n_items * sv.n_kv_heads) return;
+  const int32_t item = (int32_t)(w / sv.n_kv_heads);
+  const int32_t g = (int32_t)(w % sv.n_kv_heads);
+  const int4 it = pl.items[item];
+  const int32_t doc = pl.group_doc[it.x];
+  const int32_t L = sv.doc_len[doc];
+  const int64_t blk = sv.doc_off[doc];
+  const float kb = fmaxf(
+      pl.kown[0],
+      sv.kmax[((int64_t)doc * sv.n_layers + layer) * sv.n_kv_heads + g]);
+  const bool over = c * pl.kown[1] * kb * 1.001f > no_ref_bound;
+  const int64_t ko = k_offset(blk, L, sv.n_kv_heads, layer, g, sv.head_dim);
+  const int64_t vo = vt_offset(blk, L, sv.n_kv_heads, layer, g, sv.head_dim);
+  pl.units[2 * w] = make_int4(it.y, it.z, it.w, over ? -1 : L);
+  pl.units[2 * w + 1] = make_int4((int32_t)(uint32_t)ko, (int32_t)(ko >> 32),
+                                  (int32_t)(uint32_t)vo, (int32_t)(vo >> 32));
+}
+
 // Step 6: rotary table, (cos, sin)(pos * omega_i) for i < half = D/2, in
 // double, stored as float; omega_i = theta^(-2i/D), or the caller's
 // inv_freq[i].
@@ -401,6 +447,14 @@ Plan carve(void *ws, const PlanShape &s, size_t *bytes) {
   pl.unit_w = c.take<uint16_t>(kHeadDim);
   pl.rope_pos = s.max_len + s.max_tokens;
   pl.rope = c.take<float2>((int64_t)pl.rope_pos * (s.head_dim / 2));
+  pl.zero = c.take<uint16_t>(128);
+  pl.kh = s.stream ? c.take<uint16_t>(s.total_tokens * s.n_kv_heads *
+                                      s.head_dim)
+                   : nullptr;
+  pl.units = s.stream ? c.take<int4>(cap * 2 * (s.n_kv_heads > 0
+                                                    ? s.n_kv_heads
+                                                    : 1))
+                      : nullptr;
   *bytes = c.off;
   return pl;
 }
@@ -431,7 +485,7 @@ hipError_t launch_plan(const AttnCall &c, const Plan &pl,
   PlanArgs pa{a->doc_ids,        a->cu_seqlens,      c.st->d_len,
               c.st->n_docs,      a->total_tokens,    a->n_pairs,
               c.n_rep,           a->max_tokens,      shape.rows_per_item,
-              c.st->d_status,    shape.score_only};
+              c.st->d_status,    shape.score_only, false};
   int64_t *totals = plan_totals(pl);
   const int64_t P = a->n_pairs;
   const int64_t init_n = c.st->n_docs > kCounters ? c.st->n_docs : kCounters;
@@ -467,6 +521,13 @@ hipError_t launch_plan(const AttnCall &c, const Plan &pl,
                      static_cast<const uint16_t *>(a->k_norm_w),
                      static_cast<const uint16_t *>(a->q_norm_w), pl.kown,
                      pl.unit_w);
+  if (pl.units) {
+    const int64_t n_units = (int64_t)pl.items_cap * c.st->n_kv_heads;
+    hipLaunchKernelGGL(k_unit_table, dim3(blocks_for(n_units, kThreads)),
+                       dim3(kThreads), 0, s, pl, c.st->view(), c.layer,
+                       a->softmax_scale * 1.4426950408889634f, kNoRefBound,
+                       totals);
+  }
   const double log_theta = std::log((double)a->rope_theta);
   hipLaunchKernelGGL(k_rope_table,
                      dim3(blocks_for((int64_t)pl.rope_pos * (D / 2),

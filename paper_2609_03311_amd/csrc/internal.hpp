@@ -19,6 +19,10 @@ constexpr int kAlign = 256;
 // unit (the kernel variant and the planner's item size both follow it).
 constexpr int32_t kScoreRowsMaxLen = 512;
 
+// The attention's reference-free softmax serves a work unit when every
+// logit (log2 units) lies in [-kNoRefBound, kNoRefBound].
+constexpr float kNoRefBound = 64.f;
+
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 __host__ __device__ inline int32_t pad8(int32_t n) { return (n + 7) & ~7; }
 
@@ -111,7 +115,7 @@ struct Plan {
   int64_t *prow;        // [P+1] stacked-row offsets, sorted pair order
   int64_t *item_scan;   // [P+1] work items per group, scanned
   int32_t *blk_pair;    // [blk_cap] sorted pair owning row 32*b
-  int4 *items;          // [items_cap] (group, row0, row1, 0)
+  int4 *items;          // [items_cap] (group, row0, row1, first sorted pair)
   int32_t *fix;         // [items_cap * Hkv] work units for the SAFE pass
   int4 *spair;          // [P+1] sorted pair: (tok0, T, first stacked row)
   int2 *utok;           // [stacked tokens] (batch token, position)
@@ -120,6 +124,11 @@ struct Plan {
                         // (0 when there is no QK-norm: no bound is known)
   uint16_t *unit_w;     // [D] bf16 ones: the gains when there is no QK-norm
   float2 *rope;         // [rope_pos][D/2] (cos, sin)
+  uint16_t *kh;         // [Hkv][Ntok][D] own keys k^ (pass kernel), or NULL
+  int4 *units;          // [items_cap * Hkv][2] work units (pass kernel):
+                        // (row0, row1, first pair, L or -1 when over the
+                        // logit bound), (K offset lo, hi, V^T offset lo, hi)
+  uint16_t *zero;       // 256 zero bytes (streaming kernel loads past row ends)
   int32_t items_cap;
   int32_t blk_cap;
   int32_t rope_pos;
@@ -134,6 +143,8 @@ struct PlanShape {
   int32_t max_len, n_kv_heads;
   int32_t head_dim = kHeadDim;
   bool score_only = false;
+  bool stream = false;  // the pass kernel runs: room for k^ of every token
+                        // and the work-unit table
 };
 
 size_t plan_bytes(const PlanShape &s);

@@ -49,7 +49,7 @@ RAGGED = dict(lens=[256, 0, 33, 100, 7, 192, 65, 1], n_pairs=24,
 LONG = dict(lens=[700, 513, 64], n_pairs=10, t_choices=[1, 17, 40])
 
 
-@pytest.mark.parametrize("variant", [0, 1, 2, 3, 4, 5, 6])
+@pytest.mark.parametrize("variant", [0, 1, 2, 3, 4, 5, 6, 8])
 def test_ragged_all_shapes(variant):
     """QK-norm at D = 64, every tile shape (0 automatic, 4 exact mode, 5
     self-check: every unit recomputed exactly), all rows vs the oracle."""
@@ -61,7 +61,7 @@ def test_ragged_all_shapes(variant):
     _free()
 
 
-@pytest.mark.parametrize("variant", [0, 1, 6])
+@pytest.mark.parametrize("variant", [0, 1, 6, 8])
 def test_long_prefix_segments(variant):
     st = _structure(4, name="d64_long", **LONG)
     case = setup(st, seed=4, kernel_variant=variant)

@@ -67,7 +67,7 @@ SWEEP = [
 ]
 
 
-@pytest.mark.parametrize("variant", [1, 2, 3, 4, 6])
+@pytest.mark.parametrize("variant", [1, 2, 3, 4, 6, 8])
 @pytest.mark.parametrize("i", range(len(SWEEP)))
 def test_shape_sweep(i, variant):
     Hq, Hkv, lens, P, Ts = SWEEP[i]
@@ -164,7 +164,7 @@ def test_deterministic_and_tiling_invariant():
     o1 = a.step.out.clone()
     run(a)
     assert torch.equal(o1, a.step.out)
-    for vb in (2, 6):
+    for vb in (2, 6, 8):
         b = setup(st, seed=2, kernel_variant=vb)
         run(b)
         diff = (o1.float() - b.step.out.float()).abs().max().item()
