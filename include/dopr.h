@@ -201,6 +201,30 @@ dopr_status_t dopr_prefix_attn_workspace(dopr_store_t st,
 dopr_status_t dopr_prefix_attn(dopr_store_t st, int32_t layer,
                                const dopr_attn_args_t *args, void *stream);
 
+/* dopr_prefix_attn for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc).  Same arguments, results and errors as dopr_prefix_attn,
+ * except:
+ *   - args->workspace must be NULL and args->workspace_bytes 0: the plan is
+ *     laid out in a scratch array that the library holds, one copy per
+ *     device, from the first use on that device until the process ends;
+ *   - the scratch holds at most 64 MiB (DOPR_NOALLOC_SCRATCH_BYTES).  A call
+ *     whose plan needs more returns DOPR_ERR_WORKSPACE and launches nothing;
+ *     dopr_prefix_attn_workspace gives the size, except that here the
+ *     automatic choice (kernel_variant 0) and the self-check variant 5 never
+ *     take the pass kernel (8), whose plan grows with every token; variant 8
+ *     is run only when asked for and its plan fits;
+ *   - the call allocates nothing: no hipMalloc, hipFree or allocating
+ *     library routine.
+ * Every call on one device shares that device's scratch: calls that overlap
+ * on one device (other streams, other threads) race and must be ordered by
+ * the caller.  The plan's kernels clear what must start at zero.  Outputs
+ * are bitwise identical to dopr_prefix_attn's for the same inputs.        */
+#define DOPR_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+dopr_status_t dopr_prefix_attn_noalloc(dopr_store_t st, int32_t layer,
+                                       const dopr_attn_args_t *args,
+                                       void *stream);
+
 /* ------------------------------------------------------------------------ */
 /* Score head (Sec. 3.2.3): s(q,d) from the score token's hidden state h.
  * Read as RMSNorm followed by a two-row linear head (yes, no):

@@ -108,6 +108,9 @@ EXPORTS = {
                                     ctypes.c_void_p], ctypes.c_int),
     "dopr_prefix_attn": ([ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p,
                           ctypes.c_void_p], ctypes.c_int),
+    "dopr_prefix_attn_noalloc": ([ctypes.c_void_p, ctypes.c_int32,
+                                  ctypes.c_void_p, ctypes.c_void_p],
+                                 ctypes.c_int),
     "dopr_score_logits": ([ctypes.c_void_p, ctypes.c_void_p], ctypes.c_int),
     "dopr_prefix_attn_score_workspace": ([ctypes.c_void_p, ctypes.c_void_p,
                                           ctypes.c_void_p], ctypes.c_int),
@@ -326,6 +329,27 @@ def dopr_prefix_attn(store: Store, layer: int, doc_ids, cu_seqlens, q, k, v,
                    rope_inv_freq=rope_inv_freq)
     _check(lib().dopr_prefix_attn(store.handle, layer, ctypes.byref(a),
                                   _stream(stream)))
+
+
+def dopr_prefix_attn_noalloc(store: Store, layer: int, doc_ids, cu_seqlens,
+                             q, k, v, q_norm_w, k_norm_w, out, *, max_tokens,
+                             lse=None, total_tokens=None, rms_eps=1e-6,
+                             rope_theta=1e6, softmax_scale=None,
+                             kernel_variant=0, timing=None,
+                             rope_inv_freq=None, stream=None):
+    """dopr_prefix_attn without a workspace: the plan goes to the library's
+    own per-device scratch (at most DOPR_NOALLOC_SCRATCH_BYTES)."""
+    a = _attn_args(store, doc_ids, cu_seqlens, q, k, v, q_norm_w, k_norm_w,
+                   out, lse, None, max_tokens=max_tokens,
+                   total_tokens=total_tokens, rms_eps=rms_eps,
+                   rope_theta=rope_theta, softmax_scale=softmax_scale,
+                   kernel_variant=kernel_variant, timing=timing,
+                   rope_inv_freq=rope_inv_freq)
+    _check(lib().dopr_prefix_attn_noalloc(store.handle, layer,
+                                          ctypes.byref(a), _stream(stream)))
+
+
+DOPR_NOALLOC_SCRATCH_BYTES = 64 << 20
 
 
 def dopr_prefix_attn_score(store: Store, layer: int, doc_ids, cu_seqlens, q,

@@ -1,15 +1,24 @@
 // api.hip -- host side of the C ABI declared in include/dopr.h: argument
 // validation, store layout, workspace sizing and kernel launches.  Nothing
-// here allocates device memory; every device buffer comes from the caller.
+// here allocates device memory; every device buffer comes from the caller,
+// except the fixed scratch array below that dopr_prefix_attn_noalloc uses.
 #include <algorithm>
 #include <cmath>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
 #include "internal.hpp"
 
 using namespace dopr;
+
+// Scratch of dopr_prefix_attn_noalloc: the attention plan of one call.  The
+// code object holds one copy per device that loads it, for the life of the
+// process.  In host code `scratch` names a host-side stand-in, not device
+// memory: the device address comes from hipGetSymbolAddress (scratch_ptr
+// below) and only that address is ever handed to a kernel.
+static __device__ __align__(256) char scratch[dopr::kNoAllocScratchBytes];
 
 namespace {
 
@@ -319,16 +328,49 @@ dopr_status_t dopr_prefix_attn_workspace(dopr_store_t st,
 
 namespace {
 
+// Device address of `scratch` on device `dev`, looked up once per device
+// (with that device current) and kept.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices] = {};
+
+dopr_status_t scratch_ptr(int dev, void **out) {
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(DOPR_ERR_UNSUPPORTED, "device index beyond the scratch table");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void *p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    if (!p || reinterpret_cast<uintptr_t>(p) % kAlign)
+      return fail(DOPR_ERR_HIP, "scratch address is NULL or misaligned");
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return DOPR_OK;
+}
+
 // The attention call in both modes: every online row (head == NULL) or the
-// score token's rows with the fused score head.
+// score token's rows with the fused score head.  no_alloc: the plan goes to
+// the library's scratch array instead of the caller's workspace; the
+// automatic kernel choice then keeps to the block kernels (the pass kernel's
+// k^ buffer grows with the batch), and variant 8 is taken only when asked for.
 dopr_status_t run_attention(dopr_store_t st, int32_t layer,
                             const dopr_attn_args_t *a,
-                            const dopr_score_head_t *head, void *stream) {
+                            const dopr_score_head_t *head, void *stream,
+                            bool no_alloc = false) {
   const bool score = head != nullptr;
   PlanShape shape;
   int32_t n_rep = 0;
   dopr_status_t s = check_attn(st, a, &shape, &n_rep, score);
   if (s != DOPR_OK) return s;
+  if (no_alloc) {
+    if (a->workspace || a->workspace_bytes)
+      return fail(DOPR_ERR_INVALID_ARG,
+                  "workspace must be NULL with 0 bytes: the no-alloc call "
+                  "uses the library's scratch");
+    shape.stream = a->kernel_variant == 8;
+  }
   if (layer < 0 || layer >= st->n_layers)
     return fail(DOPR_ERR_INVALID_ARG, "layer out of range");
   if (score) {
@@ -338,7 +380,7 @@ dopr_status_t run_attention(dopr_store_t st, int32_t layer,
   }
   if (a->n_pairs == 0) return ok();
   if (!a->doc_ids || !a->cu_seqlens || !a->q || !a->k || !a->v ||
-      (!a->out && !score) || !a->workspace)
+      (!a->out && !score) || (!a->workspace && !no_alloc))
     return fail(DOPR_ERR_INVALID_ARG, "NULL buffer");
   if (!a->q_norm_w != !a->k_norm_w)
     return fail(DOPR_ERR_INVALID_ARG,
@@ -356,16 +398,30 @@ dopr_status_t run_attention(dopr_store_t st, int32_t layer,
       return fail(DOPR_ERR_INVALID_ARG,
                   "head norm_w and w_head must be 16-byte aligned");
   }
-  if (reinterpret_cast<uintptr_t>(a->workspace) % kAlign)
-    return fail(DOPR_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
   const size_t need = plan_bytes(shape);
-  if (a->workspace_bytes < need)
-    return fail(DOPR_ERR_WORKSPACE,
-                "workspace holds " + std::to_string(a->workspace_bytes) +
-                    " bytes, needs " + std::to_string(need));
+  void *ws = a->workspace;
+  if (no_alloc) {
+    if (need > kNoAllocScratchBytes)
+      return fail(DOPR_ERR_WORKSPACE,
+                  "the call needs " + std::to_string(need) +
+                      " bytes of scratch; the no-alloc entry point holds " +
+                      std::to_string(kNoAllocScratchBytes) +
+                      " (use dopr_prefix_attn with a workspace)");
+  } else {
+    if (reinterpret_cast<uintptr_t>(a->workspace) % kAlign)
+      return fail(DOPR_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+    if (a->workspace_bytes < need)
+      return fail(DOPR_ERR_WORKSPACE,
+                  "workspace holds " + std::to_string(a->workspace_bytes) +
+                      " bytes, needs " + std::to_string(need));
+  }
   s = check_device(st);
   if (s != DOPR_OK) return s;
-  const Plan plan = plan_carve(a->workspace, shape);
+  if (no_alloc) {
+    s = scratch_ptr(st->device, &ws);
+    if (s != DOPR_OK) return s;
+  }
+  const Plan plan = plan_carve(ws, shape);
   AttnCall call{st, layer, a, n_rep, head};
   hipStream_t hs = as_stream(stream);
   hipError_t e = launch_plan(call, plan, shape, hs);
@@ -382,6 +438,12 @@ extern "C" {
 dopr_status_t dopr_prefix_attn(dopr_store_t st, int32_t layer,
                                const dopr_attn_args_t *a, void *stream) {
   return run_attention(st, layer, a, nullptr, stream);
+}
+
+dopr_status_t dopr_prefix_attn_noalloc(dopr_store_t st, int32_t layer,
+                                       const dopr_attn_args_t *a,
+                                       void *stream) {
+  return run_attention(st, layer, a, nullptr, stream, true);
 }
 
 dopr_status_t dopr_prefix_attn_score_workspace(dopr_store_t st,

@@ -942,15 +942,19 @@ hipError_t launch_attention(const AttnCall &c, const Plan &pl,
   // Tile shape.  Automatic: for score rows, one wave per work unit (shape
   // 7) unless some prefix is longer than kScoreRowsMaxLen (each 32-row unit
   // streams its whole prefix, so long prefixes shared by many pairs are
-  // cheaper staged once per item by shape 6); else two 4-wave blocks per CU
-  // (half the LDS each: 96 prefix slots resident at D = 128, 256 at
-  // D = 64) when every prefix fits, and one 8-wave block per CU with 256
-  // (512) slots resident otherwise.  Variants 2 and 6 keep the block-wide
-  // kernels for score rows (1 and 3 map to 6).
+  // cheaper staged once per item by shape 6).  For full rows the pass kernel
+  // (shape 8) when the plan holds k^ of every token; without that buffer two
+  // 4-wave blocks per CU (half the LDS each: 96 prefix slots resident at
+  // D = 128, 256 at D = 64) when every prefix fits, else one 8-wave block per
+  // CU with 256 (512) slots resident.  Variants 2 and 6 keep the block-wide
+  // kernels for score rows (1, 3 and 8 map to 6).
   const int D = st.head_dim;
   int shape_v = a->kernel_variant;
   if (shape_v == 0 || shape_v == 5)
-    shape_v = score ? (st.max_len <= kScoreRowsMaxLen ? 7 : 6) : 8;
+    shape_v = score ? (st.max_len <= kScoreRowsMaxLen ? 7 : 6)
+              : pl.kh ? 8
+              : st.max_len <= small_chunks(D) * KC ? 6
+                                                   : 2;
   if (score && (shape_v == 1 || shape_v == 3 || shape_v >= 8)) shape_v = 6;
   if (shape_v >= 8 && !pl.kh) return hipErrorInvalidValue;
   e = D == 128 ? launch_passes<128>(p, kp, a->n_pairs, shape_v, score, s)

@@ -23,6 +23,10 @@ constexpr int32_t kScoreRowsMaxLen = 512;
 // logit (log2 units) lies in [-kNoRefBound, kNoRefBound].
 constexpr float kNoRefBound = 64.f;
 
+// Largest attention plan dopr_prefix_attn_noalloc lays out in the library's
+// own scratch array (one copy per device).
+constexpr size_t kNoAllocScratchBytes = DOPR_NOALLOC_SCRATCH_BYTES;
+
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 __host__ __device__ inline int32_t pad8(int32_t n) { return (n + 7) & ~7; }
 
