@@ -213,8 +213,15 @@ def layer_work(st, hidden, inter):
     return dict(proj=proj, mlp=mlp, attention=att, total=proj + mlp + att)
 
 
-def cpu_baseline_layer(st, k_src, v_src, doc_off, x, wts, prm, seconds):
-    """The float64 layer oracle on a bounded sample of pairs."""
+# The decoder layer's elementwise bound: |y - y_ref| <= atol + rtol |y_ref|
+# (about six bf16 roundings feed an output element; the output is bf16).
+LAYER_ATOL, LAYER_RTOL = 2e-2, 2.0 ** -7
+
+
+def cpu_baseline_layer(st, k_src, v_src, doc_off, x, wts, prm, seconds,
+                       y=None):
+    """The float64 layer oracle on a bounded sample of pairs; with y (the
+    GPU layer's output), its rows of the sampled pairs are compared."""
     import torch
 
     import oracle
@@ -243,23 +250,45 @@ def cpu_baseline_layer(st, k_src, v_src, doc_off, x, wts, prm, seconds):
         xs = bits(x.index_select(0, tt))
         pk, pv = bits(k_src.index_select(0, it)), bits(v_src.index_select(0, it))
         t0 = time.perf_counter()
-        oracle.decoder_layer(xs, st.doc_ids[pairs], scu, st.doc_len, sub_off,
-                             pk, pv, wb, bits(prm["q_norm_w"]),
-                             bits(prm["k_norm_w"]), n_q_heads=st.n_q_heads,
-                             n_kv_heads=st.n_kv_heads, L=L)
-        return time.perf_counter() - t0
+        yr, _, _ = oracle.decoder_layer(xs, st.doc_ids[pairs], scu,
+                                        st.doc_len, sub_off, pk, pv, wb,
+                                        bits(prm["q_norm_w"]),
+                                        bits(prm["k_norm_w"]),
+                                        n_q_heads=st.n_q_heads,
+                                        n_kv_heads=st.n_kv_heads, L=L)
+        dt = time.perf_counter() - t0
+        if y is not None:
+            g = y.index_select(0, tt).double().cpu().numpy()
+            d = np.abs(g - yr)
+            par["max_abs_y"] = max(par["max_abs_y"], float(d.max()))
+            par["max_bound_ratio"] = max(
+                par["max_bound_ratio"],
+                float((d / (LAYER_ATOL + LAYER_RTOL * np.abs(yr))).max()))
+            par["pairs"] += len(pairs)
+            par["rows"] += int(yr.shape[0])
+        return dt
 
+    par = {"max_abs_y": 0.0, "max_bound_ratio": 0.0, "pairs": 0, "rows": 0}
     total_t, total_n, i = 0.0, 0, 0
     while total_t < seconds and i < st.n_pairs:
         n = min(max(1, total_n), st.n_pairs - i)   # doubling batches
         total_t += run(order[i:i + n])
         total_n += n
         i += n
-    return {"value": round(total_n / total_t, 3), "unit": "pairs/s",
-            "cores": int(threads), "kind": "oracle",
-            "sample": f"{total_n} of {st.n_pairs} pairs (seeded random "
-                      f"order), float64 decoder-layer oracle (numpy "
-                      f"projections, C attention), {total_t:.1f}s"}
+    model, n_aff = host_cpu()
+    res = {"value": round(total_n / total_t, 3), "unit": "pairs/s",
+           "cores": int(min(threads, n_aff)), "kind": "oracle",
+           "sample": f"{total_n} of {st.n_pairs} pairs (seeded random "
+                     f"order), float64 decoder-layer oracle (numpy "
+                     f"projections, C attention), {total_t:.1f}s",
+           "cpu_model": model, "affinity_cpus": n_aff,
+           "omp_threads": int(threads)}
+    if y is not None:
+        for k in ("max_abs_y", "max_bound_ratio"):
+            par[k] = float(f"{par[k]:.3e}")
+        par["bound"] = f"|dy| <= {LAYER_ATOL} + 2^-7 |y|"
+        res["parity"] = par
+    return res
 
 
 def measured_traffic(config, variant, path_kind="full"):
@@ -285,16 +314,37 @@ def bits(t):
         np.uint16)
 
 
+PARITY_TOL = 2e-2   # max-abs on O, lse and s (bf16 inputs, fp32 accumulation)
+
+
+def host_cpu():
+    """The host's CPU model and the number of CPUs this process may run on."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return model, len(os.sched_getaffinity(0))
+
+
 def cpu_baseline(st, k_src, v_src, doc_off, online, prm, seconds,
-                 last_only=False, family=None):
+                 last_only=False, family=None, got=None):
     """The float64 oracle on a bounded sample of the same workload's pairs
     (deterministic order), on this host's cores.  last_only: the oracle of
-    last-layer scoring (score-token rows only)."""
+    last-layer scoring (score-token rows only).  got: the GPU step's
+    outputs (out, lse or None, score), compared with the oracle on every
+    sampled pair; the maximum absolute differences go to result["parity"]."""
     import torch
 
     import oracle
     L = oracle.lib()
     threads = oracle.max_threads(L)
+    par = {"max_abs_O": 0.0, "max_abs_lse": None, "max_abs_s": 0.0,
+           "pairs": 0, "rows": 0}
     rng = np.random.default_rng(99)
     order = rng.permutation(st.n_pairs)
     cu = st.cu_seqlens.astype(np.int64)
@@ -329,12 +379,31 @@ def cpu_baseline(st, k_src, v_src, doc_off, online, prm, seconds,
                    "rope_inv_freq": family["rope_inv_freq"].double().cpu()
                    .numpy()}
         t0 = time.perf_counter()
-        out, _, _ = oracle.prefix_attn(*args, n_q_heads=st.n_q_heads,
-                                       n_kv_heads=st.n_kv_heads,
-                                       last_only=last_only, L=L, **fam)
+        out, lse, _ = oracle.prefix_attn(*args, n_q_heads=st.n_q_heads,
+                                         n_kv_heads=st.n_kv_heads,
+                                         last_only=last_only, L=L, **fam)
         h = (out if last_only else out[scu[1:] - 1]).reshape(len(pairs), -1)
-        oracle.score(h, nw, wh, L=L)
-        return time.perf_counter() - t0
+        _, s = oracle.score(h, nw, wh, L=L)
+        dt = time.perf_counter() - t0
+        if got is not None:
+            pt = torch.from_numpy(pairs.astype(np.int64)).to(dev)
+            rows = pt if last_only else tt
+            if got.get("out") is not None:
+                g_out = got["out"].index_select(0, rows).double().cpu().numpy()
+                par["max_abs_O"] = max(par["max_abs_O"],
+                                       float(np.abs(g_out - out).max()))
+            if got.get("lse") is not None:
+                g_lse = got["lse"].index_select(0, rows).double().cpu().numpy()
+                fin = np.isfinite(lse)
+                e = float(np.abs(g_lse[fin] - lse[fin]).max()) if fin.any() \
+                    else 0.0
+                par["max_abs_lse"] = max(par["max_abs_lse"] or 0.0, e)
+            g_s = got["score"].index_select(0, pt).double().cpu().numpy()
+            par["max_abs_s"] = max(par["max_abs_s"],
+                                   float(np.abs(g_s - s).max()))
+            par["pairs"] += len(pairs)
+            par["rows"] += int(out.shape[0] * out.shape[1])
+        return dt
 
     # calibrate on one pair per thread, then size the sample to the budget
     first = order[:min(threads, st.n_pairs)]
@@ -348,12 +417,22 @@ def cpu_baseline(st, k_src, v_src, doc_off, online, prm, seconds,
         more = order[len(first):len(first) + n_more]
         total_t += run(more)
         total_n += len(more)
-    return {"value": round(total_n / total_t, 3), "unit": "pairs/s",
-            "cores": int(threads), "kind": "oracle",
-            "sample": f"{total_n} of {st.n_pairs} pairs (seeded random "
-                      f"order), float64 C oracle"
-                      f"{' of the score-token rows' if last_only else ''} "
-                      f"incl. score head, {total_t:.1f}s"}
+    model, n_aff = host_cpu()
+    res = {"value": round(total_n / total_t, 3), "unit": "pairs/s",
+           "cores": int(min(threads, n_aff)), "kind": "oracle",
+           "sample": f"{total_n} of {st.n_pairs} pairs (seeded random "
+                     f"order), float64 C oracle"
+                     f"{' of the score-token rows' if last_only else ''} "
+                     f"incl. score head, {total_t:.1f}s",
+           "cpu_model": model, "affinity_cpus": n_aff,
+           "omp_threads": int(threads)}
+    if got is not None:
+        for k in ("max_abs_O", "max_abs_lse", "max_abs_s"):
+            if par[k] is not None:
+                par[k] = float(f"{par[k]:.3e}")
+        par["tol"] = PARITY_TOL
+        res["parity"] = par
+    return res
 
 
 def salience_work(lens, hq, D=128):
@@ -848,13 +927,35 @@ def main():
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a bounded sample")
         if layer_path:
-            result["cpu_baseline"] = cpu_baseline_layer(
-                st, k_src, v_src, doc_off, x, wts, prm, args.cpu_seconds)
+            cb = cpu_baseline_layer(st, k_src, v_src, doc_off, x, wts, prm,
+                                    args.cpu_seconds, y=step.y)
+            result["parity"] = cb.pop("parity", None)
+            result["cpu_baseline"] = cb
         else:
-            result["cpu_baseline"] = cpu_baseline(
-                st, k_src, v_src, doc_off, online, prm, args.cpu_seconds,
-                last_only=score_path, family=fam)
+            got = None
+            if score_path:
+                got = {"out": step.out, "lse": step.lse, "score": step.score}
+            elif not score_path:
+                # one more (untimed) step that also writes the LSE; the
+                # outputs are deterministic, so O and s are those timed
+                step.lse = torch.empty((st.n_tokens, st.n_q_heads),
+                                       dtype=torch.float32, device=dev)
+                one_step()
+                torch.cuda.synchronize()
+                got = {"out": step.out, "lse": step.lse, "score": step.score}
+            cb = cpu_baseline(st, k_src, v_src, doc_off, online, prm,
+                              args.cpu_seconds, last_only=score_path,
+                              family=fam, got=got)
+            result["parity"] = cb.pop("parity", None)
+            result["cpu_baseline"] = cb
     print(json.dumps(result), flush=True)
+    par = result.get("parity")
+    if par and "max_bound_ratio" in par:
+        if par["max_bound_ratio"] > 1.0:
+            raise SystemExit(f"layer parity beyond its bound: {par}")
+    elif par and max(par["max_abs_O"], par["max_abs_s"],
+                     par["max_abs_lse"] or 0.0) > PARITY_TOL:
+        raise SystemExit(f"parity above {PARITY_TOL}: {par}")
 
 
 if __name__ == "__main__":

@@ -27,7 +27,9 @@
  * Conventions shared by every call
  *   - All device buffers are allocated by the caller and passed as raw device
  *     pointers; the library never calls hipMalloc/hipFree.  Buffers must stay
- *     alive until the stream has passed the call.
+ *     alive until the stream has passed the call.  (The one exception is
+ *     dopr_prefix_attn_noalloc, whose plan lives in a fixed scratch array
+ *     that the library's code object holds on each device.)
  *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
  *     Every call is asynchronous on that stream unless stated otherwise.
  *   - bf16 means IEEE bfloat16 bit patterns (uint16); fp32 means IEEE float.
@@ -151,14 +153,20 @@ typedef struct {
   int32_t n_pairs;          /* P >= 0                                       */
   int32_t n_q_heads;        /* Hq, multiple of the store's Hkv              */
   int32_t max_tokens;       /* upper bound on every T_p (>= 1)              */
-  int32_t kernel_variant;   /* 0 = automatic; 1, 2, 3, 6 select a tile
-                               shape (identical results; for tuning
+  int32_t kernel_variant;   /* 0 = automatic (8); 1, 2, 3, 6, 8 select a
+                               kernel (identical results; for tuning
                                sweeps): 1 = 4 waves x 64 rows, 2 = 8 waves
                                x 32 rows, 3 = 4 waves x 32 rows (each one
                                block per CU, 256 prefix slots resident;
                                512 at D = 64), 6 = 4 waves x 32 rows, two
                                blocks per CU, 96 slots resident (256 at
-                               D = 64);
+                               D = 64); 8 = the pass kernel: one 8-wave
+                               block per CU takes a (work item, kv head)
+                               unit, keeps the prefix in LDS for all its
+                               passes of 256 rows, and reads the own keys
+                               from a k^ buffer in the workspace (2 Hkv D
+                               bytes per online token) filled by a
+                               separate normalise-and-rotate kernel;
                                4 = exact running-max softmax for every row
                                (slower; the reference for the fast path);
                                5 = self-check: the fast pass queues every
@@ -174,7 +182,7 @@ typedef struct {
   const void *k_norm_w;     /* dev bf16 [D], or NULL (see q_norm_w)         */
   float rms_eps;            /* e.g. 1e-6                                    */
   float rope_theta;         /* e.g. 1e6                                     */
-  float softmax_scale;      /* e.g. 1/sqrt(D)                               */
+  float softmax_scale;      /* e.g. 1/sqrt(D); finite and > 0               */
   void *out;                /* dev bf16 [Ntok, Hq, D]                       */
   float *lse;               /* dev fp32 [Ntok, Hq] natural-log sum-exp of
                                the scaled logits, or NULL                   */
@@ -187,6 +195,13 @@ typedef struct {
   const float *rope_inv_freq; /* dev fp32 [D/2] rotation frequencies
                                omega_i (e.g. a family's rescaled ones), or
                                NULL for rope_theta^(-2i/D); 4-byte aligned */
+  int32_t rows_per_item;    /* 0 = automatic.  Else the size, in stacked
+                               rows (token x q head of one kv head), of the
+                               work items a document's rows are cut into:
+                               a multiple of 32 in [64, 2^20].  Outputs do
+                               not depend on it (a tuning and test knob).
+                               Full-row calls only: must be 0 for
+                               dopr_prefix_attn_score (INVALID_ARG).        */
 } dopr_attn_args_t;
 
 /* Workspace bytes needed by dopr_prefix_attn for these arguments (host). */
@@ -332,8 +347,6 @@ dopr_status_t dopr_decoder_layer(dopr_store_t st, int32_t layer,
                                  const dopr_layer_args_t *lw, void *stream);
 
 /* ------------------------------------------------------------------------ */
-/* Exports used by the bit-exact tests of the integer steps.               */
-
 /* ------------------------------------------------------------------------ */
 /* Offline salience selection (Sec. 3.2.1, applied offline in Sec. 3.3): for
  * each document, independently encoded at positions 0..n_d-1, with the final
@@ -358,7 +371,7 @@ typedef struct {
   int32_t n_q_heads;         /* Hq, multiple of n_kv_heads                 */
   int32_t n_kv_heads;        /* Hkv >= 1                                   */
   int32_t top_p;             /* p, 1..64                                   */
-  float softmax_scale;       /* e.g. 1/sqrt(D)                             */
+  float softmax_scale;       /* e.g. 1/sqrt(D); finite and > 0             */
   int64_t total_tokens;      /* Ntok = cu_doclens[n_docs]                  */
   int64_t total_select;      /* cu_select[n_docs] (ignored if selected is
                                 NULL)                                      */
@@ -404,7 +417,12 @@ dopr_status_t dopr_salience(const dopr_salience_args_t *args, void *stream);
 dopr_status_t dopr_select_top_k(const dopr_salience_args_t *args,
                                 void *stream);
 
-/* Doc-id grouping in canonical form: valid pairs (doc id in range and
+/* ------------------------------------------------------------------------ */
+/* Exports used by the bit-exact tests of the integer steps.               */
+
+/* Doc-id grouping (Sec. 3.4 with Sec. 4.5.2: the pairs that retrieve the
+ * same document share its stored prefix, so they are batched by document)
+ * in canonical form: valid pairs (doc id in range and
  * resident) sorted by (doc id, pair index).  group_doc[G] ascending doc ids,
  * group_ptr[G+1] offsets into pair_order[], pair_order[n_valid] pair indices.
  * Capacities: group_doc and pair_order >= n_pairs, group_ptr >= n_pairs+1.
@@ -418,6 +436,7 @@ dopr_status_t dopr_group_pairs(dopr_store_t st, int32_t n_pairs,
                                void *stream);
 
 /* Gather the prefix K/V states of doc_ids[i] for one layer out of the store
+ * (Sec. 3.4: a candidate's stored prefix states are fetched by its id)
  * into canonical layout: k_out/v_out dev bf16 [out_cu_slots[n], Hkv, D],
  * pair i's slots at rows out_cu_slots[i] .. out_cu_slots[i+1]-1.  A bad doc
  * id, or a slot range that differs from L_d, leaves its rows untouched and
@@ -426,6 +445,9 @@ dopr_status_t dopr_gather_prefix(dopr_store_t st, int32_t layer, int32_t n,
                                  const int32_t *doc_ids,
                                  const int64_t *out_cu_slots, void *k_out,
                                  void *v_out, void *stream);
+
+/* ------------------------------------------------------------------------ */
+/* Status (library plumbing; no passage of the paper defines it).          */
 
 /* Synchronise `stream`, then return (and clear) the first deferred device
  * error raised by calls on this store since the last check, else DOPR_OK.  */

@@ -77,9 +77,15 @@ def load_library(path: str):
 
 
 def lib():
+    """The oracle library, built on first use.  DOPR_ORACLE_LIB names another
+    build of the same source to load instead (the sanitizer test's)."""
     global _lib
     with _lock:
         if _lib is None:
+            other = os.environ.get("DOPR_ORACLE_LIB")
+            if other:
+                _lib = load_library(other)
+                return _lib
             if not os.path.exists(_LIB) or (
                     os.path.getmtime(_LIB) < os.path.getmtime(_SRC)):
                 build()

@@ -51,7 +51,8 @@ class _AttnArgs(ctypes.Structure):
                 ("workspace_bytes", ctypes.c_size_t),
                 ("timing_begin", ctypes.c_void_p),
                 ("timing_end", ctypes.c_void_p),
-                ("rope_inv_freq", ctypes.c_void_p)]
+                ("rope_inv_freq", ctypes.c_void_p),
+                ("rows_per_item", ctypes.c_int32)]
 
 
 class _ScoreArgs(ctypes.Structure):
@@ -260,7 +261,8 @@ def dopr_store_copy_docs(dst: Store, src: Store, stream=None):
 def _attn_args(store, doc_ids, cu_seqlens, q, k, v, q_norm_w, k_norm_w, out,
                lse, workspace, *, max_tokens, total_tokens=None,
                rms_eps=1e-6, rope_theta=1e6, softmax_scale=None,
-               kernel_variant=0, timing=None, rope_inv_freq=None):
+               kernel_variant=0, timing=None, rope_inv_freq=None,
+               rows_per_item=0):
     n_q_heads = q.shape[1] if q is not None else store.n_kv_heads
     if total_tokens is None:
         total_tokens = q.shape[0]
@@ -275,12 +277,13 @@ def _attn_args(store, doc_ids, cu_seqlens, q, k, v, q_norm_w, k_norm_w, out,
                      float(rope_theta), float(softmax_scale), _ptr(out),
                      _ptr(lse), _ptr(workspace), ws_bytes,
                      *(timing if timing is not None else (None, None)),
-                     _ptr(rope_inv_freq))
+                     _ptr(rope_inv_freq), int(rows_per_item))
 
 
 def _shape_args(n_pairs, n_q_heads, max_tokens, total_tokens,
-                kernel_variant):
+                kernel_variant, rows_per_item=0):
     a = _AttnArgs()
+    a.rows_per_item = rows_per_item
     a.n_pairs = n_pairs
     a.n_q_heads = n_q_heads
     a.max_tokens = max_tokens
@@ -292,9 +295,9 @@ def _shape_args(n_pairs, n_q_heads, max_tokens, total_tokens,
 
 def dopr_prefix_attn_workspace(store: Store, *, n_pairs, n_q_heads,
                                max_tokens, total_tokens,
-                               kernel_variant=0) -> int:
+                               kernel_variant=0, rows_per_item=0) -> int:
     a = _shape_args(n_pairs, n_q_heads, max_tokens, total_tokens,
-                    kernel_variant)
+                    kernel_variant, rows_per_item)
     n = ctypes.c_size_t(0)
     _check(lib().dopr_prefix_attn_workspace(store.handle, ctypes.byref(a),
                                             ctypes.byref(n)))
@@ -316,17 +319,19 @@ def dopr_prefix_attn(store: Store, layer: int, doc_ids, cu_seqlens, q, k, v,
                      q_norm_w, k_norm_w, out, workspace, *, max_tokens,
                      lse=None, total_tokens=None, rms_eps=1e-6,
                      rope_theta=1e6, softmax_scale=None, kernel_variant=0,
-                     timing=None, rope_inv_freq=None, stream=None):
+                     timing=None, rope_inv_freq=None, stream=None,
+                     rows_per_item=0):
     """`timing` is an optional (begin, end) pair of raw hipEvent_t handles
     recorded around the attention kernel.  q_norm_w and k_norm_w may both
     be None (no QK-norm); rope_inv_freq is an optional fp32 [D/2] device
-    tensor of rotation frequencies."""
+    tensor of rotation frequencies; rows_per_item 0 is the automatic work
+    item size."""
     a = _attn_args(store, doc_ids, cu_seqlens, q, k, v, q_norm_w, k_norm_w,
                    out, lse, workspace, max_tokens=max_tokens,
                    total_tokens=total_tokens, rms_eps=rms_eps,
                    rope_theta=rope_theta, softmax_scale=softmax_scale,
                    kernel_variant=kernel_variant, timing=timing,
-                   rope_inv_freq=rope_inv_freq)
+                   rope_inv_freq=rope_inv_freq, rows_per_item=rows_per_item)
     _check(lib().dopr_prefix_attn(store.handle, layer, ctypes.byref(a),
                                   _stream(stream)))
 

@@ -153,9 +153,21 @@ dopr_status_t check_attn(const dopr_store *st, const dopr_attn_args_t *a,
   shape->n_pairs = a->n_pairs;
   shape->n_rep = *n_rep;
   shape->max_tokens = a->max_tokens;
+  if (a->rows_per_item != 0) {
+    if (score_only)
+      return fail(DOPR_ERR_INVALID_ARG,
+                  "rows_per_item must be 0 for last-layer scoring");
+    // near-equal cuts of >= 32 rows each keep every item non-empty
+    if (a->rows_per_item < 64 || a->rows_per_item > (1 << 20) ||
+        a->rows_per_item % 32)
+      return fail(DOPR_ERR_INVALID_ARG,
+                  "rows_per_item must be 0 or a multiple of 32 in "
+                  "[64, 2^20]");
+  }
   shape->rows_per_item =
-      default_rows_per_item(a->kernel_variant, score_only, st->max_len,
-                            *n_rep);
+      a->rows_per_item ? a->rows_per_item
+                       : default_rows_per_item(a->kernel_variant, score_only,
+                                               st->max_len, *n_rep);
   shape->n_docs = st->n_docs;
   shape->total_tokens = a->total_tokens;
   shape->max_len = st->max_len;
@@ -709,8 +721,11 @@ dopr_status_t check_salience(const dopr_salience_args_t *a, bool full,
       return fail(a->top_p > kSalienceMaxP ? DOPR_ERR_UNSUPPORTED
                                            : DOPR_ERR_INVALID_ARG,
                   "top_p must be in [1, 64]");
-    if (!std::isfinite(a->softmax_scale))
-      return fail(DOPR_ERR_INVALID_ARG, "softmax_scale must be finite");
+    // the row pass scales each chunk's largest logit once: a positive
+    // scale keeps it the largest scaled logit
+    if (!(a->softmax_scale > 0.f) || !std::isfinite(a->softmax_scale))
+      return fail(DOPR_ERR_INVALID_ARG,
+                  "softmax_scale must be finite and > 0");
   }
   if (a->n_docs == 0 || !ptrs) return ok();
   if (!a->cu_doclens || !a->u)

@@ -41,7 +41,8 @@ class OnlineStep:
     store, then the score head on each pair's score-token output row."""
 
     def __init__(self, store, *, n_pairs, n_q_heads, total_tokens,
-                 max_tokens, kernel_variant=0, device="cuda", with_lse=False):
+                 max_tokens, kernel_variant=0, device="cuda", with_lse=False,
+                 rows_per_item=0):
         import torch
         self.store = store
         self.n_pairs = n_pairs
@@ -49,10 +50,11 @@ class OnlineStep:
         self.total_tokens = total_tokens
         self.max_tokens = max_tokens
         self.kernel_variant = kernel_variant
+        self.rows_per_item = rows_per_item
         nbytes = dopr_prefix_attn_workspace(
             store, n_pairs=n_pairs, n_q_heads=n_q_heads,
             max_tokens=max_tokens, total_tokens=total_tokens,
-            kernel_variant=kernel_variant)
+            kernel_variant=kernel_variant, rows_per_item=rows_per_item)
         self.workspace = torch.empty(max(nbytes, 256), dtype=torch.uint8,
                                      device=device)
         self.out = torch.empty((total_tokens, n_q_heads, store.head_dim),
@@ -70,7 +72,7 @@ class OnlineStep:
                          max_tokens=self.max_tokens, lse=self.lse,
                          total_tokens=self.total_tokens,
                          kernel_variant=self.kernel_variant, stream=stream,
-                         **kw)
+                         rows_per_item=self.rows_per_item, **kw)
 
     def score_head(self, cu_seqlens, norm_w, w_head, stream=None,
                    rms_eps=1e-6):

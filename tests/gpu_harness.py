@@ -173,6 +173,53 @@ def sample_pairs(st, n_random, seed=0, include_largest_group=True,
     return np.array(sorted(picks), np.int64)
 
 
+def pass_strata(st, rows_per_item=2048, pass_rows=256):
+    """Where each valid pair sits among the 256-row passes of its work item,
+    from the canonical grouping (pairs of a document in pair order, T_p *
+    n_rep stacked rows each, a group's rows cut into near-equal items on
+    32-row boundaries): 0 = its first row is in the item's first pass,
+    2 = its last row is in the item's last pass (and not 0), 1 = neither.
+    Pairs without a valid document get -1."""
+    gd, gp, order = oracle.group(st.doc_ids, st.doc_len)
+    n_rep = st.n_q_heads // st.n_kv_heads
+    rows = st.seqlens[order].astype(np.int64) * n_rep
+    prow = np.zeros(len(order) + 1, np.int64)
+    np.cumsum(rows, out=prow[1:])
+    pos = np.full(st.n_pairs, -1, np.int64)
+    for g in range(len(gd)):
+        s0, s1 = int(gp[g]), int(gp[g + 1])
+        base, R = int(prow[s0]), int(prow[s1] - prow[s0])
+        n_it = -(-R // rows_per_item)
+        cuts = np.array([base + ((k * R // n_it) & ~31) for k in range(n_it)]
+                        + [base + R], np.int64)
+        for s in range(s0, s1):
+            r0, r1 = int(prow[s]), int(prow[s + 1]) - 1
+            k = min(int(np.searchsorted(cuts, r0, "right")) - 1, n_it - 1)
+            a, b = int(cuts[k]), int(cuts[k + 1])
+            n_pass = -(-(b - a) // pass_rows)
+            first = (r0 - a) // pass_rows == 0
+            k1 = min(int(np.searchsorted(cuts, r1, "right")) - 1, n_it - 1)
+            a1, b1 = int(cuts[k1]), int(cuts[k1 + 1])
+            last = (r1 - a1) // pass_rows == -(-(b1 - a1) // pass_rows) - 1
+            pos[order[s]] = 0 if first else (2 if last else 1)
+    return pos
+
+
+def stratified_pairs(st, per_stratum, seed=0, max_group=None):
+    """per_stratum pairs (or all there are) from each pass_strata class, plus
+    the most-reused document's group and the first and last pair."""
+    rng = np.random.default_rng(4321 + seed)
+    pos = pass_strata(st)
+    picks = set()
+    for c in (0, 1, 2):
+        m = np.nonzero(pos == c)[0]
+        if len(m):
+            picks.update(rng.choice(m, min(per_stratum, len(m)),
+                                    replace=False).tolist())
+    picks.update(sample_pairs(st, 0, seed, max_group=max_group).tolist())
+    return np.array(sorted(picks), np.int64), pos
+
+
 # ---------------------------------------------------------------------------
 # Last-layer scoring (score-token rows with the fused score head).
 

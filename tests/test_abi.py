@@ -196,6 +196,17 @@ def test_salience_host_validation_and_workspace():
     assert "q and k" in D.dopr_last_error()
     a.q, a.k = 256, 256
     assert L.dopr_salience(ctypes.byref(a), None) == D.DOPR_ERR_WORKSPACE
+    # the row pass relies on a positive scale (the chunk maximum stays the
+    # largest scaled logit): zero, negative and non-finite scales are refused
+    for bad in (0.0, -0.088, float("inf"), float("nan")):
+        a.softmax_scale = bad
+        assert L.dopr_salience(ctypes.byref(a), None) == \
+            D.DOPR_ERR_INVALID_ARG, bad
+        assert "softmax_scale" in D.dopr_last_error()
+        n = ctypes.c_size_t(0)
+        assert L.dopr_salience_workspace(ctypes.byref(a), ctypes.byref(n)) \
+            == D.DOPR_ERR_INVALID_ARG, bad
+    a.softmax_scale = 0.088
     a.selected = 256
     assert L.dopr_select_top_k(ctypes.byref(a), None) == \
         D.DOPR_ERR_INVALID_ARG
