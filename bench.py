@@ -291,21 +291,36 @@ def cpu_baseline_layer(st, k_src, v_src, doc_off, x, wts, prm, seconds,
     return res
 
 
-def measured_traffic(config, variant, path_kind="full"):
-    """HBM bytes per attention launch from the committed rocprofv3 counter
-    summary of this workload, or None when there is none or the kernel's
-    sources changed since the counters were taken."""
+def _profile_value(config, variant, path_kind, what, key):
+    """A figure of the committed rocprofv3 summary of this workload's
+    attention (what: "traffic" or "pmc"), or None when there is none, the
+    run used a non-default kernel, or the kernels' sources changed since the
+    counters were taken."""
     from paper_2609_03311_amd import profiling
-    tag = "k_prefix_attn_score" if path_kind == "score" else "k_prefix_attn"
-    path = os.path.join(ROOT, "profiles", f"{tag}_{config}_traffic.txt")
+    tag = "k_score_rows" if path_kind == "score" else "k_pass_attn"
+    path = os.path.join(ROOT, "profiles", f"{tag}_{config}_{what}.txt")
     vals = profiling.read_summary(path)
-    if variant != 0 or "traffic_bytes_per_launch" not in vals:
+    if variant != 0 or key not in vals:
         return None
     if vals.get("kernel_source_sha") != profiling.kernel_source_sha():
         log(f"{os.path.basename(path)} describes other kernel sources; "
-            "traffic = null")
+            f"{key} = null")
         return None
-    return int(float(vals["traffic_bytes_per_launch"]))
+    return float(vals[key])
+
+
+def measured_traffic(config, variant, path_kind="full"):
+    """HBM bytes (FETCH_SIZE + WRITE_SIZE, calibrated) per attention step."""
+    v = _profile_value(config, variant, path_kind, "traffic",
+                       "traffic_bytes_per_launch")
+    return None if v is None else int(v)
+
+
+def measured_mfma_util(config, variant, path_kind="full"):
+    """Fraction of the SIMDs' cycles their MFMA units were busy during the
+    attention launches (SQ_VALU_MFMA_BUSY_CYCLES over SIMDs x active
+    cycles), from the committed counter summary."""
+    return _profile_value(config, variant, path_kind, "pmc", "mfma_busy_frac")
 
 
 def bits(t):
@@ -858,12 +873,13 @@ def main():
                  flops=lw["attention"],
                  unique_docs=len(np.unique(st.doc_ids)))
         achieved = lw["total"] / (ms_step * 1e-3) / 1e12
-        traffic = None
+        traffic = mfma_util = None
     else:
         w = (algorithmic_work_score(st, not args.no_score_rows) if score_path
              else algorithmic_work(st))
         achieved = w["total"] / (attn_avg * 1e-3) / 1e9
         traffic = measured_traffic(args.config, args.variant, args.path)
+        mfma_util = measured_mfma_util(args.config, args.variant, args.path)
     if score_path and args.no_score_rows:
         traffic = None
     result = {
@@ -918,6 +934,9 @@ def main():
             "frac": round(achieved / PEAK_HBM_GBS, 4),
             "traffic": traffic,
         }),
+        # MFMA busy fraction of the attention launches, from the committed
+        # rocprofv3 --pmc summary of the same workload (null without one)
+        "mfma_util": mfma_util,
     }
     if layer_path:
         result["algorithmic_gb"] = None   # MFMA-bound: flops, not bytes

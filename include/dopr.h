@@ -153,7 +153,9 @@ typedef struct {
   int32_t n_pairs;          /* P >= 0                                       */
   int32_t n_q_heads;        /* Hq, multiple of the store's Hkv              */
   int32_t max_tokens;       /* upper bound on every T_p (>= 1)              */
-  int32_t kernel_variant;   /* 0 = automatic (8); 1, 2, 3, 6, 8 select a
+  int32_t kernel_variant;   /* 0 = automatic: 8, or 6 when every prefix is
+                               at most 96 slots at D = 128; 1, 2, 3, 6, 8
+                               select a
                                kernel (identical results; for tuning
                                sweeps): 1 = 4 waves x 64 rows, 2 = 8 waves
                                x 32 rows, 3 = 4 waves x 32 rows (each one

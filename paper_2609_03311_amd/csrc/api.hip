@@ -94,16 +94,13 @@ dopr_status_t layout_store(const dopr_store_desc_t *d, StoreLayout *lay,
   return DOPR_OK;
 }
 
-bool uses_stream_kernel(int32_t variant);
+bool uses_stream_kernel(int32_t variant, const dopr_store *st);
 
-// Rows per work item: long items for the block-wide kernels (a document's
-// prefix is staged once per item), 32 for the one-wave-per-unit score
-// kernel that the automatic choice takes when every prefix is at most
-// kScoreRowsMaxLen slots, and one pass (256 rows; at most 64 pairs) for the
-// streaming kernel: a document's items then sit next to each other in one XCD's
-// queue, neighbouring CUs take them at the same time, and its prefix and
-// own-key chunks are fetched from HBM once and read from that XCD's L2 by
-// the others.
+// Rows per work item: long items for the full layer (the block kernels and
+// the pass kernel stage a document's prefix once per item and walk the item
+// in passes), and 32 for the one-wave-per-unit score kernel that the
+// automatic choice takes when every prefix is at most kScoreRowsMaxLen
+// slots.
 int32_t default_rows_per_item(int32_t variant, bool score_only,
                               int32_t max_len, int32_t n_rep) {
   if (score_only)
@@ -114,10 +111,15 @@ int32_t default_rows_per_item(int32_t variant, bool score_only,
   return 2048;
 }
 
-// The full layer runs the streaming kernel in the automatic choice, the
-// self-check mode and variant 8 (its plan then holds k^ of every token).
-bool uses_stream_kernel(int32_t variant) {
-  return variant == 0 || variant == 5 || variant == 8;
+// The full layer runs the pass kernel for variant 8 and, in the automatic
+// choice and the self-check mode, unless every prefix is short at head size
+// 128 (at most 96 slots: two 4-wave blocks per CU keep it resident, and the
+// pass kernel's per-pass costs outweigh its savings there).  Its plan then
+// holds k^ of every token.
+bool uses_stream_kernel(int32_t variant, const dopr_store *st) {
+  if (variant == 8) return true;
+  if (variant != 0 && variant != 5) return false;
+  return !(st->head_dim == 128 && st->max_len <= kShortPrefix128);
 }
 
 // Validation shared by the workspace query and the attention call.
@@ -174,7 +176,7 @@ dopr_status_t check_attn(const dopr_store *st, const dopr_attn_args_t *a,
   shape->n_kv_heads = st->n_kv_heads;
   shape->head_dim = st->head_dim;
   shape->score_only = score_only;
-  shape->stream = !score_only && uses_stream_kernel(a->kernel_variant);
+  shape->stream = !score_only && uses_stream_kernel(a->kernel_variant, st);
   return DOPR_OK;
 }
 

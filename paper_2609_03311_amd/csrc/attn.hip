@@ -955,6 +955,8 @@ hipError_t launch_attention(const AttnCall &c, const Plan &pl,
               : pl.kh ? 8
               : st.max_len <= small_chunks(D) * KC ? 6
                                                    : 2;
+  static_assert(small_chunks(128) * KC == kShortPrefix128,
+                "short prefixes are those two blocks per CU keep resident");
   if (score && (shape_v == 1 || shape_v == 3 || shape_v >= 8)) shape_v = 6;
   if (shape_v >= 8 && !pl.kh) return hipErrorInvalidValue;
   e = D == 128 ? launch_passes<128>(p, kp, a->n_pairs, shape_v, score, s)

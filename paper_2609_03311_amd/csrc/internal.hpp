@@ -27,6 +27,10 @@ constexpr float kNoRefBound = 64.f;
 // own scratch array (one copy per device).
 constexpr size_t kNoAllocScratchBytes = DOPR_NOALLOC_SCRATCH_BYTES;
 
+// Longest prefix for which the automatic choice at head size 128 runs two
+// 4-wave blocks per CU (96 slots resident each) instead of the pass kernel.
+constexpr int32_t kShortPrefix128 = 96;
+
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 __host__ __device__ inline int32_t pad8(int32_t n) { return (n + 7) & ~7; }
 

@@ -9,9 +9,14 @@ into a per-kernel table.  `traffic` turns two `--pmc FETCH_SIZE` /
 `--pmc WRITE_SIZE` runs of `bench.py --copy-calibration` into HBM bytes per
 launch of the attention kernel: each counter (KiB per dispatch) is scaled by
 what the same counter reads for the calibration kernel, a plain streaming
-kernel that reads and writes exactly `CALIB_BYTES`.  The summary records a
-hash of the kernel's sources so a reader can tell whether the figures still
-describe the code.
+kernel that reads and writes exactly `CALIB_BYTES`.  `pmc` condenses
+`--pmc` runs of shader counters into MFMA, VALU and LDS utilisation and wait
+fractions per kernel.  Every summary records a hash of the kernels' sources
+so a reader can tell whether the figures still describe the code.
+
+The full layer's attention is two launches: `k_own_khat` (k^ of every
+online token) and the pass kernel `k_pass_attn`; both are timed and
+counted together as one attention step.
 """
 import argparse
 import csv
@@ -21,14 +26,15 @@ import re
 import sys
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-KERNEL_SOURCES = ("csrc/attn.hip", "csrc/internal.hpp")
-# the dominant kernel of each path on the Qwen3-8B-shaped workload (head
-# size 128): 8 waves, 256 slots resident (full layer); two 4-wave blocks per
-# CU (score rows).  At head size 64 the same shapes hold 512 and 192 slots.
-ATTN_KERNEL = r"k_prefix_attn<8, ?1, ?false, ?false, ?128, ?8>"
-SCORE_KERNEL = r"k_prefix_attn<4, ?1, ?false, ?true, ?128, ?3>"
-ATTN_KERNEL_D64 = r"k_prefix_attn<8, ?1, ?false, ?false, ?64, ?16>"
-SCORE_KERNEL_D64 = r"k_prefix_attn<4, ?1, ?false, ?true, ?64, ?6>"
+KERNEL_SOURCES = ("csrc/attn.hip", "csrc/attn_common.hpp", "csrc/stream.hip",
+                  "csrc/internal.hpp")
+# the attention launches of each path on the Qwen3-8B-shaped workload (head
+# size 128): k^ precompute + pass kernel (full layer); one wave per 32-row
+# unit (score rows, every prefix at most 512 slots).  Same at head size 64.
+ATTN_KERNEL = r"k_own_khat<128>|k_pass_attn<128>"
+SCORE_KERNEL = r"k_score_rows<128>"
+ATTN_KERNEL_D64 = r"k_own_khat<64>|k_pass_attn<64>"
+SCORE_KERNEL_D64 = r"k_score_rows<64>"
 CALIB_KERNEL = r"bitwise_not"
 CALIB_BYTES = 1 << 30
 
@@ -69,26 +75,37 @@ def stats(trace_dir, command, top=12):
 
 
 def _counter(run_dir, counter, pattern):
-    vals = []
+    """Values of one counter, per dispatch, of every kernel matching
+    `pattern`: {kernel name: [values]}."""
+    vals = {}
     for r in _rows(os.path.join(run_dir, "run_counter_collection.csv")):
         if r["Counter_Name"] == counter and re.search(pattern,
                                                       r["Kernel_Name"]):
-            vals.append(float(r["Counter_Value"]))
+            vals.setdefault(short_name(r["Kernel_Name"]), []).append(
+                float(r["Counter_Value"]))
     if not vals:
         raise SystemExit(f"no {counter} rows for /{pattern}/ in {run_dir}")
     return vals
 
 
+def _per_step(vals):
+    """Sum over the matched kernels of each one's mean per dispatch (one
+    attention step launches each of them once)."""
+    return sum(sum(v) / len(v) for v in vals.values())
+
+
 def traffic(fetch_dir, write_dir, command, kernel=ATTN_KERNEL):
     f_att = _counter(fetch_dir, "FETCH_SIZE", kernel)
     w_att = _counter(write_dir, "WRITE_SIZE", kernel)
-    f_cal = _counter(fetch_dir, "FETCH_SIZE", CALIB_KERNEL)
-    w_cal = _counter(write_dir, "WRITE_SIZE", CALIB_KERNEL)
+    f_cal = [x for v in _counter(fetch_dir, "FETCH_SIZE", CALIB_KERNEL).values()
+             for x in v]
+    w_cal = [x for v in _counter(write_dir, "WRITE_SIZE", CALIB_KERNEL).values()
+             for x in v]
     kib = 1024.0
     f_scale = CALIB_BYTES / (max(f_cal) * kib)
     w_scale = CALIB_BYTES / (max(w_cal) * kib)
-    f_avg = sum(f_att) / len(f_att)
-    w_avg = sum(w_att) / len(w_att)
+    f_avg = _per_step(f_att)
+    w_avg = _per_step(w_att)
     read_b = f_avg * kib * f_scale
     write_b = w_avg * kib * w_scale
     out = [
@@ -96,7 +113,13 @@ def traffic(fetch_dir, write_dir, command, kernel=ATTN_KERNEL):
         f"command: {command}",
         f"kernel: /{kernel}/",
         f"kernel_source_sha: {kernel_source_sha()}",
-        f"dispatches: fetch {len(f_att)}, write {len(w_att)}",
+        "dispatches: " + ", ".join(
+            f"{k} fetch {len(f_att[k])} write {len(w_att.get(k, []))}"
+            for k in sorted(f_att)),
+        *[f"fetch_kib_per_dispatch[{k}]: {sum(v) / len(v):.1f}"
+          for k, v in sorted(f_att.items())],
+        *[f"write_kib_per_dispatch[{k}]: {sum(v) / len(v):.1f}"
+          for k, v in sorted(w_att.items())],
         f"fetch_kib_per_dispatch: {f_avg:.1f}",
         f"write_kib_per_dispatch: {w_avg:.1f}",
         f"calibration: /{CALIB_KERNEL}/ reads and writes {CALIB_BYTES} B; "
@@ -107,6 +130,99 @@ def traffic(fetch_dir, write_dir, command, kernel=ATTN_KERNEL):
         f"write_bytes_per_launch: {write_b:.0f}",
         f"traffic_bytes_per_launch: {read_b + write_b:.0f}",
     ]
+    return "\n".join(out) + "\n"
+
+
+# Shader counters summarised by `pmc` (each pass of rocprofv3 --pmc holds
+# at most 8 SQ counters and GRBM_GUI_ACTIVE; one pass per group).
+PMC_PASSES = (
+    "SQ_VALU_MFMA_BUSY_CYCLES SQ_BUSY_CYCLES SQ_INSTS_VALU_MFMA_MOPS_BF16 "
+    "SQ_INSTS_MFMA SQ_INSTS_VALU SQ_ACTIVE_INST_VALU SQ_INSTS_LDS "
+    "SQ_WAVE_CYCLES GRBM_GUI_ACTIVE",
+    "SQ_WAIT_ANY SQ_WAIT_INST_ANY SQ_WAIT_INST_LDS SQ_ACTIVE_INST_ANY "
+    "SQ_ACTIVE_INST_LDS SQ_LDS_BANK_CONFLICT SQ_LDS_IDX_ACTIVE "
+    "SQ_ACTIVE_INST_VMEM GRBM_GUI_ACTIVE",
+)
+
+
+def _agent(run_dir):
+    for r in _rows(os.path.join(run_dir, "run_agent_info.csv")):
+        if r.get("Name", "").startswith("gfx"):
+            return r
+    raise SystemExit(f"no GPU agent in {run_dir}")
+
+
+def pmc(run_dirs, command, kernel=ATTN_KERNEL):
+    """Per matched kernel: the mean per dispatch of every counter found in
+    the runs, and the utilisations the ROCm derived metrics define.
+    GRBM_GUI_ACTIVE is summed over the chip's XCDs in the counter file, so
+    the busy-cycle denominators use it divided by the XCD count."""
+    ag = _agent(run_dirs[0])
+    n_xcc, n_cu = int(ag["Num_Xcc"]), int(ag["Cu_Count"])
+    n_simd = int(ag["Simd_Count"])
+    per = {}    # kernel -> counter -> [values]
+    meta = {}   # kernel -> resources and duration
+    for d in run_dirs:
+        for r in _rows(os.path.join(d, "run_counter_collection.csv")):
+            if not re.search(kernel, r["Kernel_Name"]):
+                continue
+            k = short_name(r["Kernel_Name"])
+            per.setdefault(k, {}).setdefault(r["Counter_Name"], []).append(
+                float(r["Counter_Value"]))
+            meta.setdefault(k, {
+                "arch_vgpr": r["VGPR_Count"], "accum_vgpr": r["Accum_VGPR_Count"],
+                "sgpr": r["SGPR_Count"], "lds_bytes": r["LDS_Block_Size"],
+                "scratch_bytes_per_lane": r["Scratch_Size"],
+                "workgroup": r["Workgroup_Size"], "grid": r["Grid_Size"]})
+            meta[k].setdefault("dur", []).append(
+                int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
+    if not per:
+        raise SystemExit(f"no counter rows for /{kernel}/ in {run_dirs}")
+    out = ["# Shader counters of the attention launches (rocprofv3 --pmc)",
+           f"command: {command}", f"kernel: /{kernel}/",
+           f"kernel_source_sha: {kernel_source_sha()}",
+           f"agent: {ag['Name']}, {n_xcc} XCDs, {n_cu} CUs, {n_simd} SIMDs",
+           ""]
+    tot_busy = tot_cycles = tot_mops = tot_dur = 0.0
+    for k in sorted(per):
+        c = {n: sum(v) / len(v) for n, v in per[k].items()}
+        m = meta[k]
+        dur = sum(m["dur"]) / len(m["dur"])
+        gui = c.get("GRBM_GUI_ACTIVE", 0.0) / n_xcc   # cycles per XCD
+        out.append(f"[{k}]")
+        out.append(f"  mean_duration_us: {dur / 1e3:.1f}")
+        for key in ("arch_vgpr", "accum_vgpr", "sgpr", "lds_bytes",
+                    "scratch_bytes_per_lane", "workgroup", "grid"):
+            out.append(f"  {key}: {m[key]}")
+        for n in sorted(c):
+            out.append(f"  {n}: {c[n]:.6g}")
+        if gui > 0:
+            busy = c.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0)
+            out.append(f"  mfma_busy_pct: {100 * busy / (gui * n_simd):.2f}")
+            out.append("  valu_busy_pct: "
+                       f"{100 * c.get('SQ_ACTIVE_INST_VALU', 0.0) / n_cu / gui:.2f}")
+            out.append("  lds_util_pct: "
+                       f"{100 * c.get('SQ_LDS_IDX_ACTIVE', 0.0) / n_cu / gui:.2f}")
+            out.append("  lds_bank_conflict_pct: "
+                       f"{100 * c.get('SQ_LDS_BANK_CONFLICT', 0.0) / n_cu / gui:.2f}")
+            tot_busy += busy
+            tot_cycles += gui * n_simd
+        if c.get("SQ_WAVE_CYCLES"):
+            w = c["SQ_WAVE_CYCLES"]
+            for n in ("SQ_WAIT_ANY", "SQ_WAIT_INST_ANY", "SQ_ACTIVE_INST_ANY"):
+                if n in c:
+                    out.append(f"  {n.lower()}_frac_of_wave_cycles: "
+                               f"{c[n] / w:.3f}")
+        if "SQ_INSTS_VALU_MFMA_MOPS_BF16" in c and dur > 0:
+            fl = 512 * c["SQ_INSTS_VALU_MFMA_MOPS_BF16"]
+            out.append(f"  mfma_bf16_flop: {fl:.6g}")
+            out.append(f"  mfma_bf16_tflops: {fl / (dur * 1e-9) / 1e12:.1f}")
+            tot_mops += fl
+            tot_dur += dur
+    if tot_cycles > 0:
+        out += ["", f"mfma_busy_frac: {tot_busy / tot_cycles:.4f}"]
+    if tot_dur > 0:
+        out.append(f"mfma_bf16_tflops: {tot_mops / (tot_dur * 1e-9) / 1e12:.1f}")
     return "\n".join(out) + "\n"
 
 
@@ -134,9 +250,15 @@ def main(argv=None):
     b.add_argument("write_dir")
     b.add_argument("--command", required=True)
     b.add_argument("--kernel", default=ATTN_KERNEL)
+    c = sub.add_parser("pmc")
+    c.add_argument("run_dirs", nargs="+")
+    c.add_argument("--command", required=True)
+    c.add_argument("--kernel", default=ATTN_KERNEL)
     args = ap.parse_args(argv)
     if args.cmd == "stats":
         sys.stdout.write(stats(args.trace_dir, args.command))
+    elif args.cmd == "pmc":
+        sys.stdout.write(pmc(args.run_dirs, args.command, args.kernel))
     else:
         sys.stdout.write(traffic(args.fetch_dir, args.write_dir, args.command,
                                  args.kernel))
