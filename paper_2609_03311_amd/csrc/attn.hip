@@ -511,7 +511,9 @@ __device__ __forceinline__ void own_v_transpose(const AttnParams &P,
                                                 key_stride, int nvalid,
                                                 uint16_t *ov) {
   constexpr int DL = D / 8;  // head dims per lane
-  const int lane = threadIdx.x & 63;
+  // (lane offsets from an opaque zero: formed per call, not held across
+  // the caller's loops)
+  const int lane = (threadIdx.x & 63) + opaque_zero();
   const int m = lane & 7, d0 = DL * (lane >> 3);
   uint4 r[4][DL / 8];
 #pragma unroll
@@ -575,7 +577,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(
   __shared__ __attribute__((aligned(16))) uint16_t sov[4][D * KC];
   __shared__ __attribute__((aligned(16))) uint16_t skw[D];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int lq = lane & 31, hf = lane >> 5, prow = perm32(lq);
   // the k gains, once per block (the block's only barrier)
   if (threadIdx.x < D / 8)
     reinterpret_cast<uint4 *>(skw)[threadIdx.x] =
@@ -585,7 +586,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(
   int64_t n_items = P.totals[kTotItems];
   if (n_items > P.items_cap) n_items = P.items_cap;
   const int64_t n_work = n_items * P.Hkv;
-  const Frag<D> fo = frag_offsets<D>(lq, hf);
   uint16_t *ov = sov[wave];
 
   for (;;) {
@@ -613,6 +613,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(
     bool bad = false;
     for (int t0 = it.y; !unscored && t0 < it.z; t0 += 32) {
       const int t1 = t0 + 32 < it.z ? t0 + 32 : it.z;
+      // the lane's row, head-dim and fragment offsets, formed per tile from
+      // an opaque lane index (held across the kernel they are spilled)
+      const int lt_ = lane + opaque_zero();
+      const int lq = lt_ & 31, hf = lt_ >> 5, prow = perm32(lq);
+      const Frag<D> fo = frag_offsets<D>(lq, hf);
       // this lane's row: stacked token u is the sorted pair
       const int r = t0 + lq;
       const bool valid = r < t1;
@@ -645,11 +650,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(
           kf[s] = *reinterpret_cast<const bf16x8 *>(
               Kp + (int64_t)krow * D + 16 * s + 8 * hf);
         if constexpr (D == 128) qk_regs<D>(kf, qf, S);
+        // (the row offsets are formed here, per chunk, from an opaque
+        // zero: hoisted out of the loop they would hold four 64-bit
+        // addresses across the whole tile)
+        const int vrow = prow + opaque_zero();
 #pragma unroll
         for (int f = 0; f < D / 16; ++f) {
           const int key = c0 + 16 * hf + 8 * (f & 1);
           vf[f] = key < Lp ? *reinterpret_cast<const bf16x8 *>(
-                                 VTp + (int64_t)(32 * (f >> 1) + prow) * Lp +
+                                 VTp + (int64_t)(32 * (f >> 1) + vrow) * Lp +
                                  key)
                            : bf16x8{};
         }

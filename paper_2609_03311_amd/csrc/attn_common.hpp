@@ -584,9 +584,11 @@ __device__ __forceinline__ void softmax_part(floatx16 *S, Acc<D> *acc, int hf,
 #pragma unroll
   for (int qb = 0; qb < NQB; ++qb) {
     if (MODE == 1) {
+      // key 16 hf + i is visible when i <= lim - 16 hf (comparing the
+      // immediate i, so no register holds each lane's key indices)
+      const int li = lim[qb] - 16 * hf;
 #pragma unroll
-      for (int i = 0; i < 16; ++i)
-        S[qb][i] = 16 * hf + i <= lim[qb] ? S[qb][i] : -INFINITY;
+      for (int i = 0; i < 16; ++i) S[qb][i] = i <= li ? S[qb][i] : -INFINITY;
     }
     Acc<D> &A = acc[qb];
     if (SMX == 2) {
