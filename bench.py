@@ -721,6 +721,9 @@ def main():
                     choices=sorted(DESCRIPTIONS) +
                     sorted(SALIENCE_DESCRIPTIONS))
     ap.add_argument("--variant", type=int, default=0)
+    ap.add_argument("--queue-order", type=int, choices=[0, 1, 2], default=0,
+                    help="work-queue order: 0 automatic, 1 natural, "
+                         "2 longest-first")
     ap.add_argument("--path", choices=["full", "score", "layer", "salience",
                                        "ingest"],
                     default="full",
@@ -802,13 +805,15 @@ def main():
                                   total_tokens=st.n_tokens,
                                   max_tokens=int(st.seqlens.max()),
                                   kernel_variant=args.variant, device=dev,
-                                  with_rows=not args.no_score_rows)
+                                  with_rows=not args.no_score_rows,
+                                  queue_order=args.queue_order)
     else:
         step = pipeline.OnlineStep(store, n_pairs=st.n_pairs,
                                    n_q_heads=st.n_q_heads,
                                    total_tokens=st.n_tokens,
                                    max_tokens=int(st.seqlens.max()),
-                                   kernel_variant=args.variant, device=dev)
+                                   kernel_variant=args.variant, device=dev,
+                                   queue_order=args.queue_order)
     doc_ids = torch.from_numpy(st.doc_ids).to(dev)
     cu = torch.from_numpy(st.cu_seqlens).to(dev)
     torch.cuda.synchronize()
@@ -907,6 +912,7 @@ def main():
             "online_tokens": st.n_tokens,
             "unique_docs": w["unique_docs"],
             "kernel_variant": args.variant,
+            "queue_order": args.queue_order,
             "path": ("decoder layer (hidden %d, intermediate %d)" % (
                 hidden, inter) if layer_path else
                      "last-layer scoring" + (", no score rows written"

@@ -204,6 +204,16 @@ typedef struct {
                                not depend on it (a tuning and test knob).
                                Full-row calls only: must be 0 for
                                dopr_prefix_attn_score (INVALID_ARG).        */
+  int32_t queue_order;      /* order in which each of the 8 work queues
+                               (one per XCD) hands out its (item, kv head)
+                               units.  0 = automatic: longest-first while
+                               the CUs average at most 128 units each,
+                               else natural; 1 = natural (item order);
+                               2 = longest-first (costliest document group
+                               first, item order within a cost class) up to
+                               32768 units, natural beyond.  Outputs do not
+                               depend on it (a tuning and test knob); other
+                               values are INVALID_ARG.                      */
 } dopr_attn_args_t;
 
 /* Workspace bytes needed by dopr_prefix_attn for these arguments (host). */

@@ -52,7 +52,8 @@ class _AttnArgs(ctypes.Structure):
                 ("timing_begin", ctypes.c_void_p),
                 ("timing_end", ctypes.c_void_p),
                 ("rope_inv_freq", ctypes.c_void_p),
-                ("rows_per_item", ctypes.c_int32)]
+                ("rows_per_item", ctypes.c_int32),
+                ("queue_order", ctypes.c_int32)]
 
 
 class _ScoreArgs(ctypes.Structure):
@@ -262,7 +263,7 @@ def _attn_args(store, doc_ids, cu_seqlens, q, k, v, q_norm_w, k_norm_w, out,
                lse, workspace, *, max_tokens, total_tokens=None,
                rms_eps=1e-6, rope_theta=1e6, softmax_scale=None,
                kernel_variant=0, timing=None, rope_inv_freq=None,
-               rows_per_item=0):
+               rows_per_item=0, queue_order=0):
     n_q_heads = q.shape[1] if q is not None else store.n_kv_heads
     if total_tokens is None:
         total_tokens = q.shape[0]
@@ -277,7 +278,8 @@ def _attn_args(store, doc_ids, cu_seqlens, q, k, v, q_norm_w, k_norm_w, out,
                      float(rope_theta), float(softmax_scale), _ptr(out),
                      _ptr(lse), _ptr(workspace), ws_bytes,
                      *(timing if timing is not None else (None, None)),
-                     _ptr(rope_inv_freq), int(rows_per_item))
+                     _ptr(rope_inv_freq), int(rows_per_item),
+                     int(queue_order))
 
 
 def _shape_args(n_pairs, n_q_heads, max_tokens, total_tokens,
@@ -320,18 +322,20 @@ def dopr_prefix_attn(store: Store, layer: int, doc_ids, cu_seqlens, q, k, v,
                      lse=None, total_tokens=None, rms_eps=1e-6,
                      rope_theta=1e6, softmax_scale=None, kernel_variant=0,
                      timing=None, rope_inv_freq=None, stream=None,
-                     rows_per_item=0):
+                     rows_per_item=0, queue_order=0):
     """`timing` is an optional (begin, end) pair of raw hipEvent_t handles
     recorded around the attention kernel.  q_norm_w and k_norm_w may both
     be None (no QK-norm); rope_inv_freq is an optional fp32 [D/2] device
     tensor of rotation frequencies; rows_per_item 0 is the automatic work
-    item size."""
+    item size; queue_order 0/1/2 is the automatic, natural or
+    longest-first order of the work queues."""
     a = _attn_args(store, doc_ids, cu_seqlens, q, k, v, q_norm_w, k_norm_w,
                    out, lse, workspace, max_tokens=max_tokens,
                    total_tokens=total_tokens, rms_eps=rms_eps,
                    rope_theta=rope_theta, softmax_scale=softmax_scale,
                    kernel_variant=kernel_variant, timing=timing,
-                   rope_inv_freq=rope_inv_freq, rows_per_item=rows_per_item)
+                   rope_inv_freq=rope_inv_freq, rows_per_item=rows_per_item,
+                   queue_order=queue_order)
     _check(lib().dopr_prefix_attn(store.handle, layer, ctypes.byref(a),
                                   _stream(stream)))
 
@@ -341,7 +345,7 @@ def dopr_prefix_attn_noalloc(store: Store, layer: int, doc_ids, cu_seqlens,
                              lse=None, total_tokens=None, rms_eps=1e-6,
                              rope_theta=1e6, softmax_scale=None,
                              kernel_variant=0, timing=None,
-                             rope_inv_freq=None, stream=None):
+                             rope_inv_freq=None, stream=None, queue_order=0):
     """dopr_prefix_attn without a workspace: the plan goes to the library's
     own per-device scratch (at most DOPR_NOALLOC_SCRATCH_BYTES)."""
     a = _attn_args(store, doc_ids, cu_seqlens, q, k, v, q_norm_w, k_norm_w,
@@ -349,7 +353,7 @@ def dopr_prefix_attn_noalloc(store: Store, layer: int, doc_ids, cu_seqlens,
                    total_tokens=total_tokens, rms_eps=rms_eps,
                    rope_theta=rope_theta, softmax_scale=softmax_scale,
                    kernel_variant=kernel_variant, timing=timing,
-                   rope_inv_freq=rope_inv_freq)
+                   rope_inv_freq=rope_inv_freq, queue_order=queue_order)
     _check(lib().dopr_prefix_attn_noalloc(store.handle, layer,
                                           ctypes.byref(a), _stream(stream)))
 
@@ -363,7 +367,7 @@ def dopr_prefix_attn_score(store: Store, layer: int, doc_ids, cu_seqlens, q,
                            lse=None, total_tokens=None, rms_eps=1e-6,
                            head_rms_eps=1e-6, rope_theta=1e6,
                            softmax_scale=None, kernel_variant=0, timing=None,
-                           rope_inv_freq=None, stream=None):
+                           rope_inv_freq=None, stream=None, queue_order=0):
     """Last-layer scoring: the score token's attention rows (out [P, Hq, D]
     or None, lse [P, Hq] or None) with the score head fused (score [P],
     logits [P, 2] or None)."""
@@ -372,7 +376,7 @@ def dopr_prefix_attn_score(store: Store, layer: int, doc_ids, cu_seqlens, q,
                    total_tokens=total_tokens, rms_eps=rms_eps,
                    rope_theta=rope_theta, softmax_scale=softmax_scale,
                    kernel_variant=kernel_variant, timing=timing,
-                   rope_inv_freq=rope_inv_freq)
+                   rope_inv_freq=rope_inv_freq, queue_order=queue_order)
     h = _ScoreHead(_ptr(norm_w), _ptr(w_head), float(head_rms_eps),
                    _ptr(logits), _ptr(score))
     _check(lib().dopr_prefix_attn_score(store.handle, layer, ctypes.byref(a),

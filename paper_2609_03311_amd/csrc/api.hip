@@ -166,6 +166,8 @@ dopr_status_t check_attn(const dopr_store *st, const dopr_attn_args_t *a,
                   "rows_per_item must be 0 or a multiple of 32 in "
                   "[64, 2^20]");
   }
+  if (a->queue_order < 0 || a->queue_order > 2)
+    return fail(DOPR_ERR_INVALID_ARG, "queue_order must be 0, 1 or 2");
   shape->rows_per_item =
       a->rows_per_item ? a->rows_per_item
                        : default_rows_per_item(a->kernel_variant, score_only,

@@ -292,12 +292,14 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(
   const int lq = lane & 31, hf = lane >> 5;
   const int queue = SAFE ? kFixQueue : (blockIdx.x & 7);
   int64_t n_work;
+  const int32_t *qo = nullptr;
   if (SAFE) {
     n_work = P.counters[kCntFix];
   } else {
     int64_t n_items = P.totals[kTotItems];
     if (n_items > P.items_cap) n_items = P.items_cap;
     n_work = n_items * P.Hkv;
+    if (P.totals[kTotUnits]) qo = P.qorder;
   }
   const Frag<D> fo = frag_offsets<D>(lq, hf);
 
@@ -305,7 +307,7 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(
     if (threadIdx.x == 0) sm.words()[0] = atomicAdd(&P.next[queue], 1);
     __syncthreads();
     const int slot = sm.words()[0];
-    int64_t w = SAFE ? (int64_t)slot : queue + 8 * (int64_t)slot;
+    int64_t w = SAFE ? (int64_t)slot : unit_at(qo, queue, slot, n_work);
     if (w >= n_work) break;
     bool wave_bad = false;
     bool unscored = false;
@@ -586,13 +588,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(
   int64_t n_items = P.totals[kTotItems];
   if (n_items > P.items_cap) n_items = P.items_cap;
   const int64_t n_work = n_items * P.Hkv;
+  const int32_t *qo = P.totals[kTotUnits] ? P.qorder : nullptr;
   uint16_t *ov = sov[wave];
 
   for (;;) {
     int slot = 0;
     if (lane == 0) slot = atomicAdd(&P.next[queue], 1);
     slot = __builtin_amdgcn_readfirstlane(slot);
-    const int64_t w = queue + 8 * (int64_t)slot;
+    const int64_t w = unit_at(qo, queue, slot, n_work);
     if (w >= n_work) break;
     const int item = (int)(w / P.Hkv), g = (int)(w % P.Hkv);
     const int4 it = P.items[item];
@@ -919,6 +922,7 @@ hipError_t launch_attention(const AttnCall &c, const Plan &pl,
   p.kh = pl.kh;
   p.zero = pl.zero;
   p.units = pl.units;
+  p.qorder = pl.qorder;
   p.ntok = a->total_tokens;
   KhatParams kp{};
   kp.k = p.k;

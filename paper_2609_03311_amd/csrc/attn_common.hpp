@@ -43,6 +43,8 @@ struct AttnParams {
   const uint16_t *kh, *zero;
   const int4 *units;
   int64_t ntok;
+  // work units of each queue, costliest first (see unit_at)
+  const int32_t *qorder;
   int32_t items_cap, Hq, Hkv, n_rep, layer, n_layers;
   int32_t flag_all;  // queue every unit for the SAFE pass (self-check mode)
   int32_t norm;      // per-head RMSNorm of q and k (0: no QK-norm, unit gains)
@@ -75,8 +77,6 @@ typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 
 constexpr int KC = 32;      // keys per MFMA chunk
-constexpr int kTotDocs = 0;   // (distinct docs << 32) | valid pairs
-constexpr int kTotItems = 2;
 constexpr int kFixQueue = 8;  // cursor slot of the fixup pass
 constexpr float kLn2 = 0.69314718055994530942f;
 constexpr float kTau = 8.0f;       // SAFE mode: lazy-rescale threshold

@@ -29,7 +29,6 @@ constexpr int kScanThreads = 1024;
 constexpr int kScanTile = 2 * kScanThreads;
 constexpr int kThreads = 256;
 
-enum Total { kTotDocs = 0, kTotRows = 1, kTotItems = 2, kTotals = 4 };
 enum NextSlots { kNextQueues = 16 };  // 8 XCD queues + the SAFE pass
 
 inline unsigned blocks_for(int64_t n, int t) {
@@ -208,6 +207,13 @@ __global__ __launch_bounds__(kThreads) void k_rank(Plan pl, PlanArgs a,
   const int64_t packed = pl.doc_scan[d];
   const int32_t s0 = (int32_t)(packed & 0xffffffff);
   const int32_t c = pl.cnt[d];
+  if (c > kBigGroup) {
+    // ordered by k_rank_big instead (a scan per pair would cost c^2)
+    if (i == s0)
+      pl.big[atomicAdd(&pl.counters[kCntBig], 1)] =
+          make_int4(s0, c, d, (int32_t)(packed >> 32));
+    return;
+  }
   int32_t rank = 0;
   for (int32_t k = s0; k < s0 + c; ++k) rank += pl.tmp_order[k] < v;
   pl.pair_order[s0 + rank] = v;
@@ -218,6 +224,78 @@ __global__ __launch_bounds__(kThreads) void k_rank(Plan pl, PlanArgs a,
     const int32_t gi = (int32_t)(packed >> 32);
     pl.group_doc[gi] = d;
     pl.group_ptr[gi] = s0;
+  }
+}
+
+// Step 3b for groups of more than kBigGroup pairs, one block per group: the
+// group's slots are sorted by pair index in LDS in tiles of kSortTile
+// (bitonic), and a pair's rank is its index in its tile plus the number of
+// smaller pair indices in each other tile (binary search; pair indices are
+// distinct).  Writes the canonical order, the stacked-row counts and the
+// group table, as k_rank does for the others.
+constexpr int32_t kSortTile = 16384;
+
+__global__ __launch_bounds__(1024) void k_rank_big(Plan pl, PlanArgs a) {
+  __shared__ int32_t key[kSortTile];
+  const int32_t nb = pl.counters[kCntBig];
+  for (int32_t b = blockIdx.x; b < nb; b += gridDim.x) {
+    const int4 g = pl.big[b];
+    const int32_t s0 = g.x, c = g.y;
+    if (threadIdx.x == 0) {
+      pl.group_doc[g.w] = g.z;
+      pl.group_ptr[g.w] = s0;
+    }
+    const int32_t n_tiles = (c + kSortTile - 1) / kSortTile;
+    for (int32_t k = 0; k < n_tiles; ++k) {
+      const int32_t base = s0 + k * kSortTile;
+      const int32_t n = c - k * kSortTile < kSortTile ? c - k * kSortTile
+                                                      : kSortTile;
+      int32_t N = 1;
+      while (N < n) N <<= 1;
+      __syncthreads();  // the previous tile's writes are done
+      for (int32_t t = threadIdx.x; t < N; t += blockDim.x)
+        key[t] = t < n ? pl.tmp_order[base + t] : INT32_MAX;
+      __syncthreads();
+      for (int32_t size = 2; size <= N; size <<= 1)
+        for (int32_t stride = size >> 1; stride > 0; stride >>= 1) {
+          for (int32_t t = threadIdx.x; t < N / 2; t += blockDim.x) {
+            const int32_t lo = 2 * t - (t & (stride - 1));
+            const int32_t hi = lo + stride;
+            const bool up = (lo & size) == 0;
+            const int32_t x = key[lo], y = key[hi];
+            if ((x > y) == up) {
+              key[lo] = y;
+              key[hi] = x;
+            }
+          }
+          __syncthreads();
+        }
+      for (int32_t t = threadIdx.x; t < n; t += blockDim.x)
+        pl.tmp_order[base + t] = key[t];
+    }
+    __syncthreads();  // every sorted tile is visible to the block
+    for (int32_t e = threadIdx.x; e < c; e += blockDim.x) {
+      const int32_t k = e / kSortTile;
+      const int32_t v = pl.tmp_order[s0 + e];
+      int32_t rank = e - k * kSortTile;
+      for (int32_t k2 = 0; k2 < n_tiles; ++k2) {
+        if (k2 == k) continue;
+        int32_t lo = s0 + k2 * kSortTile;
+        int32_t hi = lo + (c - k2 * kSortTile < kSortTile ? c - k2 * kSortTile
+                                                          : kSortTile);
+        const int32_t start = lo;
+        while (lo < hi) {  // first slot not below v
+          const int32_t mid = (lo + hi) >> 1;
+          if (pl.tmp_order[mid] < v) lo = mid + 1; else hi = mid;
+        }
+        rank += lo - start;
+      }
+      pl.pair_order[s0 + rank] = v;
+      const int64_t T = a.cu && !a.score_only
+                            ? (int64_t)(a.cu[v + 1] - a.cu[v])
+                            : 1;
+      pl.prow[s0 + rank] = T * a.n_rep;
+    }
   }
 }
 
@@ -233,6 +311,15 @@ __global__ __launch_bounds__(kThreads) void k_items_count(Plan pl, PlanArgs a,
   }
   const int64_t rows = pl.prow[pl.group_ptr[g + 1]] - pl.prow[pl.group_ptr[g]];
   pl.item_scan[g] = (rows + a.rows_per_item - 1) / a.rows_per_item;
+}
+
+// The longest-first cost class of a document group: kCostBuckets - 1 -
+// floor(log2(stacked rows * (prefix slots + 32))), clamped to the buckets
+// (0 = costliest).
+__device__ __forceinline__ uint8_t cost_class(int64_t rows, int32_t L) {
+  const int64_t cost = rows * ((int64_t)L + 32);
+  const int b = cost > 0 ? 63 - __clzll((unsigned long long)cost) : 0;
+  return (uint8_t)(kCostBuckets - 1 - (b < kCostBuckets ? b : kCostBuckets - 1));
 }
 
 // Step 5b: split a group's rows into items, boundaries on multiples of 32
@@ -251,9 +338,11 @@ __global__ __launch_bounds__(kThreads) void k_items_emit(Plan pl, PlanArgs a,
   const int64_t n_it = pl.item_scan[g + 1] - first;
   const int64_t base = pl.prow[pl.group_ptr[g]];
   const int64_t R = pl.prow[pl.group_ptr[g + 1]] - base;
+  const uint8_t cls = cost_class(R, a.doc_len[pl.group_doc[g]]);
   for (int64_t it = 0; it < n_it; ++it) {
     const int64_t idx = first + it;
     if (idx >= pl.items_cap) break;
+    pl.item_cls[idx] = cls;
     const int64_t b0 =
         a.exact_items ? base + it * a.rows_per_item
                       : base + ((it * R / n_it) & ~(int64_t)31);
@@ -377,6 +466,88 @@ __global__ __launch_bounds__(kThreads) void k_unit_table(
                                   (int32_t)(uint32_t)vo, (int32_t)(vo >> 32));
 }
 
+// Step 5f: the longest-first order of the work-unit queues.  Unit w =
+// item * Hkv + kv head goes to queue w % 8, which the blocks b with
+// b % 8 == queue serve; blocks are dealt round-robin to the 8 XCDs, so with
+// 8 kv heads each head's prefix K/V is read through one XCD's L2.  Within
+// a queue, units are handed out by the cost class of their document group
+// (floor(log2(group rows * (L + 32)))), costliest first, so long groups
+// start early and short ones fill the tail, and in unit order within a
+// class: the items of one group stay adjacent and share its prefix in L2,
+// and the queues still walk the items in step.  This pays only while the
+// CUs get few units each: with many, the blocks' finishing times even out
+// by themselves, and the queues keep the natural order (w = queue + 8 *
+// slot), which the kernels take when totals[kTotUnits] is 0.
+//
+// One block of 8 waves sorts stably: wave q takes queue q's units (w = q
+// + 8 s), counts them per class in its lanes (lane c holds class c), scans
+// the counts into cursors and walks the units again, placing each one at
+// its class's cursor; the classes of a 64-unit chunk are grouped with
+// ballots, so each step costs a few instructions per distinct class.
+constexpr int kOrderWaves = 8;
+static_assert(kCostBuckets <= 64, "one lane per cost class");
+// Longest-first only while the CUs average at most this many units each.
+constexpr int64_t kLptUnitsPerCu = 128;
+// Units one sort takes (128 per CU on 256 CUs); beyond it the queues keep
+// the natural order.
+constexpr int32_t kOrderMaxUnits = 32768;
+
+__global__ __launch_bounds__(kOrderWaves * 64) void k_unit_order(
+    Plan pl, int32_t hkv, int64_t lpt_units, int64_t *totals) {
+  __shared__ uint8_t cls_s[kOrderMaxUnits];  // item classes
+  const int64_t n_items = totals[kTotItems] < pl.items_cap
+                              ? totals[kTotItems]
+                              : pl.items_cap;
+  const int64_t n64 = n_items * hkv;
+  const bool ordered = n64 > 0 && n64 <= lpt_units && n64 <= kOrderMaxUnits;
+  if (threadIdx.x == 0) totals[kTotUnits] = ordered ? 1 : 0;
+  if (!ordered) return;  // block-uniform
+  const int n = (int)n64;
+  for (int i = threadIdx.x; i < (int)n_items; i += kOrderWaves * 64)
+    cls_s[i] = pl.item_cls[i];
+  __syncthreads();
+  const int lane = threadIdx.x & 63, q = threadIdx.x >> 6;
+  const uint64_t lt = (1ull << lane) - 1;
+  const int per = n / 8, rem = n % 8;
+  const int n_q = per + (q < rem ? 1 : 0);
+  const int start = q * per + (q < rem ? q : rem);
+  // counts per class
+  int cnt = 0;
+  for (int s0 = 0; s0 < n_q; s0 += 64) {
+    const int slot = s0 + lane;
+    const int cls = slot < n_q ? cls_s[(q + 8 * slot) / hkv] : -1;
+    uint64_t todo = __ballot(cls >= 0);
+    while (todo) {  // wave-uniform
+      const int k = __builtin_amdgcn_readlane(cls, __builtin_ctzll(todo));
+      const uint64_t m = __ballot(cls == k);
+      if (lane == k) cnt += __popcll(m);
+      todo &= ~m;
+    }
+  }
+  // cursors: start of the queue + the counts of the costlier classes
+  int incl = cnt;
+  for (int off = 1; off < 64; off <<= 1) {
+    const int y = __shfl_up(incl, off, 64);
+    if (lane >= off) incl += y;
+  }
+  int cur = start + incl - cnt;
+  // placement, in unit order within each class
+  for (int s0 = 0; s0 < n_q; s0 += 64) {
+    const int slot = s0 + lane;
+    const int w = q + 8 * slot;
+    const int cls = slot < n_q ? cls_s[w / hkv] : -1;
+    uint64_t todo = __ballot(cls >= 0);
+    while (todo) {  // wave-uniform
+      const int k = __builtin_amdgcn_readlane(cls, __builtin_ctzll(todo));
+      const uint64_t m = __ballot(cls == k);
+      const int b0 = __builtin_amdgcn_readlane(cur, k);
+      if (cls == k) pl.qorder[b0 + __popcll(m & lt)] = w;
+      if (lane == k) cur += __popcll(m);
+      todo &= ~m;
+    }
+  }
+}
+
 // Step 6: rotary table, (cos, sin)(pos * omega_i) for i < half = D/2, in
 // double, stored as float; omega_i = theta^(-2i/D), or the caller's
 // inv_freq[i].
@@ -420,6 +591,10 @@ Plan carve(void *ws, const PlanShape &s, size_t *bytes) {
   pl.cnt = c.take<int32_t>(s.n_docs);
   pl.fill = c.take<int32_t>(s.n_docs);
   pl.doc_scan = c.take<int64_t>(s.n_docs);
+  const int64_t stacked = s.score_only ? P : s.total_tokens;
+  const int64_t rows = stacked * s.n_rep;
+  const int64_t cap = P + (rows + s.rows_per_item - 1) / s.rows_per_item + 1;
+  const int64_t hkv = s.n_kv_heads > 0 ? s.n_kv_heads : 1;
   const int64_t scan_n = s.n_docs > P + 1 ? s.n_docs : P + 1;
   pl.scan_blocks_cap = (scan_n + kScanTile - 1) / kScanTile;
   pl.blk = c.take<int64_t>(pl.scan_blocks_cap);
@@ -427,18 +602,18 @@ Plan carve(void *ws, const PlanShape &s, size_t *bytes) {
   pl.invalid = c.take<int32_t>(P);
   pl.tmp_order = c.take<int32_t>(P);
   pl.pair_order = c.take<int32_t>(P);
+  pl.big = c.take<int4>(P / (kBigGroup + 1) + 1);
   pl.group_doc = c.take<int32_t>(P);
   pl.group_ptr = c.take<int32_t>(P + 1);
   pl.prow = c.take<int64_t>(P + 1);
   pl.item_scan = c.take<int64_t>(P + 1);
-  const int64_t stacked = s.score_only ? P : s.total_tokens;
-  const int64_t rows = stacked * s.n_rep;
-  const int64_t cap = P + (rows + s.rows_per_item - 1) / s.rows_per_item + 1;
   pl.items_cap = (int32_t)cap;
   pl.items = c.take<int4>(cap);
   pl.blk_cap = (int32_t)((rows + 31) / 32 + 1);
   pl.blk_pair = c.take<int32_t>(pl.blk_cap);
   pl.fix = c.take<int32_t>(cap * (s.n_kv_heads > 0 ? s.n_kv_heads : 1));
+  pl.qorder = c.take<int32_t>(cap * hkv);
+  pl.item_cls = c.take<uint8_t>(cap);
   pl.spair = c.take<int4>(P + 1);
   pl.utok = c.take<int2>(stacked);
   pl.part = s.score_only ? c.take<float>(P * s.n_rep * s.n_kv_heads * 3)
@@ -503,6 +678,11 @@ hipError_t launch_plan(const AttnCall &c, const Plan &pl,
                      0, s, pl, pa);
   hipLaunchKernelGGL(k_rank, dim3(blocks_for(P + 1, kThreads)),
                      dim3(kThreads), 0, s, pl, pa, totals);
+  {
+    const int64_t cap = P / (kBigGroup + 1) + 1;
+    hipLaunchKernelGGL(k_rank_big, dim3((unsigned)(cap < 256 ? cap : 256)),
+                       dim3(1024), 0, s, pl, pa);
+  }
   e = exclusive_scan(pl.prow, P + 1, pl.blk, totals + kTotRows, s);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_items_count, dim3(blocks_for(P + 1, kThreads)),
@@ -521,6 +701,16 @@ hipError_t launch_plan(const AttnCall &c, const Plan &pl,
                      static_cast<const uint16_t *>(a->k_norm_w),
                      static_cast<const uint16_t *>(a->q_norm_w), pl.kown,
                      pl.unit_w);
+  int dev = 0, n_cu = 0;
+  e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  e = hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess) return e;
+  const int64_t lpt_units = a->queue_order == 1   ? 0
+                            : a->queue_order == 2 ? kOrderMaxUnits
+                                                  : kLptUnitsPerCu * n_cu;
+  hipLaunchKernelGGL(k_unit_order, dim3(1), dim3(kOrderWaves * 64), 0, s, pl,
+                     c.st->n_kv_heads, lpt_units, totals);
   if (pl.units) {
     const int64_t n_units = (int64_t)pl.items_cap * c.st->n_kv_heads;
     hipLaunchKernelGGL(k_unit_table, dim3(blocks_for(n_units, kThreads)),

@@ -97,6 +97,39 @@ struct dopr_store {
 namespace dopr {
 
 // ---------------------------------------------------------------------------
+// Groups with more pairs than this are put in pair order by a sort (one
+// block per group) instead of a scan of the group per pair.
+constexpr int32_t kBigGroup = 256;
+// Cost classes of work units for the longest-first order: floor(log2) of
+// stacked rows x (prefix slots + 32).
+constexpr int32_t kCostBuckets = 40;
+
+// The plan's int64 totals.
+enum Total {
+  kTotDocs = 0,   // (distinct docs << 32) | valid pairs
+  kTotRows = 1,   // stacked rows of the valid pairs
+  kTotItems = 2,  // work items
+  kTotUnits = 3,  // 1 if the queues follow the longest-first order, else 0
+  kTotals = 4
+};
+
+// Work unit handed out as the `slot`-th claim of queue `queue` (0..7):
+// queue q serves the units w with w % 8 == q, in natural order (w = q +
+// 8 * slot) when qorder is null, else costliest class first as the
+// planner's qorder lists them; n_work when the queue is empty.
+__device__ __forceinline__ int64_t unit_at(const int32_t *qorder, int queue,
+                                           int64_t slot, int64_t n_work) {
+  if (!qorder) {
+    const int64_t w = queue + 8 * slot;
+    return w < n_work ? w : n_work;
+  }
+  const int64_t per = n_work / 8, rem = n_work % 8;
+  const int64_t n_q = per + (queue < rem ? 1 : 0);
+  if (slot >= n_q) return n_work;
+  const int64_t start = queue * per + (queue < rem ? queue : rem);
+  return qorder[start + slot];
+}
+
 // Per-call plan built on the device by the grouping kernels (workspace).
 enum Counter {
   kCntValid = 0,     // pairs with a valid, resident document
@@ -105,6 +138,7 @@ enum Counter {
   kCntInvalid = 3,   // pairs whose outputs must be zeroed
   kCntRows = 4,      // stacked rows (tokens * n_rep) of valid pairs (low)
   kCntFix = 5,       // work units queued for the exact (SAFE) pass
+  kCntBig = 6,       // groups of more than kBigGroup pairs (ordered apart)
   kCounters = 16
 };
 
@@ -118,6 +152,13 @@ struct Plan {
   int32_t *invalid;     // [P] pairs whose outputs are zeroed
   int32_t *tmp_order;   // [P]
   int32_t *pair_order;  // [P]
+  int4 *big;            // [P / (kBigGroup + 1) + 1] groups of more than
+                        // kBigGroup pairs: (first slot, pairs, doc, group)
+  int32_t *qorder;      // [items_cap * Hkv] work units by queue (w % 8),
+                        // costliest class first within each queue, unit
+                        // order within a class (when totals[kTotUnits]
+                        // is 1)
+  uint8_t *item_cls;    // [items_cap] cost class of each item's group
   int32_t *group_doc;   // [P]
   int32_t *group_ptr;   // [P+1]
   int64_t *prow;        // [P+1] stacked-row offsets, sorted pair order

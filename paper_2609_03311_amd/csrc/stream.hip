@@ -238,11 +238,11 @@ __device__ __forceinline__ PUnit unit_from_words(int w, int x) {
 // taken) and the unit's table words x.  Units over the logit bound are
 // handed to the exact pass unscored and replaced by further claims (rare:
 // those waits are not hidden).  w = -1 past the end of the queue.
-__device__ PUnit pass_claim_finish(const AttnParams &P, int queue,
-                                   int64_t n_work, int lane, int slot,
-                                   int x) {
+__device__ PUnit pass_claim_finish(const AttnParams &P, const int32_t *qo,
+                                   int queue, int64_t n_work, int lane,
+                                   int slot, int x) {
   for (;;) {
-    const int64_t w = queue + 8 * (int64_t)slot;
+    const int64_t w = unit_at(qo, queue, slot, n_work);
     if (w >= n_work) {
       PUnit u{};
       u.w = -1;
@@ -259,7 +259,7 @@ __device__ PUnit pass_claim_finish(const AttnParams &P, int queue,
       s2 = atomicAdd(&P.next[queue], 1);
     }
     slot = rfl(s2);
-    const int64_t w2 = queue + 8 * (int64_t)slot;
+    const int64_t w2 = unit_at(qo, queue, slot, n_work);
     x = w2 < n_work ? unit_words(P, (int)w2, lane) : 0;
   }
 }
@@ -386,6 +386,7 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(
   int64_t n_items = P.totals[kTotItems];
   if (n_items > P.items_cap) n_items = P.items_cap;
   const int64_t n_work = n_items * P.Hkv;
+  const int32_t *qo = P.totals[kTotUnits] ? P.qorder : nullptr;
   const int n_valid = (int)(cld(P.totals, kTotDocs) & 0xffffffff);
   // rows per pass: one 32-row tile per wave, and at most 64 pairs (a pair
   // has n_rep rows per token, and one pair record per lane)
@@ -412,9 +413,9 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(
     int slot = 0;
     if (lane == 0) slot = atomicAdd(&P.next[queue], 1);
     slot = rfl(slot);
-    const int64_t w = queue + 8 * (int64_t)slot;
+    const int64_t w = unit_at(qo, queue, slot, n_work);
     const int x = w < n_work ? unit_words(P, (int)w, lane) : 0;
-    const PUnit u0 = pass_claim_finish(P, queue, n_work, lane, slot, x);
+    const PUnit u0 = pass_claim_finish(P, qo, queue, n_work, lane, slot, x);
     if (lane == 0) unit_put(wd + 4 * kWordUnit, u0);
   }
   lds_barrier();
@@ -493,7 +494,7 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(
       // wave 0: the next unit's table words (its atomic has returned)
       if (wave == 0 && pass0 == u.row0) {
         next_slot = rfl(next_slot);
-        const int64_t w = queue + 8 * (int64_t)next_slot;
+        const int64_t w = unit_at(qo, queue, next_slot, n_work);
         if (w < n_work) next_x = unit_words(P, (int)w, lane);
       }
 
@@ -571,7 +572,7 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(
 
     PUnit nu{};
     if (wave == 0)
-      nu = pass_claim_finish(P, queue, n_work, lane, next_slot, next_x);
+      nu = pass_claim_finish(P, qo, queue, n_work, lane, next_slot, next_x);
     // hand-over: the waves' range flags and the next unit
     if (lane == 0) lds_put(wd + 4 * (1 + wave), wave_bad);
     if (wave == 0 && lane == 0) unit_put(wd + 4 * kWordUnit, nu);

@@ -42,7 +42,7 @@ class OnlineStep:
 
     def __init__(self, store, *, n_pairs, n_q_heads, total_tokens,
                  max_tokens, kernel_variant=0, device="cuda", with_lse=False,
-                 rows_per_item=0):
+                 rows_per_item=0, queue_order=0):
         import torch
         self.store = store
         self.n_pairs = n_pairs
@@ -51,6 +51,7 @@ class OnlineStep:
         self.max_tokens = max_tokens
         self.kernel_variant = kernel_variant
         self.rows_per_item = rows_per_item
+        self.queue_order = queue_order
         nbytes = dopr_prefix_attn_workspace(
             store, n_pairs=n_pairs, n_q_heads=n_q_heads,
             max_tokens=max_tokens, total_tokens=total_tokens,
@@ -72,7 +73,8 @@ class OnlineStep:
                          max_tokens=self.max_tokens, lse=self.lse,
                          total_tokens=self.total_tokens,
                          kernel_variant=self.kernel_variant, stream=stream,
-                         rows_per_item=self.rows_per_item, **kw)
+                         rows_per_item=self.rows_per_item,
+                         **{"queue_order": self.queue_order, **kw})
 
     def score_head(self, cu_seqlens, norm_w, w_head, stream=None,
                    rms_eps=1e-6):
@@ -96,7 +98,7 @@ class ScoreStep:
 
     def __init__(self, store, *, n_pairs, n_q_heads, total_tokens,
                  max_tokens, kernel_variant=0, device="cuda",
-                 with_rows=True):
+                 with_rows=True, queue_order=0):
         import torch
         self.store = store
         self.n_pairs = n_pairs
@@ -104,6 +106,7 @@ class ScoreStep:
         self.total_tokens = total_tokens
         self.max_tokens = max_tokens
         self.kernel_variant = kernel_variant
+        self.queue_order = queue_order
         nbytes = dopr_prefix_attn_score_workspace(
             store, n_pairs=n_pairs, n_q_heads=n_q_heads,
             max_tokens=max_tokens, total_tokens=total_tokens,
@@ -126,7 +129,8 @@ class ScoreStep:
             k_norm_w, self.out, self.workspace, norm_w, w_head, self.score,
             max_tokens=self.max_tokens, logits=self.logits, lse=self.lse,
             total_tokens=self.total_tokens,
-            kernel_variant=self.kernel_variant, stream=stream, **kw)
+            kernel_variant=self.kernel_variant, stream=stream,
+            **{"queue_order": self.queue_order, **kw})
 
 
 # names of the layer weights in the generator's dict -> the C struct fields

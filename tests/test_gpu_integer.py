@@ -27,8 +27,22 @@ def _ws(store, P):
     return torch.empty(n, dtype=torch.uint8, device="cuda")
 
 
+def _hot_batch(seed, hot_pairs, other_pairs):
+    """One Zipf-hot document shared by `hot_pairs` pairs, shuffled among
+    `other_pairs` pairs over 200 other documents (a few of them invalid)."""
+    rng = np.random.default_rng(seed)
+    doc_len = rng.integers(0, 9, 201).astype(np.int32)
+    doc_len[7] = 5
+    ids = np.concatenate([np.full(hot_pairs, 7, np.int32),
+                          rng.integers(-2, 203, other_pairs).astype(np.int32)])
+    return doc_len, ids[rng.permutation(len(ids))]
+
+
+# hot16k: one document shared by 16,384 pairs (one sort tile of the large-
+# group path); hot40k: 40,000 pairs (three tiles, ranked across tiles)
 @pytest.mark.parametrize("name", ["tiny", "qwen3_0p6b", "qwen3_4b",
-                                  "qwen3_8b", "qwen3_8b_ragged", "random"])
+                                  "qwen3_8b", "qwen3_8b_ragged", "random",
+                                  "hot16k", "hot40k"])
 def test_grouping_bit_exact(name):
     import torch
     from paper_2609_03311_amd import (DOPR_ERR_DOC_RANGE, dopr_check_status,
@@ -37,6 +51,10 @@ def test_grouping_bit_exact(name):
         rng = np.random.default_rng(0)
         doc_len = rng.integers(-1, 9, 300).astype(np.int32)
         doc_ids = rng.integers(-5, 310, 5000).astype(np.int32)
+    elif name == "hot16k":
+        doc_len, doc_ids = _hot_batch(5, 16384, 3000)
+    elif name == "hot40k":
+        doc_len, doc_ids = _hot_batch(6, 40000, 500)
     else:
         st = workloads.make(name)
         doc_len, doc_ids = st.doc_len, st.doc_ids

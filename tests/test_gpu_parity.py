@@ -118,6 +118,75 @@ def test_sharp_softmax_keys_x4():
     _free()
 
 
+@pytest.mark.parametrize("name", ["qwen3_4b", "qwen3_0p6b"])
+def test_queues_cover_every_unit(name):
+    """Every output row is written exactly as the sampled parity checks
+    assume: the rows start as NaN and none is left.  qwen3_4b has about 52
+    work units per CU, so its queues take the longest-first order (a sort
+    on the device); qwen3_0p6b has about 150 and keeps the natural order."""
+    import torch
+    st = workloads.make(name)
+    case = setup(st)
+    case.step.out.fill_(float("nan"))
+    case.step.lse.fill_(float("nan"))
+    assert run(case) == 0
+    assert not torch.isnan(case.step.out).any()
+    assert not torch.isnan(case.step.lse).any()
+    _free()
+
+
+def test_outputs_do_not_depend_on_queue_order():
+    """Units are scored independently, so the order the work queues hand
+    them out in must not change a bit: natural and longest-first order
+    against the automatic choice, on qwen3_4b (about 52 units per CU, where
+    the automatic choice is longest-first), for the block kernel the
+    automatic choice takes there, the pass kernel and last-layer scoring."""
+    import torch
+    import paper_2609_03311_amd as D
+    from paper_2609_03311_amd import pipeline
+    st = workloads.make("qwen3_4b")
+    case = setup(st)
+    assert run(case) == 0
+    o, p = case.online, case.prm
+    ref_out, ref_lse = case.step.out.clone(), case.step.lse.clone()
+    for variant in (0, 8):
+        for order in (1, 2):
+            step = pipeline.OnlineStep(
+                case.store, n_pairs=st.n_pairs, n_q_heads=st.n_q_heads,
+                total_tokens=st.n_tokens, max_tokens=int(st.seqlens.max()),
+                kernel_variant=variant, with_lse=True, queue_order=order)
+            step.attention(0, case.doc_ids, case.cu, o["q"], o["k"], o["v"],
+                           p["q_norm_w"], p["k_norm_w"])
+            torch.cuda.synchronize()
+            log(f"variant {variant} queue_order {order}")
+            assert torch.equal(step.out, ref_out), (variant, order)
+            assert torch.equal(step.lse, ref_lse), (variant, order)
+            del step
+    g = torch.Generator().manual_seed(5)
+    W = st.n_q_heads * st.head_dim
+    norm_w = (1 + 0.1 * torch.randn(W, generator=g)).to(torch.bfloat16).cuda()
+    w_head = (0.02 * torch.randn(2, W, generator=g)).to(torch.bfloat16).cuda()
+    scores = []
+    for order in (0, 1, 2):
+        sc = pipeline.ScoreStep(
+            case.store, n_pairs=st.n_pairs, n_q_heads=st.n_q_heads,
+            total_tokens=st.n_tokens, max_tokens=int(st.seqlens.max()),
+            queue_order=order)
+        sc.run(0, case.doc_ids, case.cu, o["q"], o["k"], o["v"],
+               p["q_norm_w"], p["k_norm_w"], norm_w, w_head)
+        torch.cuda.synchronize()
+        scores.append((sc.out.clone(), sc.score.clone()))
+        del sc
+    for out, score in scores[1:]:
+        assert torch.equal(out, scores[0][0])
+        assert torch.equal(score, scores[0][1])
+    with pytest.raises(D.DoprError) as e:
+        case.step.attention(0, case.doc_ids, case.cu, o["q"], o["k"], o["v"],
+                            p["q_norm_w"], p["k_norm_w"], queue_order=3)
+    assert e.value.status == D.DOPR_ERR_INVALID_ARG
+    _free()
+
+
 def test_score_token_only_and_empty_prefix():
     st = workloads.custom([0, 3], [0, 1, 0, 1], [1, 1, 2, 1], 16, 8,
                           name="t1")
