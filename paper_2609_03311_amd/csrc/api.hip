@@ -835,7 +835,9 @@ dopr_status_t dopr_salience(const dopr_salience_args_t *a, void *stream) {
   p.abar_stride = (int64_t)a->max_doclen * a->max_doclen;
   p.u = a->u;
   p.status = a->status;
-  const int hr = p.n_rep % 4 == 0 ? 4 : p.n_rep % 2 == 0 ? 2 : 1;
+  // q heads per row-LSE sweep: two where the group allows (four q heads'
+  // fragments plus the key fragments no longer fit two waves per SIMD)
+  const int hr = p.n_rep % 2 == 0 ? 2 : 1;
   const int pm = a->top_p <= 8 ? 8 : a->top_p <= 16 ? 16
                : a->top_p <= 32 ? 32 : 64;
   hipStream_t hs = as_stream(stream);

@@ -15,10 +15,14 @@
 //                 log-sum-exp of every row of every q head of the group
 //                 (scaled logits; one flash-style sweep over the visible
 //                 keys with a running maximum).
-//   k_mean_attn   per (row block, key block) of 128 x 128 below the
+//   k_mean_attn   per (row block, key block) of 128 x 128 on or below the
 //                 diagonal: every head's probabilities exp2(S - lse2),
 //                 summed over heads in head order, times 1/Hq, stored as
 //                 fp32 row-major [n, n] (only i <= j is written).
+// In both attention kernels the key blocks strictly below the diagonal,
+// which every row of the block sees whole, take a path without masks or
+// branches inside the head or sub-tile loops, so that one sub-tile's
+// exponentials can be scheduled against the next sub-tile's products.
 //   k_col_topp    per strip of 64 columns: each lane keeps the PM largest
 //                 values of its column in a sorted register list while four
 //                 waves stream interleaved rows; the lists are merged and
@@ -102,6 +106,16 @@ __device__ __forceinline__ void wait_vmem() {
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 }
 
+// The A-operand fragments of key sub-tile st (keys 32 st .. 32 st + 31 of
+// the staged block, row order perm) for lane half hf.
+__device__ __forceinline__ void key_frags(const uint16_t *kbuf, int st,
+                                          int kr, int hf, bf16x8 (&kf)[8]) {
+  const int row = 32 * st + kr;
+#pragma unroll
+  for (int s = 0; s < 8; ++s)
+    kf[s] = ld8(kbuf + row * D + (((2 * s + hf) ^ swz(row)) << 3));
+}
+
 // ---------------------------------------------------------------------------
 // Row log-sum-exp.  grid (row blocks of 128, kv head, docs); each wave owns
 // 32 rows and keeps the HR q heads of the group in registers while the
@@ -137,11 +151,11 @@ __global__ __launch_bounds__(256, 2) void k_row_lse(SalienceParams P) {
     for (int r = 0; r < HR; ++r) {
       m[r] = -INFINITY;
       l[r] = 0.f;
-      if (active) {
+      // (a wave past the document's end loads its clamped rows too: it
+      // computes below the diagonal and stores nothing)
 #pragma unroll
-        for (int s = 0; s < 8; ++s)
-          qf[r][s] = ld8(P.q + (qrow + hbase + r) * D + 16 * s + 8 * hf);
-      }
+      for (int s = 0; s < 8; ++s)
+        qf[r][s] = ld8(P.q + (qrow + hbase + r) * D + 16 * s + 8 * hf);
     }
     if (h0 > 0) __syncthreads();  // the previous heads are done with ks[0]
     stage_keys(P, doc, 0, g, ks[0]);
@@ -150,9 +164,44 @@ __global__ __launch_bounds__(256, 2) void k_row_lse(SalienceParams P) {
       __syncthreads();  // block kb staged; every wave done with the other
       if (kb + 1 < n_kb)
         stage_keys(P, doc, (kb + 1) * kKeyBlock, g, ks[(kb + 1) & 1]);
-      if (!active) continue;
       const uint16_t *kbuf = ks[kb & 1];
       const int key0 = kb * kKeyBlock;
+      if (kb < rb) {
+        // below the diagonal every row sees all 128 keys: four sub-tiles
+        // in straight-line code (no masks, no branches), the same
+        // arithmetic as the masked path with every key visible; the next
+        // sub-tile's fragments are read once the last head's products
+        // have consumed the current ones
+        bf16x8 kf[8];
+        key_frags(kbuf, 0, kr, hf, kf);
+#pragma unroll
+        for (int st = 0; st < 4; ++st) {
+#pragma unroll
+          for (int r = 0; r < HR; ++r) {
+            floatx16 S;
+#pragma unroll
+            for (int i = 0; i < 16; ++i) S[i] = 0.f;
+#pragma unroll
+            for (int s = 0; s < 8; ++s)
+              S = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[s], qf[r][s], S,
+                                                          0, 0, 0);
+            if (r == HR - 1 && st + 1 < 4)
+              key_frags(kbuf, st + 1, kr, hf, kf);
+            float mx = S[0];
+#pragma unroll
+            for (int i = 1; i < 16; ++i) mx = fmaxf(mx, S[i]);
+            const float mn = fmaxf(m[r], mx * P.c);
+            float add = 0.f;
+#pragma unroll
+            for (int i = 0; i < 16; ++i)
+              add += __builtin_amdgcn_exp2f(fmaf(S[i], P.c, -mn));
+            l[r] = l[r] * __builtin_amdgcn_exp2f(m[r] - mn) + add;
+            m[r] = mn;
+          }
+        }
+        continue;
+      }
+      if (!active) continue;
       const int nt = min(4, (last - key0) / 32 + 1);
 #pragma unroll
       for (int st = 0; st < 4; ++st) {
@@ -210,29 +259,23 @@ __global__ __launch_bounds__(256, 2) void k_row_lse(SalienceParams P) {
 }
 
 // ---------------------------------------------------------------------------
-// Head-averaged attention.  grid (triangular tile index, docs); unit (rb, kb)
-// with kb <= rb covers rows rb*128 .. +127 and keys kb*128 .. +127.  Each
-// kv head's 128 key rows are staged in LDS with direct global->LDS loads,
-// double-buffered so the next kv head's keys arrive while the current one
-// is used; each wave walks the q heads one at a time with the next head's
-// q fragments and row log-sum-exp loaded one head ahead.
-struct HeadQ {
-  bf16x8 f[8];
-  float L;
-};
-
-__global__ __launch_bounds__(256, 2) void k_mean_attn(SalienceParams P) {
-  __shared__ __attribute__((aligned(16))) uint16_t ks[2][kLdsK];
-  const int d = P.d0 + blockIdx.y;
-  const Doc doc = doc_at(P, d);
-  if (!doc.ok) return;
-  // tile t -> (rb, kb), t = rb (rb + 1) / 2 + kb
-  const int t = blockIdx.x;
-  int rb = (int)((sqrtf(8.f * t + 1.f) - 1.f) * 0.5f);
-  while ((rb + 1) * (rb + 2) / 2 <= t) ++rb;
-  while (rb * (rb + 1) / 2 > t) --rb;
-  const int kb = t - rb * (rb + 1) / 2;
-  if (rb * kRowBlock >= doc.n) return;  // block-uniform, before barriers
+// Head-averaged attention.  Unit (rb, kb), kb <= rb, covers rows rb*128 ..
+// +127 and keys kb*128 .. +127, with a code path of its own for the units
+// below the diagonal (kb < rb: every row sees all 128 keys, no masks and
+// no branches in the head loop, so a sub-tile's exponentials can overlap
+// the next sub-tile's products) and for the diagonal units (kb == rb,
+// causal masks).  Each kv head's 128 key rows are staged in
+// LDS with direct global->LDS loads, double-buffered so the next kv head's
+// keys arrive while the current one is used.  Each wave walks the q heads
+// one at a time; a sub-tile's key fragments are read from LDS while the
+// previous sub-tile's exponentials run, and the next head's q fragments
+// (into the registers of the current head's, after its last product) while
+// the last sub-tile's run.
+template <bool DIAG>
+__device__ __forceinline__ void mean_attn_unit(const SalienceParams &P,
+                                               const Doc &doc, int d, int rb,
+                                               int kb,
+                                               uint16_t (&ks)[2][kLdsK]) {
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int hf = lane >> 5, lq = lane & 31;
   const int row0 = rb * kRowBlock + wave * 32;
@@ -243,8 +286,9 @@ __global__ __launch_bounds__(256, 2) void k_mean_attn(SalienceParams P) {
   // key sub-tiles 0 .. nt-1 hold a key some row of this wave can see
   const int last_row = min(row0 + 31, doc.n - 1);
   const int nt = active ? min(4, (last_row - key0) / 32 + 1) : 0;
-  const bool diag = kb == rb;
   const int64_t qrow = (doc.t0 + jl) * P.hq;
+  const int64_t lcol = doc.t0 + jl;
+  const int kr = perm(lq);
 
   floatx16 acc[4];
 #pragma unroll
@@ -252,62 +296,75 @@ __global__ __launch_bounds__(256, 2) void k_mean_attn(SalienceParams P) {
 #pragma unroll
     for (int i = 0; i < 16; ++i) acc[s][i] = 0.f;
 
-  auto load_head = [&](int h, HeadQ &q) {
+  bf16x8 qf[8];
+  float L = 0.f, L_next = 0.f;
+  auto load_q = [&](int h) {
 #pragma unroll
     for (int s = 0; s < 8; ++s)
-      q.f[s] = ld8(P.q + (qrow + h) * D + 16 * s + 8 * hf);
-    q.L = P.lse2[(int64_t)h * P.total_tokens + doc.t0 + jl];
+      qf[s] = ld8(P.q + (qrow + h) * D + 16 * s + 8 * hf);
+    L_next = P.lse2[(int64_t)h * P.total_tokens + lcol];
   };
-  const int kr = perm(lq);
-  // Head h: on a new kv head, wait for its keys (and for every wave to be
-  // done with the other buffer), then start the next kv head's keys; issue
-  // the next head's q loads; then this head's products and probabilities.
-  int g_cur = -1;
-  auto head = [&](int h, const HeadQ &cur, HeadQ &nxt) {
+  stage_keys(P, doc, key0, 0, ks[0]);
+  // below the diagonal a wave past the document's end (rows clamped to
+  // its last row) computes anyway and stores nothing, keeping the head
+  // loop free of branches
+  if (!DIAG || active) load_q(0);
+  int g_cur = 0;
+  for (int h = 0; h < P.hq; ++h) {
+    // on a new kv head, wait for its keys (and for every wave to be done
+    // with the other buffer), then start the next kv head's keys
     const int g = h / P.n_rep;
-    if (g != g_cur) {
+    if (h == 0 || g != g_cur) {
       wait_vmem();
       __syncthreads();
       if (g + 1 < P.hkv) stage_keys(P, doc, key0, g + 1, ks[(g + 1) & 1]);
       g_cur = g;
     }
-    if (active && h + 1 < P.hq) load_head(h + 1, nxt);
     const uint16_t *kbuf = ks[g & 1];
-#pragma unroll
-    for (int st = 0; st < 4; ++st) {
-      if (st >= nt) break;
-      const int row = 32 * st + kr;
+    L = L_next;
+    const int hn = h + 1 < P.hq ? h + 1 : h;  // the last head reloads its own
+    if (!DIAG) {
       bf16x8 kf[8];
+      key_frags(kbuf, 0, kr, hf, kf);
 #pragma unroll
-      for (int s = 0; s < 8; ++s)
-        kf[s] = ld8(kbuf + row * D + (((2 * s + hf) ^ swz(row)) << 3));
-      floatx16 S;
+      for (int st = 0; st < 4; ++st) {
+        floatx16 S;
 #pragma unroll
-      for (int i = 0; i < 16; ++i) S[i] = 0.f;
+        for (int i = 0; i < 16; ++i) S[i] = 0.f;
 #pragma unroll
-      for (int s = 0; s < 8; ++s)
-        S = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[s], cur.f[s], S, 0, 0,
-                                                    0);
-      const int lim = j - key0 - 32 * st - 16 * hf;  // visible: i <= lim
-      if (diag) {
-#pragma unroll
-        for (int i = 0; i < 16; ++i)
-          acc[st][i] += i <= lim ? __builtin_amdgcn_exp2f(
-                                       fmaf(S[i], P.c, -cur.L))
-                                 : 0.f;
-      } else {
+        for (int s = 0; s < 8; ++s)
+          S = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[s], qf[s], S, 0, 0,
+                                                      0);
+        if (st + 1 < 4)
+          key_frags(kbuf, st + 1, kr, hf, kf);
+        else
+          load_q(hn);
 #pragma unroll
         for (int i = 0; i < 16; ++i)
-          acc[st][i] += __builtin_amdgcn_exp2f(fmaf(S[i], P.c, -cur.L));
+          acc[st][i] += __builtin_amdgcn_exp2f(fmaf(S[i], P.c, -L));
       }
+    } else {
+      if (!active) continue;
+#pragma unroll
+      for (int st = 0; st < 4; ++st) {
+        if (st >= nt) break;
+        bf16x8 kf[8];
+        key_frags(kbuf, st, kr, hf, kf);
+        floatx16 S;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) S[i] = 0.f;
+#pragma unroll
+        for (int s = 0; s < 8; ++s)
+          S = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[s], qf[s], S, 0, 0,
+                                                      0);
+        const int lim = j - key0 - 32 * st - 16 * hf;  // visible: i <= lim
+#pragma unroll
+        for (int i = 0; i < 16; ++i)
+          acc[st][i] += i <= lim ? __builtin_amdgcn_exp2f(fmaf(S[i], P.c, -L))
+                                 : 0.f;
+      }
+      load_q(hn);
     }
-  };
-  stage_keys(P, doc, key0, 0, ks[0]);
-  HeadQ qa, qb;
-  if (active) load_head(0, qa);
-  for (int h = 0; h < P.hq; h += 2) {
-    head(h, qa, qb);
-    if (h + 1 < P.hq) head(h + 1, qb, qa);
   }
   if (!active || j >= doc.n) return;
   float *out = P.abar + (int64_t)(d - P.d0) * P.abar_stride +
@@ -330,6 +387,30 @@ __global__ __launch_bounds__(256, 2) void k_mean_attn(SalienceParams P) {
       for (int i = 0; i < 16; ++i)
         if (i0 + i <= j) out[i0 + i] = v[i];
     }
+  }
+}
+
+// grid (units, docs): the nb diagonal units first (their waves see 1 to 4
+// sub-tiles, so they are kept out of the launch's tail), then the units
+// below the diagonal, unit nb + t with t = rb (rb - 1) / 2 + kb.
+__global__ __launch_bounds__(256, 2) void k_mean_attn(SalienceParams P,
+                                                      int32_t nb) {
+  __shared__ __attribute__((aligned(16))) uint16_t ks[2][kLdsK];
+  const int d = P.d0 + blockIdx.y;
+  const Doc doc = doc_at(P, d);
+  if (!doc.ok) return;
+  if ((int)blockIdx.x < nb) {  // block-uniform
+    const int rb = blockIdx.x;
+    if (rb * kRowBlock >= doc.n) return;  // before any barrier
+    mean_attn_unit<true>(P, doc, d, rb, rb, ks);
+  } else {
+    const int t = blockIdx.x - nb;
+    int rb = (int)((sqrtf(8.f * t + 1.f) + 1.f) * 0.5f);
+    while (rb * (rb - 1) / 2 > t) --rb;
+    while ((rb + 1) * rb / 2 <= t) ++rb;
+    const int kb = t - rb * (rb - 1) / 2;
+    if (rb * kRowBlock >= doc.n) return;  // before any barrier
+    mean_attn_unit<false>(P, doc, d, rb, kb, ks);
   }
 }
 
@@ -504,14 +585,12 @@ hipError_t launch_salience_chunk(const SalienceParams &p, int32_t n_docs,
   const dim3 g_lse(nb, p.hkv, n_docs);
   const dim3 g_att(nb * (nb + 1) / 2, n_docs);
   const dim3 g_col((p.max_len + kStrip - 1) / kStrip, n_docs);
-  if (hr == 4) {
-    hipLaunchKernelGGL(k_row_lse<4>, g_lse, dim3(256), 0, s, p);
-  } else if (hr == 2) {
+  if (hr == 2) {
     hipLaunchKernelGGL(k_row_lse<2>, g_lse, dim3(256), 0, s, p);
   } else {
     hipLaunchKernelGGL(k_row_lse<1>, g_lse, dim3(256), 0, s, p);
   }
-  hipLaunchKernelGGL(k_mean_attn, g_att, dim3(256), 0, s, p);
+  hipLaunchKernelGGL(k_mean_attn, g_att, dim3(256), 0, s, p, (int32_t)nb);
   if (pm == 8)
     hipLaunchKernelGGL(k_col_topp<8>, g_col, dim3(256), 0, s, p);
   else if (pm == 16)
