@@ -1,39 +1,21 @@
-// stream.hip -- the streaming attention kernel of the full online layer
-// and the k^ precompute it reads (see the overview below).  Built as its own
-// translation unit: its chunk-stream cursor must stay in scalar registers,
-// which needs the compiler's common-code sinking off (it would otherwise
-// merge stores to different cursor fields into one through a pointer and
-// move the cursor to scratch memory).
+// stream.hip -- the pass kernel of the full online layer (the automatic
+// choice unless every prefix is at most 96 slots at head size 128) and the
+// k^ precompute it reads.  Built as its own
+// translation unit with the compiler's common-code sinking off: that
+// transformation would merge stores of different unit fields into one
+// through a pointer and move wave-uniform state to scratch memory.
 #include "attn_common.hpp"
 
 namespace dopr {
 namespace {
 
 // ---------------------------------------------------------------------------
-// Streaming kernel (full layer).  The block kernels above keep the prefix
-// resident and stage own keys cooperatively chunk by chunk, so every pass
-// waits for its own-key loads and all waves of a block move through the
-// same phases together.  Here every chunk a pass needs -- the document's
-// prefix chunks, then its pairs' own-key chunks -- is one element of a
-// single stream that flows through a ring of LDS slots:
-//   - k^ of every online token is formed once per batch by k_own_khat (the
-//     arithmetic of own_stage), so an own chunk, like a prefix chunk, is a
-//     plain copy: direct global->LDS loads of K rows (swizzled as prefix
-//     K) and of raw v rows in their natural [key][D] layout, which the PV
-//     product reads with gfx950's transposing LDS read as V^T fragments;
-//   - the loads of chunk c + R - 1 are issued while chunk c is consumed, so
-//     a chunk's memory latency hides behind the R - 1 chunks before it,
-//     across pass and work-unit boundaries;
-//   - one LDS-only barrier per chunk (it frees the slot of the chunk
-//     before); each wave waits only for its own loads of the chunk it is
-//     about to read (vmcnt, counted from the loads issued after it).
-// Work units are claimed one ahead by thread 0 and handed to every wave
-// through a small LDS table.  A row sees the same chunks in the same order
-// with the same operand values as in the block kernels, so the outputs are
-// bit-identical to theirs.  Only the reference-free softmax (mode 0) runs
-// here: units over the logit bound and units with a normaliser out of range
-// go to the exact pass, as in the fast block kernels.
-
+// k^ precompute.  One block per sorted pair: RMSNorm, gain and rotation of
+// every online key of the pair at positions L + j, for every kv head, with
+// the arithmetic of the block kernels' own-key staging (own_stage), rounded
+// to bf16 and written as k^ [Hkv][Ntok][D].  The pass kernel then copies
+// own keys like prefix keys, and a pair's keys are normed once per batch
+// instead of once per pass that reads them.
 template <int D>
 __global__ __launch_bounds__(256) void k_own_khat(KhatParams P) {
   constexpr int NSUB = D / 16, ROWS = 256 / NSUB;
@@ -101,8 +83,8 @@ __device__ __forceinline__ void lds_barrier() {
 // V^T fragments of an own chunk from v rows [32][D] in LDS, by gfx950's
 // transposing LDS read (4 keys of one head dim per lane and read, two
 // reads per fragment).  Issued through inline assembly: the compiler
-// would otherwise wait for every outstanding direct-to-LDS load of the
-// ring before each of these reads.  The results are not ready until
+// would otherwise wait for every outstanding direct-to-LDS load in
+// flight before each of these reads.  The results are not ready until
 // lgkm_ready() has run on them.  vaddr is this lane's LDS byte address
 // (row 16*hf + e, column perm32(16*(lq/16) + 4q) of the lane's (e, q) role
 // in its 16-lane group); ex selects the row swizzle.
@@ -179,25 +161,30 @@ __device__ __forceinline__ void attend_own(const uint16_t *kblk,
 }
 
 // ---------------------------------------------------------------------------
-// Pass kernel (full layer).  One work unit is one pass: at most 256 stacked
-// rows of one document's pairs for one kv head, one 32-row tile per wave
-// (the planner cuts items of exactly 256 rows).  The document's prefix is
-// staged in LDS for the unit and its chunks run back to back with no
-// barrier, as in the block kernels; what differs is everything around them:
-//   - a document's units are neighbours in one XCD's queue, so neighbouring
-//     CUs stage the same prefix at about the same time and all but the
-//     first read it from that XCD's L2, not from HBM;
+// Pass kernel (full layer).  A work unit is one item of one document's
+// stacked rows (up to rows_per_item, 2048 by default) for one kv head,
+// walked in passes of 256 rows, one 32-row tile per wave of the 8-wave
+// block.  The document's prefix (up to 256 slots at head size 128) is
+// staged in LDS once per unit and read by every pass with no barrier, as
+// in the block kernels; what differs is everything around it:
 //   - own keys come precomputed (k_own_khat), so an own chunk is a plain
 //     copy: K rows and raw v rows go straight to LDS with direct loads into
-//     two slots, and the PV product reads v with the transposing LDS read;
-//     the first two own chunks are issued together with the prefix, later
-//     ones while the chunk before them is consumed;
-//   - the prefix and first own chunks are in flight while the q rows load
-//     and the q^ prologue runs, so one memory latency covers all of them;
-//   - wave 0 claims the next unit while the current one is in progress.
+//     two slots, and the PV product reads v with gfx950's transposing LDS
+//     read; a pass's first two own chunks are issued before its prefix
+//     products, later ones while the chunk before them is consumed;
+//   - the pass's q rows load while the prefix and first own chunks are in
+//     flight, so one memory latency covers all of them;
+//   - wave 0 claims the next unit while the current one is in progress and
+//     hands it to the other waves through a small LDS table.
 // Per row the chunk order and operand values are those of the block
-// kernels, so the outputs are bit-identical to theirs.  Units over the
-// logit bound and rows with a normaliser out of range go to the exact pass.
+// kernels, so the outputs are bit-identical to theirs.  Only the
+// reference-free softmax (mode 0) runs here: units over the logit bound
+// and units with a normaliser out of range go to the exact pass.
+//
+// Loop exits are wave- or block-uniform: the unit loop ends on the unit
+// wave 0 published in LDS (read after a barrier), the pass loop on
+// wave-uniform unit fields, the pair search on a ballot, and the own-chunk
+// loop on positions taken from the pair records with readlane.
 
 // A work unit as wave 0 found it (every field wave-uniform).
 struct PUnit {
@@ -459,7 +446,6 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(
       const int rtok = rec.x, rT = rec.y;
       const int rj = rec.y - 1 - (lo_row - rec.z) / P.n_rep;
 
-      
       // the pass's first two own chunks
       OwnPos o0, o1, o2;
       own_at(o0, 0, rtok, rT, rj);

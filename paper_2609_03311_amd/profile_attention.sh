@@ -8,10 +8,13 @@
 # (last-layer scoring).  Raw output stays in gpurun_out/prof_<path>_<config>/;
 # the summaries are written to gpurun_out/summaries/.
 # usage: bash paper_2609_03311_amd/profile_attention.sh CONFIG full|score [D]
+#        [summarize]   (the last form only rewrites the summaries from the
+#                       raw output already in gpurun_out/prof_<path>_<config>/)
 set -o pipefail
 cfg=$1
 path=$2
 D=${3:-128}
+only_summarize=$4
 R=$(cd "$(dirname "$0")/.." && pwd)
 out=$R/gpurun_out/prof_${path}_${cfg}
 sum=$R/gpurun_out/summaries
@@ -39,12 +42,14 @@ step() {  # name, extra bench options, rocprofv3 options...
   return $rc
 }
 
-step stats "" --kernel-trace --stats &&
-  step fetch --copy-calibration --pmc FETCH_SIZE &&
-  step write --copy-calibration --pmc WRITE_SIZE &&
-  step pmc_a "" --pmc $(python3 -c "import sys; sys.path.insert(0, '$R'); from paper_2609_03311_amd import profiling as p; print(p.PMC_PASSES[0])") &&
-  step pmc_b "" --pmc $(python3 -c "import sys; sys.path.insert(0, '$R'); from paper_2609_03311_amd import profiling as p; print(p.PMC_PASSES[1])") ||
-  exit $?
+if [ "$only_summarize" != summarize ]; then
+  step stats "" --kernel-trace --stats &&
+    step fetch --copy-calibration --pmc FETCH_SIZE &&
+    step write --copy-calibration --pmc WRITE_SIZE &&
+    step pmc_a "" --pmc $(python3 -c "import sys; sys.path.insert(0, '$R'); from paper_2609_03311_amd import profiling as p; print(p.PMC_PASSES[0])") &&
+    step pmc_b "" --pmc $(python3 -c "import sys; sys.path.insert(0, '$R'); from paper_2609_03311_amd import profiling as p; print(p.PMC_PASSES[1])") ||
+    exit $?
+fi
 
 cd "$R" &&
   python3 -m paper_2609_03311_amd.profiling stats "$out/stats" \

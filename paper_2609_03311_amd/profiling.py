@@ -3,6 +3,9 @@
     python3 -m paper_2609_03311_amd.profiling stats TRACE_DIR --command CMD
     python3 -m paper_2609_03311_amd.profiling traffic FETCH_DIR WRITE_DIR \
         --command CMD [--kernel REGEX]
+    python3 -m paper_2609_03311_amd.profiling pmc RUN_DIR... --command CMD
+    python3 -m paper_2609_03311_amd.profiling benchtable JSONL... \
+        --command CMD
 
 `stats` condenses `rocprofv3 --kernel-trace --stats` (run_kernel_stats.csv)
 into a per-kernel table.  `traffic` turns two `--pmc FETCH_SIZE` /
@@ -39,11 +42,20 @@ CALIB_KERNEL = r"bitwise_not"
 CALIB_BYTES = 1 << 30
 
 
+def _code_only(text):
+    """The source without comments and with whitespace runs collapsed, so
+    that an edit to a comment leaves the hash alone."""
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", " ", text)
+    return " ".join(text.split())
+
+
 def kernel_source_sha():
+    """Hash of the attention kernels' code (comments and layout ignored)."""
     h = hashlib.sha256()
     for rel in KERNEL_SOURCES:
-        with open(os.path.join(HERE, rel), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(HERE, rel), encoding="utf-8") as f:
+            h.update(_code_only(f.read()).encode())
     return h.hexdigest()[:16]
 
 
@@ -239,6 +251,53 @@ def read_summary(path):
     return vals
 
 
+def bench_table(paths, command):
+    """One row per bench.py JSON line (files of JSON lines; other lines are
+    skipped): workload, path, queue order, step and attention times, the
+    roofline figures and the throughput."""
+    import json
+    out = ["# bench.py on each workload and path (one MI355X)",
+           f"command: {command}", "",
+           f"{'workload':20s} {'path':34s} {'qo':>2s} {'step ms':>9s} "
+           f"{'attn ms':>9s} {'achieved':>16s} {'frac':>6s} "
+           f"{'throughput':>22s} {'traffic':>8s} {'mfma':>6s}"]
+    for path in paths:
+        with open(path) as f:
+            for line in f:
+                line = line.strip()
+                if not line.startswith("{"):
+                    continue
+                try:
+                    d = json.loads(line)
+                except ValueError:
+                    continue
+                cfg = d.get("config", {})
+                r = d.get("roofline") or {}
+                qo = cfg.get("queue_order")
+                attn = d.get("attention_ms")
+                tr = r.get("traffic")
+                mu = d.get("mfma_util")
+                out.append(
+                    f"{str(cfg.get('name', '?')):20s} "
+                    f"{str(cfg.get('path', '?'))[:34]:34s} "
+                    f"{'' if qo is None else qo:>2} "
+                    f"{d.get('ms_per_step', float('nan')):9.3f} "
+                    f"{'' if attn is None else f'{attn:9.3f}':>9s} "
+                    f"{r.get('achieved', float('nan')):9.1f} "
+                    f"{str(r.get('unit', '')):>6s} "
+                    f"{r.get('frac', float('nan')):6.4f} "
+                    f"{d.get('value', float('nan')):12.1f} "
+                    f"{str(d.get('unit', ''))[:9]:>9s} "
+                    f"{'' if tr is None else f'{tr:8.2f}':>8s} "
+                    f"{'' if mu is None else f'{mu:6.3f}':>6s}")
+                cb = d.get("cpu_baseline")
+                if cb:
+                    out.append(f"{'':20s}   cpu_baseline {cb.get('value')} "
+                               f"{cb.get('unit')} on {cb.get('cores')} "
+                               f"threads ({cb.get('kind')})")
+    return "\n".join(out) + "\n"
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__)
     sub = ap.add_subparsers(dest="cmd", required=True)
@@ -254,8 +313,13 @@ def main(argv=None):
     c.add_argument("run_dirs", nargs="+")
     c.add_argument("--command", required=True)
     c.add_argument("--kernel", default=ATTN_KERNEL)
+    t = sub.add_parser("benchtable")
+    t.add_argument("jsonl", nargs="+")
+    t.add_argument("--command", required=True)
     args = ap.parse_args(argv)
-    if args.cmd == "stats":
+    if args.cmd == "benchtable":
+        sys.stdout.write(bench_table(args.jsonl, args.command))
+    elif args.cmd == "stats":
         sys.stdout.write(stats(args.trace_dir, args.command))
     elif args.cmd == "pmc":
         sys.stdout.write(pmc(args.run_dirs, args.command, args.kernel))
