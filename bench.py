@@ -885,8 +885,9 @@ def main():
         achieved = w["total"] / (attn_avg * 1e-3) / 1e9
         traffic = measured_traffic(args.config, args.variant, args.path)
         mfma_util = measured_mfma_util(args.config, args.variant, args.path)
-    if score_path and args.no_score_rows:
-        traffic = None
+    if (score_path and args.no_score_rows) or args.queue_order != 0:
+        traffic = None  # the committed profiles were taken without these
+        mfma_util = None if args.queue_order != 0 else mfma_util
     result = {
         "metric": (METRIC_LAYER if layer_path else
                    METRIC_SCORE if score_path else METRIC),

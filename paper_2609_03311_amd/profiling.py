@@ -254,13 +254,15 @@ def read_summary(path):
 def bench_table(paths, command):
     """One row per bench.py JSON line (files of JSON lines; other lines are
     skipped): workload, path, queue order, step and attention times, the
-    roofline figures and the throughput."""
+    roofline figures, the throughput, and where a committed profile of the
+    kernel exists for the current sources, its measured HBM bytes per
+    launch and MFMA busy fraction."""
     import json
     out = ["# bench.py on each workload and path (one MI355X)",
            f"command: {command}", "",
            f"{'workload':20s} {'path':34s} {'qo':>2s} {'step ms':>9s} "
            f"{'attn ms':>9s} {'achieved':>16s} {'frac':>6s} "
-           f"{'throughput':>22s} {'traffic':>8s} {'mfma':>6s}"]
+           f"{'throughput':>22s} {'HBM GB':>8s} {'mfma':>6s}"]
     for path in paths:
         with open(path) as f:
             for line in f:
@@ -277,9 +279,12 @@ def bench_table(paths, command):
                 attn = d.get("attention_ms")
                 tr = r.get("traffic")
                 mu = d.get("mfma_util")
+                label = cfg.get("path") or (
+                    "full layer, prefix budget sweep" if "k_infer" in cfg
+                    else d.get("metric", "?"))
                 out.append(
                     f"{str(cfg.get('name', '?')):20s} "
-                    f"{str(cfg.get('path', '?'))[:34]:34s} "
+                    f"{str(label)[:34]:34s} "
                     f"{'' if qo is None else qo:>2} "
                     f"{d.get('ms_per_step', float('nan')):9.3f} "
                     f"{'' if attn is None else f'{attn:9.3f}':>9s} "
@@ -288,8 +293,15 @@ def bench_table(paths, command):
                     f"{r.get('frac', float('nan')):6.4f} "
                     f"{d.get('value', float('nan')):12.1f} "
                     f"{str(d.get('unit', ''))[:9]:>9s} "
-                    f"{'' if tr is None else f'{tr:8.2f}':>8s} "
+                    f"{'' if tr is None else f'{tr / 1e9:8.2f}':>8s} "
                     f"{'' if mu is None else f'{mu:6.3f}':>6s}")
+                if "k_infer" in cfg:
+                    out.append(f"{'':20s}   K_infer {cfg['k_infer']}: store "
+                               f"{d.get('store_gb_per_layer')} GB per layer, "
+                               f"{d.get('doc_state_kb_all_layers')} KB per "
+                               f"document over 36 layers, "
+                               f"{d.get('us_per_pair')} us per pair, "
+                               f"algorithmic {d.get('algorithmic_gb')} GB")
                 cb = d.get("cpu_baseline")
                 if cb:
                     out.append(f"{'':20s}   cpu_baseline {cb.get('value')} "
