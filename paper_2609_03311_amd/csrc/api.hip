@@ -747,7 +747,7 @@ dopr_status_t check_salience(const dopr_salience_args_t *a, bool full,
 }
 
 struct SalienceWs {
-  size_t lse_bytes = 0, abar_bytes = 0, total = 0;
+  size_t lse_bytes = 0, kn_bytes = 0, abar_bytes = 0, total = 0;
   int32_t chunk = 0;  // documents per pass
 };
 
@@ -756,6 +756,8 @@ SalienceWs salience_ws(const dopr_salience_args_t *a) {
   const size_t M = (size_t)a->max_doclen;
   w.lse_bytes = align_up(sizeof(float) * (size_t)a->n_q_heads *
                              (size_t)a->total_tokens, kAlign);
+  w.kn_bytes = align_up(sizeof(float) * (size_t)a->n_docs *
+                            (size_t)a->n_kv_heads, kAlign);
   if (a->attn_mean) {
     w.chunk = a->n_docs;
   } else {
@@ -766,7 +768,7 @@ SalienceWs salience_ws(const dopr_salience_args_t *a) {
     w.chunk = (int32_t)c;
     w.abar_bytes = align_up(per * c, kAlign);
   }
-  w.total = w.lse_bytes + w.abar_bytes;
+  w.total = w.lse_bytes + w.kn_bytes + w.abar_bytes;
   return w;
 }
 
@@ -804,14 +806,15 @@ dopr_status_t dopr_salience(const dopr_salience_args_t *a, void *stream) {
   // the least workspace holds the row statistics and one document's Abar;
   // more room lets more documents share a pass
   const size_t per = sizeof(float) * (size_t)a->max_doclen * a->max_doclen;
-  const size_t least = w.lse_bytes + (a->attn_mean ? 0 : per);
+  const size_t fixed = w.lse_bytes + w.kn_bytes;
+  const size_t least = fixed + (a->attn_mean ? 0 : per);
   if (!a->workspace || a->workspace_bytes < least)
     return fail(DOPR_ERR_WORKSPACE,
                 "workspace needs at least " + std::to_string(least) +
                     " bytes");
   if (!a->attn_mean)
     w.chunk = (int32_t)std::min<size_t>(
-        (size_t)a->n_docs, (a->workspace_bytes - w.lse_bytes) / per);
+        (size_t)a->n_docs, (a->workspace_bytes - fixed) / per);
   if (reinterpret_cast<uintptr_t>(a->workspace) % kAlign)
     return fail(DOPR_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
   char *base = static_cast<char *>(a->workspace);
@@ -830,8 +833,9 @@ dopr_status_t dopr_salience(const dopr_salience_args_t *a, void *stream) {
   p.c = a->softmax_scale * 1.4426950408889634f;
   p.inv_hq = 1.0f / (float)a->n_q_heads;
   p.lse2 = reinterpret_cast<float *>(base);
+  p.kmax = reinterpret_cast<float *>(base + w.lse_bytes);
   p.abar = a->attn_mean ? a->attn_mean
-                        : reinterpret_cast<float *>(base + w.lse_bytes);
+                        : reinterpret_cast<float *>(base + fixed);
   p.abar_stride = (int64_t)a->max_doclen * a->max_doclen;
   p.u = a->u;
   p.status = a->status;
@@ -842,6 +846,7 @@ dopr_status_t dopr_salience(const dopr_salience_args_t *a, void *stream) {
                : a->top_p <= 32 ? 32 : 64;
   hipStream_t hs = as_stream(stream);
   hipError_t e = launch_salience_check(p, hs);
+  if (e == hipSuccess) e = launch_key_norms(p, hs);
   for (int32_t d0 = 0; e == hipSuccess && d0 < a->n_docs; d0 += w.chunk) {
     p.d0 = d0;
     const int32_t nd = std::min(w.chunk, a->n_docs - d0);

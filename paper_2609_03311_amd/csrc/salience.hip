@@ -36,6 +36,7 @@
 // that lane half hf's 16 accumulators hold 16 consecutive keys 16 hf + i
 // for the lane's query column.
 #include <cmath>
+#include <type_traits>
 
 #include "internal.hpp"
 
@@ -117,12 +118,66 @@ __device__ __forceinline__ void key_frags(const uint16_t *kbuf, int st,
 }
 
 // ---------------------------------------------------------------------------
+// Largest key norm of each (document, kv head).  grid (docs, kv heads);
+// 16 lanes per key row (16 bytes each), four rows per wave and step, four
+// steps in flight.
+__global__ __launch_bounds__(256) void k_key_norm(SalienceParams P) {
+  __shared__ float wmax[4];
+  const int d = blockIdx.x, g = blockIdx.y;
+  const Doc doc = doc_at(P, d);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int sub = lane & 15, r0 = 4 * wave + (lane >> 4);  // 16 rows a step
+  float mx = 0.f;
+  if (doc.ok) {
+    for (int i0 = 0; i0 < doc.n; i0 += 64) {
+      float ss[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int i = i0 + 16 * u + r0;
+        ss[u] = 0.f;
+        if (i < doc.n) {
+          const uint4 w = *reinterpret_cast<const uint4 *>(
+              P.k + ((doc.t0 + i) * P.hkv + g) * D + 8 * sub);
+          const uint32_t v[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float lo = __uint_as_float(v[e] << 16);
+            const float hi = __uint_as_float(v[e] & 0xffff0000u);
+            ss[u] = fmaf(lo, lo, fmaf(hi, hi, ss[u]));
+          }
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+#pragma unroll
+        for (int off = 8; off > 0; off >>= 1)
+          ss[u] += __shfl_xor(ss[u], off, 64);
+        mx = fmaxf(mx, ss[u]);
+      }
+    }
+  }
+#pragma unroll
+  for (int off = 16; off < 64; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off, 64));
+  if (lane == 0) wmax[wave] = mx;
+  __syncthreads();
+  if (threadIdx.x == 0)
+    P.kmax[(int64_t)d * P.hkv + g] =
+        sqrtf(fmaxf(fmaxf(wmax[0], wmax[1]), fmaxf(wmax[2], wmax[3])));
+}
+
 // Row log-sum-exp.  grid (row blocks of 128, kv head, docs); each wave owns
 // 32 rows and keeps the HR q heads of the group in registers while the
 // document's keys 0 .. (last row of the block) stream through LDS, one
 // 128-key block at a time, shared by the block's four waves.  Per row and
-// head: a running maximum and sum over the visible keys (scaled logits in
-// log2 units), combined across the two lane halves at the end.
+// head the sum of 2^(logit - m) over the visible keys (scaled logits in log2
+// units) with one of two references m:
+//   - fixed: m = c |q^_j| max_i |k^_i| bounds every logit of the row from
+//     above (Cauchy-Schwarz), and from below by -m, so with m <= 60 every
+//     term lies in [2^-120, 1] and no maximum is tracked at all;
+//   - running: the exact running maximum, for waves where some row's bound
+//     exceeds 60.
+// The two lane halves are combined at the end.
+constexpr float kFixedRefMax = 60.f;
 template <int HR>
 __global__ __launch_bounds__(256, 2) void k_row_lse(SalienceParams P) {
   __shared__ __attribute__((aligned(16))) uint16_t ks[2][kLdsK];
@@ -143,19 +198,36 @@ __global__ __launch_bounds__(256, 2) void k_row_lse(SalienceParams P) {
   const int kr = perm(lq);
   const int n_kb = rb + 1;  // key blocks 0 .. rb
 
+  const float kmax = P.kmax[(int64_t)d * P.hkv + g];
   for (int h0 = 0; h0 < P.n_rep; h0 += HR) {
     const int hbase = g * P.n_rep + h0;
     bf16x8 qf[HR][8];
     float m[HR], l[HR];
+    bool fits = true;
 #pragma unroll
     for (int r = 0; r < HR; ++r) {
-      m[r] = -INFINITY;
       l[r] = 0.f;
       // (a wave past the document's end loads its clamped rows too: it
       // computes below the diagonal and stores nothing)
+      float ss = 0.f;
 #pragma unroll
-      for (int s = 0; s < 8; ++s)
+      for (int s = 0; s < 8; ++s) {
         qf[r][s] = ld8(P.q + (qrow + hbase + r) * D + 16 * s + 8 * hf);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float x = (float)qf[r][s][e];
+          ss = fmaf(x, x, ss);
+        }
+      }
+      ss += __shfl_xor(ss, 32, 64);
+      m[r] = P.c * sqrtf(ss) * kmax;
+      fits = fits && m[r] <= kFixedRefMax;
+    }
+    // wave-uniform choice of the reference
+    const bool fixed = __all(fits);
+    if (!fixed) {
+#pragma unroll
+      for (int r = 0; r < HR; ++r) m[r] = -INFINITY;
     }
     if (h0 > 0) __syncthreads();  // the previous heads are done with ks[0]
     stage_keys(P, doc, 0, g, ks[0]);
@@ -166,12 +238,13 @@ __global__ __launch_bounds__(256, 2) void k_row_lse(SalienceParams P) {
         stage_keys(P, doc, (kb + 1) * kKeyBlock, g, ks[(kb + 1) & 1]);
       const uint16_t *kbuf = ks[kb & 1];
       const int key0 = kb * kKeyBlock;
-      if (kb < rb) {
-        // below the diagonal every row sees all 128 keys: four sub-tiles
-        // in straight-line code (no masks, no branches), the same
-        // arithmetic as the masked path with every key visible; the next
-        // sub-tile's fragments are read once the last head's products
-        // have consumed the current ones
+      // below the diagonal every row sees all 128 keys: four sub-tiles in
+      // straight-line code (no masks, no branches), the same arithmetic as
+      // the masked path with every key visible; the next sub-tile's
+      // fragments are read once the last head's products have consumed
+      // the current ones
+      auto full_block = [&](auto fixed_ref) {
+        constexpr bool FIXED = decltype(fixed_ref)::value;
         bf16x8 kf[8];
         key_frags(kbuf, 0, kr, hf, kf);
 #pragma unroll
@@ -187,18 +260,32 @@ __global__ __launch_bounds__(256, 2) void k_row_lse(SalienceParams P) {
                                                           0, 0, 0);
             if (r == HR - 1 && st + 1 < 4)
               key_frags(kbuf, st + 1, kr, hf, kf);
-            float mx = S[0];
+            if (FIXED) {
+              float add = 0.f;
 #pragma unroll
-            for (int i = 1; i < 16; ++i) mx = fmaxf(mx, S[i]);
-            const float mn = fmaxf(m[r], mx * P.c);
-            float add = 0.f;
+              for (int i = 0; i < 16; ++i)
+                add += __builtin_amdgcn_exp2f(fmaf(S[i], P.c, -m[r]));
+              l[r] += add;
+            } else {
+              float mx = S[0];
 #pragma unroll
-            for (int i = 0; i < 16; ++i)
-              add += __builtin_amdgcn_exp2f(fmaf(S[i], P.c, -mn));
-            l[r] = l[r] * __builtin_amdgcn_exp2f(m[r] - mn) + add;
-            m[r] = mn;
+              for (int i = 1; i < 16; ++i) mx = fmaxf(mx, S[i]);
+              const float mn = fmaxf(m[r], mx * P.c);
+              float add = 0.f;
+#pragma unroll
+              for (int i = 0; i < 16; ++i)
+                add += __builtin_amdgcn_exp2f(fmaf(S[i], P.c, -mn));
+              l[r] = l[r] * __builtin_amdgcn_exp2f(m[r] - mn) + add;
+              m[r] = mn;
+            }
           }
         }
+      };
+      if (kb < rb) {
+        if (fixed)
+          full_block(std::true_type{});
+        else
+          full_block(std::false_type{});
         continue;
       }
       if (!active) continue;
@@ -231,7 +318,7 @@ __global__ __launch_bounds__(256, 2) void k_row_lse(SalienceParams P) {
             x[i] = masked && i > lim ? -INFINITY : S[i];
             mx = fmaxf(mx, x[i]);
           }
-          const float mn = fmaxf(m[r], mx * P.c);
+          const float mn = fixed ? m[r] : fmaxf(m[r], mx * P.c);
           if (mn > -INFINITY) {
             float add = 0.f;
 #pragma unroll
@@ -599,6 +686,13 @@ hipError_t launch_salience_chunk(const SalienceParams &p, int32_t n_docs,
     hipLaunchKernelGGL(k_col_topp<32>, g_col, dim3(256), 0, s, p);
   else
     hipLaunchKernelGGL(k_col_topp<64>, g_col, dim3(256), 0, s, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_key_norms(const SalienceParams &p, hipStream_t s) {
+  if (p.n_docs == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_key_norm, dim3((unsigned)p.n_docs, (unsigned)p.hkv),
+                     dim3(256), 0, s, p);
   return hipGetLastError();
 }
 

@@ -129,6 +129,27 @@ def test_salience_parity_edges(i):
     _free()
 
 
+def test_salience_row_references():
+    """The row log-sum-exp takes a fixed reference (the Cauchy-Schwarz bound
+    c |q_j| max|k|) where every row of a wave has a bound of at most 60, and
+    the exact running maximum elsewhere.  Here a band of rows has its
+    queries scaled by 8 (bounds near 160), so waves of both kinds, and
+    waves next to each other in one block, meet the oracle."""
+    import torch
+    lens, hq, hkv, p = [256, 300], 32, 8, 8
+    q, k = workloads.salience_inputs(lens, hq, hkv, "cuda", 23)
+    q = q.clone()
+    q[40:72] = (q[40:72].float() * 8).to(torch.bfloat16)       # doc 0
+    q[256 + 200:256 + 232] = (q[256 + 200:256 + 232].float() * 8).to(
+        torch.bfloat16)                                        # doc 1
+    step, _, _ = run_case(lens, hq, hkv, p, q=q, k=k)
+    ora = oracle_for(step, q, k, p, range(len(lens)))
+    worst = max(check_doc(step, d, ora) for d in range(len(lens)))
+    log(f"mixed references: max |du| {worst:.3e}")
+    del step
+    _free()
+
+
 def test_salience_uniform_closed_form():
     """q = 0: Abar[j, i] = 1/(j+1) and u strictly decreasing, so the top-K
     are the first K positions."""
