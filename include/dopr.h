@@ -411,10 +411,11 @@ typedef struct {
 } dopr_salience_args_t;
 
 /* Workspace bytes for these arguments (host): the row log-sum-exp of every
- * (token, q head) and, unless attn_mean is given, Abar for as many documents
- * at a time as fit in 1 GiB (at least one).  dopr_salience accepts any
- * workspace that holds the row statistics plus one document's Abar
- * (4 M^2 bytes) and processes as many documents per pass as fit. */
+ * (token, q head), the largest key norm of every (document, kv head) and,
+ * unless attn_mean is given, Abar for as many documents at a time as fit
+ * in 1 GiB (at least one).  dopr_salience accepts any workspace that holds
+ * the row statistics and key norms plus one document's Abar (4 M^2 bytes)
+ * and processes as many documents per pass as fit. */
 dopr_status_t dopr_salience_workspace(const dopr_salience_args_t *args,
                                       size_t *bytes);
 

@@ -153,22 +153,28 @@ def test_host_validation_codes():
 
 def test_salience_host_validation_and_workspace():
     """Salience argument checks and workspace sizes (host arithmetic only):
-    the row log-sum-exp of every (token, q head), plus the head-averaged
-    matrix of as many documents as fit in 1 GiB unless the caller keeps it."""
+    the row log-sum-exp of every (token, q head), the largest key norm of
+    every (document, kv head), plus the head-averaged matrix of as many
+    documents as fit in 1 GiB unless the caller keeps it."""
     D = _D()
     L = D.lib()
+
+    def up(n):
+        return -(-n // 256) * 256
+
     ws = D.dopr_salience_workspace(n_docs=64, max_doclen=2048, n_q_heads=32,
                                    n_kv_heads=8, top_p=8,
                                    total_tokens=64 * 2048)
     lse = 4 * 32 * 64 * 2048
-    assert ws == lse + (1 << 30)          # 64 docs of 16 MiB in one pass
+    kn = up(4 * 64 * 8)
+    assert ws == lse + kn + (1 << 30)     # 64 docs of 16 MiB in one pass
     ws = D.dopr_salience_workspace(n_docs=3, max_doclen=2048, n_q_heads=32,
                                    n_kv_heads=8, top_p=8, total_tokens=5000)
-    assert ws == -(-4 * 32 * 5000 // 256) * 256 + 3 * 2048 * 2048 * 4
+    assert ws == up(4 * 32 * 5000) + up(4 * 3 * 8) + 3 * 2048 * 2048 * 4
     ws = D.dopr_salience_workspace(n_docs=3, max_doclen=2048, n_q_heads=32,
                                    n_kv_heads=8, top_p=8, total_tokens=5000,
                                    with_attention=True)
-    assert ws == -(-4 * 32 * 5000 // 256) * 256
+    assert ws == up(4 * 32 * 5000) + up(4 * 3 * 8)
     assert D.dopr_salience_workspace(n_docs=0, max_doclen=5, n_q_heads=2,
                                      n_kv_heads=1, top_p=1,
                                      total_tokens=0) == 0
