@@ -411,7 +411,8 @@ typedef struct {
 } dopr_salience_args_t;
 
 /* Workspace bytes for these arguments (host): the row log-sum-exp of every
- * (token, q head), the largest key norm of every (document, kv head) and,
+ * (token, q head), eight partial maxima of the key norms of every
+ * (document, kv head) and,
  * unless attn_mean is given, Abar for as many documents at a time as fit
  * in 1 GiB (at least one).  dopr_salience accepts any workspace that holds
  * the row statistics and key norms plus one document's Abar (4 M^2 bytes)

@@ -756,7 +756,7 @@ SalienceWs salience_ws(const dopr_salience_args_t *a) {
   const size_t M = (size_t)a->max_doclen;
   w.lse_bytes = align_up(sizeof(float) * (size_t)a->n_q_heads *
                              (size_t)a->total_tokens, kAlign);
-  w.kn_bytes = align_up(sizeof(float) * (size_t)a->n_docs *
+  w.kn_bytes = align_up(sizeof(float) * kKeyNormParts * (size_t)a->n_docs *
                             (size_t)a->n_kv_heads, kAlign);
   if (a->attn_mean) {
     w.chunk = a->n_docs;

@@ -274,7 +274,8 @@ struct SalienceParams {
   float c;                   // softmax_scale * log2(e)
   float inv_hq;
   float *lse2;               // [Hq][Ntok] log2-domain row log-sum-exp
-  float *kmax;               // [n_docs][Hkv] largest key norm per document
+  float *kmax;               // [n_docs][Hkv][kKeyNormParts] partial maxima
+                             // of the key norms per document
   float *abar;               // doc d - d0 at (d - d0) * abar_stride
   int64_t abar_stride;       // max_len * max_len
   float *u;                  // [Ntok]
@@ -292,6 +293,7 @@ struct TopkParams {
 
 hipError_t launch_salience_check(const SalienceParams &p, hipStream_t s);
 hipError_t launch_key_norms(const SalienceParams &p, hipStream_t s);
+constexpr int kKeyNormParts = 8;  // partial maxima per (document, kv head)
 hipError_t launch_salience_chunk(const SalienceParams &p, int32_t n_docs,
                                  int hr, int pm, hipStream_t s);
 hipError_t launch_topk(const TopkParams &p, int32_t n_docs, hipStream_t s);

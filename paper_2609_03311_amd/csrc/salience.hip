@@ -118,18 +118,19 @@ __device__ __forceinline__ void key_frags(const uint16_t *kbuf, int st,
 }
 
 // ---------------------------------------------------------------------------
-// Largest key norm of each (document, kv head).  grid (docs, kv heads);
+// Largest key norm of each (document, kv head), as kKeyNormParts partial
+// maxima over interleaved 64-row slices.  grid (docs, kv heads, parts);
 // 16 lanes per key row (16 bytes each), four rows per wave and step, four
 // steps in flight.
 __global__ __launch_bounds__(256) void k_key_norm(SalienceParams P) {
   __shared__ float wmax[4];
-  const int d = blockIdx.x, g = blockIdx.y;
+  const int d = blockIdx.x, g = blockIdx.y, part = blockIdx.z;
   const Doc doc = doc_at(P, d);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int sub = lane & 15, r0 = 4 * wave + (lane >> 4);  // 16 rows a step
   float mx = 0.f;
   if (doc.ok) {
-    for (int i0 = 0; i0 < doc.n; i0 += 64) {
+    for (int i0 = 64 * part; i0 < doc.n; i0 += 64 * kKeyNormParts) {
       float ss[4];
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
@@ -161,7 +162,7 @@ __global__ __launch_bounds__(256) void k_key_norm(SalienceParams P) {
   if (lane == 0) wmax[wave] = mx;
   __syncthreads();
   if (threadIdx.x == 0)
-    P.kmax[(int64_t)d * P.hkv + g] =
+    P.kmax[((int64_t)d * P.hkv + g) * kKeyNormParts + part] =
         sqrtf(fmaxf(fmaxf(wmax[0], wmax[1]), fmaxf(wmax[2], wmax[3])));
 }
 
@@ -198,7 +199,10 @@ __global__ __launch_bounds__(256, 2) void k_row_lse(SalienceParams P) {
   const int kr = perm(lq);
   const int n_kb = rb + 1;  // key blocks 0 .. rb
 
-  const float kmax = P.kmax[(int64_t)d * P.hkv + g];
+  float kmax = 0.f;
+#pragma unroll
+  for (int i = 0; i < kKeyNormParts; ++i)
+    kmax = fmaxf(kmax, P.kmax[((int64_t)d * P.hkv + g) * kKeyNormParts + i]);
   for (int h0 = 0; h0 < P.n_rep; h0 += HR) {
     const int hbase = g * P.n_rep + h0;
     bf16x8 qf[HR][8];
@@ -691,7 +695,8 @@ hipError_t launch_salience_chunk(const SalienceParams &p, int32_t n_docs,
 
 hipError_t launch_key_norms(const SalienceParams &p, hipStream_t s) {
   if (p.n_docs == 0) return hipSuccess;
-  hipLaunchKernelGGL(k_key_norm, dim3((unsigned)p.n_docs, (unsigned)p.hkv),
+  hipLaunchKernelGGL(k_key_norm,
+                     dim3((unsigned)p.n_docs, (unsigned)p.hkv, kKeyNormParts),
                      dim3(256), 0, s, p);
   return hipGetLastError();
 }

@@ -166,15 +166,15 @@ def test_salience_host_validation_and_workspace():
                                    n_kv_heads=8, top_p=8,
                                    total_tokens=64 * 2048)
     lse = 4 * 32 * 64 * 2048
-    kn = up(4 * 64 * 8)
+    kn = up(4 * 8 * 64 * 8)               # 8 partial maxima per doc, head
     assert ws == lse + kn + (1 << 30)     # 64 docs of 16 MiB in one pass
     ws = D.dopr_salience_workspace(n_docs=3, max_doclen=2048, n_q_heads=32,
                                    n_kv_heads=8, top_p=8, total_tokens=5000)
-    assert ws == up(4 * 32 * 5000) + up(4 * 3 * 8) + 3 * 2048 * 2048 * 4
+    assert ws == up(4 * 32 * 5000) + up(4 * 8 * 3 * 8) + 3 * 2048 * 2048 * 4
     ws = D.dopr_salience_workspace(n_docs=3, max_doclen=2048, n_q_heads=32,
                                    n_kv_heads=8, top_p=8, total_tokens=5000,
                                    with_attention=True)
-    assert ws == up(4 * 32 * 5000) + up(4 * 3 * 8)
+    assert ws == up(4 * 32 * 5000) + up(4 * 8 * 3 * 8)
     assert D.dopr_salience_workspace(n_docs=0, max_doclen=5, n_q_heads=2,
                                      n_kv_heads=1, top_p=1,
                                      total_tokens=0) == 0
