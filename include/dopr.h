@@ -162,9 +162,10 @@ typedef struct {
                                block per CU, 256 prefix slots resident;
                                512 at D = 64), 6 = 4 waves x 32 rows, two
                                blocks per CU, 96 slots resident (256 at
-                               D = 64); 8 = the pass kernel: one 8-wave
-                               block per CU takes a (work item, kv head)
-                               unit, keeps the prefix in LDS for all its
+                               D = 64); 8 = the pass kernel: an 8-wave
+                               block (one per CU at D = 128, two at D = 64)
+                               takes a (work item, kv head) unit, keeps a
+                               prefix of up to 256 slots in LDS for all its
                                passes of 256 rows, and reads the own keys
                                from a k^ buffer in the workspace (2 Hkv D
                                bytes per online token) filled by a

@@ -164,8 +164,8 @@ __device__ __forceinline__ void attend_own(const uint16_t *kblk,
 // Pass kernel (full layer).  A work unit is one item of one document's
 // stacked rows (up to rows_per_item, 2048 by default) for one kv head,
 // walked in passes of 256 rows, one 32-row tile per wave of the 8-wave
-// block.  The document's prefix (up to 256 slots at head size 128) is
-// staged in LDS once per unit and read by every pass with no barrier, as
+// block.  The document's prefix (up to 256 slots) is staged in LDS once
+// per unit and read by every pass with no barrier, as
 // in the block kernels; what differs is everything around it:
 //   - own keys come precomputed (k_own_khat), so an own chunk is a plain
 //     copy: K rows and raw v rows go straight to LDS with direct loads into
@@ -356,10 +356,14 @@ __device__ __forceinline__ void own_dma(const AttnParams &P, int g,
   }
 }
 
+// At head size 64 a 256-slot prefix and the own slots take 80 KB, so two
+// blocks share a CU (four waves per SIMD within 128 registers): the two
+// blocks' passes are in independent phases, and each hides the other's
+// waits.  At 128 the 256-slot prefix fills the LDS: one block per CU.
 template <int D>
 __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(
-    2, 2))) void k_pass_attn(AttnParams P) {
-  constexpr int NCHK = big_chunks(D);
+    D == 64 ? 4 : 2, D == 64 ? 4 : 2))) void k_pass_attn(AttnParams P) {
+  constexpr int NCHK = D == 64 ? small_chunks(D) : big_chunks(D);
   using SM = Smem<D, NCHK>;
   constexpr int PSEG = SM::PSEG;
   constexpr int OWN_DMA = 2 * (KC * D * 2 / 1024) / 8;  // per wave, chunk
@@ -574,9 +578,9 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(
 
 }  // namespace
 
-// The pass kernel: k^ of every token first, then one 8-wave block per CU
-// (the prefix and two own slots fill the LDS), a multiple of 8 blocks so
-// block b serves queue b % 8.
+// The pass kernel: k^ of every token first, then 8-wave blocks, one per CU
+// at head size 128 (the prefix and two own slots fill the LDS) and two at
+// 64, a multiple of 8 blocks so block b serves queue b % 8.
 hipError_t launch_stream(int D, const AttnParams &p, const KhatParams &kp,
                          int32_t n_pairs, hipStream_t s) {
   int dev = 0, n_cu = 0;
@@ -594,7 +598,7 @@ hipError_t launch_stream(int D, const AttnParams &p, const KhatParams &kp,
     if (n_pairs > 0)
       hipLaunchKernelGGL(k_own_khat<64>, dim3((unsigned)n_pairs), dim3(256),
                          0, s, kp);
-    hipLaunchKernelGGL(k_pass_attn<64>, dim3(grid), dim3(512), 0, s, p);
+    hipLaunchKernelGGL(k_pass_attn<64>, dim3(2 * grid), dim3(512), 0, s, p);
   }
   return hipGetLastError();
 }
