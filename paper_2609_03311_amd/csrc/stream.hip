@@ -69,6 +69,18 @@ __device__ __forceinline__ int swvo(int r) {
     return ((r >> 1) & 1) << 2;
 }
 
+// A lane-derived index formed again where it is used, at head size 64, where
+// the pass kernel runs in 128 registers: per-lane pointers the compiler would
+// otherwise hoist to the kernel's start (and spill) are rebuilt per use.  At
+// 128 the plain index keeps the schedule it has.
+template <int D>
+__device__ __forceinline__ int lane_here(int x) {
+  if constexpr (D == 64)
+    return x + opaque_zero();
+  else
+    return x;
+}
+
 template <int N>
 __device__ __forceinline__ void vm_wait() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
@@ -431,8 +443,9 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(
     for (int pass0 = u.row0; pass0 < u.row1; pass0 += PR) {
       const int pass_end = pass0 + PR < u.row1 ? pass0 + PR : u.row1;
       // the pass's first pair: the last pair starting at or before pass0
+      const int lane_p = lane_here<D>(lane);
       for (;;) {
-        const int si = s_first + lane;
+        const int si = s_first + lane_p;
         const int z = si < n_valid ? P.spair[si].z : 0x7fffffff;
         const uint64_t le = __ballot(z <= pass0);
         const int k = 63 - __clzll(le);  // highest such lane (lane 0 is)
@@ -441,7 +454,7 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(
       }
       // pair records, lane i: the pass's i-th pair (tok0, T, latest
       // position in the pass; positions are stacked latest first)
-      const int si = s_first + lane;
+      const int si = s_first + lane_p;
       int4 rec = make_int4(0, 0, pass_end, 0);
       if (si < n_valid) rec = P.spair[si];
       const bool in = si < n_valid && rec.z < pass_end;
@@ -453,10 +466,11 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(
       // the pass's first two own chunks
       OwnPos o0, o1, o2;
       own_at(o0, 0, rtok, rT, rj);
-      own_dma<D>(P, u.g, o0, sm.ok[0], sm.ov[0], wave, lane);
+      own_dma<D>(P, u.g, o0, sm.ok[0], sm.ov[0], wave, lane_here<D>(lane));
       o1 = o0;
       bool has1 = own_next(o1, np, rtok, rT, rj);
-      if (has1) own_dma<D>(P, u.g, o1, sm.ok[1], sm.ov[1], wave, lane);
+      if (has1)
+        own_dma<D>(P, u.g, o1, sm.ok[1], sm.ov[1], wave, lane_here<D>(lane));
 
       // this wave's rows and q^
       const int r = pass0 + wave * 32 + lq;
@@ -471,8 +485,8 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(
         const int2 tj = P.utok[ut];
         tokq = tj.x;
         q_fragments<D>(P.q + ((int64_t)tokq * P.Hq + head) * D, P.qw,
-                       P.rope + (int64_t)(u.L + tj.y) * (D / 2), hf, P.eps,
-                       P.c, P.norm != 0, qf[0]);
+                       P.rope + (int64_t)(u.L + tj.y) * (D / 2),
+                       lane_here<D>(hf), P.eps, P.c, P.norm != 0, qf[0]);
       }
       Acc<D> acc[1];
       acc[0].m = 0.f;
@@ -525,7 +539,8 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(
         const bool has2 = own_next(o2, np, rtok, rT, rj);
         lds_barrier();  // every wave is done with slot b
         if (has2) {
-          own_dma<D>(P, u.g, o2, sm.ok[b], sm.ov[b], wave, lane);
+          own_dma<D>(P, u.g, o2, sm.ok[b], sm.ov[b], wave,
+                     lane_here<D>(lane));
           vm_wait<OWN_DMA>();  // this wave's loads of chunk c + 1 are in
         } else {
           vm_wait<0>();
