@@ -31,6 +31,14 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 KERNEL_SOURCES = ("csrc/attn.hip", "csrc/attn_common.hpp", "csrc/stream.hip",
                   "csrc/internal.hpp")
+# the sources each kind of summary describes (its hash is recorded with it)
+SOURCE_SETS = {
+    "attention": KERNEL_SOURCES,
+    "salience": ("csrc/salience.hip", "csrc/internal.hpp"),
+    "store": ("csrc/store.hip", "csrc/internal.hpp"),
+    "layer": ("csrc/layer.hip", "csrc/group.hip", "csrc/score.hip")
+    + KERNEL_SOURCES,
+}
 # the attention launches of each path on the Qwen3-8B-shaped workload (head
 # size 128): k^ precompute + pass kernel (full layer); one wave per 32-row
 # unit (score rows, every prefix at most 512 slots).  Same at head size 64.
@@ -50,13 +58,21 @@ def _code_only(text):
     return " ".join(text.split())
 
 
-def kernel_source_sha():
-    """Hash of the attention kernels' code (comments and layout ignored)."""
+def kernel_source_sha(kind="attention"):
+    """Hash of one kind of kernel's code (comments and layout ignored)."""
     h = hashlib.sha256()
-    for rel in KERNEL_SOURCES:
+    for rel in SOURCE_SETS[kind]:
         with open(os.path.join(HERE, rel), encoding="utf-8") as f:
             h.update(_code_only(f.read()).encode())
     return h.hexdigest()[:16]
+
+
+def _sha_lines(kind):
+    lines = [f"kernel_source_sha: {kernel_source_sha(kind)}"]
+    if kind != "attention":
+        lines.append("kernel_sources: " + " ".join(
+            os.path.basename(r) for r in SOURCE_SETS[kind]))
+    return lines
 
 
 def short_name(name, width=72):
@@ -70,11 +86,11 @@ def _rows(path):
         return list(csv.DictReader(f))
 
 
-def stats(trace_dir, command, top=12):
+def stats(trace_dir, command, top=12, sources="attention"):
     rows = _rows(os.path.join(trace_dir, "run_kernel_stats.csv"))
     rows.sort(key=lambda r: -float(r["TotalDurationNs"]))
     out = ["# rocprofv3 kernel statistics", f"command: {command}",
-           f"kernel_source_sha: {kernel_source_sha()}", "",
+           *_sha_lines(sources), "",
            f"{'kernel':<72} {'calls':>6} {'avg_us':>11} {'min_us':>11} "
            f"{'max_us':>11} {'pct':>6}"]
     for r in rows[:top]:
@@ -106,7 +122,8 @@ def _per_step(vals):
     return sum(sum(v) / len(v) for v in vals.values())
 
 
-def traffic(fetch_dir, write_dir, command, kernel=ATTN_KERNEL):
+def traffic(fetch_dir, write_dir, command, kernel=ATTN_KERNEL,
+            sources="attention"):
     f_att = _counter(fetch_dir, "FETCH_SIZE", kernel)
     w_att = _counter(write_dir, "WRITE_SIZE", kernel)
     f_cal = [x for v in _counter(fetch_dir, "FETCH_SIZE", CALIB_KERNEL).values()
@@ -124,7 +141,7 @@ def traffic(fetch_dir, write_dir, command, kernel=ATTN_KERNEL):
         "# HBM traffic of the attention kernel (rocprofv3 --pmc)",
         f"command: {command}",
         f"kernel: /{kernel}/",
-        f"kernel_source_sha: {kernel_source_sha()}",
+        *_sha_lines(sources),
         "dispatches: " + ", ".join(
             f"{k} fetch {len(f_att[k])} write {len(w_att.get(k, []))}"
             for k in sorted(f_att)),
@@ -164,7 +181,7 @@ def _agent(run_dir):
     raise SystemExit(f"no GPU agent in {run_dir}")
 
 
-def pmc(run_dirs, command, kernel=ATTN_KERNEL):
+def pmc(run_dirs, command, kernel=ATTN_KERNEL, sources="attention"):
     """Per matched kernel: the mean per dispatch of every counter found in
     the runs, and the utilisations the ROCm derived metrics define.
     GRBM_GUI_ACTIVE is summed over the chip's XCDs in the counter file, so
@@ -190,9 +207,10 @@ def pmc(run_dirs, command, kernel=ATTN_KERNEL):
                 int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
     if not per:
         raise SystemExit(f"no counter rows for /{kernel}/ in {run_dirs}")
-    out = ["# Shader counters of the attention launches (rocprofv3 --pmc)",
+    what = "attention launches" if sources == "attention" else "launches"
+    out = [f"# Shader counters of the {what} (rocprofv3 --pmc)",
            f"command: {command}", f"kernel: /{kernel}/",
-           f"kernel_source_sha: {kernel_source_sha()}",
+           *_sha_lines(sources),
            f"agent: {ag['Name']}, {n_xcc} XCDs, {n_cu} CUs, {n_simd} SIMDs",
            ""]
     tot_busy = tot_cycles = tot_mops = tot_dur = 0.0
@@ -316,15 +334,18 @@ def main(argv=None):
     a = sub.add_parser("stats")
     a.add_argument("trace_dir")
     a.add_argument("--command", required=True)
+    a.add_argument("--sources", default="attention", choices=SOURCE_SETS)
     b = sub.add_parser("traffic")
     b.add_argument("fetch_dir")
     b.add_argument("write_dir")
     b.add_argument("--command", required=True)
     b.add_argument("--kernel", default=ATTN_KERNEL)
+    b.add_argument("--sources", default="attention", choices=SOURCE_SETS)
     c = sub.add_parser("pmc")
     c.add_argument("run_dirs", nargs="+")
     c.add_argument("--command", required=True)
     c.add_argument("--kernel", default=ATTN_KERNEL)
+    c.add_argument("--sources", default="attention", choices=SOURCE_SETS)
     t = sub.add_parser("benchtable")
     t.add_argument("jsonl", nargs="+")
     t.add_argument("--command", required=True)
@@ -332,12 +353,14 @@ def main(argv=None):
     if args.cmd == "benchtable":
         sys.stdout.write(bench_table(args.jsonl, args.command))
     elif args.cmd == "stats":
-        sys.stdout.write(stats(args.trace_dir, args.command))
+        sys.stdout.write(stats(args.trace_dir, args.command,
+                               sources=args.sources))
     elif args.cmd == "pmc":
-        sys.stdout.write(pmc(args.run_dirs, args.command, args.kernel))
+        sys.stdout.write(pmc(args.run_dirs, args.command, args.kernel,
+                             args.sources))
     else:
         sys.stdout.write(traffic(args.fetch_dir, args.write_dir, args.command,
-                                 args.kernel))
+                                 args.kernel, args.sources))
 
 
 if __name__ == "__main__":
