@@ -233,6 +233,69 @@ __device__ __forceinline__ void q_fragments_quad(const uint16_t *qrow,
 #undef DPP_ROT
 #undef DPP_Q
 
+// Per-phase cycle counters of the pass kernel, compiled in only for the
+// measurement library (-DDOPR_PASS_TIMERS): each wave adds the s_memtime
+// cycles between consecutive marks to the total of the phase the mark
+// closes, and adds its totals to a device array when it exits.  In the
+// product library the marks are empty.
+enum PassPhase {
+  kPtUnit,        // unit hand-over (the claimed unit read from LDS)
+  kPtStage,       // the resident prefix's loads issued
+  kPtSearch,      // the pass's pair records found
+  kPtOwnIssue,    // the first two own chunks' loads issued
+  kPtQ,           // q rows loaded and q^ formed
+  kPtWaitLoads,   // waiting for the pass's loads
+  kPtBarrierPre,  // the barrier before the products
+  kPtPrefix,      // prefix chunks
+  kPtOwnCompute,  // own chunks: products
+  kPtOwnBarrier,  // own chunks: the two barriers per chunk
+  kPtOwnLoads,    // own chunks: next chunk's loads issued and waited for
+  kPtEpilogue,    // normalise and store O and the LSE
+  kPtPassEnd,     // the barrier at the end of a pass
+  kPtUnitEnd,     // the next unit's claim and the hand-over
+  kPtUnits,       // count: units
+  kPtPasses,      // count: passes
+  kPtTailCycles,  // cycles of passes with at most 32 rows
+  kPtTails,       // count: such passes
+  kPtSlots
+};
+#ifdef DOPR_PASS_TIMERS
+__device__ unsigned long long g_pass_phase[8][kPtSlots];
+#define PT_NOW() ((int64_t)__builtin_amdgcn_s_memtime())
+#define PT_DECL()                    \
+  int64_t pt_acc[kPtSlots] = {};     \
+  int64_t pt_last = PT_NOW(), pt_pass = pt_last
+#define PT_MARK(k)                   \
+  do {                               \
+    const int64_t pt_t = PT_NOW();   \
+    pt_acc[k] += pt_t - pt_last;     \
+    pt_last = pt_t;                  \
+  } while (0)
+#define PT_COUNT(k) (pt_acc[k] += 1)
+#define PT_PASS_START() (pt_pass = PT_NOW())
+#define PT_PASS_END(rows)                   \
+  do {                                      \
+    if ((rows) <= 32) {                     \
+      pt_acc[kPtTailCycles] += pt_last - pt_pass; \
+      pt_acc[kPtTails] += 1;                \
+    }                                       \
+  } while (0)
+#define PT_FLUSH(wave, lane)                                          \
+  do {                                                                \
+    if ((lane) == 0)                                                  \
+      for (int pt_i = 0; pt_i < kPtSlots; ++pt_i)                     \
+        atomicAdd(&g_pass_phase[wave][pt_i],                          \
+                  (unsigned long long)pt_acc[pt_i]);                  \
+  } while (0)
+#else
+#define PT_DECL() ((void)0)
+#define PT_MARK(k) ((void)0)
+#define PT_COUNT(k) ((void)0)
+#define PT_PASS_START() ((void)0)
+#define PT_PASS_END(rows) ((void)0)
+#define PT_FLUSH(wave, lane) ((void)0)
+#endif
+
 template <int N>
 __device__ __forceinline__ void vm_wait() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
@@ -564,6 +627,7 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(
       (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void *)
           sm.ok[0];
 
+  PT_DECL();
   if (wave == 0) {
     int slot = 0;
     if (lane == 0) slot = atomicAdd(&P.next[queue], 1);
@@ -579,6 +643,8 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(
     const PUnit u = unit_get(wd + 4 * kWordUnit);
     if (u.w < 0) break;
     lds_barrier();  // every wave has the unit before slot 0 is refilled
+    PT_MARK(kPtUnit);
+    PT_COUNT(kPtUnits);
     // wave 0 claims the next unit: the atomic is issued here, its table
     // words read once the first pass's loads are in, and used at the end
     int next_slot = 0, next_x = 0;
@@ -592,7 +658,10 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(
     if (resident && u.L > 0) stage_prefix<8, D, NCHK>(Kp, VTp, u.L, 0, u.L, sm);
     bool wave_bad = false;
     int s_first = u.s_lo;
+    PT_MARK(kPtStage);
     for (int pass0 = u.row0; pass0 < u.row1; pass0 += PR) {
+      PT_PASS_START();
+      PT_COUNT(kPtPasses);
       const int pass_end = pass0 + PR < u.row1 ? pass0 + PR : u.row1;
       // the pass's first pair: the last pair starting at or before pass0
       const int lane_p = lane_here<D>(lane);
@@ -615,6 +684,7 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(
       const int rtok = rec.x, rT = rec.y;
       const int rj = rec.y - 1 - (lo_row - rec.z) / P.n_rep;
 
+      PT_MARK(kPtSearch);
       // the pass's first two own chunks
       OwnPos o0, o1, o2;
       own_at(o0, 0, rtok, rT, rj);
@@ -624,6 +694,7 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(
       if (has1)
         own_dma<D>(P, u.g, o1, sm.ok[1], sm.ov[1], wave, lane_here<D>(lane));
 
+      PT_MARK(kPtOwnIssue);
       // this wave's rows and q^
       const int r = pass0 + wave * 32 + lq;
       const bool valid = wave * 32 < PR && r < pass_end;
@@ -660,9 +731,12 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(
         if (w < n_work) next_x = unit_words(P, (int)w, lane);
       }
 
+      PT_MARK(kPtQ);
       // document prefix: every row sees all L slots
       wait_vmem();
+      PT_MARK(kPtWaitLoads);
       lds_barrier();
+      PT_MARK(kPtBarrierPre);
       for (int sg = 0; sg < n_seg; ++sg) {
         const int seg0 = sg * PSEG;
         const int n = u.L - seg0 < PSEG ? u.L - seg0 : PSEG;
@@ -683,6 +757,7 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(
         }
       }
 
+      PT_MARK(kPtPrefix);
       // own keys: chunk c in slot c % 2; chunk c + 2 is loaded into that
       // slot once every wave is done with chunk c
       int b = 0;
@@ -692,10 +767,12 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(
         if (__any(valid && lim[0] >= 0))
           attend_own<D>(sm.ok[b], (b ? ov1 : ov0) + v_lane_b, ex, fo, qf,
                         acc, hf, lim);
+        PT_MARK(kPtOwnCompute);
         if (!has1) break;
         o2 = o1;
         const bool has2 = own_next(o2, np, rtok, rT, rj);
         lds_barrier();  // every wave is done with slot b
+        PT_MARK(kPtOwnBarrier);
         if (has2) {
           own_dma<D>(P, u.g, o2, sm.ok[b], sm.ov[b], wave,
                      lane_here<D>(lane));
@@ -703,7 +780,9 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(
         } else {
           vm_wait<0>();
         }
+        PT_MARK(kPtOwnLoads);
         lds_barrier();  // every wave's loads of chunk c + 1 are in
+        PT_MARK(kPtOwnBarrier);
         o0 = o1;
         o1 = o2;
         has1 = has2;
@@ -730,7 +809,10 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(
         if (P.lse && hf == 0) P.lse[orow] = __log2f(lt) * kLn2;
       }
       wave_bad = wave_bad || __any(bad);
+      PT_MARK(kPtEpilogue);
       lds_barrier();  // the own slots are free for the next pass
+      PT_MARK(kPtPassEnd);
+      PT_PASS_END(pass_end - pass0);
     }
 
     PUnit nu{};
@@ -746,7 +828,9 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(
         any_bad = any_bad || lds_get(wd + 4 * (1 + i));
       if (any_bad) P.fix[atomicAdd(&P.counters[kCntFix], 1)] = u.w;
     }
+    PT_MARK(kPtUnitEnd);
   }
+  PT_FLUSH(wave, lane);
 }
 
 }  // namespace
@@ -754,6 +838,20 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(
 // The pass kernel: k^ of every token first, then 8-wave blocks, one per CU
 // at head size 128 (the prefix and two own slots fill the LDS) and two at
 // 64, a multiple of 8 blocks so block b serves queue b % 8.
+#ifdef DOPR_PASS_TIMERS
+// The measurement library's phase totals, [8 waves][kPtSlots], summed over
+// every block since the last reset; reset != 0 clears them afterwards.
+extern "C" int dopr_pass_phase_read(unsigned long long *out, int reset) {
+  hipError_t e = hipMemcpyFromSymbol(out, HIP_SYMBOL(g_pass_phase),
+                                     sizeof(g_pass_phase));
+  if (e == hipSuccess && reset) {
+    static const unsigned long long zero[8][kPtSlots] = {};
+    e = hipMemcpyToSymbol(HIP_SYMBOL(g_pass_phase), zero, sizeof(zero));
+  }
+  return (int)e;
+}
+#endif
+
 hipError_t launch_stream(int D, const AttnParams &p, const KhatParams &kp,
                          int32_t n_pairs, hipStream_t s) {
   int dev = 0, n_cu = 0;
