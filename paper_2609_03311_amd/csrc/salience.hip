@@ -88,12 +88,13 @@ constexpr int kLdsK = kKeyBlock * D;  // bf16 elements (swizzled rows)
 // a 1 KB block (4 key rows), fetching the global granule that the swizzled
 // layout puts in its slot, so slot p of row r holds granule p ^ swz(r).
 // Rows past the document's end repeat row n-1 (masked by the causal test).
+template <int WAVES = 4>
 __device__ __forceinline__ void stage_keys(const SalienceParams &P,
                                            const Doc &doc, int key0, int g,
                                            uint16_t *dst) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
 #pragma unroll
-  for (int b = wave; b < kKeyBlock / 4; b += 4) {
+  for (int b = wave; b < kKeyBlock / 4; b += WAVES) {
     const int row = 4 * b + (lane >> 4), p = lane & 15;
     const int key = min(key0 + row, doc.n - 1);
     __builtin_amdgcn_global_load_lds(
@@ -179,25 +180,56 @@ __global__ __launch_bounds__(256) void k_key_norm(SalienceParams P) {
 //     exceeds 60.
 // The two lane halves are combined at the end.
 constexpr float kFixedRefMax = 60.f;
-template <int HR>
-__global__ __launch_bounds__(256, 2) void k_row_lse(SalienceParams P) {
+// row blocks (of 128) from which the LSE sweep groups three per block
+constexpr int kLseGroupMinBlocks = 6;
+
+// Sum and maximum of a tile's 16 values per lane in four interleaved
+// partials, so the adds (or maxima) form chains of four, not one chain of
+// sixteen behind the exponentials.
+__device__ __forceinline__ float sum16(const float (&e)[16]) {
+  float a[4] = {e[0], e[1], e[2], e[3]};
+#pragma unroll
+  for (int i = 4; i < 16; ++i) a[i & 3] += e[i];
+  return (a[0] + a[1]) + (a[2] + a[3]);
+}
+__device__ __forceinline__ float max16(const floatx16 &x) {
+  float a[4] = {x[0], x[1], x[2], x[3]};
+#pragma unroll
+  for (int i = 4; i < 16; ++i) a[i & 3] = fmaxf(a[i & 3], x[i]);
+  return fmaxf(fmaxf(a[0], a[1]), fmaxf(a[2], a[3]));
+}
+
+// grid (row groups, kv heads, documents), longest rows first.  A block of
+// WAVES waves covers RBS = WAVES / 4 consecutive row blocks (four waves of
+// 32 rows each) and stages each key block once for all of them.  Groups
+// are aligned to the last row block, so a partial group holds the
+// shortest rows; its waves below row block 0 load clamped rows and
+// compute nothing.  Four waves: two blocks per CU in 256 registers; twelve:
+// one block per CU, three waves per SIMD in 168 registers.
+template <int HR, int WAVES>
+__global__ __launch_bounds__(64 * WAVES) __attribute__((amdgpu_waves_per_eu(
+    WAVES == 4 ? 2 : 3, WAVES == 4 ? 2 : 3))) void k_row_lse(SalienceParams P) {
+  constexpr int RBS = WAVES / 4;
   __shared__ __attribute__((aligned(16))) uint16_t ks[2][kLdsK];
   const int d = P.d0 + blockIdx.z;
   const Doc doc = doc_at(P, d);
   if (!doc.ok) return;
-  const int rb = gridDim.x - 1 - blockIdx.x;  // longest rows first
-  if (rb * kRowBlock >= doc.n) return;        // block-uniform, before barriers
+  const int nb_doc = (doc.n + kRowBlock - 1) / kRowBlock;
+  const int top = (P.max_len + kRowBlock - 1) / kRowBlock - 1 -
+                  RBS * (int)blockIdx.x;
+  if (top - RBS + 1 >= nb_doc) return;  // block-uniform, before barriers
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int hf = lane >> 5, lq = lane & 31;
-  const int row0 = rb * kRowBlock + wave * 32;
-  const bool active = row0 < doc.n;
+  const int rb = top - RBS + 1 + (wave >> 2);  // this wave's row block
+  const int row0 = rb * kRowBlock + (wave & 3) * 32;
+  const bool active = rb >= 0 && row0 < doc.n;
   const int g = blockIdx.y;
   const int j = row0 + lq;
-  const int jl = min(j, doc.n - 1);
+  const int jl = min(max(j, 0), doc.n - 1);
   const int last = min(row0 + 31, doc.n - 1);
   const int64_t qrow = (doc.t0 + jl) * P.hq;
   const int kr = perm(lq);
-  const int n_kb = rb + 1;  // key blocks 0 .. rb
+  const int n_kb = min(top, nb_doc - 1) + 1;  // key blocks 0 .. the last
 
   float kmax = 0.f;
 #pragma unroll
@@ -234,12 +266,15 @@ __global__ __launch_bounds__(256, 2) void k_row_lse(SalienceParams P) {
       for (int r = 0; r < HR; ++r) m[r] = -INFINITY;
     }
     if (h0 > 0) __syncthreads();  // the previous heads are done with ks[0]
-    stage_keys(P, doc, 0, g, ks[0]);
+    stage_keys<WAVES>(P, doc, 0, g, ks[0]);
     for (int kb = 0; kb < n_kb; ++kb) {
       wait_vmem();
       __syncthreads();  // block kb staged; every wave done with the other
       if (kb + 1 < n_kb)
-        stage_keys(P, doc, (kb + 1) * kKeyBlock, g, ks[(kb + 1) & 1]);
+        stage_keys<WAVES>(P, doc, (kb + 1) * kKeyBlock, g, ks[(kb + 1) & 1]);
+      // past this wave's diagonal, or a row block outside the document
+      // (wave-uniform; the block's barriers are all above)
+      if (RBS > 1 && (kb > rb || rb >= nb_doc)) continue;
       const uint16_t *kbuf = ks[kb & 1];
       const int key0 = kb * kKeyBlock;
       // below the diagonal every row sees all 128 keys: four sub-tiles in
@@ -265,21 +300,18 @@ __global__ __launch_bounds__(256, 2) void k_row_lse(SalienceParams P) {
             if (r == HR - 1 && st + 1 < 4)
               key_frags(kbuf, st + 1, kr, hf, kf);
             if (FIXED) {
-              float add = 0.f;
+              float e[16];
 #pragma unroll
               for (int i = 0; i < 16; ++i)
-                add += __builtin_amdgcn_exp2f(fmaf(S[i], P.c, -m[r]));
-              l[r] += add;
+                e[i] = __builtin_amdgcn_exp2f(fmaf(S[i], P.c, -m[r]));
+              l[r] += sum16(e);
             } else {
-              float mx = S[0];
-#pragma unroll
-              for (int i = 1; i < 16; ++i) mx = fmaxf(mx, S[i]);
-              const float mn = fmaxf(m[r], mx * P.c);
-              float add = 0.f;
+              const float mn = fmaxf(m[r], max16(S) * P.c);
+              float e[16];
 #pragma unroll
               for (int i = 0; i < 16; ++i)
-                add += __builtin_amdgcn_exp2f(fmaf(S[i], P.c, -mn));
-              l[r] = l[r] * __builtin_amdgcn_exp2f(m[r] - mn) + add;
+                e[i] = __builtin_amdgcn_exp2f(fmaf(S[i], P.c, -mn));
+              l[r] = l[r] * __builtin_amdgcn_exp2f(m[r] - mn) + sum16(e);
               m[r] = mn;
             }
           }
@@ -316,19 +348,17 @@ __global__ __launch_bounds__(256, 2) void k_row_lse(SalienceParams P) {
                                                         0, 0, 0);
           // the scale c > 0 commutes with the max, so it is applied once
           // to the chunk's max and fused into each exponent's argument
-          float x[16], mx = -INFINITY;
+          floatx16 x;
 #pragma unroll
-          for (int i = 0; i < 16; ++i) {
+          for (int i = 0; i < 16; ++i)
             x[i] = masked && i > lim ? -INFINITY : S[i];
-            mx = fmaxf(mx, x[i]);
-          }
-          const float mn = fixed ? m[r] : fmaxf(m[r], mx * P.c);
+          const float mn = fixed ? m[r] : fmaxf(m[r], max16(x) * P.c);
           if (mn > -INFINITY) {
-            float add = 0.f;
+            float e[16];
 #pragma unroll
             for (int i = 0; i < 16; ++i)
-              add += __builtin_amdgcn_exp2f(fmaf(x[i], P.c, -mn));
-            l[r] = l[r] * __builtin_amdgcn_exp2f(m[r] - mn) + add;
+              e[i] = __builtin_amdgcn_exp2f(fmaf(x[i], P.c, -mn));
+            l[r] = l[r] * __builtin_amdgcn_exp2f(m[r] - mn) + sum16(e);
             m[r] = mn;
           }
         }
@@ -676,10 +706,16 @@ hipError_t launch_salience_chunk(const SalienceParams &p, int32_t n_docs,
   const dim3 g_lse(nb, p.hkv, n_docs);
   const dim3 g_att(nb * (nb + 1) / 2, n_docs);
   const dim3 g_col((p.max_len + kStrip - 1) / kStrip, n_docs);
-  if (hr == 2) {
-    hipLaunchKernelGGL(k_row_lse<2>, g_lse, dim3(256), 0, s, p);
+  // long documents: three row blocks per block at three waves per SIMD
+  // (one q head per sweep); short ones keep enough blocks with one row
+  // block each
+  if (nb >= kLseGroupMinBlocks) {
+    hipLaunchKernelGGL((k_row_lse<1, 12>), dim3((nb + 2) / 3, p.hkv, n_docs),
+                       dim3(768), 0, s, p);
+  } else if (hr == 2) {
+    hipLaunchKernelGGL((k_row_lse<2, 4>), g_lse, dim3(256), 0, s, p);
   } else {
-    hipLaunchKernelGGL(k_row_lse<1>, g_lse, dim3(256), 0, s, p);
+    hipLaunchKernelGGL((k_row_lse<1, 4>), g_lse, dim3(256), 0, s, p);
   }
   hipLaunchKernelGGL(k_mean_attn, g_att, dim3(256), 0, s, p, (int32_t)nb);
   if (pm == 8)
