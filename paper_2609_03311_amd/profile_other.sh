@@ -48,7 +48,7 @@ cd "$R" &&
     --command "$me (rocprofv3 --kernel-trace --stats -- python3 bench.py $sal)" \
     > "$sum/salience_qwen3_8b_docs_kernel_stats.txt" &&
   $P pmc "$out/sal_pmc_a" "$out/sal_pmc_b" --sources salience \
-    --kernel "k_row_lse<2>|k_mean_attn" \
+    --kernel "k_row_lse<|k_mean_attn" \
     --command "$me (rocprofv3 --pmc <PMC_PASSES[0]>, then <PMC_PASSES[1]> -- python3 bench.py $sal)" \
     > "$sum/salience_qwen3_8b_docs_pmc.txt" &&
   for c in qwen3_0p6b qwen3_8b; do
