@@ -172,6 +172,17 @@ dopr_status_t check_attn(const dopr_store *st, const dopr_attn_args_t *a,
       a->rows_per_item ? a->rows_per_item
                        : default_rows_per_item(a->kernel_variant, score_only,
                                                st->max_len, *n_rep);
+  // work units (item, kv head) are numbered in 32 bits by the scheduler's
+  // queues: the plan's item capacity times the kv heads must stay below
+  // 2^31
+  const int64_t rows = stacked * (int64_t)(*n_rep);
+  const int64_t items_cap =
+      a->n_pairs + (rows + shape->rows_per_item - 1) / shape->rows_per_item +
+      1;
+  if (items_cap * (int64_t)st->n_kv_heads > INT32_MAX)
+    return fail(DOPR_ERR_UNSUPPORTED,
+                "too many work units (pairs and items times kv heads must be "
+                "< 2^31)");
   shape->n_docs = st->n_docs;
   shape->total_tokens = a->total_tokens;
   shape->max_len = st->max_len;

@@ -585,9 +585,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(
         reinterpret_cast<const uint4 *>(P.kw)[threadIdx.x];
   __syncthreads();
   const int queue = blockIdx.x & 7;
-  int64_t n_items = P.totals[kTotItems];
-  if (n_items > P.items_cap) n_items = P.items_cap;
-  const int64_t n_work = n_items * P.Hkv;
+  const int64_t n_items64 = P.totals[kTotItems];
+  const int n_items = n_items64 < P.items_cap ? (int)n_items64 : P.items_cap;
+  // (32-bit unit numbers: below 2^31 by argument validation)
+  const int n_work = n_items * P.Hkv;
   const int32_t *qo = P.totals[kTotUnits] ? P.qorder : nullptr;
   uint16_t *ov = sov[wave];
 
@@ -595,9 +596,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(
     int slot = 0;
     if (lane == 0) slot = atomicAdd(&P.next[queue], 1);
     slot = __builtin_amdgcn_readfirstlane(slot);
-    const int64_t w = unit_at(qo, queue, slot, n_work);
+    const int w = unit_at32(qo, queue, slot, n_work);
     if (w >= n_work) break;
-    const int item = (int)(w / P.Hkv), g = (int)(w % P.Hkv);
+    const int item = w / P.Hkv, g = w % P.Hkv;
     const int4 it = P.items[item];
     const int doc = P.group_doc[it.x];
     const int L = P.doc_len[doc], Lp = pad8(L);

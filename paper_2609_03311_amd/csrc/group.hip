@@ -593,6 +593,7 @@ Plan carve(void *ws, const PlanShape &s, size_t *bytes) {
   pl.doc_scan = c.take<int64_t>(s.n_docs);
   const int64_t stacked = s.score_only ? P : s.total_tokens;
   const int64_t rows = stacked * s.n_rep;
+  // (the item capacity; argument validation keeps cap * n_kv_heads < 2^31)
   const int64_t cap = P + (rows + s.rows_per_item - 1) / s.rows_per_item + 1;
   const int64_t hkv = s.n_kv_heads > 0 ? s.n_kv_heads : 1;
   const int64_t scan_n = s.n_docs > P + 1 ? s.n_docs : P + 1;

@@ -130,6 +130,22 @@ __device__ __forceinline__ int64_t unit_at(const int32_t *qorder, int queue,
   return qorder[start + slot];
 }
 
+// The same in 32 bits: argument validation keeps every unit number (and
+// n_work) below 2^31.
+__device__ __forceinline__ int unit_at32(const int32_t *qorder, int queue,
+                                         int slot, int n_work) {
+  if (!qorder) {
+    // slot >= the queue's unit count, tested without forming q + 8 * slot
+    if (slot >= (n_work - queue + 7) / 8) return n_work;
+    return queue + 8 * slot;
+  }
+  const int per = n_work / 8, rem = n_work % 8;
+  const int n_q = per + (queue < rem ? 1 : 0);
+  if (slot >= n_q) return n_work;
+  const int start = queue * per + (queue < rem ? queue : rem);
+  return qorder[start + slot];
+}
+
 // Per-call plan built on the device by the grouping kernels (workspace).
 enum Counter {
   kCntValid = 0,     // pairs with a valid, resident document

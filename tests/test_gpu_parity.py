@@ -306,6 +306,16 @@ def test_outputs_do_not_depend_on_rows_per_item():
                 max_tokens=int(st.seqlens.max()), total_tokens=st.n_tokens,
                 rows_per_item=bad)
         assert e.value.status == D.DOPR_ERR_INVALID_ARG
+    # work units (item, kv head) are numbered in 32 bits: a batch whose
+    # item capacity times the kv heads reaches 2^31 is refused up front
+    # (one q head per kv head keeps the stacked rows themselves below 2^31)
+    n_big = 300_000_000
+    with pytest.raises(D.DoprError) as e:
+        D.dopr_prefix_attn_workspace(
+            case.store, n_pairs=n_big, n_q_heads=case.store.n_kv_heads,
+            max_tokens=1, total_tokens=n_big)
+    assert e.value.status == D.DOPR_ERR_UNSUPPORTED
+    assert "work units" in D.dopr_last_error()
     _free()
 
 
