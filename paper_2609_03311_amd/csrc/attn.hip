@@ -101,10 +101,16 @@ __device__ __forceinline__ bool run_unit(const AttnParams &P,
       const int2 tj = tj_next[qb];
       tokq[qb] = tj.x;
       head[qb] = g * P.n_rep + (rc - u * P.n_rep);
-      if (live)
-        q_fragments<D>(P.q + ((int64_t)tokq[qb] * P.Hq + head[qb]) * D,
-                       P.qw, P.rope + (int64_t)(L + tj.y) * (D / 2), hf,
-                       P.eps, P.c, P.norm != 0, qf[qb]);
+      if (live) {
+        const uint16_t *qrow = P.q + ((int64_t)tokq[qb] * P.Hq + head[qb]) * D;
+        const float2 *rrow = P.rope + (int64_t)(L + tj.y) * (D / 2);
+        if ((P.n_rep & 3) == 0)
+          q_fragments_quad<D>(qrow, P.qw, rrow, hf, lq & 3, P.eps, P.c,
+                              P.norm != 0, qf[qb]);
+        else
+          q_fragments<D>(qrow, P.qw, rrow, hf, P.eps, P.c, P.norm != 0,
+                         qf[qb]);
+      }
       acc[qb].m = SMX == 2 ? -INFINITY : (SMX == 1 ? INFINITY : 0.f);
       acc[qb].l = 0.f;
 #pragma unroll
@@ -630,9 +636,16 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(
       const int head = g * P.n_rep + (rc - u * P.n_rep);
       const int2 tj = P.utok[u];
       bf16x8 qf[1][D / 16];
-      q_fragments<D>(P.q + ((int64_t)tj.x * P.Hq + head) * D, P.qw,
-                     P.rope + (int64_t)(L + tj.y) * (D / 2), hf, P.eps, P.c,
-                     P.norm != 0, qf[0]);
+      {
+        const uint16_t *qrow = P.q + ((int64_t)tj.x * P.Hq + head) * D;
+        const float2 *rrow = P.rope + (int64_t)(L + tj.y) * (D / 2);
+        if ((P.n_rep & 3) == 0)
+          q_fragments_quad<D>(qrow, P.qw, rrow, hf, lq & 3, P.eps, P.c,
+                              P.norm != 0, qf[0]);
+        else
+          q_fragments<D>(qrow, P.qw, rrow, hf, P.eps, P.c, P.norm != 0,
+                         qf[0]);
+      }
       Acc<D> acc[1];
       acc[0].m = 0.f;
       acc[0].l = 0.f;
