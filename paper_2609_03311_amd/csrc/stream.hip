@@ -16,6 +16,8 @@ namespace {
 // to bf16 and written as k^ [Hkv][Ntok][D].  The pass kernel then copies
 // own keys like prefix keys, and a pair's keys are normed once per batch
 // instead of once per pass that reads them.
+constexpr int kKhatRowsPerStep = 2;
+
 template <int D>
 __global__ __launch_bounds__(256) void k_own_khat(KhatParams P) {
   constexpr int NSUB = D / 16, ROWS = 256 / NSUB;
@@ -30,20 +32,41 @@ __global__ __launch_bounds__(256) void k_own_khat(KhatParams P) {
   const uint4 g0 = *reinterpret_cast<const uint4 *>(P.kw + 8 * sub);
   const uint4 g1 = *reinterpret_cast<const uint4 *>(P.kw + D / 2 + 8 * sub);
   const int64_t n_rows = (int64_t)T * P.Hkv;
-  for (int64_t rr = t / NSUB; rr < n_rows; rr += ROWS) {
-    const int j = (int)(rr / P.Hkv), g = (int)(rr % P.Hkv);
-    const uint16_t *kr = P.k + ((int64_t)(tok0 + j) * P.Hkv + g) * D;
-    const uint4 a0 = *reinterpret_cast<const uint4 *>(kr + 8 * sub);
-    const uint4 a1 = *reinterpret_cast<const uint4 *>(kr + D / 2 + 8 * sub);
-    const float4 *cq = reinterpret_cast<const float4 *>(
-        P.rope + (int64_t)(L + j) * (D / 2) + 8 * sub);
-    float x[16];
-    khat_part<D>(a0, a1, g0, g1, cq[0], cq[1], cq[2], cq[3], true, P.eps,
-                 P.norm != 0, x);
-    uint16_t *o = P.kh + ((int64_t)g * P.ntok + tok0 + j) * D;
-    *reinterpret_cast<uint4 *>(o + 8 * sub) = as_uint4(to_bf16x8(x));
-    *reinterpret_cast<uint4 *>(o + D / 2 + 8 * sub) =
-        as_uint4(to_bf16x8(x + 8));
+  // KB rows per thread and step, every row's loads issued before the first
+  // is used (the stores of one step cannot be moved above the next step's
+  // loads by the compiler, so one row per step leaves one load in flight)
+  constexpr int KB = kKhatRowsPerStep;
+  for (int64_t r0 = t / NSUB; r0 < n_rows; r0 += KB * ROWS) {
+    uint4 a0[KB], a1[KB];
+    const float4 *cq[KB];
+    int j[KB], g[KB];
+#pragma unroll
+    for (int k = 0; k < KB; ++k) {
+      const int64_t rr = r0 + k * ROWS < n_rows ? r0 + k * ROWS : r0;
+      j[k] = (int)(rr / P.Hkv);
+      g[k] = (int)(rr % P.Hkv);
+      const uint16_t *kr = P.k + ((int64_t)(tok0 + j[k]) * P.Hkv + g[k]) * D;
+      a0[k] = *reinterpret_cast<const uint4 *>(kr + 8 * sub);
+      a1[k] = *reinterpret_cast<const uint4 *>(kr + D / 2 + 8 * sub);
+      cq[k] = reinterpret_cast<const float4 *>(
+          P.rope + (int64_t)(L + j[k]) * (D / 2) + 8 * sub);
+    }
+    float4 c[KB][4];
+#pragma unroll
+    for (int k = 0; k < KB; ++k)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) c[k][i] = cq[k][i];
+#pragma unroll
+    for (int k = 0; k < KB; ++k) {
+      if (k > 0 && r0 + k * ROWS >= n_rows) break;
+      float x[16];
+      khat_part<D>(a0[k], a1[k], g0, g1, c[k][0], c[k][1], c[k][2], c[k][3],
+                   true, P.eps, P.norm != 0, x);
+      uint16_t *o = P.kh + ((int64_t)g[k] * P.ntok + tok0 + j[k]) * D;
+      *reinterpret_cast<uint4 *>(o + 8 * sub) = as_uint4(to_bf16x8(x));
+      *reinterpret_cast<uint4 *>(o + D / 2 + 8 * sub) =
+          as_uint4(to_bf16x8(x + 8));
+    }
   }
 }
 
