@@ -104,12 +104,8 @@ __device__ __forceinline__ bool run_unit(const AttnParams &P,
       if (live) {
         const uint16_t *qrow = P.q + ((int64_t)tokq[qb] * P.Hq + head[qb]) * D;
         const float2 *rrow = P.rope + (int64_t)(L + tj.y) * (D / 2);
-        if ((P.n_rep & 3) == 0)
-          q_fragments_quad<D>(qrow, P.qw, rrow, hf, lq & 3, P.eps, P.c,
-                              P.norm != 0, qf[qb]);
-        else
-          q_fragments<D>(qrow, P.qw, rrow, hf, P.eps, P.c, P.norm != 0,
-                         qf[qb]);
+        q_fragments_any<D>(qrow, P.qw, rrow, hf, lq, P.n_rep, P.eps, P.c,
+                           P.norm != 0, qf[qb]);
       }
       acc[qb].m = SMX == 2 ? -INFINITY : (SMX == 1 ? INFINITY : 0.f);
       acc[qb].l = 0.f;
@@ -639,12 +635,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(
       {
         const uint16_t *qrow = P.q + ((int64_t)tj.x * P.Hq + head) * D;
         const float2 *rrow = P.rope + (int64_t)(L + tj.y) * (D / 2);
-        if ((P.n_rep & 3) == 0)
-          q_fragments_quad<D>(qrow, P.qw, rrow, hf, lq & 3, P.eps, P.c,
-                              P.norm != 0, qf[0]);
-        else
-          q_fragments<D>(qrow, P.qw, rrow, hf, P.eps, P.c, P.norm != 0,
-                         qf[0]);
+        q_fragments_any<D>(qrow, P.qw, rrow, hf, lq, P.n_rep, P.eps, P.c,
+                           P.norm != 0, qf[0]);
       }
       Acc<D> acc[1];
       acc[0].m = 0.f;

@@ -263,116 +263,131 @@ __device__ __forceinline__ void q_fragments(const uint16_t *qrow,
   }
 }
 
-// ---- q^ with the rotary pairs and gains shared across lane quads ----
-// When n_rep is a multiple of 4, the four lanes of a quad hold the four
-// query heads of one token (and the same half of the head dims), so they
-// need the same (cos, sin) pairs and gains.  Each lane loads a quarter of
-// them; the multiplies that use a value read it from the owning lane
-// through a DPP quad broadcast folded into the instruction (the compiler's
-// DPP moves are not folded into these users, so the operations are
-// written out).  Every product and sum is the one q_fragments forms, in
-// the same order and rounding: fma(cos, a, sin * -b) and
-// fma(cos, b, sin * a).  s_nop 4 covers the wait states a DPP read needs
-// after a vector write of its source or of EXEC.
-#define DPP_Q(K) " quad_perm:[" #K "," #K "," #K "," #K "] row_mask:0xf bank_mask:0xf"
-#define DPP_ROT(K)                                                      \
-  "s_nop 4\n\t"                                                        \
-  "v_mul_f32_dpp %0, %9, -%5" DPP_Q(K) "\n\t"                          \
-  "v_mul_f32_dpp %1, %9, %4" DPP_Q(K) "\n\t"                           \
-  "v_fmac_f32_dpp %0, %8, %4" DPP_Q(K) "\n\t"                          \
-  "v_fmac_f32_dpp %1, %8, %5" DPP_Q(K) "\n\t"                          \
-  "v_mul_f32_dpp %2, %11, -%7" DPP_Q(K) "\n\t"                         \
-  "v_mul_f32_dpp %3, %11, %6" DPP_Q(K) "\n\t"                          \
-  "v_fmac_f32_dpp %2, %10, %6" DPP_Q(K) "\n\t"                         \
-  "v_fmac_f32_dpp %3, %10, %7" DPP_Q(K)
+// ---- q^ with the rotary pairs and gains shared across a token's lanes ----
+// When n_rep is a multiple of 4 (of 2), the four lanes of a quad (the two
+// lanes of a pair) hold query heads of one token and the same half of the
+// head dims, so they need the same (cos, sin) pairs and gains.  Each lane
+// loads its share; the multiplies that use a value read it from the owning
+// lane through a DPP broadcast within the quad folded into the instruction
+// (the compiler's DPP moves are not folded into these users, so the
+// operations are written out).  Every product and sum is the one
+// q_fragments forms, in the same order and rounding: fma(cos, a, sin * -b)
+// and fma(cos, b, sin * a).  s_nop 4 covers the wait states a DPP read
+// needs after a vector write of its source or of EXEC.
+//
+// Source codes: K = 0..3 reads quad lane K (quad_perm [K,K,K,K]); K = 4, 5
+// reads pair lane K - 4 (quad_perm [p,p,p+2,p+2]).
+#define DPP_Q(A, B, C, E) \
+  " quad_perm:[" #A "," #B "," #C "," #E "] row_mask:0xf bank_mask:0xf"
+#define DPP_ROT(A, B, C, E)                                     \
+  "s_nop 4\n\t"                                                 \
+  "v_mul_f32_dpp %0, %9, -%5" DPP_Q(A, B, C, E) "\n\t"          \
+  "v_mul_f32_dpp %1, %9, %4" DPP_Q(A, B, C, E) "\n\t"           \
+  "v_fmac_f32_dpp %0, %8, %4" DPP_Q(A, B, C, E) "\n\t"          \
+  "v_fmac_f32_dpp %1, %8, %5" DPP_Q(A, B, C, E) "\n\t"          \
+  "v_mul_f32_dpp %2, %11, -%7" DPP_Q(A, B, C, E) "\n\t"         \
+  "v_mul_f32_dpp %3, %11, %6" DPP_Q(A, B, C, E) "\n\t"          \
+  "v_fmac_f32_dpp %2, %10, %6" DPP_Q(A, B, C, E) "\n\t"         \
+  "v_fmac_f32_dpp %3, %10, %7" DPP_Q(A, B, C, E)
+#define DPP_UNPACK(A, B, C, E)                                  \
+  "s_nop 4\n\t"                                                 \
+  "v_mul_u32_u24_dpp %0, %8, %12" DPP_Q(A, B, C, E) "\n\t"      \
+  "v_and_b32_dpp %1, %8, %13" DPP_Q(A, B, C, E) "\n\t"          \
+  "v_mul_u32_u24_dpp %2, %9, %12" DPP_Q(A, B, C, E) "\n\t"      \
+  "v_and_b32_dpp %3, %9, %13" DPP_Q(A, B, C, E) "\n\t"          \
+  "v_mul_u32_u24_dpp %4, %10, %12" DPP_Q(A, B, C, E) "\n\t"     \
+  "v_and_b32_dpp %5, %10, %13" DPP_Q(A, B, C, E) "\n\t"         \
+  "v_mul_u32_u24_dpp %6, %11, %12" DPP_Q(A, B, C, E) "\n\t"     \
+  "v_and_b32_dpp %7, %11, %13" DPP_Q(A, B, C, E)
 
-// (x0[e], x1[e]) and (x0[e+1], x1[e+1]) rotated by quad lane K's pairs t =
+// (x0[e], x1[e]) and (x0[e+1], x1[e+1]) rotated by source K's pairs t =
 // (cos_e, sin_e, cos_e+1, sin_e+1); a and b are the normed, scaled inputs.
 template <int K>
-__device__ __forceinline__ void rot_pairs_quad(const float4 &t, float a0,
-                                               float b0, float a1, float b1,
-                                               float &x0a, float &x1a,
-                                               float &x0b, float &x1b) {
-#define DPP_ROT_ASM(KK)                                                      \
-  asm volatile(DPP_ROT(KK)                                                   \
+__device__ __forceinline__ void rot_pairs_shared(const float4 &t, float a0,
+                                                 float b0, float a1, float b1,
+                                                 float &x0a, float &x1a,
+                                                 float &x0b, float &x1b) {
+#define DPP_ROT_ASM(A, B, C, E)                                              \
+  asm volatile(DPP_ROT(A, B, C, E)                                           \
                : "=&v"(x0a), "=&v"(x1a), "=&v"(x0b), "=&v"(x1b)              \
                : "v"(a0), "v"(b0), "v"(a1), "v"(b1), "v"(t.x), "v"(t.y),     \
                  "v"(t.z), "v"(t.w))
-  if constexpr (K == 0) DPP_ROT_ASM(0);
-  else if constexpr (K == 1) DPP_ROT_ASM(1);
-  else if constexpr (K == 2) DPP_ROT_ASM(2);
-  else DPP_ROT_ASM(3);
+  if constexpr (K == 0) DPP_ROT_ASM(0, 0, 0, 0);
+  else if constexpr (K == 1) DPP_ROT_ASM(1, 1, 1, 1);
+  else if constexpr (K == 2) DPP_ROT_ASM(2, 2, 2, 2);
+  else if constexpr (K == 3) DPP_ROT_ASM(3, 3, 3, 3);
+  else if constexpr (K == 4) DPP_ROT_ASM(0, 0, 2, 2);
+  else DPP_ROT_ASM(1, 1, 3, 3);
 #undef DPP_ROT_ASM
 }
 
-// Quad lane K's packed bf16 gains u, unpacked as unpack8 does.
+// Source K's packed bf16 gains u, unpacked as unpack8 does.
 template <int K>
-__device__ __forceinline__ void unpack8_quad(const uint4 &u, uint32_t c16,
-                                             uint32_t hi, float *f) {
+__device__ __forceinline__ void unpack8_shared(const uint4 &u, uint32_t c16,
+                                               uint32_t hi, float *f) {
   uint32_t r[8];
-#define DPP_UNPACK_ASM(KK)                                                   \
-  asm volatile("s_nop 4\n\t"                                                 \
-               "v_mul_u32_u24_dpp %0, %8, %12" DPP_Q(KK) "\n\t"             \
-               "v_and_b32_dpp %1, %8, %13" DPP_Q(KK) "\n\t"                 \
-               "v_mul_u32_u24_dpp %2, %9, %12" DPP_Q(KK) "\n\t"             \
-               "v_and_b32_dpp %3, %9, %13" DPP_Q(KK) "\n\t"                 \
-               "v_mul_u32_u24_dpp %4, %10, %12" DPP_Q(KK) "\n\t"            \
-               "v_and_b32_dpp %5, %10, %13" DPP_Q(KK) "\n\t"                \
-               "v_mul_u32_u24_dpp %6, %11, %12" DPP_Q(KK) "\n\t"            \
-               "v_and_b32_dpp %7, %11, %13" DPP_Q(KK)                       \
+#define DPP_UNPACK_ASM(A, B, C, E)                                           \
+  asm volatile(DPP_UNPACK(A, B, C, E)                                        \
                : "=&v"(r[0]), "=&v"(r[1]), "=&v"(r[2]), "=&v"(r[3]),         \
                  "=&v"(r[4]), "=&v"(r[5]), "=&v"(r[6]), "=&v"(r[7])          \
                : "v"(u.x), "v"(u.y), "v"(u.z), "v"(u.w), "v"(c16), "v"(hi))
   // (u24 product by 65536: the low half shifted up, the high half dropped)
-  if constexpr (K == 0) DPP_UNPACK_ASM(0);
-  else if constexpr (K == 1) DPP_UNPACK_ASM(1);
-  else if constexpr (K == 2) DPP_UNPACK_ASM(2);
-  else DPP_UNPACK_ASM(3);
+  if constexpr (K == 0) DPP_UNPACK_ASM(0, 0, 0, 0);
+  else if constexpr (K == 1) DPP_UNPACK_ASM(1, 1, 1, 1);
+  else if constexpr (K == 2) DPP_UNPACK_ASM(2, 2, 2, 2);
+  else if constexpr (K == 3) DPP_UNPACK_ASM(3, 3, 3, 3);
+  else if constexpr (K == 4) DPP_UNPACK_ASM(0, 0, 2, 2);
+  else DPP_UNPACK_ASM(1, 1, 3, 3);
 #undef DPP_UNPACK_ASM
 #pragma unroll
   for (int i = 0; i < 8; ++i) f[i] = __uint_as_float(r[i]);
 }
 
-// The owning lane as a value that is constant once the caller's loops are
+// The source as a value that is constant once the caller's loops are
 // unrolled.
-__device__ __forceinline__ void rot_pairs_quad_at(int k, const float4 &t,
-                                                  float a0, float b0,
-                                                  float a1, float b1,
-                                                  float &x0a, float &x1a,
-                                                  float &x0b, float &x1b) {
+__device__ __forceinline__ void rot_pairs_at(int k, const float4 &t, float a0,
+                                             float b0, float a1, float b1,
+                                             float &x0a, float &x1a,
+                                             float &x0b, float &x1b) {
   switch (k) {
-    case 0: rot_pairs_quad<0>(t, a0, b0, a1, b1, x0a, x1a, x0b, x1b); break;
-    case 1: rot_pairs_quad<1>(t, a0, b0, a1, b1, x0a, x1a, x0b, x1b); break;
-    case 2: rot_pairs_quad<2>(t, a0, b0, a1, b1, x0a, x1a, x0b, x1b); break;
-    default: rot_pairs_quad<3>(t, a0, b0, a1, b1, x0a, x1a, x0b, x1b);
+    case 0: rot_pairs_shared<0>(t, a0, b0, a1, b1, x0a, x1a, x0b, x1b); break;
+    case 1: rot_pairs_shared<1>(t, a0, b0, a1, b1, x0a, x1a, x0b, x1b); break;
+    case 2: rot_pairs_shared<2>(t, a0, b0, a1, b1, x0a, x1a, x0b, x1b); break;
+    case 3: rot_pairs_shared<3>(t, a0, b0, a1, b1, x0a, x1a, x0b, x1b); break;
+    case 4: rot_pairs_shared<4>(t, a0, b0, a1, b1, x0a, x1a, x0b, x1b); break;
+    default: rot_pairs_shared<5>(t, a0, b0, a1, b1, x0a, x1a, x0b, x1b);
   }
 }
 
-__device__ __forceinline__ void unpack8_quad_at(int k, const uint4 &u,
-                                                uint32_t c16, uint32_t hi,
-                                                float *f) {
+__device__ __forceinline__ void unpack8_at(int k, const uint4 &u,
+                                           uint32_t c16, uint32_t hi,
+                                           float *f) {
   switch (k) {
-    case 0: unpack8_quad<0>(u, c16, hi, f); break;
-    case 1: unpack8_quad<1>(u, c16, hi, f); break;
-    case 2: unpack8_quad<2>(u, c16, hi, f); break;
-    default: unpack8_quad<3>(u, c16, hi, f);
+    case 0: unpack8_shared<0>(u, c16, hi, f); break;
+    case 1: unpack8_shared<1>(u, c16, hi, f); break;
+    case 2: unpack8_shared<2>(u, c16, hi, f); break;
+    case 3: unpack8_shared<3>(u, c16, hi, f); break;
+    case 4: unpack8_shared<4>(u, c16, hi, f); break;
+    default: unpack8_shared<5>(u, c16, hi, f);
   }
 }
 
-// q_fragments with the sharing above; qk = the lane's place in its quad.
-// Lane qk loads gain vectors s = qk*NS/4 .. + NS/4 - 1 and the rotary
-// float4 e2 = qk of every k-step pair s (q_fragments' numbering), so the
-// quad's four loads of one k-step cover 64 contiguous bytes of the row.
-template <int D>
-__device__ __forceinline__ void q_fragments_quad(const uint16_t *qrow,
-                                                 const uint16_t *w,
-                                                 const float2 *rope_row,
-                                                 int hf, int qk, float eps,
-                                                 float c, bool norm,
-                                                 bf16x8 *qf) {
-  constexpr int NS = D / 16, HS = NS / 2, GW = NS / 4;
+// q_fragments with the sharing above among GROUP = 4 or 2 lanes; qk = the
+// lane's place in its group.  Lane qk loads gain vectors s = qk*NS/GROUP ..
+// + NS/GROUP - 1 and, of every k-step pair s, the rotary float4s
+// e2 = qk*4/GROUP .. + 4/GROUP - 1 (q_fragments' numbering), so the
+// group's loads of one k-step cover contiguous bytes of the row.
+template <int D, int GROUP>
+__device__ __forceinline__ void q_fragments_shared(const uint16_t *qrow,
+                                                   const uint16_t *w,
+                                                   const float2 *rope_row,
+                                                   int hf, int qk, float eps,
+                                                   float c, bool norm,
+                                                   bf16x8 *qf) {
+  constexpr int NS = D / 16, HS = NS / 2, GW = NS / GROUP, EW = 4 / GROUP;
+  constexpr int BASE = GROUP == 4 ? 0 : 4;  // source codes of the group
   uint4 raw[NS], wr[GW];
-  float4 cs[HS];
+  float4 cs[HS * EW];
 #pragma unroll
   for (int s = 0; s < NS; ++s)
     raw[s] = *reinterpret_cast<const uint4 *>(qrow + 16 * s + 8 * hf);
@@ -382,7 +397,10 @@ __device__ __forceinline__ void q_fragments_quad(const uint16_t *qrow,
     wr[m] = *reinterpret_cast<const uint4 *>(w + 16 * (qk * GW + m) + 8 * hf);
 #pragma unroll
   for (int s = 0; s < HS; ++s)
-    cs[s] = reinterpret_cast<const float4 *>(rope_row + 16 * s + 8 * hf)[qk];
+#pragma unroll
+    for (int m = 0; m < EW; ++m)
+      cs[s * EW + m] = reinterpret_cast<const float4 *>(
+          rope_row + 16 * s + 8 * hf)[qk * EW + m];
   float ss = 0.f;
 #pragma unroll
   for (int s = 0; s < NS; ++s) ss = sumsq8(raw[s], ss);
@@ -394,8 +412,8 @@ __device__ __forceinline__ void q_fragments_quad(const uint16_t *qrow,
     float x0[8], x1[8], w0[8], w1[8];
     unpack8(raw[s], x0);
     unpack8(raw[s + HS], x1);
-    unpack8_quad_at(s / GW, wr[s % GW], c16, hi, w0);
-    unpack8_quad_at((s + HS) / GW, wr[(s + HS) % GW], c16, hi, w1);
+    unpack8_at(BASE + s / GW, wr[s % GW], c16, hi, w0);
+    unpack8_at(BASE + (s + HS) / GW, wr[(s + HS) % GW], c16, hi, w1);
 #pragma unroll
     for (int e2 = 0; e2 < 4; ++e2) {
       const int e = 2 * e2;
@@ -403,8 +421,8 @@ __device__ __forceinline__ void q_fragments_quad(const uint16_t *qrow,
       const float b0 = x1[e] * (inv * w1[e]);
       const float a1 = x0[e + 1] * (inv * w0[e + 1]);
       const float b1 = x1[e + 1] * (inv * w1[e + 1]);
-      rot_pairs_quad_at(e2, cs[s], a0, b0, a1, b1, x0[e], x1[e], x0[e + 1],
-                        x1[e + 1]);
+      rot_pairs_at(BASE + e2 / EW, cs[s * EW + e2 % EW], a0, b0, a1, b1,
+                   x0[e], x1[e], x0[e + 1], x1[e + 1]);
     }
     qf[s] = to_bf16x8(x0);
     qf[s + HS] = to_bf16x8(x1);
@@ -412,6 +430,26 @@ __device__ __forceinline__ void q_fragments_quad(const uint16_t *qrow,
     pin(qf[s + HS]);
   }
 }
+
+// q^ for a lane whose token is shared by the lanes of its quad (n_rep a
+// multiple of 4) or pair (n_rep even), else q_fragments.
+template <int D>
+__device__ __forceinline__ void q_fragments_any(const uint16_t *qrow,
+                                                const uint16_t *w,
+                                                const float2 *rope_row, int hf,
+                                                int lane, int n_rep, float eps,
+                                                float c, bool norm,
+                                                bf16x8 *qf) {
+  if ((n_rep & 3) == 0)
+    q_fragments_shared<D, 4>(qrow, w, rope_row, hf, lane & 3, eps, c, norm,
+                             qf);
+  else if ((n_rep & 1) == 0)
+    q_fragments_shared<D, 2>(qrow, w, rope_row, hf, lane & 1, eps, c, norm,
+                             qf);
+  else
+    q_fragments<D>(qrow, w, rope_row, hf, eps, c, norm, qf);
+}
+#undef DPP_UNPACK
 #undef DPP_ROT
 #undef DPP_Q
 

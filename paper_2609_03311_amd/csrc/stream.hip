@@ -581,13 +581,9 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(
         tokq = tj.x;
         const uint16_t *qrow = P.q + ((int64_t)tokq * P.Hq + head) * D;
         const float2 *rrow = P.rope + (int64_t)(u.L + tj.y) * (D / 2);
-        if ((P.n_rep & 3) == 0)
-          q_fragments_quad<D>(qrow, P.qw, rrow, lane_here<D>(hf),
-                              lane_here<D>(lane & 3), P.eps, P.c,
-                              P.norm != 0, qf[0]);
-        else
-          q_fragments<D>(qrow, P.qw, rrow, lane_here<D>(hf), P.eps, P.c,
-                         P.norm != 0, qf[0]);
+        q_fragments_any<D>(qrow, P.qw, rrow, lane_here<D>(hf),
+                           lane_here<D>(lane), P.n_rep, P.eps, P.c,
+                           P.norm != 0, qf[0]);
       }
       Acc<D> acc[1];
       acc[0].m = 0.f;
