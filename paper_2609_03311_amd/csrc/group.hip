@@ -326,39 +326,45 @@ __device__ __forceinline__ uint8_t cost_class(int64_t rows, int32_t L) {
 // rows: near-equal items (the block kernels, which walk an item in passes),
 // or, with exact_items, items of exactly rows_per_item rows and a shorter
 // last one (the streaming kernel serves an item in one pass, so no item
-// may exceed it).
+// may exceed it).  One wave per group, its lanes taking the items in turn:
+// a hot document's group has hundreds of items, each with its own search.
+// The waves stride over the groups, so the grid stays bounded.
 __global__ __launch_bounds__(kThreads) void k_items_emit(Plan pl, PlanArgs a,
                                                          const int64_t *totals) {
-  const int32_t g = blockIdx.x * kThreads + threadIdx.x;
+  const int64_t wave0 = ((int64_t)blockIdx.x * kThreads + threadIdx.x) >> 6;
+  const int64_t n_waves = ((int64_t)gridDim.x * kThreads) >> 6;
+  const int lane = threadIdx.x & 63;
   const int32_t n_groups = (int32_t)(totals[kTotDocs] >> 32);
-  if (g >= n_groups) return;
-  if (g == 0 && totals[kTotItems] > pl.items_cap)
+  if (wave0 == 0 && lane == 0 && totals[kTotItems] > pl.items_cap)
     raise_status(a.status, DOPR_ERR_SEQLEN);
-  const int64_t first = pl.item_scan[g];
-  const int64_t n_it = pl.item_scan[g + 1] - first;
-  const int64_t base = pl.prow[pl.group_ptr[g]];
-  const int64_t R = pl.prow[pl.group_ptr[g + 1]] - base;
-  const uint8_t cls = cost_class(R, a.doc_len[pl.group_doc[g]]);
-  for (int64_t it = 0; it < n_it; ++it) {
-    const int64_t idx = first + it;
-    if (idx >= pl.items_cap) break;
-    pl.item_cls[idx] = cls;
-    const int64_t b0 =
-        a.exact_items ? base + it * a.rows_per_item
-                      : base + ((it * R / n_it) & ~(int64_t)31);
-    const int64_t b1 =
-        it + 1 < n_it
-            ? (a.exact_items ? base + (it + 1) * a.rows_per_item
-                             : base + (((it + 1) * R / n_it) & ~(int64_t)31))
-            : base + R;
-    // the item's first sorted pair: the last of the group's pairs whose
-    // stacked rows start at or before b0
-    int32_t lo = pl.group_ptr[g], hi = pl.group_ptr[g + 1] - 1;
-    while (lo < hi) {
-      const int32_t mid = (lo + hi + 1) >> 1;
-      if (pl.prow[mid] <= b0) lo = mid; else hi = mid - 1;
+  for (int64_t gw = wave0; gw < n_groups; gw += n_waves) {
+    const int32_t g = (int32_t)gw;
+    const int64_t first = pl.item_scan[g];
+    const int64_t n_it = pl.item_scan[g + 1] - first;
+    const int64_t base = pl.prow[pl.group_ptr[g]];
+    const int64_t R = pl.prow[pl.group_ptr[g + 1]] - base;
+    const uint8_t cls = cost_class(R, a.doc_len[pl.group_doc[g]]);
+    for (int64_t it = lane; it < n_it; it += 64) {
+      const int64_t idx = first + it;
+      if (idx >= pl.items_cap) break;
+      pl.item_cls[idx] = cls;
+      const int64_t b0 =
+          a.exact_items ? base + it * a.rows_per_item
+                        : base + ((it * R / n_it) & ~(int64_t)31);
+      const int64_t b1 =
+          it + 1 < n_it
+              ? (a.exact_items ? base + (it + 1) * a.rows_per_item
+                               : base + (((it + 1) * R / n_it) & ~(int64_t)31))
+              : base + R;
+      // the item's first sorted pair: the last of the group's pairs whose
+      // stacked rows start at or before b0
+      int32_t lo = pl.group_ptr[g], hi = pl.group_ptr[g + 1] - 1;
+      while (lo < hi) {
+        const int32_t mid = (lo + hi + 1) >> 1;
+        if (pl.prow[mid] <= b0) lo = mid; else hi = mid - 1;
+      }
+      pl.items[idx] = make_int4(g, (int32_t)b0, (int32_t)b1, lo);
     }
-    pl.items[idx] = make_int4(g, (int32_t)b0, (int32_t)b1, lo);
   }
 }
 
@@ -690,7 +696,8 @@ hipError_t launch_plan(const AttnCall &c, const Plan &pl,
                      dim3(kThreads), 0, s, pl, pa, totals);
   e = exclusive_scan(pl.item_scan, P + 1, pl.blk, totals + kTotItems, s);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_items_emit, dim3(blocks_for(P, kThreads)),
+  hipLaunchKernelGGL(k_items_emit,
+                     dim3(std::min(blocks_for(P * 64, kThreads), 65536u)),
                      dim3(kThreads), 0, s, pl, pa, totals);
   hipLaunchKernelGGL(k_blk_pair, dim3(blocks_for(P, kThreads)),
                      dim3(kThreads), 0, s, pl, totals);
