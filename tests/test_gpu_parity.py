@@ -104,6 +104,25 @@ def test_group_split_into_many_items():
     _free()
 
 
+def test_more_groups_than_item_waves():
+    """300,000 single-token pairs, each on a document of its own: more
+    document groups than the waves of the item split's bounded grid
+    (65,536 blocks of four waves), so those waves stride over the groups.
+    Pairs from both ends of the group order and a random sample must
+    match the oracle."""
+    P = 300_000
+    rng = np.random.default_rng(11)
+    doc_len = rng.integers(0, 5, P).astype(np.int32)
+    st = workloads.custom(doc_len, np.arange(P, dtype=np.int32),
+                          np.ones(P, np.int32), 4, 1, name="many_groups")
+    case = setup(st, seed=5)
+    assert run(case) == 0
+    picks = np.r_[np.arange(64), np.arange(P - 64, P),
+                  rng.choice(P, 128, replace=False)]
+    compare(case, np.unique(picks))
+    _free()
+
+
 def test_sharp_softmax_keys_x4():
     """Prefix keys scaled x4: peaked softmax, frequent running-max
     rescaling.  Tolerance derived from the bf16 rounding of the MFMA
