@@ -107,9 +107,18 @@ __global__ __launch_bounds__(kScanThreads) void k_scan_apply(
   if (i0 + 1 < n) data[i0 + 1] = pre + a0;
 }
 
+// Arrays up to this many values are scanned by one block walking them tile
+// by tile (k_scan_top on the data itself): one launch instead of three.
+constexpr int64_t kScanOneBlock = 8 * kScanTile;
+
 // In-place exclusive scan of n int64 values; the grand total goes to *total.
 hipError_t exclusive_scan(int64_t *data, int64_t n, int64_t *blk,
                           int64_t *total, hipStream_t s) {
+  if (n <= kScanOneBlock) {
+    hipLaunchKernelGGL(k_scan_top, dim3(1), dim3(kScanThreads), 0, s, data,
+                       n, total);
+    return hipGetLastError();
+  }
   const unsigned nb = blocks_for(n, kScanTile);
   hipLaunchKernelGGL(k_scan_reduce, dim3(nb), dim3(kScanThreads), 0, s, data,
                      n, blk);
